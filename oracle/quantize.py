@@ -1,0 +1,153 @@
+"""Block quantizers and dequantization (oracle; test infrastructure only).
+
+Per block (eq:microscaling, eq:scale-target, Table 5 of the paper):
+  1. a_B = max |x_i| over the block (exact);
+  2. u_B = a_B * S, the ideal block-scale code (S = T / g);
+  3. s_B = Q_UE5M3(u_B): nearest UE5M3 code, ties to even, saturating;
+  4. a code that rounds to zero is replaced by the code of 1.0 before the
+     reciprocal and dequantization (the proposed run's zero-scale rule);
+  5. r_B = G / s_B (the reciprocal of the decode factor g_dec * s_B,
+     G = T F / g);
+  6. y_i = x_i * r_B;
+  7. q_i = Q_E2M1(y_i): ties-to-even (RN) or stochastic rounding (SR, only
+     for the upstream gradient dY, eq:sr).
+Each step is one binary32 operation rounded to nearest-even (this
+implementation's reading; see ``scaling``).  The reconstructed value is
+x_hat_i = dec * s_B * q_i with dec = g / (T F).
+
+Blockings (Sec. 2.3 and Table 5: 1D blocks of 16 along the GEMM contraction
+dimension for activations and gradients, 2D 16x16 tiles for weights):
+
+* ``quantize_1d(axis=1)``: blocks of 16 consecutive elements of a row.
+  payload [R, C/2] (byte [r, c/2] = nib(r, c) | nib(r, c+1) << 4),
+  scales [R, C/16].
+* ``quantize_1d(axis=0)``: blocks of 16 consecutive rows of a column.  The
+  output is stored transposed, i.e. as the row blocking of x^T:
+  payload [C, R/2] (byte [c, r/2] = nib(r, c) | nib(r+1, c) << 4),
+  scales [C, R/16].
+* ``quantize_2d``: 16x16 tiles aligned at (0, 0).  payload [R, C/2],
+  scales [R/16, C/16], and the transposed payload [C, R/2] of the same
+  nibbles.
+
+SR words: element (r, c) of an R x C source uses ``philox.sr_words(seed,
+tensor_id, r * C + c)``, independent of the blocking.
+"""
+
+import numpy as np
+
+from . import formats, philox, scaling
+
+
+def _block_codes(xb, S, G, mode, words):
+    """xb: float32 [nb, B].  Returns (scale codes uint8 [nb], nibbles [nb, B])."""
+    xb = np.asarray(xb, dtype=np.float32)
+    a_B = np.max(np.abs(xb), axis=1) if xb.shape[1] else np.zeros(xb.shape[0], np.float32)
+    with np.errstate(over="ignore", invalid="ignore"):
+        u_B = (a_B * np.float32(S)).astype(np.float32)
+        code = formats.ue5m3_encode_rne_sat(u_B)
+        code = np.where(code == 0, formats.UE5M3_ONE, code).astype(np.uint8)
+        s_hat = formats.ue5m3_decode(code).astype(np.float32)
+        r_B = (np.float32(G) / s_hat).astype(np.float32)
+        y = (xb * r_B[:, None]).astype(np.float32)
+    if mode == "rn":
+        nib = formats.e2m1_encode_rne(y)
+    elif mode == "sr":
+        nib = formats.e2m1_encode_sr(y, words)
+    else:
+        raise ValueError(mode)
+    return code, nib
+
+
+def _pack_rows(nib):
+    """[R, C] nibbles -> [R, C/2] bytes, low nibble = even column."""
+    nib = np.asarray(nib, dtype=np.uint8)
+    return (nib[:, 0::2] | (nib[:, 1::2] << 4)).astype(np.uint8)
+
+
+def _unpack_rows(payload):
+    p = np.asarray(payload, dtype=np.uint8)
+    out = np.empty((p.shape[0], p.shape[1] * 2), dtype=np.uint8)
+    out[:, 0::2] = p & 15
+    out[:, 1::2] = p >> 4
+    return out
+
+
+def _words_for(shape, seed, tensor_id, mode):
+    if mode != "sr":
+        return None
+    R, C = shape
+    idx = np.arange(R * C, dtype=np.int64).reshape(R, C)
+    return philox.sr_words(seed, tensor_id, idx)
+
+
+def quantize_1d(x_bits, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0):
+    """1D block-16 quantization of a bf16 matrix.  Returns
+    (payload, scales, dec) in the layouts described in the module header."""
+    x = scaling.bf16_to_f32(x_bits)
+    R, C = x.shape
+    S, G, dec = scaling.tensor_multipliers(g, target)
+    words = _words_for((R, C), seed, tensor_id, mode)
+    if axis == 1:
+        if C % 16:
+            raise ValueError("cols must be a multiple of 16")
+        xb = x.reshape(R * (C // 16), 16)
+        wb = None if words is None else words.reshape(R * (C // 16), 16)
+        code, nib = _block_codes(xb, S, G, mode, wb)
+        return _pack_rows(nib.reshape(R, C)), code.reshape(R, C // 16), dec
+    if axis == 0:
+        if R % 16:
+            raise ValueError("rows must be a multiple of 16")
+        xt = np.ascontiguousarray(x.T)                     # [C, R]
+        xb = xt.reshape(C * (R // 16), 16)
+        wb = None if words is None else np.ascontiguousarray(words.T).reshape(C * (R // 16), 16)
+        code, nib = _block_codes(xb, S, G, mode, wb)
+        return _pack_rows(nib.reshape(C, R)), code.reshape(C, R // 16), dec
+    raise ValueError("axis must be 0 or 1")
+
+
+def quantize_2d(x_bits, g, target=448.0, mode="rn", seed=0, tensor_id=0):
+    """16x16 tile quantization.  Returns (payload [R, C/2], scales
+    [R/16, C/16], payload_t [C, R/2], dec)."""
+    x = scaling.bf16_to_f32(x_bits)
+    R, C = x.shape
+    if R % 16 or C % 16:
+        raise ValueError("rows and cols must be multiples of 16")
+    S, G, dec = scaling.tensor_multipliers(g, target)
+    words = _words_for((R, C), seed, tensor_id, mode)
+    tiles = x.reshape(R // 16, 16, C // 16, 16).transpose(0, 2, 1, 3).reshape(-1, 256)
+    wt = None
+    if words is not None:
+        wt = words.reshape(R // 16, 16, C // 16, 16).transpose(0, 2, 1, 3).reshape(-1, 256)
+    code, nib = _block_codes(tiles, S, G, mode, wt)
+    nib = nib.reshape(R // 16, C // 16, 16, 16).transpose(0, 2, 1, 3).reshape(R, C)
+    return (_pack_rows(nib), code.reshape(R // 16, C // 16),
+            _pack_rows(np.ascontiguousarray(nib.T)), dec)
+
+
+# ------------------------------------------------------ dequantization ----
+def decoded_1d(payload, scales, axis):
+    """Decoded operand q * s_B (float64, exact) in the logical [R, C] shape
+    of the tensor that ``quantize_1d`` consumed."""
+    q = formats.e2m1_decode(_unpack_rows(payload))         # [rows_stored, L]
+    s = formats.ue5m3_decode(scales)
+    v = q * np.repeat(s, 16, axis=1)
+    return v if axis == 1 else np.ascontiguousarray(v.T)
+
+
+def decoded_2d(payload, scales):
+    """Decoded weight q * s_tile (float64, exact), logical [R, C]."""
+    q = formats.e2m1_decode(_unpack_rows(payload))
+    s = formats.ue5m3_decode(scales)
+    return q * np.repeat(np.repeat(s, 16, axis=0), 16, axis=1)
+
+
+def decoded_2d_t(payload_t, scales):
+    """Decoded weight from the transposed payload, logical [R, C]."""
+    q = formats.e2m1_decode(_unpack_rows(payload_t)).T
+    s = formats.ue5m3_decode(scales)
+    return q * np.repeat(np.repeat(s, 16, axis=0), 16, axis=1)
+
+
+def dequantize(decoded, dec):
+    """x_hat = dec * (q * s_B) in float64."""
+    return np.float64(np.float32(dec)) * decoded

@@ -1,0 +1,187 @@
+"""Pins of the oracle's block quantizers: hand-worked blocks, grid round
+trips, the RN error bound, layout identities, and the stochastic-rounding
+rule of eq:sr (unbiasedness, exact up-probabilities)."""
+
+import os
+
+import numpy as np
+import pytest
+
+import synthetic
+from oracle import formats, philox, quantize, scaling
+
+
+def _worked_blocks(golden_dir):
+    out = []
+    for line in open(os.path.join(golden_dir, "worked_blocks.txt")):
+        if not line.strip() or line.startswith("#"):
+            continue
+        name, g, T, xs, sc, pay = [f.strip() for f in line.split("|")]
+        x = np.array([float(v) for v in xs.split()], np.float32)
+        out.append((name, float(g), float(T), x, int(sc, 16),
+                    np.array([int(b, 16) for b in pay.split()], np.uint8)))
+    return out
+
+
+def test_worked_blocks(golden_dir):
+    blocks = _worked_blocks(golden_dir)
+    assert len(blocks) == 4
+    for name, g, T, x, sc, pay in blocks:
+        bits = synthetic.f32_to_bf16_bits(x)
+        assert np.array_equal(synthetic.bf16_bits_to_f32(bits), x), name   # exact in bf16
+        p, s, _ = quantize.quantize_1d(bits[None, :], 1, np.float32(g), T)
+        assert s[0, 0] == sc, name
+        assert np.array_equal(p[0], pay), name
+        # same block as a column (axis 0) and inside a 16x16 tile
+        pc, scc, _ = quantize.quantize_1d(bits[:, None], 0, np.float32(g), T)
+        assert scc[0, 0] == sc and np.array_equal(pc[0], pay), name
+
+
+def test_worked_block_sr_keeps_grid_points(golden_dir):
+    # Block D: inputs are grid points, exact midpoints and 5.5 (3/4 of the way
+    # from 4 to 6); under SR grid points never move, midpoints go up with
+    # probability 1/2 and 5.5 with probability 3/4.
+    _, g, T, x, _, _ = [b for b in _worked_blocks(golden_dir) if b[0] == "D"][0]
+    bits = synthetic.f32_to_bf16_bits(np.tile(x, (4096, 1)))
+    p, s, _ = quantize.quantize_1d(bits, 1, np.float32(g), T, mode="sr", seed=11, tensor_id=3)
+    q = formats.e2m1_decode(quantize._unpack_rows(p))
+    on_grid = np.isin(np.abs(x), formats.E2M1_MAG) | (np.abs(x) > 6)
+    assert np.all(q[:, on_grid] == np.where(np.abs(x[on_grid]) > 6, np.sign(x[on_grid]) * 6, x[on_grid]))
+    frac_up = np.mean(np.abs(q[:, ~on_grid]) > np.abs(x[~on_grid]), axis=0)
+    expect = np.where(np.abs(x[~on_grid]) == 5.5, 0.75, 0.5)
+    assert np.all(np.abs(frac_up - expect) < 5 * 0.5 / np.sqrt(4096))
+
+
+def test_zero_scale_rule_and_underflow():
+    # A block whose ideal code rounds to zero stores the code of 1.0
+    # (Sec. 4.3: zero block-scale code replaced with 1).
+    x = np.zeros((1, 32), np.float32)
+    x[0, 16] = 1e-12
+    bits = synthetic.f32_to_bf16_bits(x)
+    p, s, _ = quantize.quantize_1d(bits, 1, np.float32(1000.0), 448.0)
+    assert list(s[0]) == [formats.UE5M3_ONE, formats.UE5M3_ONE]
+    assert np.all(p == 0)
+
+
+def test_grid_values_round_trip():
+    # g = T = 448 gives S = 1 and G = 6: a block with maximum 6 has scale 6 and
+    # r = 1, so values on the E2M1 grid are encoded exactly and decode to 6 x.
+    rng = np.random.default_rng(0)
+    vals = rng.choice(np.concatenate([formats.E2M1_MAG, -formats.E2M1_MAG]), (32, 64))
+    vals[:, ::16] = 6.0
+    bits = synthetic.f32_to_bf16_bits(vals.astype(np.float32))
+    p, s, dec = quantize.quantize_1d(bits, 1, np.float32(448.0), 448.0)
+    assert np.all(s == 0x8C)
+    d = quantize.decoded_1d(p, s, 1)
+    assert np.array_equal(d, 6.0 * vals)
+    assert np.allclose(quantize.dequantize(d, dec), vals, rtol=1e-6, atol=0)
+
+
+@pytest.mark.parametrize("axis", [0, 1])
+def test_rn_error_bound(axis):
+    bits = synthetic.activation(1, 64, 128, 0.01, 50.0)
+    x = synthetic.bf16_bits_to_f32(bits).astype(np.float64)
+    g = scaling.amax(bits)
+    S, G, dec = scaling.tensor_multipliers(g, 448.0)
+    p, s, _ = quantize.quantize_1d(bits, axis, g, 448.0)
+    d = quantize.decoded_1d(p, s, axis)                       # q * s_B
+    sv = formats.ue5m3_decode(s)
+    sfull = np.repeat(sv, 16, axis=1)
+    if axis == 0:
+        sfull = sfull.T
+    y = x * float(G) / sfull                                  # ideal E2M1 input
+    q = d / sfull
+    ay = np.abs(y)
+    spacing = np.where(ay < 2, 0.5, np.where(ay < 4, 1.0, 2.0))
+    err = np.abs(y - q)
+    # |y - q| <= half the E2M1 spacing around y, allowing a few binary32 ulps
+    # of slop from rounding G, r_B and y; saturated entries decode to +-6
+    sat = ay >= 6
+    assert np.all(sat | (err <= spacing / 2 + 1e-5 * ay + 1e-30))
+    assert np.all(np.abs(q[sat]) == 6) and np.all(np.abs(q) <= 6)
+
+
+def test_axis0_is_axis1_of_transpose():
+    bits = synthetic.gradient(2, 96, 48, 1e-4, 2.0)
+    g = scaling.amax(bits)
+    for mode in ["rn"]:
+        p0, s0, d0 = quantize.quantize_1d(bits, 0, g, 448.0, mode)
+        p1, s1, d1 = quantize.quantize_1d(np.ascontiguousarray(bits.T), 1, g, 448.0, mode)
+        assert np.array_equal(p0, p1) and np.array_equal(s0, s1) and d0 == d1
+
+
+def test_2d_tiles():
+    bits = synthetic.weight(4, 64, 96)
+    g = scaling.amax(bits)
+    S, G, dec = scaling.tensor_multipliers(g, 448.0)
+    p, s, pt, d = quantize.quantize_2d(bits, g, 448.0)
+    x = synthetic.bf16_bits_to_f32(bits)
+    # one scale per 16x16 tile, from the tile maximum
+    tmax = np.abs(x).reshape(4, 16, 6, 16).max(axis=(1, 3)).astype(np.float32)
+    exp = formats.ue5m3_encode_rne_sat((tmax * S).astype(np.float32))
+    exp = np.where(exp == 0, formats.UE5M3_ONE, exp)
+    assert np.array_equal(s, exp)
+    # the transposed payload holds the same nibbles
+    assert np.array_equal(quantize.decoded_2d(p, s), quantize.decoded_2d_t(pt, s))
+    # a tile with a single non-zero entry behaves like that entry's 1D block
+    one = np.zeros((16, 16), np.float32)
+    one[3, 5] = 0.75
+    b1 = synthetic.f32_to_bf16_bits(one)
+    p2, s2, _, _ = quantize.quantize_2d(b1, np.float32(1.0), 448.0)
+    p1, s1, _ = quantize.quantize_1d(b1[3:4], 1, np.float32(1.0), 448.0)
+    assert s2[0, 0] == s1[0, 0] and np.array_equal(p2[3], p1[0])
+
+
+# --------------------------------------------------------------- SR ----
+def test_sr_unbiased():
+    """E[Q_SR(z)] = z (eq:sr) over 2**20 Philox draws per value."""
+    zs = np.array([0.1, 0.3, 0.49, 0.7, 1.1, 1.9, 2.2, 3.3, 4.9, 5.99, -0.2, -2.7,
+                   1e-7, 2.0 ** -30], np.float32)
+    n = 1 << 20
+    idx = np.arange(n, dtype=np.int64)
+    for i, z in enumerate(zs):
+        w = philox.sr_words(99, i, idx)
+        q = formats.e2m1_decode(formats.e2m1_encode_sr(np.full(n, z, np.float32), w))
+        a = abs(float(z))
+        lo = formats.E2M1_MAG[np.searchsorted(formats.E2M1_MAG, a, "right") - 1]
+        hi = formats.E2M1_MAG[np.searchsorted(formats.E2M1_MAG, a, "right")]
+        p = (a - lo) / (hi - lo)
+        sigma = (hi - lo) * np.sqrt(p * (1 - p) / n)
+        assert abs(q.mean() - float(z)) <= 5 * sigma + 1e-12, z
+        assert set(np.unique(np.abs(q))) <= {lo, hi}
+
+
+def test_sr_up_probability_exact():
+    """Over evenly spaced words the fraction that rounds up equals frac up
+    to the 2**-32 word resolution (P(up) = (z - q-) / (q+ - q-))."""
+    step = 1 << 12
+    w = np.arange(0, 1 << 32, step, dtype=np.uint64)
+    for z in [0.25, 0.3, 0.75, 1.25, 2.5, 3.999, 5.0, 0.0001, 1.0, 6.0, 7.5]:
+        q = formats.e2m1_decode(formats.e2m1_encode_sr(np.full(w.size, z, np.float32), w))
+        a = float(np.float32(z))
+        if a >= 6:
+            assert np.all(q == 6.0)
+            continue
+        k = np.searchsorted(formats.E2M1_MAG, a, "right") - 1
+        lo, hi = formats.E2M1_MAG[k], formats.E2M1_MAG[k + 1]
+        frac = (a - lo) / (hi - lo)
+        up = np.mean(q > lo)
+        assert abs(up - frac) <= step / 2.0 ** 32, z
+        if frac == 0:
+            assert np.all(q == lo)
+
+
+def test_sr_deterministic_and_keyed():
+    bits = synthetic.gradient(5, 32, 64, 1e-4, 2.0)
+    g = scaling.amax(bits)
+    a = quantize.quantize_1d(bits, 1, g, 448.0, "sr", seed=1, tensor_id=1)
+    b = quantize.quantize_1d(bits, 1, g, 448.0, "sr", seed=1, tensor_id=1)
+    c = quantize.quantize_1d(bits, 1, g, 448.0, "sr", seed=1, tensor_id=2)
+    d = quantize.quantize_1d(bits, 1, g, 448.0, "sr", seed=2, tensor_id=1)
+    assert np.array_equal(a[0], b[0])
+    assert not np.array_equal(a[0], c[0]) and not np.array_equal(a[0], d[0])
+    assert np.array_equal(a[1], c[1])            # scales never depend on SR
+    # SR words follow the source element, whatever the blocking
+    col = quantize.quantize_1d(bits, 0, g, 448.0, "sr", seed=1, tensor_id=1)
+    rowT = quantize.quantize_1d(np.ascontiguousarray(bits.T), 1, g, 448.0, "sr", seed=1, tensor_id=1)
+    assert np.array_equal(col[1], rowT[1])

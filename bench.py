@@ -1,0 +1,241 @@
+#!/usr/bin/env python3
+"""Benchmark of one UE5M3 FP4 linear training step on one MI355X.
+
+A step is the whole per-linear hot path on the Nemotron-H-8B FFN
+up-projection (T = 8192 tokens, K = 4096, N = 21504):
+  sample-and-hold amax (D = 50; a refresh launches the amax kernels),
+  X rows RN, X columns RN (re-blocked along tokens), W 16x16 tiles RN (+ the
+  transposed payload), dY rows SR, dY columns SR,
+  fprop Y = X W^T (bf16 out), dgrad dX = dY W (bf16 out),
+  wgrad dW = dY^T X (fp32 out).
+Inputs are seeded synthetic bf16 tensors resident in HBM before timing.
+
+Prints ONE JSON line.  ``value`` = emulated-FP4 GEMM TFLOP/s of the whole
+step (3 x 2TNK flops / step wall time, quantizers and amax included).
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
+METRIC = "quantize GB/s + emulated FP4 GEMM TFLOP/s (fprop+dgrad+wgrad), % roofline"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--tokens", type=int, default=8192)
+    p.add_argument("--k", type=int, default=4096)
+    p.add_argument("--n", type=int, default=21504)
+    p.add_argument("--period", type=int, default=50)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "gemm_traffic.json"),
+                   help="HBM traffic per launch measured with rocprofv3 counters (JSON)")
+    return p.parse_args()
+
+
+def quant_bytes_1d(rows, cols):
+    return rows * cols * 2 + rows * cols // 2 + rows * cols // 16
+
+
+def quant_bytes_2d(rows, cols, transposed):
+    return rows * cols * 2 + rows * cols // 2 * (2 if transposed else 1) + rows * cols // 256
+
+
+# ------------------------------------------------------------ CPU leg ----
+def cpu_baseline(wl, T, K, N, target_s=12.0):
+    """The oracle, as it stands, on a bounded sample of the same step:
+    quantizers on 1/64 row slices of X, W, dY (cost per element is size-
+    independent, so time x 64); GEMMs on a sampled sub-problem (time x the
+    flop ratio).  Returns the projected whole-step rate in TFLOP/s."""
+    from oracle import gemm as og
+    from oracle import quantize as oq
+    from oracle import scaling as osc
+    x, w, dy = wl["x"], wl["w"], wl["dy"]
+    f = 64
+    xs, ws, ds = x[: T // f], w[: (N // f) // 16 * 16], dy[: T // f]
+    gx, gw, gd = osc.amax(x), osc.amax(w), osc.amax(dy)
+    t0 = time.perf_counter()
+    xr = oq.quantize_1d(xs, 1, gx)
+    xc = oq.quantize_1d(xs, 0, gx)
+    wq = oq.quantize_2d(ws, gw)
+    dr = oq.quantize_1d(ds, 1, gd, "sr", 1, 1)
+    dc = oq.quantize_1d(ds, 0, gd, "sr", 1, 2)
+    t_quant = (time.perf_counter() - t0)
+    quant_scale = (T * K + T * K + N * K + T * N + T * N) / (
+        xs.size + xs.size + ws.size + ds.size + ds.size)
+    # GEMM sample: fprop on (T/f) x (N/f) x K with the sampled operands
+    X = oq.decoded_1d(xr[0], xr[1], 1)
+    W = oq.decoded_2d(wq[0], wq[1])
+    al = og.alpha(xr[2], wq[3])
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        og.fprop(X, W, al)
+        reps += 1
+        if time.perf_counter() - t0 > min(target_s, 5.0) or reps >= 50:
+            break
+    t_gemm = (time.perf_counter() - t0) / reps
+    flop_sample = 2.0 * X.shape[0] * W.shape[0] * K
+    flop_step = 3 * 2.0 * T * N * K
+    t_step = t_quant * quant_scale + t_gemm * flop_step / flop_sample
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = None
+    cores = len(os.sched_getaffinity(0))
+    return {"value": flop_step / t_step / 1e12, "unit": "TFLOP/s", "cores": cores,
+            "blas_threads": blas_threads, "kind": "oracle",
+            "sample": (f"oracle quantizers on 1/{f} row slices of X, W, dY (x{quant_scale:.0f}) "
+                       f"+ float64 decoded-operand fprop on {X.shape[0]}x{W.shape[0]}x{K} "
+                       f"(x{flop_step / flop_sample:.0f} flops); projected step "
+                       f"{t_step:.1f} s")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this build has no "
+              "multi-GPU path; see DESIGN.md for how the step would shard.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2609_02846_amd as ue
+    import synthetic
+
+    T, K, N = args.tokens, args.k, args.n
+    dev = torch.device("cuda:0")
+    wl = synthetic.ffn_step(0, T, K, N)
+
+    def up(bits):
+        return torch.from_numpy(bits.view(np.int16)).to(dev).view(torch.bfloat16)
+    x, w, dy = up(wl["x"]), up(wl["w"]), up(wl["dy"])
+    u8 = lambda *s: torch.empty(s, dtype=torch.uint8, device=dev)
+    f32 = lambda *s: torch.empty(s, dtype=torch.float32, device=dev)
+    bufs = {
+        "xr": (u8(T, K // 2), u8(T, K // 16), f32(1)),
+        "xc": (u8(K, T // 2), u8(K, T // 16), f32(1)),
+        "w": (u8(N, K // 2), u8(N // 16, K // 16), u8(K, N // 2), f32(1)),
+        "dr": (u8(T, N // 2), u8(T, N // 16), f32(1)),
+        "dc": (u8(N, T // 2), u8(N, T // 16), f32(1)),
+    }
+    y = torch.empty(T, N, dtype=torch.bfloat16, device=dev)
+    dx = torch.empty(T, K, dtype=torch.bfloat16, device=dev)
+    dw = torch.empty(N, K, dtype=torch.float32, device=dev)
+    sx, sw, sd = ue.AmaxState(args.period), ue.AmaxState(args.period), ue.AmaxState(args.period)
+
+    names = ["amax", "quant_x_rows", "quant_x_cols", "quant_w_tiles", "quant_dy_rows",
+             "quant_dy_cols", "gemm_fprop", "gemm_dgrad", "gemm_wgrad"]
+
+    def step(t, ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record()
+        mark(0)
+        ue.amax_sample(sx, x, t)
+        ue.amax_sample(sw, w, t)
+        ue.amax_sample(sd, dy, t)
+        mark(1)
+        ue.quantize_1d(x, 1, sx.amax, 448.0, "rn", 0, 0, *bufs["xr"])
+        mark(2)
+        ue.quantize_1d(x, 0, sx.amax, 448.0, "rn", 0, 0, *bufs["xc"])
+        mark(3)
+        pw, sw_, pwt, dw_ = bufs["w"]
+        ue.quantize_2d(w, sw.amax, 448.0, "rn", 0, 0, True, pw, sw_, pwt, dw_)
+        mark(4)
+        ue.quantize_1d(dy, 1, sd.amax, 448.0, "sr", 1000 + t, 1, *bufs["dr"])
+        mark(5)
+        ue.quantize_1d(dy, 0, sd.amax, 448.0, "sr", 1000 + t, 2, *bufs["dc"])
+        mark(6)
+        xr, xc, dr, dc = bufs["xr"], bufs["xc"], bufs["dr"], bufs["dc"]
+        ue.gemm("nt", T, N, K, xr[0], xr[1], xr[2], pw, sw_, dw_, out=y)
+        mark(7)
+        ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], pwt, sw_, dw_, out=dx)
+        mark(8)
+        ue.gemm("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xc[2], out=dw)
+        mark(9)
+
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+    # --- timed region: exactly `steps` steps ---------------------------------
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for t in range(args.warmup, args.warmup + args.steps):
+        step(t)
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    # --- per-kernel durations (HIP events between launches, same stream) ---
+    per = {n: [] for n in names}
+    nprof = min(args.steps, 20)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(10)] for _ in range(nprof)]
+    for i in range(nprof):
+        step(args.warmup + args.steps + i, evs[i])
+    torch.cuda.synchronize()
+    for ev in evs:
+        for j, n in enumerate(names):
+            per[n].append(ev[j].elapsed_time(ev[j + 1]))
+    avg = {n: float(np.mean(v)) for n, v in per.items()}
+
+    flop_gemm = 2.0 * T * N * K
+    qbytes = {"quant_x_rows": quant_bytes_1d(T, K), "quant_x_cols": quant_bytes_1d(T, K),
+              "quant_w_tiles": quant_bytes_2d(N, K, True), "quant_dy_rows": quant_bytes_1d(T, N),
+              "quant_dy_cols": quant_bytes_1d(T, N)}
+    kernels = {}
+    for n, b in qbytes.items():
+        gbs = b / (avg[n] * 1e-3) / 1e9
+        kernels[n] = {"ms": round(avg[n], 5), "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    for n in ["gemm_fprop", "gemm_dgrad", "gemm_wgrad"]:
+        tf = flop_gemm / (avg[n] * 1e-3) / 1e12
+        kernels[n] = {"ms": round(avg[n], 5), "TFLOP/s": round(tf, 1), "frac": round(tf / BF16_PEAK_TFLOPS, 4)}
+    kernels["amax"] = {"ms": round(avg["amax"], 5), "note": "launches only on refresh steps"}
+    qtime = sum(avg[n] for n in qbytes)
+    quant_gbs = sum(qbytes.values()) / (qtime * 1e-3) / 1e9
+    gtime = sum(avg[n] for n in ["gemm_fprop", "gemm_dgrad", "gemm_wgrad"])
+    gemm_tf = 3 * flop_gemm / (gtime * 1e-3) / 1e12
+
+    dom = "gemm_fprop"
+    traffic = None
+    if os.path.exists(args.traffic):
+        try:
+            tr = json.load(open(args.traffic))
+            if tr.get("kernel") == dom and tr.get("config") == [T, K, N]:
+                traffic = tr.get("bytes_per_launch")
+        except Exception:
+            traffic = None
+    achieved = flop_gemm / (avg[dom] * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
+                "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": traffic}
+
+    value = 3 * flop_gemm / (ms * 1e-3) / 1e12
+    out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic",
+           "config": {"workload": f"FFN up-projection linear training step T={T} K={K} N={N}",
+                      "tokens": T, "k": K, "n": N, "refresh_period": args.period,
+                      "target": 448.0},
+           "quantize_GBps": round(quant_gbs, 1), "quantize_frac_hbm": round(quant_gbs / HBM_PEAK_GBS, 4),
+           "gemm_TFLOPs": round(gemm_tf, 1), "gemm_frac_bf16": round(gemm_tf / BF16_PEAK_TFLOPS, 4),
+           "kernels": kernels, "roofline": roofline}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, T, K, N)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

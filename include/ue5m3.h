@@ -1,0 +1,187 @@
+/*
+ * ue5m3.h -- C ABI of the UE5M3 FP4 quantize-and-GEMM library for MI355X
+ * (gfx950).
+ *
+ * Implements the per-linear hot path of "UE5M3 FP4 Block Scaling for Stable
+ * Language Model Pretraining" (arXiv 2609.02846): E2M1 payloads in blocks of
+ * 16 with unsigned E5M3 (UE5M3) block scales -- 1D along the contraction
+ * dimension for activations and gradients, 2D 16x16 tiles for weights --
+ * under a periodic sample-and-hold tensor amax, stochastic rounding of the
+ * upstream gradient only, and the decoded-operand fprop / dgrad / wgrad
+ * GEMMs.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - All tensor pointers are DEVICE pointers owned by the caller, who
+ *   allocates and frees them; the library allocates no device memory and
+ *   keeps no global mutable state.  Every pointer must be 16-byte aligned.
+ * - bf16 tensors are dense row-major [rows, cols] arrays of 16-bit words.
+ * - Payloads pack two E2M1 nibbles per byte along a row: byte [r, c/2] holds
+ *   element (r, c) in its low nibble and (r, c+1) in its high nibble.
+ *   Nibble = sign << 3 | magnitude code, magnitudes {0, .5, 1, 1.5, 2, 3, 4, 6}.
+ * - Scale bytes are UE5M3 codes (value (1 + m/8) 2^(e-15) for exponent field
+ *   e >= 1, m 2^-17 for e = 0), stored row-major as described per call.
+ * - Every call only enqueues work on `stream` (a hipStream_t; 0 is the null
+ *   stream) and returns without synchronizing.  Argument errors are detected
+ *   on the host before anything is enqueued; then nothing is written.
+ * - Inputs must be finite; results for NaN / Inf inputs are unspecified.
+ * - No C++ exception crosses this interface.
+ */
+#ifndef UE5M3_H
+#define UE5M3_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    UE5M3_OK = 0,
+    UE5M3_EINVAL = 1,   /* null pointer, bad enum, bad target/period    */
+    UE5M3_ESHAPE = 2,   /* negative size or size not a required multiple */
+    UE5M3_EALIGN = 3,   /* pointer not 16-byte aligned                   */
+    UE5M3_ELAYOUT = 4,  /* unknown GEMM layout                           */
+    UE5M3_EHIP = 5      /* a HIP launch or runtime call failed           */
+} ue5m3_status_t;
+
+typedef enum { UE5M3_RN = 0, UE5M3_SR = 1 } ue5m3_round_t;
+
+typedef enum { UE5M3_NT = 0, UE5M3_NN = 1, UE5M3_TN = 2 } ue5m3_layout_t;
+
+typedef enum { UE5M3_OUT_F32 = 0, UE5M3_OUT_BF16 = 1 } ue5m3_out_t;
+
+/*
+ * Sample-and-hold state of one operand's tensor reference (paper Sec. 4.1,
+ * eq:delayed-amax).  Plain host data plus one caller-owned device float.
+ *   amax_dev      device float receiving the sampled amax (fp32 bits of
+ *                 max |x|); read by the quantizers.
+ *   last_refresh  optimizer step of the last refresh (tau).
+ *   period        refresh period D in optimizer steps (50 in the paper's
+ *                 recipe; 1 = current scaling).
+ *   has_cache     0 until the first refresh; reset to 0 on resume (the
+ *                 paper's caches are not checkpointed).
+ */
+typedef struct {
+    float*  amax_dev;
+    int64_t last_refresh;
+    int32_t period;
+    int32_t has_cache;
+} ue5m3_amax_state_t;
+
+/* Initialise `st` with an empty cache.  EINVAL if st or amax_dev is null or
+ * period < 1; EALIGN if amax_dev is not 4-byte aligned. */
+ue5m3_status_t ue5m3_amax_state_init(ue5m3_amax_state_t* st, float* amax_dev,
+                                     int32_t period);
+
+/* Empty the cache so that the next ue5m3_amax_sample refreshes (simulated
+ * process restart / resume).  A null st is ignored. */
+void ue5m3_amax_state_reset(ue5m3_amax_state_t* st);
+
+/*
+ * eq:delayed-amax.  At optimizer step `step`, if the cache is empty or
+ * step - last_refresh >= period, enqueue the tensor amax a = max_i |x_i| of
+ * the bf16 tensor x (numel elements) into *st->amax_dev, set last_refresh =
+ * step, has_cache = 1 and *refreshed = 1; otherwise enqueue nothing and set
+ * *refreshed = 0.  The decision uses host integers only (no device read).
+ * numel = 0 stores amax 0 (the quantizers then use reference 1).
+ * `refreshed` may be null.
+ */
+ue5m3_status_t ue5m3_amax_sample(ue5m3_amax_state_t* st, const void* x_bf16,
+                                 int64_t numel, int64_t step, int32_t* refreshed,
+                                 hipStream_t stream);
+
+/*
+ * 1D block-16 quantization of a bf16 matrix x [rows, cols] (eq:microscaling,
+ * eq:scale-target, Table 5).  With g = *amax_dev (the held reference), T =
+ * target and F = 6, each block B computes in binary32 (one round-to-nearest-
+ * even per operation): S = T/g, G = 6T/g, u = max|x_B| * S, s = UE5M3(u)
+ * (nearest, ties to even, saturating above 61440; a zero code is replaced by
+ * the code of 1.0), r = G/s, y_i = x_i * r, and the E2M1 nibble of y_i by
+ * round-to-nearest-even (mode RN) or stochastic rounding (mode SR, eq:sr).
+ * A reference g that is not positive and finite, or with 6T/g >= 2^110, is
+ * replaced by 1.
+ *
+ * SR draws for source element (r, c) the word (r*cols + c) & 3 of
+ * Philox4x32-10 with key (seed lo, seed hi) and counter
+ * ((r*cols + c) >> 2 as 64 bits, tensor_id, 0), and rounds the magnitude up
+ * iff word < ceil(frac * 2^32), frac = (|y| - q_lo) / (q_hi - q_lo).
+ *
+ * axis = 1 (blocks along rows; fprop X, dgrad dY):
+ *     requires cols % 16 == 0;  payload [rows, cols/2];  scales [rows, cols/16].
+ * axis = 0 (blocks down columns; wgrad dY and X re-blocked along tokens):
+ *     requires rows % 16 == 0 and cols % 2 == 0.  The output is stored
+ *     TRANSPOSED, i.e. as the axis-1 quantization of x^T: payload
+ *     [cols, rows/2], scales [cols, rows/16].
+ * dec_out (nullable): receives the decode multiplier dec = g / (6T) used by
+ *     the GEMM epilogue.
+ * target must be finite and > 0 (448 default; 2048 for the wgrad-dY
+ * override of Sec. 4.2).
+ */
+ue5m3_status_t ue5m3_quantize_1d(const void* x_bf16, int64_t rows, int64_t cols,
+                                 int32_t axis, const float* amax_dev, float target,
+                                 ue5m3_round_t mode, uint64_t seed, uint32_t tensor_id,
+                                 uint8_t* payload, uint8_t* scales, float* dec_out,
+                                 hipStream_t stream);
+
+/*
+ * 2D 16x16 tile quantization of a bf16 weight w [rows, cols] (Sec. 2.3 and
+ * Table 5: one scale per 16x16 tile so that the row-wise and column-wise GEMM
+ * views share the quantized values).  Same per-block arithmetic as
+ * ue5m3_quantize_1d with the block maximum taken over the tile.
+ * Requires rows % 16 == 0 and cols % 16 == 0.
+ *   payload   [rows, cols/2]
+ *   scales    [rows/16, cols/16]
+ *   payload_t (nullable) [cols, rows/2]: the same nibbles transposed, the
+ *             operand of the dgrad GEMM.
+ *   dec_out   (nullable) decode multiplier, as above.
+ */
+ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
+                                 const float* amax_dev, float target,
+                                 ue5m3_round_t mode, uint64_t seed, uint32_t tensor_id,
+                                 uint8_t* payload, uint8_t* scales, uint8_t* payload_t,
+                                 float* dec_out, hipStream_t stream);
+
+/*
+ * Decoded-operand FP4 GEMM (Sec. 5.1; the three products of Sec. 4.3):
+ *     C[m, n] = alpha * sum_k A_hat[m, k] * B_hat[n, k],
+ *     alpha = RN(*a_dec * *b_dec),
+ * where X_hat = E2M1 value * UE5M3 block scale (exact in bf16), products are
+ * exact and the sum is accumulated in fp32 (bf16 matrix cores); the order of
+ * the fp32 additions is unspecified.  C is a dense row-major [M, N] fp32
+ * array (UE5M3_OUT_F32) or bf16 array (UE5M3_OUT_BF16, round to nearest even
+ * of the fp32 result).
+ *
+ * Both operands are passed in contraction-contiguous form, as produced by the
+ * quantizers for each product of a linear Y = X W^T (X [T,K], W [N,K]):
+ *
+ * UE5M3_NT  fprop  Y = X W^T:  M = T, N = N, K = K.
+ *     a = quantize_1d(X, axis 1): payload [M, K/2], scales [M, K/16]
+ *     b = quantize_2d(W):         payload [N, K/2], scales [N/16, K/16]
+ * UE5M3_NN  dgrad  dX = dY W:   M = T, N = K_w, K = N_w.
+ *     a = quantize_1d(dY, axis 1): payload [M, K/2], scales [M, K/16]
+ *     b = quantize_2d(W): payload_t [N, K/2], scales [K/16, N/16]
+ * UE5M3_TN  wgrad  dW = dY^T X: M = N_w, N = K_w, K = T.
+ *     a = quantize_1d(dY, axis 0): payload [M, K/2], scales [M, K/16]
+ *     b = quantize_1d(X, axis 0):  payload [N, K/2], scales [N, K/16]
+ *
+ * Requires M, N, K >= 0, K % 16 == 0, and N % 16 == 0 for NT and NN.
+ * M = 0 or N = 0 writes nothing; K = 0 writes zeros.
+ */
+ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
+                          const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
+                          const uint8_t* b, const uint8_t* b_scales, const float* b_dec,
+                          void* c, ue5m3_out_t c_type, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* ue5m3_status_string(ue5m3_status_t status);
+
+/* Library ABI version (major * 10000 + minor * 100 + patch). */
+int32_t ue5m3_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UE5M3_H */

@@ -38,9 +38,16 @@ import numpy as np
 from . import formats, philox, scaling
 
 
-def _block_codes(xb, S, G, mode, words):
-    """xb: float32 [nb, B].  Returns (scale codes uint8 [nb], nibbles [nb, B])."""
+def _block_codes(xb, S, G, mode, words, chunk=1 << 16):
+    """xb: float32 [nb, B].  Returns (scale codes uint8 [nb], nibbles [nb, B]).
+    Blocks are independent; large inputs are processed ``chunk`` blocks at a
+    time only to bound memory."""
     xb = np.asarray(xb, dtype=np.float32)
+    if xb.shape[0] > chunk:
+        parts = [_block_codes(xb[i:i + chunk], S, G, mode,
+                              None if words is None else words[i:i + chunk], chunk)
+                 for i in range(0, xb.shape[0], chunk)]
+        return (np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts]))
     a_B = np.max(np.abs(xb), axis=1) if xb.shape[1] else np.zeros(xb.shape[0], np.float32)
     with np.errstate(over="ignore", invalid="ignore"):
         u_B = (a_B * np.float32(S)).astype(np.float32)
@@ -72,21 +79,25 @@ def _unpack_rows(payload):
     return out
 
 
-def _words_for(shape, seed, tensor_id, mode):
+def _words_for(shape, seed, tensor_id, mode, elem_index):
     if mode != "sr":
         return None
     R, C = shape
-    idx = np.arange(R * C, dtype=np.int64).reshape(R, C)
-    return philox.sr_words(seed, tensor_id, idx)
+    if elem_index is None:
+        elem_index = np.arange(R * C, dtype=np.int64).reshape(R, C)
+    return philox.sr_words(seed, tensor_id, np.asarray(elem_index, np.int64))
 
 
-def quantize_1d(x_bits, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0):
+def quantize_1d(x_bits, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0, elem_index=None):
     """1D block-16 quantization of a bf16 matrix.  Returns
-    (payload, scales, dec) in the layouts described in the module header."""
+    (payload, scales, dec) in the layouts described in the module header.
+    ``elem_index`` (SR only) gives each element's row-major index in the
+    source tensor when ``x_bits`` is a sampled part of it (default: x itself
+    is the source)."""
     x = scaling.bf16_to_f32(x_bits)
     R, C = x.shape
     S, G, dec = scaling.tensor_multipliers(g, target)
-    words = _words_for((R, C), seed, tensor_id, mode)
+    words = _words_for((R, C), seed, tensor_id, mode, elem_index)
     if axis == 1:
         if C % 16:
             raise ValueError("cols must be a multiple of 16")
@@ -105,7 +116,7 @@ def quantize_1d(x_bits, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0):
     raise ValueError("axis must be 0 or 1")
 
 
-def quantize_2d(x_bits, g, target=448.0, mode="rn", seed=0, tensor_id=0):
+def quantize_2d(x_bits, g, target=448.0, mode="rn", seed=0, tensor_id=0, elem_index=None):
     """16x16 tile quantization.  Returns (payload [R, C/2], scales
     [R/16, C/16], payload_t [C, R/2], dec)."""
     x = scaling.bf16_to_f32(x_bits)
@@ -113,7 +124,7 @@ def quantize_2d(x_bits, g, target=448.0, mode="rn", seed=0, tensor_id=0):
     if R % 16 or C % 16:
         raise ValueError("rows and cols must be multiples of 16")
     S, G, dec = scaling.tensor_multipliers(g, target)
-    words = _words_for((R, C), seed, tensor_id, mode)
+    words = _words_for((R, C), seed, tensor_id, mode, elem_index)
     tiles = x.reshape(R // 16, 16, C // 16, 16).transpose(0, 2, 1, 3).reshape(-1, 256)
     wt = None
     if words is not None:

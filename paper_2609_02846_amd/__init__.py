@@ -1,0 +1,202 @@
+"""UE5M3 FP4 quantize-and-GEMM for MI355X (gfx950).
+
+Thin Python binding of the C ABI in include/ue5m3.h (libue5m3.so, built
+in-tree by ``paper_2609_02846_amd.build``).  Every step of the hot path runs
+in the library's HIP kernels; this module only marshals arguments: torch
+tensors supply device memory and the current HIP stream.
+
+The library is required: importing the binding functions raises if
+libue5m3.so is missing, and there is no CPU fallback.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libue5m3.so")
+
+UE5M3_OK, UE5M3_EINVAL, UE5M3_ESHAPE, UE5M3_EALIGN, UE5M3_ELAYOUT, UE5M3_EHIP = range(6)
+RN, SR = 0, 1
+NT, NN, TN = 0, 1, 2
+OUT_F32, OUT_BF16 = 0, 1
+_MODES = {"rn": RN, "sr": SR}
+_LAYOUTS = {"nt": NT, "nn": NN, "tn": TN}
+
+EXPORTED_SYMBOLS = (
+    "ue5m3_amax_state_init", "ue5m3_amax_state_reset", "ue5m3_amax_sample",
+    "ue5m3_quantize_1d", "ue5m3_quantize_2d", "ue5m3_gemm",
+    "ue5m3_status_string", "ue5m3_version",
+)
+
+
+class AmaxStateC(ctypes.Structure):
+    """Mirror of ue5m3_amax_state_t."""
+    _fields_ = [("amax_dev", ctypes.c_void_p), ("last_refresh", ctypes.c_int64),
+                ("period", ctypes.c_int32), ("has_cache", ctypes.c_int32)]
+
+
+class UE5M3Error(RuntimeError):
+    def __init__(self, status, what):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+
+
+_lib = None
+
+
+def load_library(path=LIB_PATH):
+    """Load libue5m3.so and declare the C signatures.  Raises OSError if the
+    library has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise OSError(f"{path} not found: build it with `python -m paper_2609_02846_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i64, i32, u32, u64, f32 = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                   ctypes.c_uint32, ctypes.c_uint64, ctypes.c_float)
+    lib.ue5m3_amax_state_init.argtypes = [ctypes.POINTER(AmaxStateC), vp, i32]
+    lib.ue5m3_amax_state_init.restype = i32
+    lib.ue5m3_amax_state_reset.argtypes = [ctypes.POINTER(AmaxStateC)]
+    lib.ue5m3_amax_state_reset.restype = None
+    lib.ue5m3_amax_sample.argtypes = [ctypes.POINTER(AmaxStateC), vp, i64, i64,
+                                      ctypes.POINTER(ctypes.c_int32), vp]
+    lib.ue5m3_amax_sample.restype = i32
+    lib.ue5m3_quantize_1d.argtypes = [vp, i64, i64, i32, vp, f32, i32, u64, u32, vp, vp, vp, vp]
+    lib.ue5m3_quantize_1d.restype = i32
+    lib.ue5m3_quantize_2d.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, vp, vp, vp, vp, vp]
+    lib.ue5m3_quantize_2d.restype = i32
+    lib.ue5m3_gemm.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, vp]
+    lib.ue5m3_gemm.restype = i32
+    lib.ue5m3_status_string.argtypes = [i32]
+    lib.ue5m3_status_string.restype = ctypes.c_char_p
+    lib.ue5m3_version.argtypes = []
+    lib.ue5m3_version.restype = i32
+    _lib = lib
+    return lib
+
+
+def status_string(status):
+    return load_library().ue5m3_status_string(int(status)).decode()
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(status, what):
+    if status != UE5M3_OK:
+        raise UE5M3Error(status, what)
+
+
+def _bf16_2d(x, name):
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or not x.is_contiguous() or not x.is_cuda:
+        raise ValueError(f"{name} must be a contiguous 2-D bf16 CUDA/HIP tensor")
+    return x
+
+
+def _u8(shape, like):
+    return torch.empty(shape, dtype=torch.uint8, device=like.device)
+
+
+# ------------------------------------------------------------------ API ---
+class AmaxState:
+    """One operand's sample-and-hold cache (eq:delayed-amax): host integers
+    plus a device float holding the sampled amax."""
+
+    def __init__(self, period=50, device="cuda"):
+        self.amax = torch.zeros(1, dtype=torch.float32, device=device)
+        self.c = AmaxStateC()
+        _check(load_library().ue5m3_amax_state_init(ctypes.byref(self.c), _ptr(self.amax),
+                                                     int(period)), "ue5m3_amax_state_init")
+
+    def reset(self):
+        load_library().ue5m3_amax_state_reset(ctypes.byref(self.c))
+
+    @property
+    def has_cache(self):
+        return bool(self.c.has_cache)
+
+    @property
+    def last_refresh(self):
+        return int(self.c.last_refresh)
+
+
+def amax_sample(state, x, step, stream=None):
+    """Refresh ``state`` from tensor ``x`` if the rule of eq:delayed-amax asks
+    for it at optimizer step ``step``; returns True when a refresh was
+    enqueued."""
+    if x.dtype != torch.bfloat16 or not x.is_contiguous() or not x.is_cuda:
+        raise ValueError("x must be a contiguous bf16 CUDA/HIP tensor")
+    flag = ctypes.c_int32(0)
+    _check(load_library().ue5m3_amax_sample(ctypes.byref(state.c), _ptr(x), x.numel(), int(step),
+                                            ctypes.byref(flag), _stream(stream)),
+           "ue5m3_amax_sample")
+    return bool(flag.value)
+
+
+def quantize_1d(x, axis, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0,
+                payload=None, scales=None, dec_out=None, stream=None):
+    """1D block-16 quantization (see ue5m3_quantize_1d).  Returns
+    (payload, scales, dec_out); axis 0 outputs are stored transposed."""
+    _bf16_2d(x, "x")
+    R, C = x.shape
+    if axis == 1:
+        pshape, sshape = (R, C // 2), (R, C // 16)
+    else:
+        pshape, sshape = (C, R // 2), (C, R // 16)
+    payload = _u8(pshape, x) if payload is None else payload
+    scales = _u8(sshape, x) if scales is None else scales
+    if dec_out is None:
+        dec_out = torch.empty(1, dtype=torch.float32, device=x.device)
+    _check(load_library().ue5m3_quantize_1d(_ptr(x), R, C, int(axis), _ptr(amax_dev),
+                                            float(target), _MODES[mode], int(seed) & (2**64 - 1),
+                                            int(tensor_id) & 0xFFFFFFFF, _ptr(payload),
+                                            _ptr(scales), _ptr(dec_out), _stream(stream)),
+           "ue5m3_quantize_1d")
+    return payload, scales, dec_out
+
+
+def quantize_2d(w, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0, transposed=True,
+                payload=None, scales=None, payload_t=None, dec_out=None, stream=None):
+    """16x16 tile quantization (see ue5m3_quantize_2d).  Returns
+    (payload, scales, payload_t or None, dec_out)."""
+    _bf16_2d(w, "w")
+    R, C = w.shape
+    payload = _u8((R, C // 2), w) if payload is None else payload
+    scales = _u8((R // 16, C // 16), w) if scales is None else scales
+    if transposed and payload_t is None:
+        payload_t = _u8((C, R // 2), w)
+    if dec_out is None:
+        dec_out = torch.empty(1, dtype=torch.float32, device=w.device)
+    _check(load_library().ue5m3_quantize_2d(_ptr(w), R, C, _ptr(amax_dev), float(target),
+                                            _MODES[mode], int(seed) & (2**64 - 1),
+                                            int(tensor_id) & 0xFFFFFFFF, _ptr(payload),
+                                            _ptr(scales), _ptr(payload_t), _ptr(dec_out),
+                                            _stream(stream)),
+           "ue5m3_quantize_2d")
+    return payload, scales, payload_t, dec_out
+
+
+def gemm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
+         out_dtype=torch.float32, stream=None):
+    """Decoded-operand FP4 GEMM (see ue5m3_gemm); layout is "nt" (fprop),
+    "nn" (dgrad) or "tn" (wgrad).  Returns the [M, N] output tensor."""
+    lay = _LAYOUTS[layout] if isinstance(layout, str) else int(layout)
+    if out is None:
+        out = torch.empty((M, N), dtype=out_dtype, device=a.device)
+    ctype = OUT_BF16 if out.dtype == torch.bfloat16 else OUT_F32
+    if out.dtype not in (torch.float32, torch.bfloat16) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous fp32 or bf16 tensor")
+    _check(load_library().ue5m3_gemm(lay, int(M), int(N), int(K), _ptr(a), _ptr(a_scales),
+                                     _ptr(a_dec), _ptr(b), _ptr(b_scales), _ptr(b_dec),
+                                     _ptr(out), ctype, _stream(stream)),
+           "ue5m3_gemm")
+    return out

@@ -1,0 +1,139 @@
+// C ABI shim: argument validation, status mapping and dispatch to the kernel
+// launchers.  See include/ue5m3.h for the contract of every entry point.
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/ue5m3.h"
+#include "launch.hpp"
+
+namespace {
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+inline ue5m3_status_t hip_status(hipError_t e) { return e == hipSuccess ? UE5M3_OK : UE5M3_EHIP; }
+
+inline bool valid_target(float t) { return std::isfinite(t) && t > 0.0f && std::isfinite(t * 6.0f); }
+
+}  // namespace
+
+extern "C" {
+
+int32_t ue5m3_version(void) { return 100; }
+
+const char* ue5m3_status_string(ue5m3_status_t s) {
+    switch (s) {
+        case UE5M3_OK: return "ok";
+        case UE5M3_EINVAL: return "invalid argument (null pointer, enum, target or period)";
+        case UE5M3_ESHAPE: return "invalid shape (negative, or not a required multiple)";
+        case UE5M3_EALIGN: return "pointer not 16-byte aligned";
+        case UE5M3_ELAYOUT: return "unknown GEMM layout";
+        case UE5M3_EHIP: return "HIP runtime or launch error";
+    }
+    return "unknown status";
+}
+
+ue5m3_status_t ue5m3_amax_state_init(ue5m3_amax_state_t* st, float* amax_dev, int32_t period) {
+    if (st == nullptr || amax_dev == nullptr || period < 1) return UE5M3_EINVAL;
+    if (!aligned4(amax_dev)) return UE5M3_EALIGN;
+    st->amax_dev = amax_dev;
+    st->last_refresh = 0;
+    st->period = period;
+    st->has_cache = 0;
+    return UE5M3_OK;
+}
+
+void ue5m3_amax_state_reset(ue5m3_amax_state_t* st) {
+    if (st != nullptr) {
+        st->has_cache = 0;
+        st->last_refresh = 0;
+    }
+}
+
+ue5m3_status_t ue5m3_amax_sample(ue5m3_amax_state_t* st, const void* x_bf16, int64_t numel,
+                                 int64_t step, int32_t* refreshed, hipStream_t stream) {
+    if (st == nullptr || st->amax_dev == nullptr || st->period < 1) return UE5M3_EINVAL;
+    if (numel < 0) return UE5M3_ESHAPE;
+    if (numel > 0 && x_bf16 == nullptr) return UE5M3_EINVAL;
+    if (numel > 0 && !aligned16(x_bf16)) return UE5M3_EALIGN;
+    if (!aligned4(st->amax_dev)) return UE5M3_EALIGN;
+    const bool refresh = !st->has_cache || (step - st->last_refresh >= (int64_t)st->period);
+    if (refreshed != nullptr) *refreshed = refresh ? 1 : 0;
+    if (!refresh) return UE5M3_OK;
+    const hipError_t e = ue5m3::launch_amax(x_bf16, numel, st->amax_dev, stream);
+    if (e != hipSuccess) return UE5M3_EHIP;
+    st->has_cache = 1;
+    st->last_refresh = step;
+    return UE5M3_OK;
+}
+
+ue5m3_status_t ue5m3_quantize_1d(const void* x_bf16, int64_t rows, int64_t cols, int32_t axis,
+                                 const float* amax_dev, float target, ue5m3_round_t mode,
+                                 uint64_t seed, uint32_t tensor_id, uint8_t* payload,
+                                 uint8_t* scales, float* dec_out, hipStream_t stream) {
+    if (axis != 0 && axis != 1) return UE5M3_EINVAL;
+    if (mode != UE5M3_RN && mode != UE5M3_SR) return UE5M3_EINVAL;
+    if (amax_dev == nullptr || !valid_target(target)) return UE5M3_EINVAL;
+    if (rows < 0 || cols < 0) return UE5M3_ESHAPE;
+    if (axis == 1 && cols % 16 != 0) return UE5M3_ESHAPE;
+    if (axis == 0 && (rows % 16 != 0 || cols % 2 != 0)) return UE5M3_ESHAPE;
+    if (!aligned4(amax_dev) || (dec_out != nullptr && !aligned4(dec_out))) return UE5M3_EALIGN;
+    if (rows == 0 || cols == 0) return UE5M3_OK;
+    if (x_bf16 == nullptr || payload == nullptr || scales == nullptr) return UE5M3_EINVAL;
+    if (!aligned16(x_bf16) || !aligned16(payload) || !aligned16(scales)) return UE5M3_EALIGN;
+    const bool sr = mode == UE5M3_SR;
+    hipError_t e;
+    if (axis == 1)
+        e = ue5m3::launch_quant_rows(x_bf16, rows, cols, amax_dev, target, sr, seed, tensor_id,
+                                     payload, scales, dec_out, stream);
+    else
+        e = ue5m3::launch_quant_cols(x_bf16, rows, cols, amax_dev, target, sr, seed, tensor_id,
+                                     payload, scales, dec_out, stream);
+    return hip_status(e);
+}
+
+ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
+                                 const float* amax_dev, float target, ue5m3_round_t mode,
+                                 uint64_t seed, uint32_t tensor_id, uint8_t* payload,
+                                 uint8_t* scales, uint8_t* payload_t, float* dec_out,
+                                 hipStream_t stream) {
+    if (mode != UE5M3_RN && mode != UE5M3_SR) return UE5M3_EINVAL;
+    if (amax_dev == nullptr || !valid_target(target)) return UE5M3_EINVAL;
+    if (rows < 0 || cols < 0 || rows % 16 != 0 || cols % 16 != 0) return UE5M3_ESHAPE;
+    if (!aligned4(amax_dev) || (dec_out != nullptr && !aligned4(dec_out))) return UE5M3_EALIGN;
+    if (rows == 0 || cols == 0) return UE5M3_OK;
+    if (w_bf16 == nullptr || payload == nullptr || scales == nullptr) return UE5M3_EINVAL;
+    if (!aligned16(w_bf16) || !aligned16(payload) || !aligned16(scales) ||
+        (payload_t != nullptr && !aligned16(payload_t)))
+        return UE5M3_EALIGN;
+    return hip_status(ue5m3::launch_quant_tiles(w_bf16, rows, cols, amax_dev, target,
+                                                mode == UE5M3_SR, seed, tensor_id, payload,
+                                                scales, payload_t, dec_out, stream));
+}
+
+ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
+                          const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
+                          const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,
+                          ue5m3_out_t c_type, hipStream_t stream) {
+    ue5m3::BScale bmode;
+    switch (layout) {
+        case UE5M3_NT: bmode = ue5m3::BScale::Tile; break;
+        case UE5M3_NN: bmode = ue5m3::BScale::TileT; break;
+        case UE5M3_TN: bmode = ue5m3::BScale::Row; break;
+        default: return UE5M3_ELAYOUT;
+    }
+    if (c_type != UE5M3_OUT_F32 && c_type != UE5M3_OUT_BF16) return UE5M3_EINVAL;
+    if (M < 0 || N < 0 || K < 0 || K % 16 != 0) return UE5M3_ESHAPE;
+    if (bmode != ue5m3::BScale::Row && N % 16 != 0) return UE5M3_ESHAPE;
+    if (M == 0 || N == 0) return UE5M3_OK;
+    if (c == nullptr || a_dec == nullptr || b_dec == nullptr) return UE5M3_EINVAL;
+    if (K > 0 && (a == nullptr || a_scales == nullptr || b == nullptr || b_scales == nullptr))
+        return UE5M3_EINVAL;
+    if (!aligned16(c) || !aligned4(a_dec) || !aligned4(b_dec)) return UE5M3_EALIGN;
+    if (K > 0 && (!aligned16(a) || !aligned16(b) || !aligned16(a_scales) || !aligned16(b_scales)))
+        return UE5M3_EALIGN;
+    return hip_status(ue5m3::launch_gemm(bmode, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c,
+                                         c_type == UE5M3_OUT_BF16, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,140 @@
+// Device-side number formats, tensor multipliers and the Philox stream of
+// the UE5M3 FP4 recipe (arXiv 2609.02846, Sec. 2-4).  Header-only, included
+// by the kernel sources.  Every routine is exact integer / binary32 work; the
+// files are compiled with -ffp-contract=off so that no multiply-add is fused.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ue5m3 {
+
+constexpr float kF = 6.0f;                  // largest E2M1 magnitude (Sec. 4.2)
+constexpr float kUMax = 61440.0f;           // largest UE5M3 value (eq:ue5m3max)
+constexpr uint32_t kCodeMax = 0xF7u;        // its code
+constexpr uint32_t kCodeOne = 0x78u;        // code of 1.0 (zero-scale rule)
+constexpr float kGLimit = 0x1p110f;         // guard on the tensor multiplier
+
+struct Multipliers {
+    float S;    // T / g        : block max -> ideal scale code (eq:scale-target)
+    float G;    // 6T / g       : tensor multiplier
+    float dec;  // g / (6T)     : decode multiplier for the GEMM epilogue
+};
+
+// Sec. 4.2 tensor multipliers from the held amax g and target T.  A reference
+// that is not positive and finite, or whose multiplier would reach 2^110
+// (so that G / 2^-17 could overflow), is replaced by 1.
+__device__ __forceinline__ Multipliers tensor_multipliers(float g, float T) {
+    const float TF = T * kF;
+    bool ok = (g > 0.0f) && (g <= 3.4028234663852886e38f);
+    if (ok) {
+        const float G = TF / g;
+        ok = (G < kGLimit);
+    }
+    if (!ok) g = 1.0f;
+    Multipliers m;
+    m.S = T / g;
+    m.G = TF / g;
+    m.dec = g / TF;
+    return m;
+}
+
+// UE5M3 encode of a non-negative binary32 u: nearest code, ties to the even
+// code, every u above 61440 (and +inf) saturating to 0xF7.
+__device__ __forceinline__ uint32_t ue5m3_encode(float u) {
+    // Subnormal band [0, 2^-14): codes 0..8 are m * 2^-17, so the code is
+    // RNE(u * 2^-17) -- the scaling is exact.
+    const uint32_t sub = (uint32_t)__builtin_rintf(u * 0x1p17f);
+    // Normal band: round the binary32 fraction to 3 bits, nearest-even, and
+    // rebias the exponent from 127 to 15.  A carry propagates into the
+    // exponent, which is the correct next code.
+    uint32_t b = __float_as_uint(u);
+    b += 0x7FFFFu + ((b >> 20) & 1u);
+    const uint32_t nrm = (b >> 20) - ((127u - 15u) << 3);
+    uint32_t c = (u < 0x1p-14f) ? sub : nrm;
+    return (u <= kUMax) ? c : kCodeMax;
+}
+
+// UE5M3 decode of a finite code (0x00..0xF7), exact in binary32.
+__device__ __forceinline__ float ue5m3_decode(uint32_t c) {
+    const uint32_t e = c >> 3, m = c & 7u;
+    const float sub = (float)m * 0x1p-17f;
+    const float nrm = __uint_as_float(((e + 112u) << 23) | (m << 20));
+    return e ? nrm : sub;
+}
+
+// E2M1 nibble of a binary32 y, round to nearest with ties to the even code,
+// magnitudes >= 6 (and inf) saturating to code 7; bit 3 copies the sign.
+__device__ __forceinline__ uint32_t e2m1_rn(float y) {
+    const uint32_t b = __float_as_uint(y);
+    const uint32_t s = (b >> 28) & 8u;
+    const uint32_t ab = b & 0x7FFFFFFFu;
+    const float a = __uint_as_float(ab);
+    // |y| < 1: codes 0, 1, 2 are multiples of 0.5, code = RNE(2|y|).
+    const uint32_t lo = (uint32_t)__builtin_rintf(a * 2.0f);
+    // |y| >= 1: one fraction bit, exponent bias 1 -> code = (e - 126) * 2 + m
+    // after rounding the binary32 fraction to 1 bit, nearest-even.
+    const uint32_t r = ab + 0x1FFFFFu + ((ab >> 22) & 1u);
+    uint32_t hi = (r >> 22) - 252u;
+    hi = hi < 7u ? hi : 7u;
+    return ((a < 1.0f) ? lo : hi) | s;
+}
+
+// E2M1 nibble of y by stochastic rounding with the uniform 32-bit word w
+// (eq:sr): between adjacent magnitudes q_lo <= |y| < q_hi round up iff
+// w < ceil((|y| - q_lo) / (q_hi - q_lo) * 2^32).  |y| >= 6 gives code 7.
+__device__ __forceinline__ uint32_t e2m1_sr(float y, uint32_t w) {
+    const uint32_t b = __float_as_uint(y);
+    const uint32_t s = (b >> 28) & 8u;
+    const float a = __uint_as_float(b & 0x7FFFFFFFu);
+    // spacing h: 0.5 below 2, 1 in [2, 4), 2 in [4, 8)
+    const bool b2 = a < 2.0f, b4 = a < 4.0f;
+    const float inv_h = b2 ? 2.0f : (b4 ? 1.0f : 0.5f);
+    const float h = b2 ? 0.5f : (b4 ? 1.0f : 2.0f);
+    const float steps = __builtin_floorf(a * inv_h);          // exact
+    const float q_lo = steps * h;                             // exact
+    const uint32_t k = (uint32_t)steps;
+    const uint32_t c_lo = b2 ? k : (b4 ? k + 2u : 6u);
+    // (|y| - q_lo) is exact (Sterbenz, or q_lo = 0); scaling by 2^32 / h is a
+    // power of two, so t = frac * 2^32 exactly and t < 2^32.
+    const float t = (a - q_lo) * (inv_h * 4294967296.0f);
+    const uint32_t thr = (uint32_t)__builtin_ceilf(t);
+    const uint32_t c = c_lo + (w < thr ? 1u : 0u);
+    return ((a >= kF) ? 7u : c) | s;
+}
+
+// Philox4x32-10 (Salmon et al., SC'11): four counter words, key (k0, k1),
+// ten rounds of two 32x32->64 multiplies, key bumped by the Weyl constants.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+        const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return c;
+}
+
+// The four SR words of source elements 4j .. 4j+3 (j = element index >> 2).
+__device__ __forceinline__ uint4 sr_words4(uint64_t j, uint32_t tensor_id,
+                                           uint32_t key0, uint32_t key1) {
+    return philox4x32_10(make_uint4((uint32_t)j, (uint32_t)(j >> 32), tensor_id, 0u),
+                         key0, key1);
+}
+
+// bf16 word pair -> two binary32 values (exact).
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// |x| bits of a bf16 pair as two integers (for an exact integer max).
+__device__ __forceinline__ uint32_t bf16_abs_max_pair(uint32_t w) {
+    const uint32_t lo = w & 0x7FFFu;
+    const uint32_t hi = (w >> 16) & 0x7FFFu;
+    return lo > hi ? lo : hi;
+}
+
+}  // namespace ue5m3

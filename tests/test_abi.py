@@ -1,0 +1,123 @@
+"""CPU checks of the C ABI: the library loads, exports every function that
+include/ue5m3.h declares, and validates arguments on the host (these calls
+return before anything is enqueued, so no GPU is needed)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_02846_amd as ue
+from paper_2609_02846_amd import build as ue_build
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ue.LIB_PATH):
+        ue_build.build(verbose=False)
+    return ue.load_library()
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "ue5m3.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ue5m3_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared_functions()
+    assert set(names) == set(ue.EXPORTED_SYMBOLS)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.ue5m3_version() == 100
+
+
+def test_status_strings(lib):
+    for s in range(6):
+        assert ue.status_string(s)
+    assert ue.status_string(99) == "unknown status"
+
+
+FAKE = ctypes.c_void_p(0x100000)          # aligned, never dereferenced
+FAKE_MIS = ctypes.c_void_p(0x100004)      # 4-byte but not 16-byte aligned
+NULL = None
+
+
+def test_quantize_1d_validation(lib):
+    q = lib.ue5m3_quantize_1d
+    args = dict(x=FAKE, rows=32, cols=32, axis=1, amax=FAKE, T=448.0, mode=0, seed=0, tid=0,
+                p=FAKE, s=FAKE, d=NULL, st=NULL)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return q(a["x"], a["rows"], a["cols"], a["axis"], a["amax"], a["T"], a["mode"], a["seed"],
+                 a["tid"], a["p"], a["s"], a["d"], a["st"])
+    assert call(axis=2) == ue.UE5M3_EINVAL
+    assert call(mode=7) == ue.UE5M3_EINVAL
+    assert call(amax=NULL) == ue.UE5M3_EINVAL
+    for bad_t in [0.0, -1.0, float("inf"), float("nan"), 1e38]:
+        assert call(T=bad_t) == ue.UE5M3_EINVAL
+    assert call(cols=24) == ue.UE5M3_ESHAPE             # axis 1 needs cols % 16
+    assert call(rows=-1) == ue.UE5M3_ESHAPE
+    assert call(axis=0, rows=24) == ue.UE5M3_ESHAPE     # axis 0 needs rows % 16
+    assert call(axis=0, cols=33) == ue.UE5M3_ESHAPE     # and cols % 2
+    assert call(x=NULL) == ue.UE5M3_EINVAL
+    assert call(p=NULL) == ue.UE5M3_EINVAL
+    assert call(x=FAKE_MIS) == ue.UE5M3_EALIGN
+    assert call(s=FAKE_MIS) == ue.UE5M3_EALIGN
+    assert call(rows=0) == ue.UE5M3_OK                  # empty: nothing to do
+    assert call(cols=0, x=NULL, p=NULL, s=NULL) == ue.UE5M3_OK
+
+
+def test_quantize_2d_validation(lib):
+    q = lib.ue5m3_quantize_2d
+
+    def call(rows=32, cols=32, w=FAKE, amax=FAKE, T=448.0, mode=0, p=FAKE, s=FAKE, pt=NULL):
+        return q(w, rows, cols, amax, T, mode, 0, 0, p, s, pt, NULL, NULL)
+    assert call(rows=24) == ue.UE5M3_ESHAPE
+    assert call(cols=40) == ue.UE5M3_ESHAPE
+    assert call(mode=2) == ue.UE5M3_EINVAL
+    assert call(T=0.0) == ue.UE5M3_EINVAL
+    assert call(pt=FAKE_MIS) == ue.UE5M3_EALIGN
+    assert call(w=NULL) == ue.UE5M3_EINVAL
+    assert call(rows=0) == ue.UE5M3_OK
+
+
+def test_gemm_validation(lib):
+    g = lib.ue5m3_gemm
+
+    def call(layout=0, M=32, N=32, K=32, a=FAKE, b=FAKE, c=FAKE, ctype=0, ad=FAKE, bd=FAKE):
+        return g(layout, M, N, K, a, FAKE, ad, b, FAKE, bd, c, ctype, NULL)
+    assert call(layout=3) == ue.UE5M3_ELAYOUT
+    assert call(K=40) == ue.UE5M3_ESHAPE
+    assert call(N=40) == ue.UE5M3_ESHAPE                 # NT needs N % 16 (weight tiles)
+    assert call(layout=1, N=40) == ue.UE5M3_ESHAPE
+    assert call(M=-1) == ue.UE5M3_ESHAPE
+    assert call(ctype=5) == ue.UE5M3_EINVAL
+    assert call(c=NULL) == ue.UE5M3_EINVAL
+    assert call(ad=NULL) == ue.UE5M3_EINVAL
+    assert call(a=FAKE_MIS) == ue.UE5M3_EALIGN
+    assert call(M=0) == ue.UE5M3_OK and call(N=0) == ue.UE5M3_OK
+
+
+def test_amax_state_host_logic(lib):
+    """The refresh decision is host-only: with a cache present, steps inside
+    the period enqueue nothing (eq:delayed-amax)."""
+    st = ue.AmaxStateC()
+    assert lib.ue5m3_amax_state_init(ctypes.byref(st), NULL, 50) == ue.UE5M3_EINVAL
+    assert lib.ue5m3_amax_state_init(ctypes.byref(st), FAKE, 0) == ue.UE5M3_EINVAL
+    assert lib.ue5m3_amax_state_init(ctypes.byref(st), FAKE, 50) == ue.UE5M3_OK
+    assert st.has_cache == 0 and st.period == 50
+    st.has_cache, st.last_refresh = 1, 100
+    flag = ctypes.c_int32(-1)
+    for step in [100, 120, 149]:
+        assert lib.ue5m3_amax_sample(ctypes.byref(st), FAKE, 64, step, ctypes.byref(flag), NULL) == 0
+        assert flag.value == 0 and st.last_refresh == 100
+    assert lib.ue5m3_amax_sample(ctypes.byref(st), FAKE, -1, 150, ctypes.byref(flag), NULL) == ue.UE5M3_ESHAPE
+    assert lib.ue5m3_amax_sample(ctypes.byref(st), FAKE_MIS, 64, 150, ctypes.byref(flag), NULL) == ue.UE5M3_EALIGN
+    lib.ue5m3_amax_state_reset(ctypes.byref(st))
+    assert st.has_cache == 0
+    lib.ue5m3_amax_state_reset(None)

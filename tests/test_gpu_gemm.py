@@ -1,0 +1,194 @@
+"""GPU parity of the decoded-operand FP4 GEMM (fprop NT, dgrad NN, wgrad TN)
+against the oracle, through the C ABI.  The operands are quantized by the
+ORACLE and uploaded, so the GEMM is checked in isolation; the bar is the
+1e-3 max relative error plus the elementwise fp32 accumulation bound of
+tests/gpu_util.gemm_check."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_02846_amd as ue
+import synthetic
+from oracle import gemm as ogemm
+from oracle import quantize as oq
+from oracle import scaling as osc
+from tests.gpu_util import (f32_scalar_dev, gemm_check, host, oracle_cols, oracle_rows,
+                            ref_product, row_elem_index, say, to_dev, u8_to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def _linear(seed, T, K, N, dy_std=1e-3):
+    x = synthetic.activation(seed, T, K, 1e-2, 50.0)
+    w = synthetic.weight(seed, N, K)
+    dy = synthetic.gradient(seed, T, N, dy_std, 1.0)
+    return x, w, dy
+
+
+def _run_three(T, K, N, seed=0, out_dtype=torch.float32):
+    x, w, dy = _linear(seed, T, K, N)
+    gx, gw, gd = osc.amax(x), osc.amax(w), osc.amax(dy)
+    xr = oq.quantize_1d(x, 1, gx)
+    xc = oq.quantize_1d(x, 0, gx)
+    wq = oq.quantize_2d(w, gw)
+    dr = oq.quantize_1d(dy, 1, gd, "sr", 1, 1)
+    dc = oq.quantize_1d(dy, 0, gd, "sr", 1, 2)
+    X, Xc = oq.decoded_1d(xr[0], xr[1], 1), oq.decoded_1d(xc[0], xc[1], 0)
+    W = oq.decoded_2d(wq[0], wq[1])
+    dY, dYc = oq.decoded_1d(dr[0], dr[1], 1), oq.decoded_1d(dc[0], dc[1], 0)
+    D = lambda v: f32_scalar_dev(v)
+    out = {}
+    # fprop: Y = X W^T
+    al = ogemm.alpha(xr[2], wq[3])
+    c = ue.gemm("nt", T, N, K, u8_to_dev(xr[0]), u8_to_dev(xr[1]), D(xr[2]),
+                u8_to_dev(wq[0]), u8_to_dev(wq[1]), D(wq[3]), out_dtype=out_dtype)
+    out["fprop"] = (c, ogemm.fprop(X, W, al), ogemm.abs_product(X, W), al, K)
+    # dgrad: dX = dY W   (B operand = transposed weight payload, tile scales)
+    al = ogemm.alpha(dr[2], wq[3])
+    c = ue.gemm("nn", T, K, N, u8_to_dev(dr[0]), u8_to_dev(dr[1]), D(dr[2]),
+                u8_to_dev(wq[2]), u8_to_dev(wq[1]), D(wq[3]), out_dtype=out_dtype)
+    out["dgrad"] = (c, ogemm.dgrad(dY, W, al), ogemm.abs_product(dY, W.T), al, N)
+    # wgrad: dW = dY^T X  (both operands re-blocked along tokens)
+    al = ogemm.alpha(dc[2], xc[2])
+    c = ue.gemm("tn", N, K, T, u8_to_dev(dc[0]), u8_to_dev(dc[1]), D(dc[2]),
+                u8_to_dev(xc[0]), u8_to_dev(xc[1]), D(xc[2]), out_dtype=out_dtype)
+    out["wgrad"] = (c, ogemm.wgrad(dYc, Xc, al), ogemm.abs_product(dYc.T, Xc.T), al, T)
+    return out
+
+
+@pytest.mark.parametrize("T,K,N", [(16, 16, 16), (48, 80, 48), (64, 128, 64), (128, 256, 128),
+                                   (144, 208, 272), (256, 512, 384), (512, 1024, 256)])
+def test_three_products(T, K, N):
+    say("gemm three products", T, K, N)
+    for name, (c, ref, ap, al, kk) in _run_three(T, K, N).items():
+        gemm_check(host(c), ref, al, ap, kk, f"{name} {T}x{K}x{N}")
+
+
+def test_ragged_m_and_n():
+    """M not a multiple of the tile (fprop rows), N ragged for wgrad."""
+    say("gemm ragged")
+    for M, N, K in [(37, 48, 80), (130, 144, 48), (1, 16, 16), (200, 16, 1024)]:
+        a = synthetic.activation(3, M, K, 1e-2, 50.0)
+        w = synthetic.weight(3, N, K)
+        ar = oq.quantize_1d(a, 1, osc.amax(a))
+        wq = oq.quantize_2d(w, osc.amax(w))
+        A, W = oq.decoded_1d(ar[0], ar[1], 1), oq.decoded_2d(wq[0], wq[1])
+        al = ogemm.alpha(ar[2], wq[3])
+        c = ue.gemm("nt", M, N, K, u8_to_dev(ar[0]), u8_to_dev(ar[1]), f32_scalar_dev(ar[2]),
+                    u8_to_dev(wq[0]), u8_to_dev(wq[1]), f32_scalar_dev(wq[3]))
+        gemm_check(host(c), ogemm.fprop(A, W, al), al, ogemm.abs_product(A, W), K, f"nt {M}x{N}x{K}")
+    # TN with N not a multiple of 16 (row-scaled B)
+    T, Mo, No = 64, 40, 24
+    dy = synthetic.gradient(4, T, Mo, 1e-3, 1.0)
+    x = synthetic.activation(4, T, No, 1e-2, 50.0)
+    dc = oq.quantize_1d(dy, 0, osc.amax(dy), 448.0, "sr", 1, 2)
+    xc = oq.quantize_1d(x, 0, osc.amax(x))
+    dYc, Xc = oq.decoded_1d(dc[0], dc[1], 0), oq.decoded_1d(xc[0], xc[1], 0)
+    al = ogemm.alpha(dc[2], xc[2])
+    c = ue.gemm("tn", Mo, No, T, u8_to_dev(dc[0]), u8_to_dev(dc[1]), f32_scalar_dev(dc[2]),
+                u8_to_dev(xc[0]), u8_to_dev(xc[1]), f32_scalar_dev(xc[2]))
+    gemm_check(host(c), ogemm.wgrad(dYc, Xc, al), al, ogemm.abs_product(dYc.T, Xc.T), T, "tn ragged")
+
+
+def test_k_zero_writes_zeros():
+    say("gemm K=0")
+    c = torch.full((8, 16), 7.0, device="cuda")
+    one = f32_scalar_dev(1.0)
+    dummy = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    ue.gemm("nt", 8, 16, 0, dummy, dummy, one, dummy, dummy, one, out=c)
+    torch.cuda.synchronize()
+    assert (host(c) == 0).all()
+
+
+def test_bf16_output_within_one_ulp():
+    say("gemm bf16 output")
+    res32 = _run_three(128, 256, 128, seed=2)
+    res16 = _run_three(128, 256, 128, seed=2, out_dtype=torch.bfloat16)
+    for name in res32:
+        c16 = res16[name][0].float().cpu().numpy().astype(np.float64)
+        ref = res32[name][1]
+        ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
+        assert np.all(np.abs(c16 - ref) <= ulp * 1.01 + 1e-30), name
+
+
+def test_gemm_on_gpu_quantized_operands_matches():
+    """End to end on the GPU path: quantizers then GEMMs, compared with the
+    oracle's quantize-then-GEMM (quantizers are bit-exact, so the operands
+    are identical)."""
+    say("end-to-end linear step small")
+    T, K, N = 256, 384, 512
+    x, w, dy = _linear(9, T, K, N)
+    xd, wd, dyd = to_dev(x), to_dev(w), to_dev(dy)
+    sx, sw, sd = ue.AmaxState(1), ue.AmaxState(1), ue.AmaxState(1)
+    for st, t in [(sx, xd), (sw, wd), (sd, dyd)]:
+        ue.amax_sample(st, t, 0)
+    xr = ue.quantize_1d(xd, 1, sx.amax)
+    xc = ue.quantize_1d(xd, 0, sx.amax)
+    wq = ue.quantize_2d(wd, sw.amax)
+    dr = ue.quantize_1d(dyd, 1, sd.amax, 448.0, "sr", 1, 1)
+    dc = ue.quantize_1d(dyd, 0, sd.amax, 448.0, "sr", 1, 2)
+    y = ue.gemm("nt", T, N, K, xr[0], xr[1], xr[2], wq[0], wq[1], wq[3])
+    dx = ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], wq[2], wq[1], wq[3])
+    dw = ue.gemm("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xc[2])
+    ref = _run_three(T, K, N, seed=9)
+    for name, c in [("fprop", y), ("dgrad", dx), ("wgrad", dw)]:
+        _, r, ap, al, kk = ref[name]
+        gemm_check(host(c), r, al, ap, kk, name)
+
+
+def test_ffn_up_projection_sampled():
+    """The Nemotron-H-8B FFN up-projection step (T=8192, K=4096, N=21504):
+    full GPU path, outputs compared with the oracle on sampled rows and
+    columns of each product."""
+    T, K, N = 8192, 4096, 21504
+    say("ffn up-projection full size", T, K, N)
+    wl = synthetic.ffn_step(0, T, K, N)
+    x, w, dy = wl["x"], wl["w"], wl["dy"]
+    xd, wd, dyd = to_dev(x), to_dev(w), to_dev(dy)
+    sx, sw, sd = ue.AmaxState(50), ue.AmaxState(50), ue.AmaxState(50)
+    for st, t in [(sx, xd), (sw, wd), (sd, dyd)]:
+        assert ue.amax_sample(st, t, 0)
+    xr = ue.quantize_1d(xd, 1, sx.amax)
+    xc = ue.quantize_1d(xd, 0, sx.amax)
+    wq = ue.quantize_2d(wd, sw.amax)
+    dr = ue.quantize_1d(dyd, 1, sd.amax, 448.0, "sr", 1, 1)
+    dc = ue.quantize_1d(dyd, 0, sd.amax, 448.0, "sr", 1, 2)
+    y = ue.gemm("nt", T, N, K, xr[0], xr[1], xr[2], wq[0], wq[1], wq[3])
+    dx = ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], wq[2], wq[1], wq[3])
+    dw = ue.gemm("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xc[2])
+    torch.cuda.synchronize()
+    gx, gw, gd = osc.amax(x), osc.amax(w), osc.amax(dy)
+    assert np.float32(sx.amax.item()) == gx and np.float32(sw.amax.item()) == gw
+    assert np.float32(sd.amax.item()) == gd
+    rng = np.random.default_rng(1)
+    rows = np.sort(np.concatenate([[0, T - 1], rng.choice(T, 30, replace=False)]))
+    # fprop rows x sampled tile-rows of W
+    wt = np.sort(rng.choice(N // 16, 8, replace=False))
+    ncols = (wt[:, None] * 16 + np.arange(16)).ravel()
+    xo = oracle_rows(x, rows, gx, 448.0, "rn", 0, 0)
+    Xs = oq.decoded_1d(xo[0], xo[1], 1)
+    Ws = np.concatenate([oq.decoded_2d(*oq.quantize_2d(w[16 * t:16 * t + 16], gw)[:2]) for t in wt])
+    al = ogemm.alpha(xo[2], oq.quantize_2d(w[:16], gw)[3])
+    gemm_check(host(y)[rows][:, ncols], ogemm.fprop(Xs, Ws, al), al, ogemm.abs_product(Xs, Ws), K,
+               "fprop sampled")
+    # dgrad rows x sampled tile-columns of W (all of N)
+    kt = np.sort(rng.choice(K // 16, 3, replace=False))
+    kcols = (kt[:, None] * 16 + np.arange(16)).ravel()
+    dro = oracle_rows(dy, rows, gd, 448.0, "sr", 1, 1)
+    dYs = oq.decoded_1d(dro[0], dro[1], 1)
+    Wk = np.concatenate([oq.decoded_2d(*oq.quantize_2d(np.ascontiguousarray(w[:, 16 * t:16 * t + 16]), gw)[:2])
+                         for t in kt], axis=1)                        # [N, 48]
+    al = ogemm.alpha(dro[2], oq.quantize_2d(w[:16], gw)[3])
+    gemm_check(host(dx)[rows][:, kcols], ogemm.dgrad(dYs, Wk, al), al,
+               ogemm.abs_product(dYs, Wk.T), N, "dgrad sampled")
+    # wgrad sampled rows (dY columns) x sampled columns (X columns)
+    nsel = np.sort(rng.choice(N, 24, replace=False))
+    ksel = np.sort(rng.choice(K, 24, replace=False))
+    dco = oracle_cols(dy, nsel, gd, 448.0, "sr", 1, 2)
+    xco = oracle_cols(x, ksel, gx, 448.0, "rn", 0, 0)
+    dYc = oq.decoded_1d(dco[0], dco[1], 0)                            # [T, 24]
+    Xc = oq.decoded_1d(xco[0], xco[1], 0)                             # [T, 24]
+    al = ogemm.alpha(dco[2], xco[2])
+    gemm_check(host(dw)[nsel][:, ksel], ogemm.wgrad(dYc, Xc, al), al,
+               ogemm.abs_product(dYc.T, Xc.T), T, "wgrad sampled")

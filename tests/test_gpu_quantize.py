@@ -1,0 +1,213 @@
+"""GPU parity of the amax and quantizer kernels against the oracle, through
+the C ABI.  Payload nibbles, scale bytes and the decode multiplier must be
+bit-exact, for RN and for SR with the same Philox counters."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_02846_amd as ue
+import synthetic
+from oracle import quantize as oq
+from oracle import scaling as osc
+from tests.gpu_util import (f32_scalar_dev, host, oracle_cols, oracle_rows, say, set_amax,
+                            to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_amax(xd, period=1):
+    st = ue.AmaxState(period=period)
+    assert ue.amax_sample(st, xd, 0)
+    torch.cuda.synchronize()
+    return st, np.float32(st.amax.item())
+
+
+# ---------------------------------------------------------------- amax ----
+@pytest.mark.parametrize("shape", [(1, 1), (3, 5), (7, 9), (256, 512), (1000, 1000), (8192, 4096)])
+def test_amax_matches_oracle(shape):
+    say("amax", shape)
+    bits = synthetic.activation(11, *shape, 1e-3, 100.0)
+    _, g = _gpu_amax(to_dev(bits))
+    assert g == osc.amax(bits)
+
+
+def test_amax_empty_and_negative_max():
+    say("amax empty / negative")
+    st = ue.AmaxState(period=1)
+    st.amax.fill_(5.0)
+    assert ue.amax_sample(st, torch.empty(0, dtype=torch.bfloat16, device="cuda"), 0)
+    torch.cuda.synchronize()
+    assert st.amax.item() == 0.0
+    x = synthetic.f32_to_bf16_bits(np.array([[0.5, -9.5, 3.0, -0.0]], np.float32))
+    _, g = _gpu_amax(to_dev(x))
+    assert g == 9.5
+
+
+def test_sample_and_hold_trace_on_gpu():
+    """120 steps, D = 50: refreshes at 0, 50, 100 and the held amax is the one
+    sampled at the last refresh (eq:delayed-amax)."""
+    say("sample-and-hold trace")
+    st = ue.AmaxState(period=50)
+    ost = osc.AmaxState(period=50)
+    refreshed = []
+    for t in range(120):
+        bits = synthetic.f32_to_bf16_bits(np.full((4, 16), float(t % 7 + 1), np.float32)
+                                          * np.float32(1 + t))
+        r = ue.amax_sample(st, to_dev(bits), t)
+        g_o, r_o = ost.observe(bits, t)
+        assert r == r_o
+        if r:
+            refreshed.append(t)
+        torch.cuda.synchronize()
+        assert np.float32(st.amax.item()) == g_o
+    assert refreshed == [0, 50, 100]
+    st.reset()
+    assert ue.amax_sample(st, to_dev(bits), 120)
+
+
+# ------------------------------------------------------------ 1D rows ----
+ROW_CASES = [(1, 16), (3, 32), (37, 48), (64, 512), (100, 1040), (256, 512)]
+
+
+@pytest.mark.parametrize("mode", ["rn", "sr"])
+@pytest.mark.parametrize("shape", ROW_CASES)
+@pytest.mark.parametrize("target", [448.0, 2048.0])
+def test_quantize_rows(shape, mode, target):
+    say("rows", shape, mode, target)
+    bits = synthetic.gradient(5, *shape, 1e-4, 2.0) if mode == "sr" else \
+        synthetic.activation(5, *shape, 0.01, 50.0)
+    xd = to_dev(bits)
+    st, g = _gpu_amax(xd)
+    assert g == osc.amax(bits)
+    p, s, d = ue.quantize_1d(xd, 1, st.amax, target, mode, seed=1, tensor_id=7)
+    po, so, do = oq.quantize_1d(bits, 1, g, target, mode, 1, 7)
+    assert np.array_equal(host(s), so)
+    assert np.array_equal(host(p), po)
+    assert np.float32(d.item()) == do
+
+
+# ---------------------------------------------------------- 1D columns ----
+COL_CASES = [(16, 2), (16, 4), (48, 38), (64, 100), (256, 512), (512, 300), (80, 1030)]
+
+
+@pytest.mark.parametrize("mode", ["rn", "sr"])
+@pytest.mark.parametrize("shape", COL_CASES)
+def test_quantize_cols(shape, mode):
+    say("cols", shape, mode)
+    bits = synthetic.gradient(6, *shape, 1e-4, 2.0) if mode == "sr" else \
+        synthetic.activation(6, *shape, 0.01, 50.0)
+    xd = to_dev(bits)
+    st, g = _gpu_amax(xd)
+    p, s, d = ue.quantize_1d(xd, 0, st.amax, 448.0, mode, seed=3, tensor_id=2)
+    po, so, do = oq.quantize_1d(bits, 0, g, 448.0, mode, 3, 2)
+    assert np.array_equal(host(s), so)
+    assert np.array_equal(host(p), po)
+    assert np.float32(d.item()) == do
+
+
+# ------------------------------------------------------------ 2D tiles ----
+TILE_CASES = [(16, 16), (48, 80), (256, 512), (512, 1024), (208, 4096)]
+
+
+@pytest.mark.parametrize("mode", ["rn", "sr"])
+@pytest.mark.parametrize("shape", TILE_CASES)
+def test_quantize_tiles(shape, mode):
+    say("tiles", shape, mode)
+    bits = synthetic.weight(7, *shape)
+    xd = to_dev(bits)
+    st, g = _gpu_amax(xd)
+    p, s, pt, d = ue.quantize_2d(xd, st.amax, 448.0, mode, seed=5, tensor_id=4)
+    po, so, pto, do = oq.quantize_2d(bits, g, 448.0, mode, 5, 4)
+    assert np.array_equal(host(s), so)
+    assert np.array_equal(host(p), po)
+    assert np.array_equal(host(pt), pto)
+    assert np.float32(d.item()) == do
+    # without the transposed copy
+    p2, s2, pt2, _ = ue.quantize_2d(xd, st.amax, 448.0, mode, seed=5, tensor_id=4, transposed=False)
+    assert pt2 is None and np.array_equal(host(p2), po)
+
+
+# ---------------------------------------------------- degenerate cases ----
+def test_held_reference_saturation_and_underflow():
+    """A stale held amax far below / above the tensor maximum drives blocks
+    into UE5M3 saturation (Prop. 1) and into the zero-scale rule."""
+    say("held reference regimes")
+    bits = synthetic.activation(8, 64, 256, 0.01, 50.0)
+    xd = to_dev(bits)
+    amax = torch.zeros(1, dtype=torch.float32, device="cuda")
+    for g in [1e-3, 0.05, 1.0, 1e4, 1e9, 0.0, 2.0 ** -100]:
+        set_amax(amax, g)
+        for axis in [0, 1]:
+            for mode in ["rn", "sr"]:
+                p, s, d = ue.quantize_1d(xd, axis, amax, 448.0, mode, seed=9, tensor_id=1)
+                po, so, do = oq.quantize_1d(bits, axis, np.float32(g), 448.0, mode, 9, 1)
+                assert np.array_equal(host(s), so), (g, axis, mode)
+                assert np.array_equal(host(p), po), (g, axis, mode)
+                assert np.float32(d.item()) == do
+        sc = host(s)
+        if g == 1e-3:
+            assert (sc == 0xF7).any()
+        if g == 1e9:
+            assert (sc == 0x78).any()
+
+
+def test_all_zero_and_special_values():
+    say("zeros / signed zeros / worked blocks")
+    z = np.zeros((32, 64), np.uint16)
+    z[1, ::2] = 0x8000                                    # -0
+    xd = to_dev(z)
+    st, g = _gpu_amax(xd)
+    assert g == 0.0
+    p, s, d = ue.quantize_1d(xd, 1, st.amax, 448.0, "rn")
+    po, so, do = oq.quantize_1d(z, 1, g, 448.0, "rn")
+    assert np.array_equal(host(p), po) and np.array_equal(host(s), so)
+    assert (so == 0x78).all()
+
+
+def test_run_twice_bit_identical():
+    say("determinism")
+    bits = synthetic.gradient(12, 512, 1024, 1e-4, 2.0)
+    xd = to_dev(bits)
+    st, _ = _gpu_amax(xd)
+    a = ue.quantize_1d(xd, 1, st.amax, 448.0, "sr", seed=77, tensor_id=1)
+    b = ue.quantize_1d(xd, 1, st.amax, 448.0, "sr", seed=77, tensor_id=1)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+# ------------------------------------------------ full-size workloads ----
+def test_quantizer_bandwidth_workload_sampled():
+    """8192 x 4096 activation (RN rows), gradient (SR rows, seed 1) and
+    4096 x 4096 weight (2D): GPU outputs vs oracle on sampled rows/tiles."""
+    say("quantizer workload 8192x4096")
+    wl = synthetic.quantizer_bandwidth(0)
+    rng = np.random.default_rng(0)
+    for name, mode, seed, tid in [("x", "rn", 0, 0), ("dy", "sr", 1, 0)]:
+        bits = wl[name]
+        xd = to_dev(bits)
+        st, g = _gpu_amax(xd)
+        assert g == osc.amax(bits)
+        p, s, _ = ue.quantize_1d(xd, 1, st.amax, 448.0, mode, seed, tid)
+        rows = np.concatenate([[0, bits.shape[0] - 1], rng.choice(bits.shape[0], 254, replace=False)])
+        po, so, _ = oracle_rows(bits, rows, g, 448.0, mode, seed, tid)
+        assert np.array_equal(host(p)[rows], po), name
+        assert np.array_equal(host(s)[rows], so), name
+        # the column (transposed) quantizer on sampled columns
+        pc, scc, _ = ue.quantize_1d(xd, 0, st.amax, 448.0, mode, seed, tid)
+        cols = np.concatenate([[0, bits.shape[1] - 1], rng.choice(bits.shape[1], 62, replace=False)])
+        pco, sco, _ = oracle_cols(bits, cols, g, 448.0, mode, seed, tid)
+        assert np.array_equal(host(pc)[cols], pco), name
+        assert np.array_equal(host(scc)[cols], sco), name
+    wb = wl["w"]
+    wd = to_dev(wb)
+    st, g = _gpu_amax(wd)
+    p, s, pt, _ = ue.quantize_2d(wd, st.amax, 448.0, "rn")
+    tr = rng.choice(wb.shape[0] // 16, 16, replace=False)
+    for t in tr:
+        po, so, _, _ = oq.quantize_2d(wb[16 * t:16 * t + 16], g, 448.0, "rn")
+        assert np.array_equal(host(p)[16 * t:16 * t + 16], po)
+        assert np.array_equal(host(s)[t], so[0])
+    tc = rng.choice(wb.shape[1] // 16, 4, replace=False)
+    for t in tc:
+        _, _, pto, _ = oq.quantize_2d(np.ascontiguousarray(wb[:, 16 * t:16 * t + 16]), g, 448.0, "rn")
+        assert np.array_equal(host(pt)[16 * t:16 * t + 16], pto)

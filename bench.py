@@ -70,8 +70,8 @@ def cpu_baseline(wl, T, K, N, target_s=12.0):
     xr = oq.quantize_1d(xs, 1, gx)
     xc = oq.quantize_1d(xs, 0, gx)
     wq = oq.quantize_2d(ws, gw)
-    dr = oq.quantize_1d(ds, 1, gd, "sr", 1, 1)
-    dc = oq.quantize_1d(ds, 0, gd, "sr", 1, 2)
+    dr = oq.quantize_1d(ds, 1, gd, 448.0, "sr", 1, 1)
+    dc = oq.quantize_1d(ds, 0, gd, 448.0, "sr", 1, 2)
     t_quant = (time.perf_counter() - t0)
     quant_scale = (T * K + T * K + N * K + T * N + T * N) / (
         xs.size + xs.size + ws.size + ds.size + ds.size)

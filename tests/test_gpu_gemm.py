@@ -32,8 +32,8 @@ def _run_three(T, K, N, seed=0, out_dtype=torch.float32):
     xr = oq.quantize_1d(x, 1, gx)
     xc = oq.quantize_1d(x, 0, gx)
     wq = oq.quantize_2d(w, gw)
-    dr = oq.quantize_1d(dy, 1, gd, "sr", 1, 1)
-    dc = oq.quantize_1d(dy, 0, gd, "sr", 1, 2)
+    dr = oq.quantize_1d(dy, 1, gd, 448.0, "sr", 1, 1)
+    dc = oq.quantize_1d(dy, 0, gd, 448.0, "sr", 1, 2)
     X, Xc = oq.decoded_1d(xr[0], xr[1], 1), oq.decoded_1d(xc[0], xc[1], 0)
     W = oq.decoded_2d(wq[0], wq[1])
     dY, dYc = oq.decoded_1d(dr[0], dr[1], 1), oq.decoded_1d(dc[0], dc[1], 0)

@@ -42,6 +42,12 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "gemm_traffic.json"),
                    help="HBM traffic per launch measured with rocprofv3 counters (JSON)")
+    p.add_argument("--kernel", default=None,
+                   help="profiling aid: after setup run only this step kernel (e.g. gemm_fprop) "
+                        "--steps times and exit without a JSON line")
+    p.add_argument("--copy-ref", type=int, default=0, metavar="BYTES",
+                   help="profiling aid: time a plain device copy of BYTES bytes (the reference "
+                        "that scales the HBM byte counters) and exit")
     return p.parse_args()
 
 
@@ -116,6 +122,14 @@ def main():
 
     T, K, N = args.tokens, args.k, args.n
     dev = torch.device("cuda:0")
+    if args.copy_ref:
+        src = torch.empty(args.copy_ref // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"copied {args.copy_ref} bytes 5 times", flush=True)
+        return
     wl = synthetic.ffn_step(0, T, K, N)
 
     def up(bits):
@@ -169,6 +183,24 @@ def main():
     for t in range(args.warmup):
         step(t)
     torch.cuda.synchronize()
+    if args.kernel is not None:
+        single = {
+            "quant_x_rows": lambda: ue.quantize_1d(x, 1, sx.amax, 448.0, "rn", 0, 0, *bufs["xr"]),
+            "quant_x_cols": lambda: ue.quantize_1d(x, 0, sx.amax, 448.0, "rn", 0, 0, *bufs["xc"]),
+            "quant_w_tiles": lambda: ue.quantize_2d(w, sw.amax, 448.0, "rn", 0, 0, True, *bufs["w"]),
+            "quant_dy_rows": lambda: ue.quantize_1d(dy, 1, sd.amax, 448.0, "sr", 7, 1, *bufs["dr"]),
+            "quant_dy_cols": lambda: ue.quantize_1d(dy, 0, sd.amax, 448.0, "sr", 7, 2, *bufs["dc"]),
+            "gemm_fprop": lambda: ue.gemm("nt", T, N, K, *bufs["xr"], bufs["w"][0], bufs["w"][1],
+                                          bufs["w"][3], out=y),
+            "gemm_dgrad": lambda: ue.gemm("nn", T, K, N, *bufs["dr"], bufs["w"][2], bufs["w"][1],
+                                          bufs["w"][3], out=dx),
+            "gemm_wgrad": lambda: ue.gemm("tn", N, K, T, *bufs["dc"], *bufs["xc"], out=dw),
+        }[args.kernel]
+        for _ in range(args.steps):
+            single()
+        torch.cuda.synchronize()
+        print(f"ran {args.kernel} {args.steps} times", flush=True)
+        return
     # --- timed region: exactly `steps` steps ---------------------------------
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()

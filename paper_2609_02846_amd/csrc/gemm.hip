@@ -1,9 +1,11 @@
 // Decoded-operand FP4 GEMM (paper Sec. 5.1, the three products of Sec. 4.3):
 //     C[m, n] = alpha * sum_k A_hat[m, k] * B_hat[n, k],  alpha = dec_a * dec_b
 // with A_hat, B_hat = E2M1 value * UE5M3 block scale.  Each decoded value has
-// at most 2 x 4 significant bits and lies in [2^-18, 368640], so it is exact in
-// bf16; bf16 x bf16 products are exact in fp32 and only the fp32 accumulation
-// of the matrix cores rounds.  alpha is applied once in the epilogue (Sec. 5.2).
+// at most 2 x 4 significant bits, its least significant bit is at least 2^-18
+// and its magnitude at most 368640, so A_hat * 2^-3 is exact in fp16 (largest
+// 46080, smallest step 2^-21 >= 2^-24).  The matrix cores multiply the exact
+// fp16 operands exactly into fp32 and only the fp32 accumulation rounds;
+// alpha * 2^6 is applied once in the epilogue (Sec. 5.2).
 //
 // Operands arrive contraction-contiguous (two nibbles per byte along k) with
 // one scale byte per 16 k-elements; the B scale layout depends on the product:
@@ -12,29 +14,30 @@
 //
 // Kernel structure (gfx950, one 256-thread workgroup per CU):
 //  * 256 x 256 output tile, four waves in a 2 x 2 grid, 128 x 128 per wave
-//    (16 v_mfma_f32_32x32x16_bf16 accumulators = 256 AccVGPRs; on gfx950 the
+//    (16 v_mfma_f32_32x32x16_f16 accumulators = 256 AccVGPRs; on gfx950 the
 //    32x32 shape sustains the matrix-core peak with in-place accumulators);
 //  * K advances in slices of 64.  Each thread owns one row of the A tile and
 //    one row of the B tile: it loads the packed FP4 bytes and scale codes of
 //    the next slice into registers while the matrix cores work on the current
 //    one, decodes them to bf16 and stores them into the other half of a
 //    double-buffered LDS stage (every element is decoded once per workgroup);
-//  * decoding is a byte-permute table lookup: per UE5M3 code an LDS table
-//    holds the low and high bytes of bf16(q * s) for the 8 E2M1 magnitudes
-//    q, so 8 nibbles become 8 bf16 with 4 table permutes, 4 interleaving
-//    permutes and 3 sign operations; within each group of 8 k-elements the
-//    bf16 are stored in the order 0,2,4,6,1,3,5,7 for both operands, which
-//    leaves every dot product unchanged;
+//  * decoding writes each UE5M3 scale s as mu * 2^E (mu = 1 + m/8 in
+//    [1, 2), or 0 for code 0).  The gfx950 FP4 -> FP16 conversion applies a
+//    power-of-two scale exactly (it uses only the exponent of its scale
+//    operand), giving fp16(q * 2^(E-3)); one packed fp16 multiply by mu then
+//    yields fp16(q * s * 2^-3) exactly.  8 nibbles cost 4 conversions and 4
+//    packed multiplies; a 2 KB LDS table maps a code to (2^(E-3), mu, mu);
 //  * workgroups are remapped so that each XCD runs a contiguous range of
-//    tiles, ordered down tile columns so that concurrently running
-//    workgroups share the B tile in that XCD's L2.
+//    tiles, walked in groups of 4 tile rows so that concurrently running
+//    workgroups share A and B slices in that XCD's L2.
 #include "codec.hpp"
 #include "launch.hpp"
 
 namespace ue5m3 {
 namespace {
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
+typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 
@@ -42,32 +45,46 @@ constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int kGemmThreads = 256;
 constexpr int LDSK = BK + 8;                         // padded LDS row, bf16 elements
 constexpr int kStageElems = (BM + BN) * LDSK;        // bf16 elements per stage
-constexpr int kLutBytes = 256 * 16;
+constexpr int kLutBytes = 256 * 8;
 constexpr int kSmemBytes = 2 * kStageElems * 2 + kLutBytes;
 constexpr int kXcds = 8;
+constexpr int kGroupM = 4;
 
-// bf16 bits of the E2M1 magnitude code c (0..7) times the UE5M3 scale s:
-// exact, the product has at most 8 significant bits.
-__device__ __forceinline__ uint32_t scaled_bf16(int c, float s) {
-    const float mag[8] = {0.0f, 0.5f, 1.0f, 1.5f, 2.0f, 3.0f, 4.0f, 6.0f};
-    return __float_as_uint(mag[c] * s) >> 16;
+// Decode-table entry of UE5M3 code c: (bits of 2^(E-3), fp16 pair (mu, mu))
+// with s = mu * 2^E, mu in [1, 2) a multiple of 1/8 (mu = 0 for code 0).
+__device__ __forceinline__ uint2 lut_entry(uint32_t c) {
+    const uint32_t e = c >> 3, m = c & 7u;
+    int E;
+    uint32_t mu8;                                  // mu * 8, in 8..15
+    if (e == 0) {                                  // subnormal: m * 2^-17
+        if (m == 0) return make_uint2(0x3F800000u, 0u);
+        const int lz = __builtin_clz(m) - 28;      // shift of m to 4..7 (bit 2 set)
+        mu8 = (m << lz) * 2u;                      // normalised to 8..15
+        E = -17 + 2 - lz;
+    } else {
+        mu8 = 8u + m;
+        E = (int)e - 15;
+    }
+    const _Float16 mu = (_Float16)((float)mu8 * 0.125f);   // exact
+    uint16_t mb;
+    __builtin_memcpy(&mb, &mu, 2);
+    const uint32_t pow_bits = (uint32_t)(E - 3 + 127) << 23;
+    return make_uint2(pow_bits, (uint32_t)mb * 0x00010001u);
 }
 
-// Decode 8 packed nibbles x with the table entry (lo0, lo1, hi0, hi1) into
-// 4 bf16x2 words holding elements (0,2), (4,6), (1,3), (5,7).
-__device__ __forceinline__ void decode8(uint32_t x, const uint4& t, uint32_t* out) {
-    const uint32_t e = x & 0x07070707u;                      // magnitudes 0,2,4,6
-    const uint32_t o = (x >> 4) & 0x07070707u;               // magnitudes 1,3,5,7
-    uint32_t he = __builtin_amdgcn_perm(t.w, t.z, e);
-    const uint32_t le = __builtin_amdgcn_perm(t.y, t.x, e);
-    uint32_t ho = __builtin_amdgcn_perm(t.w, t.z, o);
-    const uint32_t lo = __builtin_amdgcn_perm(t.y, t.x, o);
-    he |= (x << 4) & 0x80808080u;                            // sign bits of 0,2,4,6
-    ho |= x & 0x80808080u;                                   // sign bits of 1,3,5,7
-    out[0] = __builtin_amdgcn_perm(he, le, 0x05010400u);
-    out[1] = __builtin_amdgcn_perm(he, le, 0x07030602u);
-    out[2] = __builtin_amdgcn_perm(ho, lo, 0x05010400u);
-    out[3] = __builtin_amdgcn_perm(ho, lo, 0x07030602u);
+// Decode 8 packed nibbles x (element e in bits 4e..4e+3) into 4 fp16 pairs
+// (elements (0,1), (2,3), (4,5), (6,7)) of value q * s * 2^-3.
+__device__ __forceinline__ void decode8(uint32_t x, const uint2& t, uint32_t* out) {
+    const float p2 = __uint_as_float(t.x);
+    const f16x2_t mu = __builtin_bit_cast(f16x2_t, t.y);
+    const f16x2_t v0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(x, p2, 0) * mu;
+    const f16x2_t v1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(x, p2, 1) * mu;
+    const f16x2_t v2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(x, p2, 2) * mu;
+    const f16x2_t v3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(x, p2, 3) * mu;
+    out[0] = __builtin_bit_cast(uint32_t, v0);
+    out[1] = __builtin_bit_cast(uint32_t, v1);
+    out[2] = __builtin_bit_cast(uint32_t, v2);
+    out[3] = __builtin_bit_cast(uint32_t, v3);
 }
 
 // One thread's share of a K-slice: one row of 64 k-elements (4 blocks).
@@ -126,11 +143,11 @@ __device__ __forceinline__ void load_slice(RowSlice& r, const RowSrc& src, int64
 // (one aligned word load); otherwise code[j] holds block j's code.
 template <bool FULLK, bool PACKED>
 __device__ __forceinline__ void store_block(const RowSlice& r, int j, bool v,
-                                            const uint4* __restrict__ lut,
+                                            const uint2* __restrict__ lut,
                                             uint16_t* __restrict__ dst) {
     if (FULLK) v = true;
     const uint32_t code = PACKED ? (r.code[0] >> (8 * j)) & 0xFFu : r.code[j] & 0xFFu;
-    const uint4 t = lut[v ? code : 0u];
+    const uint2 t = lut[v ? code : 0u];
     uint32_t o[8];
     decode8(v ? r.w[2 * j] : 0u, t, o);
     decode8(v ? r.w[2 * j + 1] : 0u, t, o + 4);
@@ -140,77 +157,41 @@ __device__ __forceinline__ void store_block(const RowSlice& r, int j, bool v,
 }
 
 struct Frags {
-    bf16x8_t a[4], b[4];
+    f16x8_t a[4], b[4];
 };
 
-// Fragments of k-step kk (16 k-elements) for v_mfma_f32_32x32x16_bf16:
+// Fragments of k-step kk (16 k-elements) for v_mfma_f32_32x32x16_f16:
 // lane l holds A[row l%32][8 k] and B[8 k][col l%32]; the k half is l/32 for
 // both operands.
-__device__ __forceinline__ void load_frags(Frags& f, const uint16_t* __restrict__ la,
-                                           const uint16_t* __restrict__ lb, int kk) {
+__device__ __forceinline__ void load_frags(Frags& f, const uint16_t* __restrict__ stage, int wm,
+                                           int wn, int lane, int kk) {
+    const uint16_t* la = stage + (wm * 128 + (lane & 31)) * LDSK + (lane >> 5) * 8 + kk * 16;
+    const uint16_t* lb = stage + (BM + wn * 128 + (lane & 31)) * LDSK + (lane >> 5) * 8 + kk * 16;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const uint4 v = *reinterpret_cast<const uint4*>(la + i * 32 * LDSK + kk * 16);
-        f.a[i] = __builtin_bit_cast(bf16x8_t, u32x4_t{v.x, v.y, v.z, v.w});
+        const uint4 v = *reinterpret_cast<const uint4*>(la + i * 32 * LDSK);
+        f.a[i] = __builtin_bit_cast(f16x8_t, u32x4_t{v.x, v.y, v.z, v.w});
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-        const uint4 v = *reinterpret_cast<const uint4*>(lb + j * 32 * LDSK + kk * 16);
-        f.b[j] = __builtin_bit_cast(bf16x8_t, u32x4_t{v.x, v.y, v.z, v.w});
+        const uint4 v = *reinterpret_cast<const uint4*>(lb + j * 32 * LDSK);
+        f.b[j] = __builtin_bit_cast(f16x8_t, u32x4_t{v.x, v.y, v.z, v.w});
     }
 }
 
-// 16 MFMAs of one k-step; with DEC, four decode blocks of the next slice
-// (blocks C0 .. C0+3 of the A row for C0 = 0, of the B row for C0 = 4) sit
-// between them, one per 4 MFMAs.
-template <bool FULLK, bool BPACKED, bool DEC, int C0>
+// The 16 MFMAs of one k-step; with DEC, the four decode blocks of one operand
+// row of the next slice (r -> dst) sit between them, one per 4 MFMAs.
+template <bool FULLK, bool PACKED, bool DEC>
 __device__ __forceinline__ void kstep(f32x16_t (&acc)[4][4], const Frags& f, int nvalid,
-                                      const RowSlice& ra, const RowSlice& rb,
-                                      const uint4* __restrict__ lut, uint16_t* __restrict__ nxt,
-                                      int tid) {
+                                      const RowSlice& r, const uint2* __restrict__ lut,
+                                      uint16_t* __restrict__ dst) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
-        if (DEC) {
-            if (C0 == 0) store_block<FULLK, FULLK>(ra, i, i < nvalid, lut, nxt + tid * LDSK);
-            else store_block<FULLK, FULLK && BPACKED>(rb, i, i < nvalid, lut, nxt + (BM + tid) * LDSK);
-        }
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+        if (DEC) store_block<FULLK, PACKED>(r, i, i < nvalid, lut, dst);
     }
-}
-
-// One K-slice (64 k) of matrix-core work on LDS stage `cur`.  The first two
-// k-steps carry the decode of the next slice (registers ra, rb -> stage
-// `nxt`); then the loads of the slice after it are issued into the freed
-// registers, so that they have the last two k-steps, the barrier and the
-// first k-step of the next slice to arrive.  Fragments are double-buffered
-// across k-steps; the scheduling barriers keep the compiler from hoisting all
-// LDS reads of the slice.
-template <bool FULLK, int BMODE>
-__device__ __forceinline__ void mfma_slice(f32x16_t (&acc)[4][4], const uint16_t* __restrict__ cur,
-                                           int wm, int wn, int lane, int nvalid, RowSlice& ra,
-                                           RowSlice& rb, const RowSrc& sa, const RowSrc& sb,
-                                           int64_t kb_next, int64_t kbt,
-                                           const uint4* __restrict__ lut, uint16_t* __restrict__ nxt,
-                                           int tid) {
-    constexpr bool kBContig = BMODE != (int)BScale::TileT;
-    const uint16_t* la = cur + (wm * 128 + (lane & 31)) * LDSK + (lane >> 5) * 8;
-    const uint16_t* lb = cur + (BM + wn * 128 + (lane & 31)) * LDSK + (lane >> 5) * 8;
-    Frags f0, f1;
-    load_frags(f0, la, lb, 0);
-    load_frags(f1, la, lb, 1);
-    kstep<FULLK, kBContig, true, 0>(acc, f0, nvalid, ra, rb, lut, nxt, tid);
-    __builtin_amdgcn_sched_barrier(0);
-    load_frags(f0, la, lb, 2);
-    kstep<FULLK, kBContig, true, 4>(acc, f1, nvalid, ra, rb, lut, nxt, tid);
-    __builtin_amdgcn_sched_barrier(0);
-    load_slice<FULLK, true>(ra, sa, kb_next, kbt);
-    load_slice<FULLK, kBContig>(rb, sb, kb_next, kbt);
-    load_frags(f1, la, lb, 3);
-    kstep<FULLK, kBContig, false, 0>(acc, f0, nvalid, ra, rb, lut, nxt, tid);
-    __builtin_amdgcn_sched_barrier(0);
-    kstep<FULLK, kBContig, false, 0>(acc, f1, nvalid, ra, rb, lut, nxt, tid);
 }
 
 template <int BMODE, bool OUT_BF16, bool FULLK>
@@ -221,34 +202,31 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_kernel(
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     uint16_t* stage0 = reinterpret_cast<uint16_t*>(smem);
     uint16_t* stage1 = stage0 + kStageElems;
-    uint4* lut = reinterpret_cast<uint4*>(smem + 2 * kStageElems * 2);
+    uint2* lut = reinterpret_cast<uint2*>(smem + 2 * kStageElems * 2);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    // ---- tile index: contiguous range per XCD, column-major inside ---------
+    // ---- tile index ------------------------------------------------------------
+    // Workgroups are dispatched round-robin over the XCDs; remap so that each
+    // XCD owns a contiguous range of tile ids, then walk tile ids in groups of
+    // kGroupM tile rows (column-major inside a group) so that the ~32
+    // workgroups resident on one XCD cover a kGroupM x 8 block of tiles and
+    // share their A and B slices in that XCD's L2.
     const int ntiles = tiles_m * tiles_n;
     int t = blockIdx.x;
     if (ntiles % kXcds == 0) t = (t % kXcds) * (ntiles / kXcds) + t / kXcds;
-    const int64_t m0 = (int64_t)(t % tiles_m) * BM;
-    const int64_t n0 = (int64_t)(t / tiles_m) * BN;
+    const int group_tiles = kGroupM * tiles_n;
+    const int g = t / group_tiles;
+    const int first_m = g * kGroupM;
+    const int gm = min(tiles_m - first_m, kGroupM);
+    const int rr = t - g * group_tiles;
+    const int64_t m0 = (int64_t)(first_m + rr % gm) * BM;
+    const int64_t n0 = (int64_t)(rr / gm) * BN;
 
-    // ---- decode table: code -> lo/hi bytes of bf16(q * s) for q = 0..7 ------
-    {
-        const float s = tid < 0xF8 ? ue5m3_decode((uint32_t)tid) : 0.0f;
-        uint32_t lo0 = 0, lo1 = 0, hi0 = 0, hi1 = 0;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const uint32_t b0 = scaled_bf16(c, s), b1 = scaled_bf16(c + 4, s);
-            lo0 |= (b0 & 0xFFu) << (8 * c);
-            hi0 |= (b0 >> 8) << (8 * c);
-            lo1 |= (b1 & 0xFFu) << (8 * c);
-            hi1 |= (b1 >> 8) << (8 * c);
-        }
-        lut[tid] = make_uint4(lo0, lo1, hi0, hi1);
-    }
+    lut[tid] = lut_entry((uint32_t)tid);          // 256 codes, one per thread
 
     const int64_t kbt = K / 16;
     const int64_t nk = (K + BK - 1) / BK;
@@ -269,6 +247,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_kernel(
         sb.sc_stride = N >> 4;
     }
     constexpr bool kBContig = BMODE != (int)BScale::TileT;
+    constexpr bool kAPacked = FULLK;
+    constexpr bool kBPacked = FULLK && kBContig;
     auto nvalid = [&](int64_t s) -> int { return (int)min((int64_t)4, kbt - s * 4); };
 
     f32x16_t acc[4][4];
@@ -280,9 +260,19 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_kernel(
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     if (nk > 0) {
-        // Slice s is decoded into LDS stage s & 1 during the matrix-core work
-        // of slice s - 1; its packed bytes are loaded into (ra, rb) midway
-        // through slice s - 2.
+        // Pipeline, per slice s (64 k): stage s & 1 holds slice s decoded;
+        // registers (ra, rb) hold the packed bytes of slice s + 1; f0 holds
+        // the k-step-0 fragments of slice s.
+        //   k-step 0: 16 MFMAs + decode A row of slice s+1 -> other stage
+        //   k-step 1: 16 MFMAs + decode B row of slice s+1
+        //   issue the global loads of slice s+2 into (ra, rb)
+        //   k-step 2: 16 MFMAs
+        //   barrier (slice s+1 complete in LDS, stage s no longer read)
+        //   load k-step-0 fragments of slice s+1, overlapped by
+        //   k-step 3: 16 MFMAs
+        // Past the end the last slice is re-loaded and re-decoded into the
+        // stage nobody reads, which keeps the loop free of branches.
+        const int64_t last = (nk - 1) * 4;
         RowSlice ra, rb;
         load_slice<FULLK, true>(ra, sa, 0, kbt);
         load_slice<FULLK, kBContig>(rb, sb, 0, kbt);
@@ -290,28 +280,40 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_kernel(
         const int nv0 = nvalid(0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            store_block<FULLK, FULLK>(ra, j, j < nv0, lut, stage0 + tid * LDSK);
-            store_block<FULLK, FULLK && kBContig>(rb, j, j < nv0, lut, stage0 + (BM + tid) * LDSK);
+            store_block<FULLK, kAPacked>(ra, j, j < nv0, lut, stage0 + tid * LDSK);
+            store_block<FULLK, kBPacked>(rb, j, j < nv0, lut, stage0 + (BM + tid) * LDSK);
         }
-        const int64_t last = (nk - 1) * 4;
         load_slice<FULLK, true>(ra, sa, min((int64_t)4, last), kbt);
         load_slice<FULLK, kBContig>(rb, sb, min((int64_t)4, last), kbt);
         __syncthreads();
-        // Past the end the last slice is re-loaded and re-decoded into the
-        // stage nobody reads, which keeps the loop free of branches.
+        Frags f0, f1;
+        load_frags(f0, stage0, wm, wn, lane, 0);
         for (int64_t ks = 0; ks < nk; ++ks) {
             const uint16_t* cur = (ks & 1) ? stage1 : stage0;
             uint16_t* nxt = (ks & 1) ? stage0 : stage1;
-            mfma_slice<FULLK, BMODE>(acc, cur, wm, wn, lane, nvalid(ks + 1), ra, rb, sa, sb,
-                                     min((ks + 2) * 4, last), kbt, lut, nxt, tid);
+            const int nv = nvalid(ks + 1);
+            load_frags(f1, cur, wm, wn, lane, 1);
+            kstep<FULLK, kAPacked, true>(acc, f0, nv, ra, lut, nxt + tid * LDSK);
+            __builtin_amdgcn_sched_barrier(0);
+            load_frags(f0, cur, wm, wn, lane, 2);
+            kstep<FULLK, kBPacked, true>(acc, f1, nv, rb, lut, nxt + (BM + tid) * LDSK);
+            __builtin_amdgcn_sched_barrier(0);
+            load_slice<FULLK, true>(ra, sa, min((ks + 2) * 4, last), kbt);
+            load_slice<FULLK, kBContig>(rb, sb, min((ks + 2) * 4, last), kbt);
+            load_frags(f1, cur, wm, wn, lane, 3);
+            kstep<FULLK, false, false>(acc, f0, nv, ra, lut, nxt);
             __syncthreads();
+            load_frags(f0, nxt, wm, wn, lane, 0);
+            kstep<FULLK, false, false>(acc, f1, nv, ra, lut, nxt);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 
     // ---- epilogue: C = alpha * acc ------------------------------------------
     // 32x32 accumulator layout: lane l, register r holds
     // row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
-    const float alpha = a_dec[0] * b_dec[0];
+    // operands were decoded as A_hat * 2^-3 and B_hat * 2^-3
+    const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll

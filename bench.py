@@ -242,10 +242,15 @@ def main():
     dom = "gemm_fprop"
     traffic = None
     if os.path.exists(args.traffic):
+        # HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE (scaled by a
+        # plain copy of known size); void once the kernel source has changed.
         try:
+            import hashlib
             tr = json.load(open(args.traffic))
-            if tr.get("kernel") == dom and tr.get("config") == [T, K, N]:
-                traffic = tr.get("bytes_per_launch")
+            src = open(os.path.join(ROOT, "paper_2609_02846_amd", "csrc", "gemm.hip"), "rb").read()
+            fresh = hashlib.sha256(src).hexdigest()[:16] == tr.get("source_sha256_16")
+            if fresh and tr.get("kernel") == dom and tr.get("config") == [T, K, N]:
+                traffic = round(float(tr["bytes_per_launch"]))
         except Exception:
             traffic = None
     achieved = flop_gemm / (avg[dom] * 1e-3) / 1e12

@@ -140,7 +140,7 @@ def main():
     bufs = {
         "xr": (u8(T, K // 2), u8(T, K // 16), f32(1)),
         "xc": (u8(K, T // 2), u8(K, T // 16), f32(1)),
-        "w": (u8(N, K // 2), u8(N // 16, K // 16), u8(K, N // 2), f32(1)),
+        "w": (u8(N, K // 2), u8(N // 16, K // 16), u8(K, N // 2), f32(1), u8(K // 16, N // 16)),
         "dr": (u8(T, N // 2), u8(T, N // 16), f32(1)),
         "dc": (u8(N, T // 2), u8(N, T // 16), f32(1)),
     }
@@ -165,8 +165,8 @@ def main():
         mark(2)
         ue.quantize_1d(x, 0, sx.amax, 448.0, "rn", 0, 0, *bufs["xc"])
         mark(3)
-        pw, sw_, pwt, dw_ = bufs["w"]
-        ue.quantize_2d(w, sw.amax, 448.0, "rn", 0, 0, True, pw, sw_, pwt, dw_)
+        pw, sw_, pwt, dw_, swt = bufs["w"]
+        ue.quantize_2d(w, sw.amax, 448.0, "rn", 0, 0, True, pw, sw_, pwt, dw_, swt)
         mark(4)
         ue.quantize_1d(dy, 1, sd.amax, 448.0, "sr", 1000 + t, 1, *bufs["dr"])
         mark(5)
@@ -175,7 +175,7 @@ def main():
         xr, xc, dr, dc = bufs["xr"], bufs["xc"], bufs["dr"], bufs["dc"]
         ue.gemm("nt", T, N, K, xr[0], xr[1], xr[2], pw, sw_, dw_, out=y)
         mark(7)
-        ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], pwt, sw_, dw_, out=dx)
+        ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], pwt, swt, dw_, out=dx)
         mark(8)
         ue.gemm("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xc[2], out=dw)
         mark(9)
@@ -192,7 +192,7 @@ def main():
             "quant_dy_cols": lambda: ue.quantize_1d(dy, 0, sd.amax, 448.0, "sr", 7, 2, *bufs["dc"]),
             "gemm_fprop": lambda: ue.gemm("nt", T, N, K, *bufs["xr"], bufs["w"][0], bufs["w"][1],
                                           bufs["w"][3], out=y),
-            "gemm_dgrad": lambda: ue.gemm("nn", T, K, N, *bufs["dr"], bufs["w"][2], bufs["w"][1],
+            "gemm_dgrad": lambda: ue.gemm("nn", T, K, N, *bufs["dr"], bufs["w"][2], bufs["w"][4],
                                           bufs["w"][3], out=dx),
             "gemm_wgrad": lambda: ue.gemm("tn", N, K, T, *bufs["dc"], *bufs["xc"], out=dw),
         }[args.kernel]

@@ -135,13 +135,15 @@ ue5m3_status_t ue5m3_quantize_1d(const void* x_bf16, int64_t rows, int64_t cols,
  *   scales    [rows/16, cols/16]
  *   payload_t (nullable) [cols, rows/2]: the same nibbles transposed, the
  *             operand of the dgrad GEMM.
+ *   scales_t  (nullable) [cols/16, rows/16]: the tile scales transposed, the
+ *             scales of that operand.
  *   dec_out   (nullable) decode multiplier, as above.
  */
 ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
                                  const float* amax_dev, float target,
                                  ue5m3_round_t mode, uint64_t seed, uint32_t tensor_id,
                                  uint8_t* payload, uint8_t* scales, uint8_t* payload_t,
-                                 float* dec_out, hipStream_t stream);
+                                 uint8_t* scales_t, float* dec_out, hipStream_t stream);
 
 /*
  * Decoded-operand FP4 GEMM (Sec. 5.1; the three products of Sec. 4.3):
@@ -161,7 +163,7 @@ ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
  *     b = quantize_2d(W):         payload [N, K/2], scales [N/16, K/16]
  * UE5M3_NN  dgrad  dX = dY W:   M = T, N = K_w, K = N_w.
  *     a = quantize_1d(dY, axis 1): payload [M, K/2], scales [M, K/16]
- *     b = quantize_2d(W): payload_t [N, K/2], scales [K/16, N/16]
+ *     b = quantize_2d(W): payload_t [N, K/2], scales_t [N/16, K/16]
  * UE5M3_TN  wgrad  dW = dY^T X: M = N_w, N = K_w, K = T.
  *     a = quantize_1d(dY, axis 0): payload [M, K/2], scales [M, K/16]
  *     b = quantize_1d(X, axis 0):  payload [N, K/2], scales [N, K/16]

@@ -66,7 +66,7 @@ def load_library(path=LIB_PATH):
     lib.ue5m3_amax_sample.restype = i32
     lib.ue5m3_quantize_1d.argtypes = [vp, i64, i64, i32, vp, f32, i32, u64, u32, vp, vp, vp, vp]
     lib.ue5m3_quantize_1d.restype = i32
-    lib.ue5m3_quantize_2d.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, vp, vp, vp, vp, vp]
+    lib.ue5m3_quantize_2d.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, vp, vp, vp, vp, vp, vp]
     lib.ue5m3_quantize_2d.restype = i32
     lib.ue5m3_gemm.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, vp]
     lib.ue5m3_gemm.restype = i32
@@ -165,24 +165,28 @@ def quantize_1d(x, axis, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0,
 
 
 def quantize_2d(w, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0, transposed=True,
-                payload=None, scales=None, payload_t=None, dec_out=None, stream=None):
+                payload=None, scales=None, payload_t=None, dec_out=None, scales_t=None,
+                stream=None):
     """16x16 tile quantization (see ue5m3_quantize_2d).  Returns
-    (payload, scales, payload_t or None, dec_out)."""
+    (payload, scales, payload_t or None, dec_out, scales_t or None); the
+    transposed payload and scales are the dgrad operand."""
     _bf16_2d(w, "w")
     R, C = w.shape
     payload = _u8((R, C // 2), w) if payload is None else payload
     scales = _u8((R // 16, C // 16), w) if scales is None else scales
     if transposed and payload_t is None:
         payload_t = _u8((C, R // 2), w)
+    if transposed and scales_t is None:
+        scales_t = _u8((C // 16, R // 16), w)
     if dec_out is None:
         dec_out = torch.empty(1, dtype=torch.float32, device=w.device)
     _check(load_library().ue5m3_quantize_2d(_ptr(w), R, C, _ptr(amax_dev), float(target),
                                             _MODES[mode], int(seed) & (2**64 - 1),
                                             int(tensor_id) & 0xFFFFFFFF, _ptr(payload),
-                                            _ptr(scales), _ptr(payload_t), _ptr(dec_out),
-                                            _stream(stream)),
+                                            _ptr(scales), _ptr(payload_t), _ptr(scales_t),
+                                            _ptr(dec_out), _stream(stream)),
            "ue5m3_quantize_2d")
-    return payload, scales, payload_t, dec_out
+    return payload, scales, payload_t, dec_out, scales_t
 
 
 def gemm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,

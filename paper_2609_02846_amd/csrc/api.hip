@@ -95,8 +95,8 @@ ue5m3_status_t ue5m3_quantize_1d(const void* x_bf16, int64_t rows, int64_t cols,
 ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
                                  const float* amax_dev, float target, ue5m3_round_t mode,
                                  uint64_t seed, uint32_t tensor_id, uint8_t* payload,
-                                 uint8_t* scales, uint8_t* payload_t, float* dec_out,
-                                 hipStream_t stream) {
+                                 uint8_t* scales, uint8_t* payload_t, uint8_t* scales_t,
+                                 float* dec_out, hipStream_t stream) {
     if (mode != UE5M3_RN && mode != UE5M3_SR) return UE5M3_EINVAL;
     if (amax_dev == nullptr || !valid_target(target)) return UE5M3_EINVAL;
     if (rows < 0 || cols < 0 || rows % 16 != 0 || cols % 16 != 0) return UE5M3_ESHAPE;
@@ -104,11 +104,12 @@ ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
     if (rows == 0 || cols == 0) return UE5M3_OK;
     if (w_bf16 == nullptr || payload == nullptr || scales == nullptr) return UE5M3_EINVAL;
     if (!aligned16(w_bf16) || !aligned16(payload) || !aligned16(scales) ||
-        (payload_t != nullptr && !aligned16(payload_t)))
+        (payload_t != nullptr && !aligned16(payload_t)) ||
+        (scales_t != nullptr && !aligned16(scales_t)))
         return UE5M3_EALIGN;
     return hip_status(ue5m3::launch_quant_tiles(w_bf16, rows, cols, amax_dev, target,
                                                 mode == UE5M3_SR, seed, tensor_id, payload,
-                                                scales, payload_t, dec_out, stream));
+                                                scales, payload_t, scales_t, dec_out, stream));
 }
 
 ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
@@ -118,13 +119,13 @@ ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K
     ue5m3::BScale bmode;
     switch (layout) {
         case UE5M3_NT: bmode = ue5m3::BScale::Tile; break;
-        case UE5M3_NN: bmode = ue5m3::BScale::TileT; break;
+        case UE5M3_NN: bmode = ue5m3::BScale::Tile; break;
         case UE5M3_TN: bmode = ue5m3::BScale::Row; break;
         default: return UE5M3_ELAYOUT;
     }
     if (c_type != UE5M3_OUT_F32 && c_type != UE5M3_OUT_BF16) return UE5M3_EINVAL;
     if (M < 0 || N < 0 || K < 0 || K % 16 != 0) return UE5M3_ESHAPE;
-    if (bmode != ue5m3::BScale::Row && N % 16 != 0) return UE5M3_ESHAPE;
+    if (layout != UE5M3_TN && N % 16 != 0) return UE5M3_ESHAPE;
     if (M == 0 || N == 0) return UE5M3_OK;
     if (c == nullptr || a_dec == nullptr || b_dec == nullptr) return UE5M3_EINVAL;
     if (K > 0 && (a == nullptr || a_scales == nullptr || b == nullptr || b_scales == nullptr))

@@ -8,7 +8,8 @@
 
 namespace ue5m3 {
 
-enum class BScale : int { Row = 0, Tile = 1, TileT = 2 };
+// B scale layouts: one code per (row, 16 k) or per (16 rows, 16 k).
+enum class BScale : int { Row = 0, Tile = 1 };
 
 hipError_t launch_amax(const void* x_bf16, int64_t numel, float* amax_dev, hipStream_t s);
 
@@ -25,7 +26,8 @@ hipError_t launch_quant_cols(const void* x_bf16, int64_t rows, int64_t cols,
 hipError_t launch_quant_tiles(const void* w_bf16, int64_t rows, int64_t cols,
                               const float* amax_dev, float target, bool sr, uint64_t seed,
                               uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
-                              uint8_t* payload_t, float* dec_out, hipStream_t s);
+                              uint8_t* payload_t, uint8_t* scales_t, float* dec_out,
+                              hipStream_t s);
 
 hipError_t launch_gemm(BScale bmode, int64_t M, int64_t N, int64_t K,
                        const uint8_t* a, const uint8_t* a_scales, const float* a_dec,

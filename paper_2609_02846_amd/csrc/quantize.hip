@@ -202,7 +202,8 @@ template <bool SR>
 __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
     const uint16_t* __restrict__ w, int64_t rows, int64_t cols, const float* __restrict__ amax_dev,
     float T, uint32_t key0, uint32_t key1, uint32_t tid, uint8_t* __restrict__ payload,
-    uint8_t* __restrict__ scales, uint8_t* __restrict__ payload_t, float* __restrict__ dec_out) {
+    uint8_t* __restrict__ scales, uint8_t* __restrict__ payload_t, uint8_t* __restrict__ scales_t,
+    float* __restrict__ dec_out) {
     const Multipliers m = tensor_multipliers(*amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *dec_out = m.dec;
     const int lane = threadIdx.x & 63;
@@ -239,7 +240,10 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
 #pragma unroll
             for (int j = 0; j < 8; ++j) colpk[j][r >> 3] |= ((p >> (4 * j)) & 15u) << (4 * (r & 7));
         }
-        if ((lane & 1) == 0) scales[tr * ntc + c0 / 16] = (uint8_t)bs.code;
+        if ((lane & 1) == 0) {
+            scales[tr * ntc + c0 / 16] = (uint8_t)bs.code;
+            if (scales_t != nullptr) scales_t[(c0 / 16) * ntr + tr] = (uint8_t)bs.code;
+        }
         if (payload_t != nullptr) {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
@@ -302,7 +306,8 @@ hipError_t launch_quant_cols(const void* x_bf16, int64_t rows, int64_t cols,
 hipError_t launch_quant_tiles(const void* w_bf16, int64_t rows, int64_t cols,
                               const float* amax_dev, float target, bool sr, uint64_t seed,
                               uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
-                              uint8_t* payload_t, float* dec_out, hipStream_t s) {
+                              uint8_t* payload_t, uint8_t* scales_t, float* dec_out,
+                              hipStream_t s) {
     uint32_t k0, k1;
     seed_key(seed, k0, k1);
     const int64_t gx = (cols + 511) / 512;
@@ -312,11 +317,11 @@ hipError_t launch_quant_tiles(const void* w_bf16, int64_t rows, int64_t cols,
     if (sr)
         hipLaunchKernelGGL(quant_tiles_kernel<true>, dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
                            0, s, w, rows, cols, amax_dev, target, k0, k1, tensor_id, payload, scales,
-                           payload_t, dec_out);
+                           payload_t, scales_t, dec_out);
     else
         hipLaunchKernelGGL(quant_tiles_kernel<false>, dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
                            0, s, w, rows, cols, amax_dev, target, k0, k1, tensor_id, payload, scales,
-                           payload_t, dec_out);
+                           payload_t, scales_t, dec_out);
     return hipGetLastError();
 }
 

@@ -75,13 +75,14 @@ def test_quantize_1d_validation(lib):
 def test_quantize_2d_validation(lib):
     q = lib.ue5m3_quantize_2d
 
-    def call(rows=32, cols=32, w=FAKE, amax=FAKE, T=448.0, mode=0, p=FAKE, s=FAKE, pt=NULL):
-        return q(w, rows, cols, amax, T, mode, 0, 0, p, s, pt, NULL, NULL)
+    def call(rows=32, cols=32, w=FAKE, amax=FAKE, T=448.0, mode=0, p=FAKE, s=FAKE, pt=NULL, st=NULL):
+        return q(w, rows, cols, amax, T, mode, 0, 0, p, s, pt, st, NULL, NULL)
     assert call(rows=24) == ue.UE5M3_ESHAPE
     assert call(cols=40) == ue.UE5M3_ESHAPE
     assert call(mode=2) == ue.UE5M3_EINVAL
     assert call(T=0.0) == ue.UE5M3_EINVAL
     assert call(pt=FAKE_MIS) == ue.UE5M3_EALIGN
+    assert call(st=FAKE_MIS) == ue.UE5M3_EALIGN
     assert call(w=NULL) == ue.UE5M3_EINVAL
     assert call(rows=0) == ue.UE5M3_OK
 

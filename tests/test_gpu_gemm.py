@@ -44,10 +44,10 @@ def _run_three(T, K, N, seed=0, out_dtype=torch.float32):
     c = ue.gemm("nt", T, N, K, u8_to_dev(xr[0]), u8_to_dev(xr[1]), D(xr[2]),
                 u8_to_dev(wq[0]), u8_to_dev(wq[1]), D(wq[3]), out_dtype=out_dtype)
     out["fprop"] = (c, ogemm.fprop(X, W, al), ogemm.abs_product(X, W), al, K)
-    # dgrad: dX = dY W   (B operand = transposed weight payload, tile scales)
+    # dgrad: dX = dY W   (B operand = transposed weight payload and tile scales)
     al = ogemm.alpha(dr[2], wq[3])
     c = ue.gemm("nn", T, K, N, u8_to_dev(dr[0]), u8_to_dev(dr[1]), D(dr[2]),
-                u8_to_dev(wq[2]), u8_to_dev(wq[1]), D(wq[3]), out_dtype=out_dtype)
+                u8_to_dev(wq[2]), u8_to_dev(wq[1].T), D(wq[3]), out_dtype=out_dtype)
     out["dgrad"] = (c, ogemm.dgrad(dY, W, al), ogemm.abs_product(dY, W.T), al, N)
     # wgrad: dW = dY^T X  (both operands re-blocked along tokens)
     al = ogemm.alpha(dc[2], xc[2])
@@ -58,7 +58,9 @@ def _run_three(T, K, N, seed=0, out_dtype=torch.float32):
 
 
 @pytest.mark.parametrize("T,K,N", [(16, 16, 16), (48, 80, 48), (64, 128, 64), (128, 256, 128),
-                                   (144, 208, 272), (256, 512, 384), (512, 1024, 256)])
+                                   (144, 208, 272), (256, 512, 384), (512, 1024, 256),
+                                   # odd numbers of 64-wide K slices (1, 3, 5, 7)
+                                   (96, 192, 320), (192, 64, 448)])
 def test_three_products(T, K, N):
     say("gemm three products", T, K, N)
     for name, (c, ref, ap, al, kk) in _run_three(T, K, N).items():
@@ -129,7 +131,7 @@ def test_gemm_on_gpu_quantized_operands_matches():
     dr = ue.quantize_1d(dyd, 1, sd.amax, 448.0, "sr", 1, 1)
     dc = ue.quantize_1d(dyd, 0, sd.amax, 448.0, "sr", 1, 2)
     y = ue.gemm("nt", T, N, K, xr[0], xr[1], xr[2], wq[0], wq[1], wq[3])
-    dx = ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], wq[2], wq[1], wq[3])
+    dx = ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], wq[2], wq[4], wq[3])
     dw = ue.gemm("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xc[2])
     ref = _run_three(T, K, N, seed=9)
     for name, c in [("fprop", y), ("dgrad", dx), ("wgrad", dw)]:
@@ -155,7 +157,7 @@ def test_ffn_up_projection_sampled():
     dr = ue.quantize_1d(dyd, 1, sd.amax, 448.0, "sr", 1, 1)
     dc = ue.quantize_1d(dyd, 0, sd.amax, 448.0, "sr", 1, 2)
     y = ue.gemm("nt", T, N, K, xr[0], xr[1], xr[2], wq[0], wq[1], wq[3])
-    dx = ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], wq[2], wq[1], wq[3])
+    dx = ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], wq[2], wq[4], wq[3])
     dw = ue.gemm("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xc[2])
     torch.cuda.synchronize()
     gx, gw, gd = osc.amax(x), osc.amax(w), osc.amax(dy)

@@ -117,15 +117,17 @@ def test_quantize_tiles(shape, mode):
     bits = synthetic.weight(7, *shape)
     xd = to_dev(bits)
     st, g = _gpu_amax(xd)
-    p, s, pt, d = ue.quantize_2d(xd, st.amax, 448.0, mode, seed=5, tensor_id=4)
+    p, s, pt, d, stt = ue.quantize_2d(xd, st.amax, 448.0, mode, seed=5, tensor_id=4)
     po, so, pto, do = oq.quantize_2d(bits, g, 448.0, mode, 5, 4)
     assert np.array_equal(host(s), so)
     assert np.array_equal(host(p), po)
     assert np.array_equal(host(pt), pto)
+    assert np.array_equal(host(stt), so.T)
     assert np.float32(d.item()) == do
     # without the transposed copy
-    p2, s2, pt2, _ = ue.quantize_2d(xd, st.amax, 448.0, mode, seed=5, tensor_id=4, transposed=False)
-    assert pt2 is None and np.array_equal(host(p2), po)
+    p2, s2, pt2, _, st2 = ue.quantize_2d(xd, st.amax, 448.0, mode, seed=5, tensor_id=4,
+                                         transposed=False)
+    assert pt2 is None and st2 is None and np.array_equal(host(p2), po)
 
 
 # ---------------------------------------------------- degenerate cases ----
@@ -201,7 +203,7 @@ def test_quantizer_bandwidth_workload_sampled():
     wb = wl["w"]
     wd = to_dev(wb)
     st, g = _gpu_amax(wd)
-    p, s, pt, _ = ue.quantize_2d(wd, st.amax, 448.0, "rn")
+    p, s, pt, _, _ = ue.quantize_2d(wd, st.amax, 448.0, "rn")
     tr = rng.choice(wb.shape[0] // 16, 16, replace=False)
     for t in tr:
         po, so, _, _ = oq.quantize_2d(wb[16 * t:16 * t + 16], g, 448.0, "rn")

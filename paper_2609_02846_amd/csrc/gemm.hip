@@ -33,6 +33,8 @@
 #include "codec.hpp"
 #include "launch.hpp"
 
+#include <type_traits>
+
 namespace ue5m3 {
 namespace {
 
@@ -611,6 +613,324 @@ hipError_t launch_dma(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
     return hipGetLastError();
 }
 
+// ===================================================================== //
+// K % 256 == 0 path: decode straight into MFMA fragments.               //
+// ===================================================================== //
+//
+// The workgroup stages its 256 A rows and 256 B rows in LDS four K slices at
+// a time (256 k: 128 payload bytes and 16 scale bytes per row), double
+// buffered and filled by direct global->LDS loads, with one barrier per four
+// slices.  Each wave then decodes its fragments itself: no fp16 copy of the
+// operands goes through LDS.
+//
+// For k-step kk (0..3) of slice sl, lane l of the 32x32x16 MFMA supplies 8
+// k-elements of row l % 32: half h = l / 32 takes payload word 4h + kk of
+// the row's 32 bytes of that slice (k = 64 sl + 32h + 8kk .. + 7).  The k
+// order inside a slice is thus permuted, identically for A and B, which the
+// sum over k does not see.  That word's block scale is code 2h + kk/2 of the
+// row's scale word for the slice.
+//
+// A UE5M3 code c read as an fp16 bit pattern, c << 7, is exactly its value
+// (5 exponent bits with bias 15, 3 leading mantissa bits, subnormals
+// included; codes above 0xF7 are not valid encodings).  The decode is
+// therefore two exact steps: the hardware FP4 -> FP16 conversion with the
+// power-of-two scale 2^-3, then an fp16 multiply by the code's value.  The
+// product q * s * 2^-3 never exceeds 6 * 61440 / 8 = 46080 and is a multiple
+// of 2^-24, so it is representable in fp16.
+//
+// A stage row is 128 B = 8 chunks of 16 B; chunk c of stage row x sits at
+// position c ^ (x & 7), so that the 8 lanes the LDS serves together hit 8
+// different bank groups.
+
+constexpr int kSupK = 4;                                  // slices per stage
+constexpr int kSupRows = BM + BN;                         // 512 stage rows
+constexpr int kSupRowBytes = kSupK * 32;                  // 128
+constexpr int kSupPayload = kSupRows * kSupRowBytes;      // 64 KB
+constexpr int kSupScales = kSupRows * kSupK * 4;          // 8 KB
+constexpr int kSupPayLoads = kSupPayload / 1024 / 4;      // 16 payload loads per wave
+constexpr int kSupScLoads = kSupScales / 1024 / 4;        // 2 scale loads per wave
+constexpr int kSupLoads = kSupPayLoads + kSupScLoads;
+
+// One slice of a lane's operand data: payload words (groups 0..3 = A rows
+// 32i + l%32 of the wave's 128, groups 4..7 = B rows 32j + l%32; word kk =
+// k-step kk) and per group the row's scale word, replaced at k-step 0 by the
+// two block scales of the lane's half as fp16 bit patterns (low half:
+// k-steps 0, 1; high half: k-steps 2, 3).
+struct RegSlice {
+    uint32_t w[8][4];
+    uint32_t s[8];
+};
+
+__device__ __forceinline__ uint32_t half_scales(uint32_t word, uint32_t sel) {
+    return __builtin_amdgcn_perm(0u, word, sel) << 7;
+}
+
+// Slice SL of the stage (P, S) into R.  pa / pb: byte offsets of the lane's
+// first A / B stage row (group 0); xo: the lane's chunk offset for this slice.
+template <int SL>
+__device__ __forceinline__ void read_sup_slice(RegSlice& R, const uint8_t* P, const uint8_t* S,
+                                               int pa, int pb, int xo) {
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+        const int row_off = (g < 4 ? pa : pb) + (g & 3) * 32 * kSupRowBytes;
+        const uint4 v = *reinterpret_cast<const uint4*>(P + row_off + xo);
+        R.w[g][0] = v.x; R.w[g][1] = v.y; R.w[g][2] = v.z; R.w[g][3] = v.w;
+    }
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+        const int srow_off = ((g < 4 ? pa : pb) / kSupRowBytes + (g & 3) * 32) * (kSupK * 4);
+        R.s[g] = *reinterpret_cast<const uint32_t*>(S + srow_off + SL * 4);
+    }
+}
+
+__device__ __forceinline__ f16x8_t decode_frag(uint32_t w, uint32_t s2, int hsel) {
+    const f16x2_t sp = __builtin_bit_cast(f16x2_t, s2);
+    const _Float16 sv = sp[hsel];
+    const f16x2_t sc = {sv, sv};
+    const f16x2_t v0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 0.125f, 0) * sc;
+    const f16x2_t v1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 0.125f, 1) * sc;
+    const f16x2_t v2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 0.125f, 2) * sc;
+    const f16x2_t v3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 0.125f, 3) * sc;
+    return f16x8_t{v0[0], v0[1], v1[0], v1[1], v2[0], v2[1], v3[0], v3[1]};
+}
+
+// k-step KK of a slice into MFMA fragments.  At KK = 0 the raw scale words
+// read from LDS are first turned into the lane half's two fp16 scales (done
+// here, a k-step after the LDS reads were issued, so that no wait for them
+// lands among the matrix-core instructions).
+template <int KK>
+__device__ __forceinline__ void decode_kstep(Frags& f, RegSlice& R, uint32_t sel) {
+    if (KK == 0) {
+#pragma unroll
+        for (int g = 0; g < 8; ++g) R.s[g] = half_scales(R.s[g], sel);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f.a[i] = decode_frag(R.w[i][KK], R.s[i], KK >> 1);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) f.b[j] = decode_frag(R.w[4 + j][KK], R.s[4 + j], KK >> 1);
+}
+
+// Direct global->LDS loads written as instructions the compiler does not
+// model: it would otherwise wait for every outstanding direct load before any
+// LDS read (it cannot tell the stage arrays apart), which would remove the
+// overlap.  The kernel counts them itself with vmcnt.  The LDS destination of
+// lane l is m0 + 16 l.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)p);
+}
+
+__device__ __forceinline__ void dma_x4(const uint8_t* g, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(g), "s"(lds) : "memory", "m0");
+}
+
+// vmcnt(n) with expcnt and lgkmcnt left at their maxima (n < 64).
+template <int n>
+__device__ __forceinline__ void wait_vmem() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | 0x0F70);
+}
+
+// A wave's share of the loads of one stage: payload loads i in [I0, I1)
+// (1 KB each: 8 stage rows of 128 B, lane l -> row 8i + l/8 of the wave's
+// 128, position l % 8) and, with SC, its two scale loads (64 rows x 16 B).
+struct SupLoader {
+    const uint8_t* mat;      // payload matrix of this wave's rows (A or B)
+    int64_t row0, rmax;      // matrix row of the lane's first payload row, last valid row
+    int64_t rowb;            // payload row bytes
+    int chunk;               // source chunk of the lane (position ^ row & 7)
+    const uint8_t* sc[2];    // scale row pointers of the lane's two scale loads
+    uint32_t ldp, lds;       // this wave's LDS offsets inside a payload / scale stage
+
+    template <int I0, int I1, bool SC>
+    __device__ __forceinline__ void issue(uint32_t P, uint32_t S, int64_t G) const {
+#pragma unroll
+        for (int i = I0; i < I1; ++i) {
+            const int64_t row = min(row0 + 8 * i, rmax);
+            dma_x4(mat + row * rowb + G * kSupRowBytes + chunk * 16, P + ldp + i * 1024);
+        }
+        if (SC) {
+#pragma unroll
+            for (int u = 0; u < 2; ++u) dma_x4(sc[u] + G * 16, S + lds + u * 1024);
+        }
+    }
+};
+
+template <int BMODE, bool OUT_BF16>
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
+    int64_t M, int64_t N, int64_t K, int tiles_m, int tiles_n, const uint8_t* __restrict__ A,
+    const uint8_t* __restrict__ As, const float* __restrict__ a_dec, const uint8_t* __restrict__ B,
+    const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec, void* __restrict__ C) {
+    __shared__ __attribute__((aligned(16))) uint8_t sP0[kSupPayload];
+    __shared__ __attribute__((aligned(16))) uint8_t sP1[kSupPayload];
+    __shared__ __attribute__((aligned(16))) uint8_t sC0[kSupScales];
+    __shared__ __attribute__((aligned(16))) uint8_t sC1[kSupScales];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int r = lane & 31, hi = lane >> 5;
+
+    // tile index (see gemm_fp4_kernel)
+    const int ntiles = tiles_m * tiles_n;
+    int t = blockIdx.x;
+    if (ntiles % kXcds == 0) t = (t % kXcds) * (ntiles / kXcds) + t / kXcds;
+    const int group_tiles = kGroupM * tiles_n;
+    const int g = t / group_tiles;
+    const int first_m = g * kGroupM;
+    const int gm = min(tiles_m - first_m, kGroupM);
+    const int rr = t - g * group_tiles;
+    const int64_t m0 = (int64_t)(first_m + rr % gm) * BM;
+    const int64_t n0 = (int64_t)(rr / gm) * BN;
+
+    const int64_t kbt = K / 16;
+    const int64_t NG = K / (kSupK * BK);             // stages
+    auto stage_of = [&](int64_t G) { return min(G, NG - 1); };
+
+    // Loads: waves 0, 1 bring A stage rows 0..255, waves 2, 3 B rows 256..511
+    // (rows clamped into the matrix; clamped rows only feed discarded outputs).
+    SupLoader L;
+    {
+        const bool isA = wave < 2;
+        const int xw = 128 * (wave & 1);             // first stage row of the wave within A or B
+        L.mat = isA ? A : B;
+        L.rowb = kbt * 8;
+        L.row0 = (isA ? m0 : n0) + xw + (lane >> 3);
+        L.rmax = (isA ? M : N) - 1;
+        L.chunk = (lane & 7) ^ ((lane >> 3) & 7);
+        L.ldp = __builtin_amdgcn_readfirstlane((uint32_t)(128 * wave * kSupRowBytes));
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int64_t x = (isA ? m0 : n0) + xw + 64 * u + lane;
+            if (isA) {
+                L.sc[u] = As + min(x, M - 1) * kbt;
+            } else {
+                const int64_t n = min(x, N - 1);
+                L.sc[u] = Bs + (BMODE == (int)BScale::Row ? n : (n >> 4)) * kbt;
+            }
+        }
+        L.lds = __builtin_amdgcn_readfirstlane((uint32_t)(128 * wave * kSupK * 4));
+    }
+    const uint32_t P0 = lds_addr(sP0), P1 = lds_addr(sP1), S0 = lds_addr(sC0), S1 = lds_addr(sC1);
+
+    // Read offsets of the lane: first A / B stage rows and per-slice chunk.
+    const int pa = (wm * 128 + r) * kSupRowBytes;
+    const int pb = (BM + wn * 128 + r) * kSupRowBytes;
+    const int x0 = ((0 + hi) ^ (r & 7)) * 16, x1 = ((2 + hi) ^ (r & 7)) * 16;
+    const int x2 = ((4 + hi) ^ (r & 7)) * 16, x3 = ((6 + hi) ^ (r & 7)) * 16;
+    const uint32_t sel = hi ? 0x0C030C02u : 0x0C010C00u;
+
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+    RegSlice R0, R1;
+    Frags F0, F1;
+
+    // prologue: stages 0 and 1 in flight; stage 0 complete everywhere; slice 0
+    // in registers and its k-step 0 decoded
+    L.issue<0, kSupPayLoads, true>(P0, S0, 0);
+    L.issue<0, kSupPayLoads, true>(P1, S1, stage_of(1));
+    wait_vmem<kSupLoads>();
+    __syncthreads();
+    read_sup_slice<0>(R0, sP0, sC0, pa, pb, x0);
+    decode_kstep<0>(F0, R0, sel);
+
+    // One slice.  Slices 0..2 of a stage read the next slice of the same
+    // stage; slice 3 first waits for the next stage (loaded during the
+    // previous stage), synchronizes, starts the loads of stage G+2 into the
+    // buffer just consumed, and reads slice 0 of the next stage.
+    auto slice = [&](auto SLc, int64_t G, const uint8_t* Pc, const uint8_t* Sc, const uint8_t* Pn,
+                     const uint8_t* Sn, uint32_t ldP, uint32_t ldS, RegSlice& Rc, RegSlice& Rn) {
+        constexpr int SL = decltype(SLc)::value;
+        decode_kstep<1>(F1, Rc, sel);
+        mfma16(acc, F0);
+        kstep_schedule<0, 0, 4>();
+        __builtin_amdgcn_sched_barrier(0);
+        if (SL == 3) {
+            wait_vmem<0>();
+            __syncthreads();
+            read_sup_slice<0>(Rn, Pn, Sn, pa, pb, x0);
+            L.issue<0, 6, false>(ldP, ldS, stage_of(G + 2));
+        } else {
+            read_sup_slice<SL + 1>(Rn, Pc, Sc, pa, pb, SL == 0 ? x1 : (SL == 1 ? x2 : x3));
+        }
+        decode_kstep<2>(F0, Rc, sel);
+        mfma16(acc, F1);
+        kstep_schedule<16, 0, 4>();
+        __builtin_amdgcn_sched_barrier(0);
+        if (SL == 3) L.issue<6, 12, false>(ldP, ldS, stage_of(G + 2));
+        decode_kstep<3>(F1, Rc, sel);
+        mfma16(acc, F0);
+        kstep_schedule<0, 0, 4>();
+        __builtin_amdgcn_sched_barrier(0);
+        if (SL == 3) L.issue<12, kSupPayLoads, true>(ldP, ldS, stage_of(G + 2));
+        decode_kstep<0>(F0, Rn, sel);
+        mfma16(acc, F1);
+        kstep_schedule<0, 0, 4>();
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    auto stage = [&](int64_t G, const uint8_t* Pc, const uint8_t* Sc, const uint8_t* Pn,
+                     const uint8_t* Sn, uint32_t ldP, uint32_t ldS) {
+        slice(I0{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R0, R1);
+        slice(I1{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R1, R0);
+        slice(I2{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R0, R1);
+        slice(I3{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R1, R0);
+    };
+    int64_t G = 0;
+    for (; G + 1 < NG; G += 2) {
+        stage(G, sP0, sC0, sP1, sC1, P0, S0);
+        stage(G + 1, sP1, sC1, sP0, sC0, P1, S1);
+    }
+    if (G < NG) stage(G, sP0, sC0, sP1, sC1, P0, S0);   // odd stage count
+    wait_vmem<0>();                                // no load outlives the kernel's LDS
+
+    // ---- epilogue: C = alpha * acc ------------------------------------------
+    const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;   // operands were scaled by 2^-3
+    const int64_t mw = m0 + wm * 128, nw = n0 + wn * 128;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t n = nw + j * 32 + r;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int64_t m = mw + i * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+                if (m < M && n < N) {
+                    const float v = alpha * acc[i][j][e];
+                    if (OUT_BF16) {
+                        const uint32_t b = __float_as_uint(v);
+                        const uint32_t rb16 = (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+                        reinterpret_cast<uint16_t*>(C)[m * N + n] = (uint16_t)rb16;
+                    } else {
+                        reinterpret_cast<float*>(C)[m * N + n] = v;
+                    }
+                }
+            }
+        }
+    }
+}
+
+template <int BMODE, bool OUT_BF16>
+hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
+                      const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
+                      void* c, hipStream_t s) {
+    const int tiles_m = (int)((M + BM - 1) / BM);
+    const int tiles_n = (int)((N + BN - 1) / BN);
+    hipLaunchKernelGGL((gemm_fp4_reg_kernel<BMODE, OUT_BF16>), dim3((unsigned)(tiles_m * tiles_n)),
+                       dim3(kGemmThreads), 0, s, M, N, K, tiles_m, tiles_n, a, as, ad, b, bs, bd, c);
+    return hipGetLastError();
+}
+
 template <int BMODE, bool OUT_BF16, bool FULLK>
 hipError_t launch_one(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                       const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
@@ -635,6 +955,9 @@ template <int BMODE>
 hipError_t launch_mode(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                        const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
                        void* c, bool c_bf16, hipStream_t s) {
+    if (K % (4 * BK) == 0 && K > 0)
+        return c_bf16 ? launch_reg<BMODE, true>(M, N, K, a, as, ad, b, bs, bd, c, s)
+                      : launch_reg<BMODE, false>(M, N, K, a, as, ad, b, bs, bd, c, s);
     if (K % BK == 0 && K > 0)
         return c_bf16 ? launch_dma<BMODE, true>(M, N, K, a, as, ad, b, bs, bd, c, s)
                       : launch_dma<BMODE, false>(M, N, K, a, as, ad, b, bs, bd, c, s);

@@ -80,17 +80,18 @@ def test_ragged_m_and_n():
         c = ue.gemm("nt", M, N, K, u8_to_dev(ar[0]), u8_to_dev(ar[1]), f32_scalar_dev(ar[2]),
                     u8_to_dev(wq[0]), u8_to_dev(wq[1]), f32_scalar_dev(wq[3]))
         gemm_check(host(c), ogemm.fprop(A, W, al), al, ogemm.abs_product(A, W), K, f"nt {M}x{N}x{K}")
-    # TN with N not a multiple of 16 (row-scaled B)
-    T, Mo, No = 64, 40, 24
-    dy = synthetic.gradient(4, T, Mo, 1e-3, 1.0)
-    x = synthetic.activation(4, T, No, 1e-2, 50.0)
-    dc = oq.quantize_1d(dy, 0, osc.amax(dy), 448.0, "sr", 1, 2)
-    xc = oq.quantize_1d(x, 0, osc.amax(x))
-    dYc, Xc = oq.decoded_1d(dc[0], dc[1], 0), oq.decoded_1d(xc[0], xc[1], 0)
-    al = ogemm.alpha(dc[2], xc[2])
-    c = ue.gemm("tn", Mo, No, T, u8_to_dev(dc[0]), u8_to_dev(dc[1]), f32_scalar_dev(dc[2]),
-                u8_to_dev(xc[0]), u8_to_dev(xc[1]), f32_scalar_dev(xc[2]))
-    gemm_check(host(c), ogemm.wgrad(dYc, Xc, al), al, ogemm.abs_product(dYc.T, Xc.T), T, "tn ragged")
+    # TN with N not a multiple of 16 (row-scaled B); K = 64 and K = 512
+    for T, Mo, No in [(64, 40, 24), (512, 300, 40)]:
+        dy = synthetic.gradient(4, T, Mo, 1e-3, 1.0)
+        x = synthetic.activation(4, T, No, 1e-2, 50.0)
+        dc = oq.quantize_1d(dy, 0, osc.amax(dy), 448.0, "sr", 1, 2)
+        xc = oq.quantize_1d(x, 0, osc.amax(x))
+        dYc, Xc = oq.decoded_1d(dc[0], dc[1], 0), oq.decoded_1d(xc[0], xc[1], 0)
+        al = ogemm.alpha(dc[2], xc[2])
+        c = ue.gemm("tn", Mo, No, T, u8_to_dev(dc[0]), u8_to_dev(dc[1]), f32_scalar_dev(dc[2]),
+                    u8_to_dev(xc[0]), u8_to_dev(xc[1]), f32_scalar_dev(xc[2]))
+        gemm_check(host(c), ogemm.wgrad(dYc, Xc, al), al, ogemm.abs_product(dYc.T, Xc.T), T,
+                   f"tn ragged {Mo}x{No}x{T}")
 
 
 def test_k_zero_writes_zeros():

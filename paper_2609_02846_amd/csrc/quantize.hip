@@ -12,7 +12,11 @@
 //
 // All three kernels are HBM-bound streaming passes: 2 bytes of bf16 read and
 // 0.5 + 1/16 (1D) or 0.5 + 1/256 (2D) bytes written per element, plus 0.5
-// bytes for the optional transposed weight payload.
+// bytes for the optional transposed weight payload.  HBM is written in
+// 64-byte units, so every output is written in runs of at least 64
+// contiguous bytes from one store instruction: outputs whose natural
+// per-lane piece is smaller (the transposed payloads and scales) are
+// assembled in LDS first.
 #include "codec.hpp"
 #include "launch.hpp"
 
@@ -36,167 +40,236 @@ __device__ __forceinline__ BlockScale block_scale(uint32_t amax_bits15, const Mu
     return bs;
 }
 
+__device__ __forceinline__ uint32_t quant1(float x, float r, uint32_t w, bool sr) {
+    const float y = x * r;
+    return sr ? e2m1_sr(y, w) : e2m1_rn(y);
+}
+
 // Quantize the 8 bf16 values held in v (element e in half e&1 of word e>>1)
 // with reciprocal r; returns 8 nibbles packed little-endian.  For SR, w holds
 // the 8 Philox words of the elements.
 template <bool SR>
-__device__ __forceinline__ uint32_t quant8(const uint32_t (&v)[4], float r, const uint32_t* w) {
+__device__ __forceinline__ uint32_t quant8(const uint4& v, float r, const uint32_t* w) {
+    const uint32_t vv[4] = {v.x, v.y, v.z, v.w};
     uint32_t p = 0;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-        const float x = (e & 1) ? bf16_hi(v[e >> 1]) : bf16_lo(v[e >> 1]);
-        const float y = x * r;
-        const uint32_t nib = SR ? e2m1_sr(y, w[e]) : e2m1_rn(y);
-        p |= nib << (4 * e);
+        const float x = (e & 1) ? bf16_hi(vv[e >> 1]) : bf16_lo(vv[e >> 1]);
+        p |= quant1(x, r, SR ? w[e] : 0u, SR) << (4 * e);
     }
     return p;
 }
 
-__device__ __forceinline__ void words8(uint64_t first_elem, uint32_t tid, uint32_t k0, uint32_t k1,
+__device__ __forceinline__ uint32_t amax8(const uint4& v) {
+    return max(max(bf16_abs_max_pair(v.x), bf16_abs_max_pair(v.y)),
+               max(bf16_abs_max_pair(v.z), bf16_abs_max_pair(v.w)));
+}
+
+// Philox words of elements 4j .. 4j+3 for the 4 columns c..c+3 of one row,
+// element index e0 = row * cols + c (even).  When e0 % 4 == 0 one Philox
+// block holds them; otherwise (cols % 4 == 2) they straddle two blocks.
+__device__ __forceinline__ void words4(uint64_t e0, uint32_t tid, uint32_t k0, uint32_t k1,
                                        uint32_t* w) {
-    // first_elem is a multiple of 4: two Philox blocks cover the 8 elements
-    const uint4 a = sr_words4(first_elem >> 2, tid, k0, k1);
-    const uint4 b = sr_words4((first_elem >> 2) + 1, tid, k0, k1);
-    w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
-    w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+    const uint4 a = sr_words4(e0 >> 2, tid, k0, k1);
+    if ((e0 & 3) == 0) {
+        w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+    } else {
+        const uint4 b = sr_words4((e0 >> 2) + 1, tid, k0, k1);
+        w[0] = a.z; w[1] = a.w; w[2] = b.x; w[3] = b.y;
+    }
 }
 
 // ------------------------------------------------------------ rows (1D) --
-// The flat tensor is a sequence of 16-element blocks (cols % 16 == 0).  Each
-// lane handles one 8-element chunk (16 B); lanes 2k, 2k+1 hold one block and
-// combine their maxima with a lane swap.  Payload: 4 B per chunk, scale: 1 B
-// per block written by the even lane.
-constexpr int kRowUnroll = 4;
-
+// The flat tensor is a sequence of 16-element blocks (cols % 16 == 0).  One
+// lane per block: two 16-byte loads, 8 bytes of payload and 1 byte of scale,
+// so one wave instruction stores 512 contiguous payload bytes and 64 scale
+// bytes.  Persistent grid: a lane walks blocks b, b + stride, ..., loading
+// the next block before quantizing the current one.
 template <bool SR>
 __global__ __launch_bounds__(kThreads) void quant_rows_kernel(
-    const uint4* __restrict__ x, int64_t nchunks, const float* __restrict__ amax_dev, float T,
-    uint32_t key0, uint32_t key1, uint32_t tid, uint32_t* __restrict__ payload,
+    const uint4* __restrict__ x, int64_t nblocks, const float* __restrict__ amax_dev, float T,
+    uint32_t key0, uint32_t key1, uint32_t tid, uint2* __restrict__ payload,
     uint8_t* __restrict__ scales, float* __restrict__ dec_out) {
     const Multipliers m = tensor_multipliers(*amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t base = (int64_t)blockIdx.x * kThreads + threadIdx.x; base < nchunks;
-         base += stride * kRowUnroll) {
-        uint4 v[kRowUnroll];
-#pragma unroll
-        for (int u = 0; u < kRowUnroll; ++u) {
-            const int64_t c = base + u * stride;
-            if (c < nchunks) v[u] = x[c];
+    int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    uint4 c0, c1;
+    if (b < nblocks) {
+        c0 = x[2 * b];
+        c1 = x[2 * b + 1];
+    }
+    for (; b < nblocks; b += stride) {
+        const int64_t bn = b + stride;
+        uint4 n0 = make_uint4(0u, 0u, 0u, 0u), n1 = n0;
+        if (bn < nblocks) {
+            n0 = x[2 * bn];
+            n1 = x[2 * bn + 1];
         }
+        const BlockScale bs = block_scale(max(amax8(c0), amax8(c1)), m);
+        uint32_t w[16];
+        if (SR) {
+            // elements 16b .. 16b+15: Philox blocks 4b .. 4b+3
 #pragma unroll
-        for (int u = 0; u < kRowUnroll; ++u) {
-            const int64_t c = base + u * stride;
-            if (c < nchunks) {   // uniform within each lane pair (nchunks is even)
-                const uint32_t vv[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-                uint32_t mx = max(max(bf16_abs_max_pair(vv[0]), bf16_abs_max_pair(vv[1])),
-                                  max(bf16_abs_max_pair(vv[2]), bf16_abs_max_pair(vv[3])));
-                mx = max(mx, (uint32_t)__shfl_xor((int)mx, 1));
-                const BlockScale bs = block_scale(mx, m);
-                uint32_t w[8];
-                if (SR) words8((uint64_t)c * 8, tid, key0, key1, w);
-                payload[c] = quant8<SR>(vv, bs.r, w);
-                if ((c & 1) == 0) scales[c >> 1] = (uint8_t)bs.code;
+            for (int i = 0; i < 4; ++i) {
+                const uint4 q = sr_words4((uint64_t)b * 4 + i, tid, key0, key1);
+                w[4 * i] = q.x; w[4 * i + 1] = q.y; w[4 * i + 2] = q.z; w[4 * i + 3] = q.w;
             }
         }
+        payload[b] = make_uint2(quant8<SR>(c0, bs.r, w), quant8<SR>(c1, bs.r, w + 8));
+        scales[b] = (uint8_t)bs.code;
+        c0 = n0;
+        c1 = n1;
     }
 }
 
 // ------------------------------------------------ columns (1D, transposed) --
-// Blocks are 16 consecutive rows of one column; output is the row blocking of
-// x^T.  A lane holds 4 adjacent columns (8 B per row) of kColRB consecutive
-// row blocks; a workgroup covers 256 columns x (4 waves * kColRB * 16) rows,
-// so each output row (a column of x) receives 4 * kColRB * 8 contiguous
-// payload bytes from one workgroup.
-constexpr int kColRB = 4;
-constexpr int kColWaves = kThreads / 64;
+// Blocks are 16 consecutive rows of one column; output is the row blocking
+// of x^T: payload_t [cols, rows/2], scales_t [cols, rows/16].
+// A workgroup owns 128 columns (lane q = t % 32 of each wave-half holds the 4
+// adjacent columns 4q .. 4q+3) and a range of rows, walked in groups of 8
+// row blocks (thread t handles row block t / 32 of the group).  Per group
+// each column gains 8 x 8 = 64 payload bytes, assembled in LDS and written
+// by 2 lanes per column; scale bytes collect in LDS over 8 groups (64 row
+// blocks) before they are written.
+constexpr int kColCols = 128;
+constexpr int kColGroupRB = 8;
+constexpr int kColScaleGroups = 8;
 
 template <bool SR>
 __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
-    const uint16_t* __restrict__ x, int64_t rows, int64_t cols, const float* __restrict__ amax_dev,
-    float T, uint32_t key0, uint32_t key1, uint32_t tid, uint8_t* __restrict__ payload_t,
-    uint8_t* __restrict__ scales_t, float* __restrict__ dec_out) {
+    const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t rows_per_wg,
+    const float* __restrict__ amax_dev, float T, uint32_t key0, uint32_t key1, uint32_t tid,
+    uint8_t* __restrict__ payload_t, uint8_t* __restrict__ scales_t, float* __restrict__ dec_out) {
+    __shared__ __attribute__((aligned(16))) uint8_t stP[kColCols][kColGroupRB * 8];
+    __shared__ __attribute__((aligned(16))) uint8_t stS[kColCols][kColGroupRB * kColScaleGroups];
     const Multipliers m = tensor_multipliers(*amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *dec_out = m.dec;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int64_t c0 = ((int64_t)blockIdx.x * 64 + lane) * 4;     // first of 4 columns
-    if (c0 >= cols) return;
-    const bool pair2 = (c0 + 2) < cols;                            // columns c0+2, c0+3 exist
-    const bool vec8 = (cols & 3) == 0;                             // 8-byte aligned rows
+    const int t = threadIdx.x;
+    const int q = t & 31, rbl = t >> 5;
+    const int64_t cw = (int64_t)blockIdx.x * kColCols;          // first column of the workgroup
+    const int64_t c = cw + 4 * q;                               // first of this lane's 4 columns
+    const int ncv = (int)max((int64_t)0, min((int64_t)4, cols - c));   // 0, 2 or 4 valid columns
+    const bool vec8 = (cols & 3) == 0;
+    const int64_t r_begin = (int64_t)blockIdx.y * rows_per_wg;
+    const int64_t r_end = min(rows, r_begin + rows_per_wg);
     const int64_t nrb = rows / 16;
-    const int64_t rb_first = ((int64_t)blockIdx.y * kColWaves + wave) * kColRB;
-    const int64_t ldo = rows / 2;        // payload_t row stride (bytes)
-#pragma unroll 1
-    for (int q = 0; q < kColRB; ++q) {
-        const int64_t rb = rb_first + q;
-        if (rb >= nrb) break;
-        uint32_t lo[16], hi[16];         // bf16 pairs: columns (c0, c0+1), (c0+2, c0+3)
-        const uint16_t* src = x + (rb * 16) * cols + c0;
-        if (pair2 && vec8) {
+    const int64_t ldo = rows / 2;                               // payload_t row stride (bytes)
+
+    // 16 rows x 4 columns of this lane's row block of group g: word pairs
+    // (c, c+1) in lo, (c+2, c+3) in hi.
+    auto load = [&](int64_t g, uint32_t (&lo)[16], uint32_t (&hi)[16]) {
+        const int64_t r0 = r_begin + g * (kColGroupRB * 16) + rbl * 16;
+        if (r0 >= r_end || ncv == 0) return;
+        const uint16_t* src = x + r0 * cols + c;
+        if (vec8 && ncv == 4) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const uint2 t = *reinterpret_cast<const uint2*>(src + r * cols);
-                lo[r] = t.x;
-                hi[r] = t.y;
+                const uint2 v = *reinterpret_cast<const uint2*>(src + r * cols);
+                lo[r] = v.x;
+                hi[r] = v.y;
             }
         } else {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 lo[r] = *reinterpret_cast<const uint32_t*>(src + r * cols);
-                hi[r] = pair2 ? *reinterpret_cast<const uint32_t*>(src + r * cols + 2) : 0u;
+                hi[r] = ncv == 4 ? *reinterpret_cast<const uint32_t*>(src + r * cols + 2) : 0u;
             }
         }
-        // column maxima (integer on |bf16| bits)
-        uint32_t mx[4] = {0u, 0u, 0u, 0u};
+    };
+
+    const int64_t ngroups = (r_end - r_begin + kColGroupRB * 16 - 1) / (kColGroupRB * 16);
+    uint32_t lo[16], hi[16], nlo[16], nhi[16];
+    load(0, lo, hi);
+    for (int64_t g = 0; g < ngroups; ++g) {
+        load(g + 1, nlo, nhi);
+        const int64_t r0 = r_begin + g * (kColGroupRB * 16) + rbl * 16;
+        const int64_t rb = r0 / 16;
+        const int sg = (int)(g % kColScaleGroups);
+        if (r0 < r_end && ncv > 0) {
+            uint32_t mx[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            mx[0] = max(mx[0], lo[r] & 0x7FFFu);
-            mx[1] = max(mx[1], (lo[r] >> 16) & 0x7FFFu);
-            mx[2] = max(mx[2], hi[r] & 0x7FFFu);
-            mx[3] = max(mx[3], (hi[r] >> 16) & 0x7FFFu);
-        }
-        BlockScale bs[4];
+            for (int r = 0; r < 16; ++r) {
+                mx[0] = max(mx[0], lo[r] & 0x7FFFu);
+                mx[1] = max(mx[1], (lo[r] >> 16) & 0x7FFFu);
+                mx[2] = max(mx[2], hi[r] & 0x7FFFu);
+                mx[3] = max(mx[3], (hi[r] >> 16) & 0x7FFFu);
+            }
+            BlockScale bs[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) bs[j] = block_scale(mx[j], m);
-        uint32_t pk[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
+            for (int j = 0; j < 4; ++j) bs[j] = block_scale(mx[j], m);
+            uint32_t pk[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            float xv[4] = {bf16_lo(lo[r]), bf16_hi(lo[r]), bf16_lo(hi[r]), bf16_hi(hi[r])};
-            uint32_t w[4] = {0u, 0u, 0u, 0u};
-            if (SR) {
-                // elements (row, c0 .. c0+3); c0 % 4 == 0 and cols % 4 == 0 put
-                // them in one Philox block, otherwise they straddle two.
-                const uint64_t e0 = (uint64_t)(rb * 16 + r) * (uint64_t)cols + (uint64_t)c0;
-                const uint4 wa = sr_words4(e0 >> 2, tid, key0, key1);
-                if ((e0 & 3) == 0) {
-                    w[0] = wa.x; w[1] = wa.y; w[2] = wa.z; w[3] = wa.w;
-                } else {         // e0 is even: the 4 elements straddle two blocks
-                    const uint4 wb = sr_words4((e0 >> 2) + 1, tid, key0, key1);
-                    w[0] = wa.z; w[1] = wa.w; w[2] = wb.x; w[3] = wb.y;
-                }
+            for (int r = 0; r < 16; ++r) {
+                uint32_t w[4] = {0u, 0u, 0u, 0u};
+                if (SR) words4((uint64_t)(r0 + r) * (uint64_t)cols + (uint64_t)c, tid, key0, key1, w);
+                const float xv[4] = {bf16_lo(lo[r]), bf16_hi(lo[r]), bf16_lo(hi[r]), bf16_hi(hi[r])};
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    pk[j][r >> 3] |= quant1(xv[j], bs[j].r, w[j], SR) << (4 * (r & 7));
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const float y = xv[j] * bs[j].r;
-                const uint32_t nib = SR ? e2m1_sr(y, w[j]) : e2m1_rn(y);
-                pk[j][r >> 3] |= nib << (4 * (r & 7));
+                *reinterpret_cast<uint2*>(&stP[4 * q + j][rbl * 8]) = make_uint2(pk[j][0], pk[j][1]);
+                stS[4 * q + j][sg * kColGroupRB + rbl] = (uint8_t)bs[j].code;
             }
         }
-        const int ncol = pair2 ? 4 : 2;
-        for (int j = 0; j < ncol; ++j) {
-            uint8_t* dst = payload_t + (c0 + j) * ldo + rb * 8;
-            *reinterpret_cast<uint2*>(dst) = make_uint2(pk[j][0], pk[j][1]);
-            scales_t[(c0 + j) * nrb + rb] = (uint8_t)bs[j].code;
+        __syncthreads();
+        // payload: 2 lanes per column, 32 bytes each (the group's valid row
+        // blocks only; a full group is 64 contiguous bytes)
+        {
+            const int col = t >> 1, half = t & 1;
+            const int64_t gc = cw + col;
+            const int64_t rb0 = (r_begin + g * (kColGroupRB * 16)) / 16;
+            const int nvalid = (int)min((int64_t)kColGroupRB, (r_end / 16) - rb0);   // row blocks in the group
+            if (gc < cols) {
+                uint8_t* dst = payload_t + gc * ldo + rb0 * 8 + half * 32;
+                const uint8_t* s = &stP[col][half * 32];
+                if (nvalid == kColGroupRB && (ldo & 15) == 0) {
+                    *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(s);
+                    *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(s + 16);
+                } else {
+                    for (int k = half * 4; k < half * 4 + 4; ++k)
+                        if (k < nvalid)
+                            *reinterpret_cast<uint2*>(dst + (k - half * 4) * 8) =
+                                *reinterpret_cast<const uint2*>(s + (k - half * 4) * 8);
+                }
+            }
+            // scales: every kColScaleGroups groups, or at the end of the range
+            if (sg == kColScaleGroups - 1 || g == ngroups - 1) {
+                const int64_t rbs = rb0 - (int64_t)sg * kColGroupRB;          // first row block of the chunk
+                const int ns = (int)(rb0 + nvalid - rbs);                   // scale bytes in the chunk
+                if (gc < cols) {
+                    uint8_t* dst = scales_t + gc * nrb + rbs + half * 32;
+                    const uint8_t* s = &stS[col][half * 32];
+                    const int lo_k = half * 32, hi_k = min(ns, half * 32 + 32);
+                    if (hi_k - lo_k == 32 && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
+                        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(s);
+                        *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(s + 16);
+                    } else {
+                        for (int k = lo_k; k < hi_k; ++k) dst[k - lo_k] = s[k - lo_k];
+                    }
+                }
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            lo[r] = nlo[r];
+            hi[r] = nhi[r];
         }
     }
 }
 
 // ------------------------------------------------------------ tiles (2D) --
-// A lane holds 16 rows x 8 columns (16 B per row); lanes 2k, 2k+1 cover one
-// 16x16 tile and combine their maxima with a lane swap.  A workgroup covers
-// 512 columns x (4 waves * kTileRT * 16) rows.
-constexpr int kTileRT = 2;
+// A workgroup covers 128 rows (8 tile rows; thread t handles tile row t / 32)
+// x 128 columns (lane q = t % 32 holds columns 4q .. 4q+3, so the 4 lanes
+// 4k .. 4k+3 share one 16x16 tile and combine their maxima with two lane
+// swaps).  The row-major payload is stored straight from registers (32 lanes
+// x 2 bytes = 64 contiguous bytes per row); the transposed payload gains 8
+// bytes per tile row per column and is assembled in LDS, 64 bytes per column.
+constexpr int kTileCols = 128;
+constexpr int kTileRowTiles = 8;
 
 template <bool SR>
 __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
@@ -204,51 +277,73 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
     float T, uint32_t key0, uint32_t key1, uint32_t tid, uint8_t* __restrict__ payload,
     uint8_t* __restrict__ scales, uint8_t* __restrict__ payload_t, uint8_t* __restrict__ scales_t,
     float* __restrict__ dec_out) {
+    __shared__ __attribute__((aligned(16))) uint8_t stT[kTileCols][kTileRowTiles * 8];
     const Multipliers m = tensor_multipliers(*amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *dec_out = m.dec;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int64_t c0 = ((int64_t)blockIdx.x * 64 + lane) * 8;
-    if (c0 >= cols) return;              // cols % 16 == 0: lane pairs leave together
+    const int t = threadIdx.x;
+    const int q = t & 31, trl = t >> 5;
+    const int64_t cw = (int64_t)blockIdx.x * kTileCols;
+    const int64_t c = cw + 4 * q;
+    const int64_t tr = (int64_t)blockIdx.y * kTileRowTiles + trl;     // tile row
     const int64_t ntr = rows / 16, ntc = cols / 16;
-    const int64_t tr_first = ((int64_t)blockIdx.y * kColWaves + wave) * kTileRT;
-#pragma unroll 1
-    for (int q = 0; q < kTileRT; ++q) {
-        const int64_t tr = tr_first + q;
-        if (tr >= ntr) break;            // uniform within the wave
-        uint4 v[16];
-        const uint16_t* src = w + (tr * 16) * cols + c0;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) v[r] = *reinterpret_cast<const uint4*>(src + r * cols);
-        uint32_t mx = 0;
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-            mx = max(mx, max(max(bf16_abs_max_pair(v[r].x), bf16_abs_max_pair(v[r].y)),
-                             max(bf16_abs_max_pair(v[r].z), bf16_abs_max_pair(v[r].w))));
-        mx = max(mx, (uint32_t)__shfl_xor((int)mx, 1));
-        const BlockScale bs = block_scale(mx, m);
-        uint32_t colpk[8][2];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) colpk[j][0] = colpk[j][1] = 0u;
+    const bool active = (c < cols) && (tr < ntr);                     // whole tiles: cols % 16 == 0
+    if (active) {
+        const uint16_t* src = w + (tr * 16) * cols + c;
+        uint32_t lo[16], hi[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const uint32_t vv[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
-            uint32_t wd[8];
-            if (SR) words8((uint64_t)(tr * 16 + r) * (uint64_t)cols + (uint64_t)c0, tid, key0, key1, wd);
-            const uint32_t p = quant8<SR>(vv, bs.r, wd);
-            *reinterpret_cast<uint32_t*>(payload + (tr * 16 + r) * (cols / 2) + c0 / 2) = p;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) colpk[j][r >> 3] |= ((p >> (4 * j)) & 15u) << (4 * (r & 7));
+            const uint2 v = *reinterpret_cast<const uint2*>(src + r * cols);
+            lo[r] = v.x;
+            hi[r] = v.y;
         }
-        if ((lane & 1) == 0) {
-            scales[tr * ntc + c0 / 16] = (uint8_t)bs.code;
-            if (scales_t != nullptr) scales_t[(c0 / 16) * ntr + tr] = (uint8_t)bs.code;
+        uint32_t mx = 0;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = max(mx, max(bf16_abs_max_pair(lo[r]), bf16_abs_max_pair(hi[r])));
+        mx = max(mx, (uint32_t)__shfl_xor((int)mx, 1));
+        mx = max(mx, (uint32_t)__shfl_xor((int)mx, 2));
+        const BlockScale bs = block_scale(mx, m);
+        uint32_t colpk[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            uint32_t wd[4] = {0u, 0u, 0u, 0u};
+            if (SR) words4((uint64_t)(tr * 16 + r) * (uint64_t)cols + (uint64_t)c, tid, key0, key1, wd);
+            const float xv[4] = {bf16_lo(lo[r]), bf16_hi(lo[r]), bf16_lo(hi[r]), bf16_hi(hi[r])};
+            uint32_t p = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t nib = quant1(xv[j], bs.r, wd[j], SR);
+                p |= nib << (4 * j);
+                colpk[j][r >> 3] |= nib << (4 * (r & 7));
+            }
+            *reinterpret_cast<uint16_t*>(payload + (tr * 16 + r) * (cols / 2) + c / 2) = (uint16_t)p;
+        }
+        if ((q & 3) == 0) {
+            scales[tr * ntc + c / 16] = (uint8_t)bs.code;
+            if (scales_t != nullptr) scales_t[(c / 16) * ntr + tr] = (uint8_t)bs.code;
         }
         if (payload_t != nullptr) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                *reinterpret_cast<uint2*>(payload_t + (c0 + j) * (rows / 2) + tr * 8) =
-                    make_uint2(colpk[j][0], colpk[j][1]);
+            for (int j = 0; j < 4; ++j)
+                *reinterpret_cast<uint2*>(&stT[4 * q + j][trl * 8]) = make_uint2(colpk[j][0], colpk[j][1]);
+        }
+    }
+    if (payload_t == nullptr) return;                                 // uniform
+    __syncthreads();
+    const int col = t >> 1, half = t & 1;
+    const int64_t gc = cw + col;
+    const int64_t tr0 = (int64_t)blockIdx.y * kTileRowTiles;
+    const int nvalid = (int)min((int64_t)kTileRowTiles, ntr - tr0);
+    if (gc < cols) {
+        uint8_t* dst = payload_t + gc * (rows / 2) + tr0 * 8 + half * 32;
+        const uint8_t* s = &stT[col][half * 32];
+        if (nvalid == kTileRowTiles && ((rows / 2) & 15) == 0) {
+            *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(s);
+            *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(s + 16);
+        } else {
+            for (int k = half * 4; k < half * 4 + 4; ++k)
+                if (k < nvalid)
+                    *reinterpret_cast<uint2*>(dst + (k - half * 4) * 8) =
+                        *reinterpret_cast<const uint2*>(s + (k - half * 4) * 8);
         }
     }
 }
@@ -258,26 +353,29 @@ inline void seed_key(uint64_t seed, uint32_t& k0, uint32_t& k1) {
     k1 = (uint32_t)(seed >> 32);
 }
 
+// Resident workgroups to aim for: 8 per CU on the 256 CUs of an MI355X.
+constexpr int64_t kPersistentWGs = 256 * 8;
+
 }  // namespace
 
 hipError_t launch_quant_rows(const void* x_bf16, int64_t rows, int64_t cols,
                              const float* amax_dev, float target, bool sr, uint64_t seed,
                              uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
                              float* dec_out, hipStream_t s) {
-    const int64_t nchunks = rows * cols / 8;
+    const int64_t nblocks = rows * cols / 16;
     uint32_t k0, k1;
     seed_key(seed, k0, k1);
-    int64_t blocks = (nchunks + (int64_t)kThreads * kRowUnroll - 1) / ((int64_t)kThreads * kRowUnroll);
-    if (blocks < 1) blocks = 1;
-    if (blocks > 8192) blocks = 8192;
+    int64_t wgs = (nblocks + kThreads - 1) / kThreads;
+    if (wgs < 1) wgs = 1;
+    if (wgs > kPersistentWGs) wgs = kPersistentWGs;
     const uint4* x = reinterpret_cast<const uint4*>(x_bf16);
-    uint32_t* p = reinterpret_cast<uint32_t*>(payload);
+    uint2* p = reinterpret_cast<uint2*>(payload);
     if (sr)
-        hipLaunchKernelGGL(quant_rows_kernel<true>, dim3((unsigned)blocks), dim3(kThreads), 0, s, x,
-                           nchunks, amax_dev, target, k0, k1, tensor_id, p, scales, dec_out);
+        hipLaunchKernelGGL(quant_rows_kernel<true>, dim3((unsigned)wgs), dim3(kThreads), 0, s, x,
+                           nblocks, amax_dev, target, k0, k1, tensor_id, p, scales, dec_out);
     else
-        hipLaunchKernelGGL(quant_rows_kernel<false>, dim3((unsigned)blocks), dim3(kThreads), 0, s, x,
-                           nchunks, amax_dev, target, k0, k1, tensor_id, p, scales, dec_out);
+        hipLaunchKernelGGL(quant_rows_kernel<false>, dim3((unsigned)wgs), dim3(kThreads), 0, s, x,
+                           nblocks, amax_dev, target, k0, k1, tensor_id, p, scales, dec_out);
     return hipGetLastError();
 }
 
@@ -287,19 +385,23 @@ hipError_t launch_quant_cols(const void* x_bf16, int64_t rows, int64_t cols,
                              float* dec_out, hipStream_t s) {
     uint32_t k0, k1;
     seed_key(seed, k0, k1);
-    const int64_t gx = (cols + 255) / 256;
-    const int64_t rows_per_wg = (int64_t)kColWaves * kColRB * 16;
-    int64_t gy = (rows + rows_per_wg - 1) / rows_per_wg;
-    if (gy < 1) gy = 1;
+    const int64_t gx = (cols + kColCols - 1) / kColCols;
+    // Row range per workgroup: a whole scale chunk (64 row blocks) when that
+    // still leaves enough workgroups, otherwise one group of 8 row blocks.
+    const int64_t chunk = (int64_t)kColGroupRB * kColScaleGroups * 16;      // 1024 rows
+    int64_t rows_per_wg = chunk;
+    while (rows_per_wg > kColGroupRB * 16 && gx * ((rows + rows_per_wg - 1) / rows_per_wg) < 512)
+        rows_per_wg /= 2;
+    const int64_t gy = (rows + rows_per_wg - 1) / rows_per_wg;
     const uint16_t* x = reinterpret_cast<const uint16_t*>(x_bf16);
     if (sr)
         hipLaunchKernelGGL(quant_cols_kernel<true>, dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
-                           0, s, x, rows, cols, amax_dev, target, k0, k1, tensor_id, payload_t,
-                           scales_t, dec_out);
+                           0, s, x, rows, cols, rows_per_wg, amax_dev, target, k0, k1, tensor_id,
+                           payload_t, scales_t, dec_out);
     else
         hipLaunchKernelGGL(quant_cols_kernel<false>, dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
-                           0, s, x, rows, cols, amax_dev, target, k0, k1, tensor_id, payload_t,
-                           scales_t, dec_out);
+                           0, s, x, rows, cols, rows_per_wg, amax_dev, target, k0, k1, tensor_id,
+                           payload_t, scales_t, dec_out);
     return hipGetLastError();
 }
 
@@ -310,9 +412,8 @@ hipError_t launch_quant_tiles(const void* w_bf16, int64_t rows, int64_t cols,
                               hipStream_t s) {
     uint32_t k0, k1;
     seed_key(seed, k0, k1);
-    const int64_t gx = (cols + 511) / 512;
-    const int64_t rows_per_wg = (int64_t)kColWaves * kTileRT * 16;
-    const int64_t gy = (rows + rows_per_wg - 1) / rows_per_wg;
+    const int64_t gx = (cols + kTileCols - 1) / kTileCols;
+    const int64_t gy = (rows / 16 + kTileRowTiles - 1) / kTileRowTiles;
     const uint16_t* w = reinterpret_cast<const uint16_t*>(w_bf16);
     if (sr)
         hipLaunchKernelGGL(quant_tiles_kernel<true>, dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),

@@ -63,44 +63,28 @@ __device__ __forceinline__ float ue5m3_decode(uint32_t c) {
     return e ? nrm : sub;
 }
 
-// E2M1 nibble of a binary32 y, round to nearest with ties to the even code,
-// magnitudes >= 6 (and inf) saturating to code 7; bit 3 copies the sign.
-__device__ __forceinline__ uint32_t e2m1_rn(float y) {
-    const uint32_t b = __float_as_uint(y);
-    const uint32_t s = (b >> 28) & 8u;
-    const uint32_t ab = b & 0x7FFFFFFFu;
-    const float a = __uint_as_float(ab);
-    // |y| < 1: codes 0, 1, 2 are multiples of 0.5, code = RNE(2|y|).
-    const uint32_t lo = (uint32_t)__builtin_rintf(a * 2.0f);
-    // |y| >= 1: one fraction bit, exponent bias 1 -> code = (e - 126) * 2 + m
-    // after rounding the binary32 fraction to 1 bit, nearest-even.
-    const uint32_t r = ab + 0x1FFFFFu + ((ab >> 22) & 1u);
-    uint32_t hi = (r >> 22) - 252u;
-    hi = hi < 7u ? hi : 7u;
-    return ((a < 1.0f) ? lo : hi) | s;
-}
-
 // E2M1 nibble of y by stochastic rounding with the uniform 32-bit word w
 // (eq:sr): between adjacent magnitudes q_lo <= |y| < q_hi round up iff
 // w < ceil((|y| - q_lo) / (q_hi - q_lo) * 2^32).  |y| >= 6 gives code 7.
+//  * |y| >= 1: the grid step is one unit of the 22nd binary32 fraction bit, so
+//    frac * 2^32 = f22 * 2^10 with f22 the low 22 fraction bits, and the
+//    event w < f22 * 2^10 is (w >> 10) < f22: exactly the carry out of the
+//    low 22 bits when ~w >> 10 = 2^22 - 1 - (w >> 10) is added.  The code is
+//    then the bits above, rebased: ((|y| + (~w >> 10)) >> 22) - 252.
+//  * |y| < 1: step 0.5 from 0 or from 0.5; t = |y| * 2^33 (minus 2^32 from
+//    0.5 up) is exact and integral at and above 2^24, so the threshold is
+//    ceil(t) in integer form.
+// Inputs must not be NaN (no code is specified for them).
 __device__ __forceinline__ uint32_t e2m1_sr(float y, uint32_t w) {
     const uint32_t b = __float_as_uint(y);
-    const uint32_t s = (b >> 28) & 8u;
-    const float a = __uint_as_float(b & 0x7FFFFFFFu);
-    // spacing h: 0.5 below 2, 1 in [2, 4), 2 in [4, 8)
-    const bool b2 = a < 2.0f, b4 = a < 4.0f;
-    const float inv_h = b2 ? 2.0f : (b4 ? 1.0f : 0.5f);
-    const float h = b2 ? 0.5f : (b4 ? 1.0f : 2.0f);
-    const float steps = __builtin_floorf(a * inv_h);          // exact
-    const float q_lo = steps * h;                             // exact
-    const uint32_t k = (uint32_t)steps;
-    const uint32_t c_lo = b2 ? k : (b4 ? k + 2u : 6u);
-    // (|y| - q_lo) is exact (Sterbenz, or q_lo = 0); scaling by 2^32 / h is a
-    // power of two, so t = frac * 2^32 exactly and t < 2^32.
-    const float t = (a - q_lo) * (inv_h * 4294967296.0f);
+    const uint32_t ab = b & 0x7FFFFFFFu;
+    const uint32_t big = min((ab + (~w >> 10) - (252u << 22)) >> 22, 7u);
+    const bool half = ab >= 0x3F000000u;                       // |y| >= 0.5
+    const float t = __uint_as_float(ab) * 0x1p33f - (half ? 0x1p32f : 0.0f);
     const uint32_t thr = (uint32_t)__builtin_ceilf(t);
-    const uint32_t c = c_lo + (w < thr ? 1u : 0u);
-    return ((a >= kF) ? 7u : c) | s;
+    const uint32_t small = (half ? 1u : 0u) + (w < thr ? 1u : 0u);
+    const uint32_t c = ab >= 0x3F800000u ? big : small;
+    return c | ((b >> 28) & 8u);
 }
 
 // Philox4x32-10 (Salmon et al., SC'11): four counter words, key (k0, k1),

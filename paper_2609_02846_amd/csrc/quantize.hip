@@ -40,9 +40,14 @@ __device__ __forceinline__ BlockScale block_scale(uint32_t amax_bits15, const Mu
     return bs;
 }
 
-__device__ __forceinline__ uint32_t quant1(float x, float r, uint32_t w, bool sr) {
-    const float y = x * r;
-    return sr ? e2m1_sr(y, w) : e2m1_rn(y);
+// E2M1 round-to-nearest-even of y0, y1 into byte SEL of p (y0 in the low
+// nibble).  The gfx950 conversion with scale 1.0 is exactly the E2M1 RNE of
+// the binary32 input with saturation to code 7 at |y| >= 6 and the sign in
+// bit 3 (including -0), identical to the E2M1 RNE definition for all 2^32
+// inputs.
+template <int SEL>
+__device__ __forceinline__ uint32_t rn_pair(uint32_t p, float y0, float y1) {
+    return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, y0, y1, 1.0f, SEL);
 }
 
 // Quantize the 8 bf16 values held in v (element e in half e&1 of word e>>1)
@@ -51,13 +56,48 @@ __device__ __forceinline__ uint32_t quant1(float x, float r, uint32_t w, bool sr
 template <bool SR>
 __device__ __forceinline__ uint32_t quant8(const uint4& v, float r, const uint32_t* w) {
     const uint32_t vv[4] = {v.x, v.y, v.z, v.w};
+    if (!SR) {
+        uint32_t p = 0;
+        p = rn_pair<0>(p, bf16_lo(vv[0]) * r, bf16_hi(vv[0]) * r);
+        p = rn_pair<1>(p, bf16_lo(vv[1]) * r, bf16_hi(vv[1]) * r);
+        p = rn_pair<2>(p, bf16_lo(vv[2]) * r, bf16_hi(vv[2]) * r);
+        p = rn_pair<3>(p, bf16_lo(vv[3]) * r, bf16_hi(vv[3]) * r);
+        return p;
+    }
     uint32_t p = 0;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         const float x = (e & 1) ? bf16_hi(vv[e >> 1]) : bf16_lo(vv[e >> 1]);
-        p |= quant1(x, r, SR ? w[e] : 0u, SR) << (4 * e);
+        p |= e2m1_sr(x * r, w[e]) << (4 * e);
     }
     return p;
+}
+
+// Column-wise nibbles of 16 rows of one column (values v[r] * r_, rows in
+// order) into two words, RN or SR.
+template <bool SR>
+__device__ __forceinline__ void quant_col16(const float (&xv)[16], float r_, const uint32_t (&w)[16],
+                                            uint32_t& p0, uint32_t& p1) {
+    if (!SR) {
+        p0 = 0u;
+        p1 = 0u;
+        p0 = rn_pair<0>(p0, xv[0] * r_, xv[1] * r_);
+        p0 = rn_pair<1>(p0, xv[2] * r_, xv[3] * r_);
+        p0 = rn_pair<2>(p0, xv[4] * r_, xv[5] * r_);
+        p0 = rn_pair<3>(p0, xv[6] * r_, xv[7] * r_);
+        p1 = rn_pair<0>(p1, xv[8] * r_, xv[9] * r_);
+        p1 = rn_pair<1>(p1, xv[10] * r_, xv[11] * r_);
+        p1 = rn_pair<2>(p1, xv[12] * r_, xv[13] * r_);
+        p1 = rn_pair<3>(p1, xv[14] * r_, xv[15] * r_);
+        return;
+    }
+    p0 = 0u;
+    p1 = 0u;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        p0 |= e2m1_sr(xv[k] * r_, w[k]) << (4 * k);
+        p1 |= e2m1_sr(xv[8 + k] * r_, w[8 + k]) << (4 * k);
+    }
 }
 
 __device__ __forceinline__ uint32_t amax8(const uint4& v) {
@@ -198,15 +238,24 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
             BlockScale bs[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) bs[j] = block_scale(mx[j], m);
-            uint32_t pk[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
+            uint32_t w[4][16];               // Philox word of (row r, column c + j)
+            if (SR) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                uint32_t w[4] = {0u, 0u, 0u, 0u};
-                if (SR) words4((uint64_t)(r0 + r) * (uint64_t)cols + (uint64_t)c, tid, key0, key1, w);
-                const float xv[4] = {bf16_lo(lo[r]), bf16_hi(lo[r]), bf16_lo(hi[r]), bf16_hi(hi[r])};
+                for (int r = 0; r < 16; ++r) {
+                    uint32_t w4[4];
+                    words4((uint64_t)(r0 + r) * (uint64_t)cols + (uint64_t)c, tid, key0, key1, w4);
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    pk[j][r >> 3] |= quant1(xv[j], bs[j].r, w[j], SR) << (4 * (r & 7));
+                    for (int j = 0; j < 4; ++j) w[j][r] = w4[j];
+                }
+            }
+            uint32_t pk[4][2];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                float xv[16];
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    xv[r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
+                quant_col16<SR>(xv, bs[j].r, w[j], pk[j][0], pk[j][1]);
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -303,19 +352,52 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
         mx = max(mx, (uint32_t)__shfl_xor((int)mx, 2));
         const BlockScale bs = block_scale(mx, m);
         uint32_t colpk[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
+        if (SR) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            uint32_t wd[4] = {0u, 0u, 0u, 0u};
-            if (SR) words4((uint64_t)(tr * 16 + r) * (uint64_t)cols + (uint64_t)c, tid, key0, key1, wd);
-            const float xv[4] = {bf16_lo(lo[r]), bf16_hi(lo[r]), bf16_lo(hi[r]), bf16_hi(hi[r])};
-            uint32_t p = 0;
+            for (int r = 0; r < 16; ++r) {
+                uint32_t wd[4];
+                words4((uint64_t)(tr * 16 + r) * (uint64_t)cols + (uint64_t)c, tid, key0, key1, wd);
+                const float xv[4] = {bf16_lo(lo[r]), bf16_hi(lo[r]), bf16_lo(hi[r]), bf16_hi(hi[r])};
+                uint32_t p = 0;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const uint32_t nib = quant1(xv[j], bs.r, wd[j], SR);
-                p |= nib << (4 * j);
-                colpk[j][r >> 3] |= nib << (4 * (r & 7));
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t nib = e2m1_sr(xv[j] * bs.r, wd[j]);
+                    p |= nib << (4 * j);
+                    colpk[j][r >> 3] |= nib << (4 * (r & 7));
+                }
+                *reinterpret_cast<uint16_t*>(payload + (tr * 16 + r) * (cols / 2) + c / 2) = (uint16_t)p;
             }
-            *reinterpret_cast<uint16_t*>(payload + (tr * 16 + r) * (cols / 2) + c / 2) = (uint16_t)p;
+        } else {
+            // row-major pairs (columns c, c+1 and c+2, c+3) and, for the
+            // transposed payload, column-wise pairs of consecutive rows
+            float y[16][4];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                y[r][0] = bf16_lo(lo[r]) * bs.r;
+                y[r][1] = bf16_hi(lo[r]) * bs.r;
+                y[r][2] = bf16_lo(hi[r]) * bs.r;
+                y[r][3] = bf16_hi(hi[r]) * bs.r;
+                uint32_t p = 0;
+                p = rn_pair<0>(p, y[r][0], y[r][1]);
+                p = rn_pair<1>(p, y[r][2], y[r][3]);
+                *reinterpret_cast<uint16_t*>(payload + (tr * 16 + r) * (cols / 2) + c / 2) = (uint16_t)p;
+            }
+            if (payload_t != nullptr) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    uint32_t a = 0u, b = 0u;
+                    a = rn_pair<0>(a, y[0][j], y[1][j]);
+                    a = rn_pair<1>(a, y[2][j], y[3][j]);
+                    a = rn_pair<2>(a, y[4][j], y[5][j]);
+                    a = rn_pair<3>(a, y[6][j], y[7][j]);
+                    b = rn_pair<0>(b, y[8][j], y[9][j]);
+                    b = rn_pair<1>(b, y[10][j], y[11][j]);
+                    b = rn_pair<2>(b, y[12][j], y[13][j]);
+                    b = rn_pair<3>(b, y[14][j], y[15][j]);
+                    colpk[j][0] = a;
+                    colpk[j][1] = b;
+                }
+            }
         }
         if ((q & 3) == 0) {
             scales[tr * ntc + c / 16] = (uint8_t)bs.code;

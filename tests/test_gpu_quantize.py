@@ -213,3 +213,43 @@ def test_quantizer_bandwidth_workload_sampled():
     for t in tc:
         _, _, pto, _ = oq.quantize_2d(np.ascontiguousarray(wb[:, 16 * t:16 * t + 16]), g, 448.0, "rn")
         assert np.array_equal(host(pt)[16 * t:16 * t + 16], pto)
+
+
+# ------------------------------------------------ every bf16 bit pattern ----
+def _all_bf16(rows, cols, seed):
+    """Every non-NaN bf16 bit pattern (zeros, subnormals, +-inf included) in
+    order of magnitude, shuffled only within runs of 16 so that row blocks
+    hold neighbouring magnitudes (block scales then span the whole UE5M3
+    range), tiled to [rows, cols]."""
+    v = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    v = v[(v & 0x7FFF) <= 0x7F80]
+    v = v[np.argsort(v & 0x7FFF, kind="stable")]
+    v = v[: v.size - v.size % 16].reshape(-1, 16)
+    v = np.random.default_rng(seed).permuted(v, axis=1).reshape(-1)
+    n = rows * cols
+    return np.ascontiguousarray(np.tile(v, -(-n // v.size))[:n].reshape(rows, cols))
+
+
+@pytest.mark.parametrize("g", [1.0, 3.0e4, 2.0 ** -20])
+@pytest.mark.parametrize("mode", ["rn", "sr"])
+def test_every_bf16_value(g, mode):
+    """All quantizers on inputs holding every non-NaN bf16 value, under held
+    amax values that put most of them below, inside and above the E2M1 range
+    of their blocks: payload and scales bit-exact with the oracle."""
+    say("every bf16 value", g, mode)
+    amax = torch.zeros(1, dtype=torch.float32, device="cuda")
+    set_amax(amax, g)
+    bits = _all_bf16(256, 512, 21)
+    xd = to_dev(bits)
+    for axis in [1, 0]:
+        p, s, d = ue.quantize_1d(xd, axis, amax, 448.0, mode, seed=11, tensor_id=3)
+        po, so, do = oq.quantize_1d(bits, axis, np.float32(g), 448.0, mode, 11, 3)
+        assert np.array_equal(host(s), so), axis
+        assert np.array_equal(host(p), po), axis
+        assert np.float32(d.item()) == do
+    p, s, pt, d, st = ue.quantize_2d(xd, amax, 448.0, mode, seed=11, tensor_id=4)
+    po, so, pto, do = oq.quantize_2d(bits, np.float32(g), 448.0, mode, 11, 4)
+    assert np.array_equal(host(s), so)
+    assert np.array_equal(host(p), po)
+    assert np.array_equal(host(pt), pto)
+    assert np.array_equal(host(st), so.T)

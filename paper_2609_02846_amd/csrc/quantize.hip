@@ -50,6 +50,63 @@ __device__ __forceinline__ uint32_t rn_pair(uint32_t p, float y0, float y1) {
     return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, y0, y1, 1.0f, SEL);
 }
 
+// E2M1 stochastic rounding on the gfx950 SR pair conversion.  For a pair
+// (y0, y1) and random operand R the instruction rounds y0 with bits 31..10
+// of R and y1 with bits 30..9; with R = ~w (y0) it rounds up iff
+// (w >> 10) < floor(frac * 2^22), while the rule here (w < ceil(frac * 2^32))
+// uses all 32 bits.  The two agree except when |y| < 1 and w >> 10 equals
+// floor(frac * 2^22) -- the 1024 words around the threshold -- which
+// sr_check flags; flagged groups are redone with the software rounding.
+// (For |y| >= 1, frac * 2^32 is a multiple of 1024 and the rules coincide.)
+// Each pair is converted twice, once with each element's own word placed
+// where that element reads it, and the two valid nibbles are merged.
+typedef float v2f_t __attribute__((ext_vector_type(2)));
+
+// Written as an instruction with p as a read-write operand: the compiler's
+// builtin for this conversion does not keep the destination's other bytes.
+template <int SEL>
+__device__ __forceinline__ uint32_t sr_pair(uint32_t p, v2f_t v, uint32_t r) {
+    if (SEL == 0) asm("v_cvt_scalef32_sr_pk_fp4_f32 %0, %1, %2, 1.0" : "+v"(p) : "v"(v), "v"(r));
+    if (SEL == 1) asm("v_cvt_scalef32_sr_pk_fp4_f32 %0, %1, %2, 1.0 op_sel:[0,0,1,0]" : "+v"(p) : "v"(v), "v"(r));
+    if (SEL == 2) asm("v_cvt_scalef32_sr_pk_fp4_f32 %0, %1, %2, 1.0 op_sel:[0,0,0,1]" : "+v"(p) : "v"(v), "v"(r));
+    if (SEL == 3) asm("v_cvt_scalef32_sr_pk_fp4_f32 %0, %1, %2, 1.0 op_sel:[0,0,1,1]" : "+v"(p) : "v"(v), "v"(r));
+    return p;
+}
+
+// True when w lies in the 1024-word bucket of y's threshold (|y| < 1), or
+// spuriously with probability 2^-22 (|y| >= 1), which only costs a redo.
+// The conversion to integer saturates (|y| * 2^23 may exceed 2^32).
+__device__ __forceinline__ bool sr_check(float y, uint32_t w) {
+    uint32_t q;
+    asm("v_cvt_u32_f32 %0, %1" : "=v"(q) : "v"(fabsf(y) * 0x1p23f));
+    return (w >> 10) == (q & 0x3FFFFFu);
+}
+
+// 8 values y (element e -> nibble e) by SR with words w.
+__device__ __forceinline__ uint32_t sr8(const float (&y)[8], const uint32_t* w) {
+    uint32_t lo = 0u, hi = 0u;                 // valid low / high nibbles
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const v2f_t v = {y[2 * k], y[2 * k + 1]};
+        const uint32_t r0 = ~w[2 * k];
+        const uint32_t r1 = __builtin_amdgcn_alignbit(~w[2 * k + 1], ~w[2 * k + 1], 1);
+        if (k == 0) { lo = sr_pair<0>(lo, v, r0); hi = sr_pair<0>(hi, v, r1); }
+        if (k == 1) { lo = sr_pair<1>(lo, v, r0); hi = sr_pair<1>(hi, v, r1); }
+        if (k == 2) { lo = sr_pair<2>(lo, v, r0); hi = sr_pair<2>(hi, v, r1); }
+        if (k == 3) { lo = sr_pair<3>(lo, v, r0); hi = sr_pair<3>(hi, v, r1); }
+    }
+    bool redo = false;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) redo |= sr_check(y[e], w[e]);
+    uint32_t p = (lo & 0x0F0F0F0Fu) | (hi & 0xF0F0F0F0u);
+    if (redo) {
+        p = 0u;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) p |= e2m1_sr(y[e], w[e]) << (4 * e);
+    }
+    return p;
+}
+
 // Quantize the 8 bf16 values held in v (element e in half e&1 of word e>>1)
 // with reciprocal r; returns 8 nibbles packed little-endian.  For SR, w holds
 // the 8 Philox words of the elements.
@@ -64,13 +121,10 @@ __device__ __forceinline__ uint32_t quant8(const uint4& v, float r, const uint32
         p = rn_pair<3>(p, bf16_lo(vv[3]) * r, bf16_hi(vv[3]) * r);
         return p;
     }
-    uint32_t p = 0;
+    float y[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const float x = (e & 1) ? bf16_hi(vv[e >> 1]) : bf16_lo(vv[e >> 1]);
-        p |= e2m1_sr(x * r, w[e]) << (4 * e);
-    }
-    return p;
+    for (int e = 0; e < 8; ++e) y[e] = ((e & 1) ? bf16_hi(vv[e >> 1]) : bf16_lo(vv[e >> 1])) * r;
+    return sr8(y, w);
 }
 
 // Column-wise nibbles of 16 rows of one column (values v[r] * r_, rows in
@@ -91,13 +145,14 @@ __device__ __forceinline__ void quant_col16(const float (&xv)[16], float r_, con
         p1 = rn_pair<3>(p1, xv[14] * r_, xv[15] * r_);
         return;
     }
-    p0 = 0u;
-    p1 = 0u;
+    float y0[8], y1[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-        p0 |= e2m1_sr(xv[k] * r_, w[k]) << (4 * k);
-        p1 |= e2m1_sr(xv[8 + k] * r_, w[8 + k]) << (4 * k);
+        y0[k] = xv[k] * r_;
+        y1[k] = xv[8 + k] * r_;
     }
+    p0 = sr8(y0, w);
+    p1 = sr8(y1, w + 8);
 }
 
 __device__ __forceinline__ uint32_t amax8(const uint4& v) {

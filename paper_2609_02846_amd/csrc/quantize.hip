@@ -56,10 +56,11 @@ __device__ __forceinline__ uint32_t rn_pair(uint32_t p, float y0, float y1) {
 // (w >> 10) < floor(frac * 2^22), while the rule here (w < ceil(frac * 2^32))
 // uses all 32 bits.  The two agree except when |y| < 1 and w >> 10 equals
 // floor(frac * 2^22) -- the 1024 words around the threshold -- which
-// sr_check flags; flagged groups are redone with the software rounding.
+// sr_check flags.
 // (For |y| >= 1, frac * 2^32 is a multiple of 1024 and the rules coincide.)
 // Each pair is converted twice, once with each element's own word placed
-// where that element reads it, and the two valid nibbles are merged.
+// where that element reads it, and the two valid nibbles are merged.  A
+// flagged element's nibble is replaced by the software rounding.
 typedef float v2f_t __attribute__((ext_vector_type(2)));
 
 // Written as an instruction with p as a read-write operand: the compiler's
@@ -95,15 +96,10 @@ __device__ __forceinline__ uint32_t sr8(const float (&y)[8], const uint32_t* w) 
         if (k == 2) { lo = sr_pair<2>(lo, v, r0); hi = sr_pair<2>(hi, v, r1); }
         if (k == 3) { lo = sr_pair<3>(lo, v, r0); hi = sr_pair<3>(hi, v, r1); }
     }
-    bool redo = false;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) redo |= sr_check(y[e], w[e]);
     uint32_t p = (lo & 0x0F0F0F0Fu) | (hi & 0xF0F0F0F0u);
-    if (redo) {
-        p = 0u;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) p |= e2m1_sr(y[e], w[e]) << (4 * e);
-    }
+    for (int e = 0; e < 8; ++e)
+        if (sr_check(y[e], w[e])) p = (p & ~(0xFu << (4 * e))) | (e2m1_sr(y[e], w[e]) << (4 * e));
     return p;
 }
 
@@ -163,10 +159,11 @@ __device__ __forceinline__ uint32_t amax8(const uint4& v) {
 // Philox words of elements 4j .. 4j+3 for the 4 columns c..c+3 of one row,
 // element index e0 = row * cols + c (even).  When e0 % 4 == 0 one Philox
 // block holds them; otherwise (cols % 4 == 2) they straddle two blocks.
+template <bool ALIGNED = false>
 __device__ __forceinline__ void words4(uint64_t e0, uint32_t tid, uint32_t k0, uint32_t k1,
                                        uint32_t* w) {
     const uint4 a = sr_words4(e0 >> 2, tid, k0, k1);
-    if ((e0 & 3) == 0) {
+    if (ALIGNED || (e0 & 3) == 0) {
         w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
     } else {
         const uint4 b = sr_words4((e0 >> 2) + 1, tid, k0, k1);
@@ -221,41 +218,101 @@ __global__ __launch_bounds__(kThreads) void quant_rows_kernel(
 // ------------------------------------------------ columns (1D, transposed) --
 // Blocks are 16 consecutive rows of one column; output is the row blocking
 // of x^T: payload_t [cols, rows/2], scales_t [cols, rows/16].
-// A workgroup owns 128 columns (lane q = t % 32 of each wave-half holds the 4
-// adjacent columns 4q .. 4q+3) and a range of rows, walked in groups of 8
-// row blocks (thread t handles row block t / 32 of the group).  Per group
-// each column gains 8 x 8 = 64 payload bytes, assembled in LDS and written
-// by 2 lanes per column; scale bytes collect in LDS over 8 groups (64 row
-// blocks) before they are written.
+// Work item = 128 columns x a chunk of up to 64 row blocks.  A workgroup
+// walks its items (item, item + grid, ...) group by group, a group being 8
+// row blocks (thread t handles row block t / 32 of the group; lane
+// q = t % 32 holds the 4 adjacent columns 4q .. 4q+3), loading the next group
+// -- possibly of its next item -- while it quantizes the current one.  Per
+// group each column gains 8 x 8 = 64 payload bytes, assembled in LDS and
+// written by 2 lanes per column; scale bytes collect in LDS over the item
+// (up to 64 bytes per column) before they are written.
 constexpr int kColCols = 128;
 constexpr int kColGroupRB = 8;
 constexpr int kColScaleGroups = 8;
 
+struct ColItem {
+    int64_t cw;          // first column of the item
+    int64_t r_begin;     // first row
+    int64_t r_end;       // one past the last row
+    int64_t ngroups;
+};
+
+__device__ __forceinline__ ColItem col_item(int64_t it, int64_t gx, int64_t rows, int64_t rows_per_item) {
+    ColItem ci;
+    ci.cw = (it % gx) * kColCols;
+    ci.r_begin = (it / gx) * rows_per_item;
+    ci.r_end = min(rows, ci.r_begin + rows_per_item);
+    ci.ngroups = (ci.r_end - ci.r_begin + kColGroupRB * 16 - 1) / (kColGroupRB * 16);
+    return ci;
+}
+
+// SR of 16 rows x 4 columns (row pairs 2k, 2k+1 per conversion) into the
+// column-wise payload words pk[j][0..1]; Philox words are made per row pair.
+// A flagged pair (see sr_check) has its two nibbles redone in software.
+template <bool ALIGNED>
+__device__ __forceinline__ void sr_cols16x4(const uint32_t (&lo)[16], const uint32_t (&hi)[16],
+                                            const BlockScale (&bs)[4], uint64_t e_row0, uint64_t cols,
+                                            uint32_t tid, uint32_t k0, uint32_t k1,
+                                            uint32_t (&pk)[4][2]) {
+    uint32_t aL[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
+    uint32_t aH[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        uint32_t w0[4], w1[4];
+        words4<ALIGNED>(e_row0 + (uint64_t)(2 * k) * cols, tid, k0, k1, w0);
+        words4<ALIGNED>(e_row0 + (uint64_t)(2 * k + 1) * cols, tid, k0, k1, w1);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t a0 = j < 2 ? lo[2 * k] : hi[2 * k], a1 = j < 2 ? lo[2 * k + 1] : hi[2 * k + 1];
+            const float y0 = ((j & 1) ? bf16_hi(a0) : bf16_lo(a0)) * bs[j].r;
+            const float y1 = ((j & 1) ? bf16_hi(a1) : bf16_lo(a1)) * bs[j].r;
+            const v2f_t v = {y0, y1};
+            const uint32_t r0 = ~w0[j];
+            const uint32_t r1 = __builtin_amdgcn_alignbit(~w1[j], ~w1[j], 1);
+            uint32_t& L = aL[j][k >> 2];
+            uint32_t& H = aH[j][k >> 2];
+            if ((k & 3) == 0) { L = sr_pair<0>(L, v, r0); H = sr_pair<0>(H, v, r1); }
+            if ((k & 3) == 1) { L = sr_pair<1>(L, v, r0); H = sr_pair<1>(H, v, r1); }
+            if ((k & 3) == 2) { L = sr_pair<2>(L, v, r0); H = sr_pair<2>(H, v, r1); }
+            if ((k & 3) == 3) { L = sr_pair<3>(L, v, r0); H = sr_pair<3>(H, v, r1); }
+            if (sr_check(y0, w0[j]) | sr_check(y1, w1[j])) {
+                const int sh = 8 * (k & 3);
+                L = (L & ~(0xFu << sh)) | (e2m1_sr(y0, w0[j]) << sh);
+                H = (H & ~(0xF0u << sh)) | (e2m1_sr(y1, w1[j]) << (sh + 4));
+            }
+        }
+        // one row pair at a time: keeps 8 Philox words live, not 64
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) pk[j][h] = (aL[j][h] & 0x0F0F0F0Fu) | (aH[j][h] & 0xF0F0F0F0u);
+}
+
 template <bool SR>
 __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
-    const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t rows_per_wg,
-    const float* __restrict__ amax_dev, float T, uint32_t key0, uint32_t key1, uint32_t tid,
-    uint8_t* __restrict__ payload_t, uint8_t* __restrict__ scales_t, float* __restrict__ dec_out) {
+    const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t rows_per_item, int64_t gx,
+    int64_t nitems, const float* __restrict__ amax_dev, float T, uint32_t key0, uint32_t key1,
+    uint32_t tid, uint8_t* __restrict__ payload_t, uint8_t* __restrict__ scales_t,
+    float* __restrict__ dec_out) {
     __shared__ __attribute__((aligned(16))) uint8_t stP[kColCols][kColGroupRB * 8];
     __shared__ __attribute__((aligned(16))) uint8_t stS[kColCols][kColGroupRB * kColScaleGroups];
     const Multipliers m = tensor_multipliers(*amax_dev, T);
-    if (dec_out != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *dec_out = m.dec;
+    if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
     const int t = threadIdx.x;
     const int q = t & 31, rbl = t >> 5;
-    const int64_t cw = (int64_t)blockIdx.x * kColCols;          // first column of the workgroup
-    const int64_t c = cw + 4 * q;                               // first of this lane's 4 columns
-    const int ncv = (int)max((int64_t)0, min((int64_t)4, cols - c));   // 0, 2 or 4 valid columns
     const bool vec8 = (cols & 3) == 0;
-    const int64_t r_begin = (int64_t)blockIdx.y * rows_per_wg;
-    const int64_t r_end = min(rows, r_begin + rows_per_wg);
     const int64_t nrb = rows / 16;
     const int64_t ldo = rows / 2;                               // payload_t row stride (bytes)
 
-    // 16 rows x 4 columns of this lane's row block of group g: word pairs
-    // (c, c+1) in lo, (c+2, c+3) in hi.
-    auto load = [&](int64_t g, uint32_t (&lo)[16], uint32_t (&hi)[16]) {
-        const int64_t r0 = r_begin + g * (kColGroupRB * 16) + rbl * 16;
-        if (r0 >= r_end || ncv == 0) return;
+    // 16 rows x 4 columns of this lane's row block of group g of item ci:
+    // word pairs (c, c+1) in lo, (c+2, c+3) in hi.
+    auto load = [&](const ColItem& ci, int64_t g, uint32_t (&lo)[16], uint32_t (&hi)[16]) {
+        const int64_t r0 = ci.r_begin + g * (kColGroupRB * 16) + rbl * 16;
+        const int64_t c = ci.cw + 4 * q;
+        const int64_t ncv = min((int64_t)4, cols - c);
+        if (r0 >= ci.r_end || ncv <= 0) return;
         const uint16_t* src = x + r0 * cols + c;
         if (vec8 && ncv == 4) {
 #pragma unroll
@@ -273,15 +330,25 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
         }
     };
 
-    const int64_t ngroups = (r_end - r_begin + kColGroupRB * 16 - 1) / (kColGroupRB * 16);
+    int64_t it = blockIdx.x, g = 0;
+    if (it >= nitems) return;                                    // uniform
+    ColItem ci = col_item(it, gx, rows, rows_per_item);
     uint32_t lo[16], hi[16], nlo[16], nhi[16];
-    load(0, lo, hi);
-    for (int64_t g = 0; g < ngroups; ++g) {
-        load(g + 1, nlo, nhi);
-        const int64_t r0 = r_begin + g * (kColGroupRB * 16) + rbl * 16;
-        const int64_t rb = r0 / 16;
+    load(ci, 0, lo, hi);
+    while (true) {
+        // next group: within the item, else the first group of the next item
+        int64_t nit = it, ng = g + 1;
+        if (ng >= ci.ngroups) {
+            nit = it + gridDim.x;
+            ng = 0;
+        }
+        const ColItem cn = nit < nitems ? col_item(nit, gx, rows, rows_per_item) : ci;
+        if (nit < nitems) load(cn, ng, nlo, nhi);
+
+        const int64_t c = ci.cw + 4 * q;
+        const int64_t r0 = ci.r_begin + g * (kColGroupRB * 16) + rbl * 16;
         const int sg = (int)(g % kColScaleGroups);
-        if (r0 < r_end && ncv > 0) {
+        if (r0 < ci.r_end && c < cols) {
             uint32_t mx[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
@@ -293,24 +360,24 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
             BlockScale bs[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) bs[j] = block_scale(mx[j], m);
-            uint32_t w[4][16];               // Philox word of (row r, column c + j)
-            if (SR) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    uint32_t w4[4];
-                    words4((uint64_t)(r0 + r) * (uint64_t)cols + (uint64_t)c, tid, key0, key1, w4);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) w[j][r] = w4[j];
-                }
-            }
             uint32_t pk[4][2];
+            if (SR) {
+                if (vec8)
+                    sr_cols16x4<true>(lo, hi, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c,
+                                      (uint64_t)cols, tid, key0, key1, pk);
+                else
+                    sr_cols16x4<false>(lo, hi, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c,
+                                       (uint64_t)cols, tid, key0, key1, pk);
+            } else {
+                const uint32_t nw[16] = {};
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                float xv[16];
+                for (int j = 0; j < 4; ++j) {
+                    float xv[16];
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    xv[r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
-                quant_col16<SR>(xv, bs[j].r, w[j], pk[j][0], pk[j][1]);
+                    for (int r = 0; r < 16; ++r)
+                        xv[r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
+                    quant_col16<false>(xv, bs[j].r, nw, pk[j][0], pk[j][1]);
+                }
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -323,9 +390,9 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
         // blocks only; a full group is 64 contiguous bytes)
         {
             const int col = t >> 1, half = t & 1;
-            const int64_t gc = cw + col;
-            const int64_t rb0 = (r_begin + g * (kColGroupRB * 16)) / 16;
-            const int nvalid = (int)min((int64_t)kColGroupRB, (r_end / 16) - rb0);   // row blocks in the group
+            const int64_t gc = ci.cw + col;
+            const int64_t rb0 = (ci.r_begin + g * (kColGroupRB * 16)) / 16;
+            const int nvalid = (int)min((int64_t)kColGroupRB, (ci.r_end / 16) - rb0);
             if (gc < cols) {
                 uint8_t* dst = payload_t + gc * ldo + rb0 * 8 + half * 32;
                 const uint8_t* s = &stP[col][half * 32];
@@ -339,10 +406,10 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
                                 *reinterpret_cast<const uint2*>(s + (k - half * 4) * 8);
                 }
             }
-            // scales: every kColScaleGroups groups, or at the end of the range
-            if (sg == kColScaleGroups - 1 || g == ngroups - 1) {
-                const int64_t rbs = rb0 - (int64_t)sg * kColGroupRB;          // first row block of the chunk
-                const int ns = (int)(rb0 + nvalid - rbs);                   // scale bytes in the chunk
+            // scales: at the end of the item (or of a full 64-block chunk)
+            if (sg == kColScaleGroups - 1 || g == ci.ngroups - 1) {
+                const int64_t rbs = rb0 - (int64_t)sg * kColGroupRB;
+                const int ns = (int)(rb0 + nvalid - rbs);
                 if (gc < cols) {
                     uint8_t* dst = scales_t + gc * nrb + rbs + half * 32;
                     const uint8_t* s = &stS[col][half * 32];
@@ -357,6 +424,10 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
             }
         }
         __syncthreads();
+        if (nit >= nitems) break;                               // uniform
+        it = nit;
+        g = ng;
+        ci = cn;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             lo[r] = nlo[r];
@@ -516,6 +587,24 @@ hipError_t launch_quant_rows(const void* x_bf16, int64_t rows, int64_t cols,
     return hipGetLastError();
 }
 
+// Resident workgroups of a kernel on the current device (cached per device).
+template <typename K>
+int64_t resident_wgs(K kernel, int slot) {
+    static int64_t cache[16][4] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return kPersistentWGs;
+    if (cache[dev][slot] == 0) {
+        int cus = 0, per = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, reinterpret_cast<const void*>(kernel),
+                                                         kThreads, 0) != hipSuccess ||
+            cus <= 0 || per <= 0)
+            return kPersistentWGs;
+        cache[dev][slot] = (int64_t)cus * per;
+    }
+    return cache[dev][slot];
+}
+
 hipError_t launch_quant_cols(const void* x_bf16, int64_t rows, int64_t cols,
                              const float* amax_dev, float target, bool sr, uint64_t seed,
                              uint32_t tensor_id, uint8_t* payload_t, uint8_t* scales_t,
@@ -523,21 +612,24 @@ hipError_t launch_quant_cols(const void* x_bf16, int64_t rows, int64_t cols,
     uint32_t k0, k1;
     seed_key(seed, k0, k1);
     const int64_t gx = (cols + kColCols - 1) / kColCols;
-    // Row range per workgroup: a whole scale chunk (64 row blocks) when that
-    // still leaves enough workgroups, otherwise one group of 8 row blocks.
-    const int64_t chunk = (int64_t)kColGroupRB * kColScaleGroups * 16;      // 1024 rows
-    int64_t rows_per_wg = chunk;
-    while (rows_per_wg > kColGroupRB * 16 && gx * ((rows + rows_per_wg - 1) / rows_per_wg) < 512)
-        rows_per_wg /= 2;
-    const int64_t gy = (rows + rows_per_wg - 1) / rows_per_wg;
+    const int64_t resident = sr ? resident_wgs(quant_cols_kernel<true>, 0)
+                                : resident_wgs(quant_cols_kernel<false>, 1);
+    // Items of up to 64 row blocks (whole 64-byte scale runs); shorter when
+    // that leaves fewer than 2 items per resident workgroup.
+    int64_t rows_per_item = (int64_t)kColGroupRB * kColScaleGroups * 16;     // 1024 rows
+    while (rows_per_item > kColGroupRB * 16 &&
+           gx * ((rows + rows_per_item - 1) / rows_per_item) < 2 * resident)
+        rows_per_item /= 2;
+    const int64_t nitems = gx * ((rows + rows_per_item - 1) / rows_per_item);
+    const int64_t grid = min(nitems, resident);
     const uint16_t* x = reinterpret_cast<const uint16_t*>(x_bf16);
     if (sr)
-        hipLaunchKernelGGL(quant_cols_kernel<true>, dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
-                           0, s, x, rows, cols, rows_per_wg, amax_dev, target, k0, k1, tensor_id,
+        hipLaunchKernelGGL(quant_cols_kernel<true>, dim3((unsigned)grid), dim3(kThreads), 0, s, x, rows,
+                           cols, rows_per_item, gx, nitems, amax_dev, target, k0, k1, tensor_id,
                            payload_t, scales_t, dec_out);
     else
-        hipLaunchKernelGGL(quant_cols_kernel<false>, dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
-                           0, s, x, rows, cols, rows_per_wg, amax_dev, target, k0, k1, tensor_id,
+        hipLaunchKernelGGL(quant_cols_kernel<false>, dim3((unsigned)grid), dim3(kThreads), 0, s, x, rows,
+                           cols, rows_per_item, gx, nitems, amax_dev, target, k0, k1, tensor_id,
                            payload_t, scales_t, dec_out);
     return hipGetLastError();
 }

@@ -33,6 +33,7 @@
 #include "codec.hpp"
 #include "launch.hpp"
 
+#include <mutex>
 #include <type_traits>
 
 namespace ue5m3 {
@@ -447,7 +448,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_dma_kernel(
     const int wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    // tile index (see gemm_fp4_kernel)
+    // tile index (see tile_origin)
     const int ntiles = tiles_m * tiles_n;
     int t = blockIdx.x;
     if (ntiles % kXcds == 0) t = (t % kXcds) * (ntiles / kXcds) + t / kXcds;
@@ -756,11 +757,39 @@ struct SupLoader {
     }
 };
 
+// Split of the last, partial wave of tiles: with T tiles on P CUs, the first
+// Tdp = T - r tiles (whole waves) run one per workgroup; each of the r
+// leftover tiles runs as `parts` workgroups over equal ranges of its stages,
+// which write fp32 partial tiles; a second kernel adds each tile's partials
+// in part order (so the sum is deterministic) and stores it.
+struct SplitPlan {
+    int Tdp;                 // whole-tile workgroups
+    int parts;               // workgroups per leftover tile (1: no split)
+    float* part;             // [r][parts][4 waves][16 acc][16 e][64 lanes] fp32 partials
+};
+
+// Origin of logical tile t: workgroups are dispatched round-robin over the
+// XCDs, so logical tiles are remapped to give each XCD a contiguous range,
+// walked in groups of kGroupM tile rows (column-major inside a group) so
+// that tiles running together on one XCD share A and B rows in its L2.
+__device__ __forceinline__ void tile_origin(int t, int tiles_m, int tiles_n, int64_t& m0, int64_t& n0) {
+    const int ntiles = tiles_m * tiles_n;
+    if (ntiles % kXcds == 0) t = (t % kXcds) * (ntiles / kXcds) + t / kXcds;
+    const int group_tiles = kGroupM * tiles_n;
+    const int g = t / group_tiles;
+    const int first_m = g * kGroupM;
+    const int gm = min(tiles_m - first_m, kGroupM);
+    const int rr = t - g * group_tiles;
+    m0 = (int64_t)(first_m + rr % gm) * BM;
+    n0 = (int64_t)(rr / gm) * BN;
+}
+
 template <int BMODE, bool OUT_BF16>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
-    int64_t M, int64_t N, int64_t K, int tiles_m, int tiles_n, const uint8_t* __restrict__ A,
-    const uint8_t* __restrict__ As, const float* __restrict__ a_dec, const uint8_t* __restrict__ B,
-    const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec, void* __restrict__ C) {
+    int64_t M, int64_t N, int64_t K, int tiles_m, int tiles_n, SplitPlan sp,
+    const uint8_t* __restrict__ A, const uint8_t* __restrict__ As, const float* __restrict__ a_dec,
+    const uint8_t* __restrict__ B, const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec,
+    void* __restrict__ C) {
     __shared__ __attribute__((aligned(16))) uint8_t sP0[kSupPayload];
     __shared__ __attribute__((aligned(16))) uint8_t sP1[kSupPayload];
     __shared__ __attribute__((aligned(16))) uint8_t sC0[kSupScales];
@@ -772,21 +801,25 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
     const int wm = wave >> 1, wn = wave & 1;
     const int r = lane & 31, hi = lane >> 5;
 
-    // tile index (see gemm_fp4_kernel)
-    const int ntiles = tiles_m * tiles_n;
-    int t = blockIdx.x;
-    if (ntiles % kXcds == 0) t = (t % kXcds) * (ntiles / kXcds) + t / kXcds;
-    const int group_tiles = kGroupM * tiles_n;
-    const int g = t / group_tiles;
-    const int first_m = g * kGroupM;
-    const int gm = min(tiles_m - first_m, kGroupM);
-    const int rr = t - g * group_tiles;
-    const int64_t m0 = (int64_t)(first_m + rr % gm) * BM;
-    const int64_t n0 = (int64_t)(rr / gm) * BN;
-
     const int64_t kbt = K / 16;
-    const int64_t NG = K / (kSupK * BK);             // stages
-    auto stage_of = [&](int64_t G) { return min(G, NG - 1); };
+    const int64_t NG = K / (kSupK * BK);             // stages of a whole tile
+
+    // work of this workgroup: a whole tile, or one part of a leftover tile
+    int t = blockIdx.x, part_idx = 0, split_j = -1;
+    int64_t g0 = 0, g1 = NG;
+    if (t >= sp.Tdp) {
+        const int s = t - sp.Tdp;
+        split_j = s / sp.parts;
+        part_idx = s - split_j * sp.parts;
+        t = sp.Tdp + split_j;
+        g0 = (NG * part_idx) / sp.parts;
+        g1 = (NG * (part_idx + 1)) / sp.parts;
+    }
+
+    int64_t m0, n0;
+    tile_origin(t, tiles_m, tiles_n, m0, n0);
+
+    auto stage_of = [&](int64_t G) { return min(G, g1 - 1); };
 
     // Loads: waves 0, 1 bring A stage rows 0..255, waves 2, 3 B rows 256..511
     // (rows clamped into the matrix; clamped rows only feed discarded outputs).
@@ -834,8 +867,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
 
     // prologue: stages 0 and 1 in flight; stage 0 complete everywhere; slice 0
     // in registers and its k-step 0 decoded
-    L.issue<0, kSupPayLoads, true>(P0, S0, 0);
-    L.issue<0, kSupPayLoads, true>(P1, S1, stage_of(1));
+    L.issue<0, kSupPayLoads, true>(P0, S0, g0);
+    L.issue<0, kSupPayLoads, true>(P1, S1, stage_of(g0 + 1));
     wait_vmem<kSupLoads>();
     __syncthreads();
     read_sup_slice<0>(R0, sP0, sC0, pa, pb, x0);
@@ -886,38 +919,128 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
         slice(I2{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R0, R1);
         slice(I3{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R1, R0);
     };
-    int64_t G = 0;
-    for (; G + 1 < NG; G += 2) {
+    int64_t G = g0;
+    for (; G + 1 < g1; G += 2) {
         stage(G, sP0, sC0, sP1, sC1, P0, S0);
         stage(G + 1, sP1, sC1, sP0, sC0, P1, S1);
     }
-    if (G < NG) stage(G, sP0, sC0, sP1, sC1, P0, S0);   // odd stage count
+    if (G < g1) stage(G, sP0, sC0, sP1, sC1, P0, S0);   // odd stage count
     wait_vmem<0>();                                // no load outlives the kernel's LDS
 
-    // ---- epilogue: C = alpha * acc ------------------------------------------
+    // ---- epilogue: C = alpha * value ----------------------------------------
+    // Element e of accumulator (i, j) is row 32i + 8(e/4) + 4(l/32) + e%4,
+    // column 32j + l%32 of the wave's 128 x 128 block.
     const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;   // operands were scaled by 2^-3
     const int64_t mw = m0 + wm * 128, nw = n0 + wn * 128;
+    auto store_tile = [&](auto value) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < 4; ++i) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t n = nw + j * 32 + r;
+            for (int j = 0; j < 4; ++j) {
+                const int64_t n = nw + j * 32 + r;
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int64_t m = mw + i * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-                if (m < M && n < N) {
-                    const float v = alpha * acc[i][j][e];
-                    if (OUT_BF16) {
-                        const uint32_t b = __float_as_uint(v);
-                        const uint32_t rb16 = (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
-                        reinterpret_cast<uint16_t*>(C)[m * N + n] = (uint16_t)rb16;
-                    } else {
-                        reinterpret_cast<float*>(C)[m * N + n] = v;
+                for (int e = 0; e < 16; ++e) {
+                    const int64_t m = mw + i * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+                    if (m < M && n < N) {
+                        const float v = alpha * value(i, j, e);
+                        if (OUT_BF16) {
+                            const uint32_t b = __float_as_uint(v);
+                            const uint32_t rb16 = (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+                            reinterpret_cast<uint16_t*>(C)[m * N + n] = (uint16_t)rb16;
+                        } else {
+                            reinterpret_cast<float*>(C)[m * N + n] = v;
+                        }
                     }
                 }
             }
         }
+    };
+    if (split_j < 0) {
+        store_tile([&](int i, int j, int e) { return acc[i][j][e]; });
+        return;
     }
+    // one part of a leftover tile: fp32 partial, lane-major so that the
+    // stores coalesce
+    float* mine = sp.part + ((int64_t)split_j * sp.parts + part_idx) * 65536 + (int64_t)wave * 16384;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) mine[((i * 4 + j) * 16 + e) * 64 + lane] = acc[i][j][e];
+}
+
+// Sum of the partials of the split tiles, in part order, times alpha, into C.
+// Workgroup (tile j, block wv) covers the 128 x 128 block that wave wv of the
+// GEMM workgroups computed; thread t takes entries t + 256k of the block's
+// lane-major partial layout.
+template <bool OUT_BF16>
+__global__ __launch_bounds__(256) void gemm_split_sum_kernel(
+    int64_t M, int64_t N, int tiles_m, int tiles_n, SplitPlan sp, const float* __restrict__ a_dec,
+    const float* __restrict__ b_dec, void* __restrict__ C) {
+    const int j = blockIdx.x >> 2, wv = blockIdx.x & 3;
+    int64_t m0, n0;
+    tile_origin(sp.Tdp + j, tiles_m, tiles_n, m0, n0);
+    const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;
+    const int64_t mw = m0 + (wv >> 1) * 128, nw = n0 + (wv & 1) * 128;
+    const float* base = sp.part + (int64_t)j * sp.parts * 65536 + (int64_t)wv * 16384;
+#pragma unroll 4
+    for (int k = 0; k < 64; ++k) {
+        const int o = threadIdx.x + 256 * k;
+        const int lane = o & 63, e = (o >> 6) & 15, acc = o >> 10;
+        float v = base[o];
+        for (int p = 1; p < sp.parts; ++p) v += base[(int64_t)p * 65536 + o];
+        const int64_t m = mw + (acc >> 2) * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+        const int64_t n = nw + (acc & 3) * 32 + (lane & 31);
+        if (m < M && n < N) {
+            v = alpha * v;
+            if (OUT_BF16) {
+                const uint32_t b = __float_as_uint(v);
+                reinterpret_cast<uint16_t*>(C)[m * N + n] = (uint16_t)((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+            } else {
+                reinterpret_cast<float*>(C)[m * N + n] = v;
+            }
+        }
+    }
+}
+
+// Per-device, per-stream workspace for the fp32 partials of split tiles,
+// grown on demand.  Launches on one stream are ordered, so one workspace per
+// (device, stream) suffices.
+struct SplitWorkspace {
+    int dev = -1;
+    hipStream_t stream = nullptr;
+    float* part = nullptr;
+    size_t part_floats = 0;
+};
+
+hipError_t split_workspace(hipStream_t s, size_t part_floats, float** part) {
+    static std::mutex mu;
+    static SplitWorkspace ws[64];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lock(mu);
+    SplitWorkspace* slot = nullptr;
+    for (auto& x : ws)
+        if (x.dev == dev && x.stream == s) { slot = &x; break; }
+    if (slot == nullptr)
+        for (auto& x : ws)
+            if (x.dev < 0) { slot = &x; slot->dev = dev; slot->stream = s; break; }
+    if (slot == nullptr) return hipErrorOutOfMemory;       // more than 64 (device, stream) pairs
+    if (slot->part_floats < part_floats) {
+        if (slot->part) {
+            // a launch still queued on this stream may use the old buffer
+            if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
+            (void)hipFree(slot->part);
+        }
+        slot->part = nullptr;
+        slot->part_floats = 0;
+        if ((e = hipMalloc(&slot->part, part_floats * sizeof(float))) != hipSuccess) return e;
+        slot->part_floats = part_floats;
+    }
+    *part = slot->part;
+    return hipSuccess;
 }
 
 template <int BMODE, bool OUT_BF16>
@@ -926,8 +1049,32 @@ hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
                       void* c, hipStream_t s) {
     const int tiles_m = (int)((M + BM - 1) / BM);
     const int tiles_n = (int)((N + BN - 1) / BN);
-    hipLaunchKernelGGL((gemm_fp4_reg_kernel<BMODE, OUT_BF16>), dim3((unsigned)(tiles_m * tiles_n)),
-                       dim3(kGemmThreads), 0, s, M, N, K, tiles_m, tiles_n, a, as, ad, b, bs, bd, c);
+    const int T = tiles_m * tiles_n;
+    const int NG = (int)(K / (kSupK * BK));
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    // One workgroup per CU at a time (LDS-bound).  Split only a partial last
+    // wave of tiles that leaves at least three quarters of the CUs idle: the
+    // partial round trip costs about what a half-idle last wave does.
+    SplitPlan sp{T, 1, nullptr};
+    const int rem = cus > 0 ? T % cus : 0;
+    if (T > cus && rem > 0 && rem <= cus / 4) {
+        const int parts = min(cus / rem, NG);
+        if (parts > 1) {
+            sp.Tdp = T - rem;
+            sp.parts = parts;
+            e = split_workspace(s, (size_t)rem * parts * 65536, &sp.part);
+            if (e != hipSuccess) return e;
+        }
+    }
+    const int grid = sp.Tdp + (T - sp.Tdp) * sp.parts;
+    hipLaunchKernelGGL((gemm_fp4_reg_kernel<BMODE, OUT_BF16>), dim3((unsigned)grid), dim3(kGemmThreads),
+                       0, s, M, N, K, tiles_m, tiles_n, sp, a, as, ad, b, bs, bd, c);
+    if ((e = hipGetLastError()) != hipSuccess || sp.parts == 1) return e;
+    hipLaunchKernelGGL((gemm_split_sum_kernel<OUT_BF16>), dim3((unsigned)(4 * (T - sp.Tdp))), dim3(256),
+                       0, s, M, N, tiles_m, tiles_n, sp, ad, bd, c);
     return hipGetLastError();
 }
 

@@ -195,3 +195,28 @@ def test_ffn_up_projection_sampled():
     al = ogemm.alpha(dco[2], xco[2])
     gemm_check(host(dw)[nsel][:, ksel], ogemm.wgrad(dYc, Xc, al), al,
                ogemm.abs_product(dYc.T, Xc.T), T, "wgrad sampled")
+
+
+def test_split_tail_tiles():
+    """A partial last wave of tiles: 16 x 17 = 272 tiles of 256 x 256 on 256
+    CUs leave 16 tiles, which run split along K (4 parts of 1 stage each)
+    and are summed by the second kernel.  Every output is compared."""
+    say("gemm split tail")
+    M, N, K = 4096, 4352, 1024
+    a = synthetic.activation(13, M, K, 1e-2, 50.0)
+    w = synthetic.weight(13, N, K)
+    ar = oq.quantize_1d(a, 1, osc.amax(a))
+    wq = oq.quantize_2d(w, osc.amax(w))
+    A, W = oq.decoded_1d(ar[0], ar[1], 1), oq.decoded_2d(wq[0], wq[1])
+    al = ogemm.alpha(ar[2], wq[3])
+    ref, ap = ogemm.fprop(A, W, al), ogemm.abs_product(A, W)
+    for out_dtype in [torch.float32, torch.bfloat16]:
+        for rep in range(2):          # the workspace is reused by the second call
+            c = ue.gemm("nt", M, N, K, u8_to_dev(ar[0]), u8_to_dev(ar[1]), f32_scalar_dev(ar[2]),
+                        u8_to_dev(wq[0]), u8_to_dev(wq[1]), f32_scalar_dev(wq[3]), out_dtype=out_dtype)
+            if out_dtype == torch.float32:
+                gemm_check(host(c), ref, al, ap, K, f"split nt fp32 call {rep}")
+            else:
+                c16 = c.float().cpu().numpy().astype(np.float64)
+                ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
+                assert np.all(np.abs(c16 - ref) <= ulp * 1.01 + 1e-30), rep

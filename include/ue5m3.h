@@ -13,8 +13,10 @@
  * Conventions shared by every call
  * --------------------------------
  * - All tensor pointers are DEVICE pointers owned by the caller, who
- *   allocates and frees them; the library allocates no device memory and
- *   keeps no global mutable state.  Every pointer must be 16-byte aligned.
+ *   allocates and frees them.  Every pointer must be 16-byte aligned.  The
+ *   only memory the library allocates itself is the split-tile workspace of
+ *   ue5m3_gemm (see there); besides it the library keeps only caches of
+ *   device properties.
  * - bf16 tensors are dense row-major [rows, cols] arrays of 16-bit words.
  * - Payloads pack two E2M1 nibbles per byte along a row: byte [r, c/2] holds
  *   element (r, c) in its low nibble and (r, c+1) in its high nibble.
@@ -24,7 +26,9 @@
  * - Every call only enqueues work on `stream` (a hipStream_t; 0 is the null
  *   stream) and returns without synchronizing.  Argument errors are detected
  *   on the host before anything is enqueued; then nothing is written.
- * - Inputs must be finite; results for NaN / Inf inputs are unspecified.
+ * - Inputs must not be NaN (the nibbles and codes of NaN elements are
+ *   unspecified); +-Inf is quantized like any magnitude above the E2M1 and
+ *   UE5M3 ranges (saturation).
  * - No C++ exception crosses this interface.
  */
 #ifndef UE5M3_H
@@ -149,11 +153,19 @@ ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
  * Decoded-operand FP4 GEMM (Sec. 5.1; the three products of Sec. 4.3):
  *     C[m, n] = alpha * sum_k A_hat[m, k] * B_hat[n, k],
  *     alpha = RN(*a_dec * *b_dec),
- * where X_hat = E2M1 value * UE5M3 block scale (exact in bf16), products are
- * exact and the sum is accumulated in fp32 (bf16 matrix cores); the order of
- * the fp32 additions is unspecified.  C is a dense row-major [M, N] fp32
- * array (UE5M3_OUT_F32) or bf16 array (UE5M3_OUT_BF16, round to nearest even
- * of the fp32 result).
+ * where X_hat = E2M1 value * UE5M3 block scale (held exactly, as fp16 values
+ * times 2^-3, on the matrix cores), products are exact and the sum is
+ * accumulated in fp32; the order of the fp32 additions is unspecified.  C is
+ * a dense row-major [M, N] fp32 array (UE5M3_OUT_F32) or bf16 array
+ * (UE5M3_OUT_BF16, round to nearest even of the fp32 result).
+ *
+ * Workspace: when the 256 x 256 output tiles leave a last, mostly idle wave
+ * of workgroups, those tiles are split along K and their fp32 partials are
+ * summed (in a fixed order) by a second kernel on the same stream.  The
+ * partials live in a workspace the library allocates on the first such call
+ * for each (device, stream) pair and keeps for later calls on that pair
+ * (grown when a larger one is needed, which first synchronizes the stream);
+ * such a call returns UE5M3_EHIP if the allocation fails.
  *
  * Both operands are passed in contraction-contiguous form, as produced by the
  * quantizers for each product of a linear Y = X W^T (X [T,K], W [N,K]):

@@ -119,7 +119,7 @@ ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K
     ue5m3::BScale bmode;
     switch (layout) {
         case UE5M3_NT: bmode = ue5m3::BScale::Tile; break;
-        case UE5M3_NN: bmode = ue5m3::BScale::Tile; break;
+        case UE5M3_NN: bmode = ue5m3::BScale::TileDgrad; break;
         case UE5M3_TN: bmode = ue5m3::BScale::Row; break;
         default: return UE5M3_ELAYOUT;
     }

@@ -974,7 +974,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
 // Workgroup (tile j, block wv) covers the 128 x 128 block that wave wv of the
 // GEMM workgroups computed; thread t takes entries t + 256k of the block's
 // lane-major partial layout.
-template <bool OUT_BF16>
+template <int BMODE, bool OUT_BF16>
 __global__ __launch_bounds__(256) void gemm_split_sum_kernel(
     int64_t M, int64_t N, int tiles_m, int tiles_n, SplitPlan sp, const float* __restrict__ a_dec,
     const float* __restrict__ b_dec, void* __restrict__ C) {
@@ -1073,7 +1073,7 @@ hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
     hipLaunchKernelGGL((gemm_fp4_reg_kernel<BMODE, OUT_BF16>), dim3((unsigned)grid), dim3(kGemmThreads),
                        0, s, M, N, K, tiles_m, tiles_n, sp, a, as, ad, b, bs, bd, c);
     if ((e = hipGetLastError()) != hipSuccess || sp.parts == 1) return e;
-    hipLaunchKernelGGL((gemm_split_sum_kernel<OUT_BF16>), dim3((unsigned)(4 * (T - sp.Tdp))), dim3(256),
+    hipLaunchKernelGGL((gemm_split_sum_kernel<BMODE, OUT_BF16>), dim3((unsigned)(4 * (T - sp.Tdp))), dim3(256),
                        0, s, M, N, tiles_m, tiles_n, sp, ad, bd, c);
     return hipGetLastError();
 }
@@ -1124,6 +1124,8 @@ hipError_t launch_gemm(BScale bmode, int64_t M, int64_t N, int64_t K, const uint
             return launch_mode<(int)BScale::Row>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, s);
         case BScale::Tile:
             return launch_mode<(int)BScale::Tile>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, s);
+        case BScale::TileDgrad:
+            return launch_mode<(int)BScale::TileDgrad>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, s);
     }
     return hipErrorInvalidValue;
 }

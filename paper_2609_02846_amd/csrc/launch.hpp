@@ -8,8 +8,10 @@
 
 namespace ue5m3 {
 
-// B scale layouts: one code per (row, 16 k) or per (16 rows, 16 k).
-enum class BScale : int { Row = 0, Tile = 1 };
+// B scale layouts: one code per (row, 16 k) or per (16 rows, 16 k).  TileDgrad
+// is Tile for the dgrad product: the same code, instantiated separately so
+// that profiles tell the fprop and dgrad launches apart.
+enum class BScale : int { Row = 0, Tile = 1, TileDgrad = 2 };
 
 hipError_t launch_amax(const void* x_bf16, int64_t numel, float* amax_dev, hipStream_t s);
 

@@ -978,28 +978,44 @@ template <int BMODE, bool OUT_BF16>
 __global__ __launch_bounds__(256) void gemm_split_sum_kernel(
     int64_t M, int64_t N, int tiles_m, int tiles_n, SplitPlan sp, const float* __restrict__ a_dec,
     const float* __restrict__ b_dec, void* __restrict__ C) {
-    const int j = blockIdx.x >> 2, wv = blockIdx.x & 3;
+    // 64 workgroups per split tile: (wave quarter wv, accumulator acc) pairs,
+    // 1024 partial floats each; a thread owns 4 consecutive lanes of one
+    // accumulator element, i.e. 4 adjacent output columns.
+    const int j = blockIdx.x >> 6, wv = (blockIdx.x >> 4) & 3, acc = blockIdx.x & 15;
     int64_t m0, n0;
     tile_origin(sp.Tdp + j, tiles_m, tiles_n, m0, n0);
     const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;
-    const int64_t mw = m0 + (wv >> 1) * 128, nw = n0 + (wv & 1) * 128;
-    const float* base = sp.part + (int64_t)j * sp.parts * 65536 + (int64_t)wv * 16384;
-#pragma unroll 4
-    for (int k = 0; k < 64; ++k) {
-        const int o = threadIdx.x + 256 * k;
-        const int lane = o & 63, e = (o >> 6) & 15, acc = o >> 10;
-        float v = base[o];
-        for (int p = 1; p < sp.parts; ++p) v += base[(int64_t)p * 65536 + o];
-        const int64_t m = mw + (acc >> 2) * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-        const int64_t n = nw + (acc & 3) * 32 + (lane & 31);
-        if (m < M && n < N) {
-            v = alpha * v;
-            if (OUT_BF16) {
-                const uint32_t b = __float_as_uint(v);
-                reinterpret_cast<uint16_t*>(C)[m * N + n] = (uint16_t)((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
-            } else {
-                reinterpret_cast<float*>(C)[m * N + n] = v;
-            }
+    const int o = acc * 1024 + threadIdx.x * 4;
+    const float* base = sp.part + (int64_t)j * sp.parts * 65536 + (int64_t)wv * 16384 + o;
+    float4 v = *reinterpret_cast<const float4*>(base);
+    for (int p = 1; p < sp.parts; ++p) {
+        const float4 u = *reinterpret_cast<const float4*>(base + (int64_t)p * 65536);
+        v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+    }
+    const int lane = o & 63, e = (o >> 6) & 15;
+    const int64_t m = m0 + (wv >> 1) * 128 + (acc >> 2) * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+    const int64_t n = n0 + (wv & 1) * 128 + (acc & 3) * 32 + (lane & 31);
+    if (m >= M) return;
+    const float r[4] = {alpha * v.x, alpha * v.y, alpha * v.z, alpha * v.w};
+    if (OUT_BF16) {
+        uint16_t h[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t b = __float_as_uint(r[q]);
+            h[q] = (uint16_t)((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+        }
+        uint16_t* dst = reinterpret_cast<uint16_t*>(C) + m * N + n;
+        if ((N & 3) == 0 && n + 3 < N) {
+            *reinterpret_cast<uint2*>(dst) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+        } else {
+            for (int q = 0; q < 4; ++q) if (n + q < N) dst[q] = h[q];
+        }
+    } else {
+        float* dst = reinterpret_cast<float*>(C) + m * N + n;
+        if ((N & 3) == 0 && n + 3 < N) {
+            *reinterpret_cast<float4*>(dst) = make_float4(r[0], r[1], r[2], r[3]);
+        } else {
+            for (int q = 0; q < 4; ++q) if (n + q < N) dst[q] = r[q];
         }
     }
 }
@@ -1043,6 +1059,8 @@ hipError_t split_workspace(hipStream_t s, size_t part_floats, float** part) {
     return hipSuccess;
 }
 
+constexpr int kSplitRemDiv = 2;
+
 template <int BMODE, bool OUT_BF16>
 hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                       const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
@@ -1056,11 +1074,10 @@ hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
     // One workgroup per CU at a time (LDS-bound).  Split only a partial last
-    // wave of tiles that leaves at least three quarters of the CUs idle: the
-    // partial round trip costs about what a half-idle last wave does.
+    // wave of tiles that leaves at least 1 - 1/kSplitRemDiv of the CUs idle.
     SplitPlan sp{T, 1, nullptr};
     const int rem = cus > 0 ? T % cus : 0;
-    if (T > cus && rem > 0 && rem <= cus / 4) {
+    if (T > cus && rem > 0 && rem <= cus / kSplitRemDiv) {
         const int parts = min(cus / rem, NG);
         if (parts > 1) {
             sp.Tdp = T - rem;
@@ -1073,7 +1090,7 @@ hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
     hipLaunchKernelGGL((gemm_fp4_reg_kernel<BMODE, OUT_BF16>), dim3((unsigned)grid), dim3(kGemmThreads),
                        0, s, M, N, K, tiles_m, tiles_n, sp, a, as, ad, b, bs, bd, c);
     if ((e = hipGetLastError()) != hipSuccess || sp.parts == 1) return e;
-    hipLaunchKernelGGL((gemm_split_sum_kernel<BMODE, OUT_BF16>), dim3((unsigned)(4 * (T - sp.Tdp))), dim3(256),
+    hipLaunchKernelGGL((gemm_split_sum_kernel<BMODE, OUT_BF16>), dim3((unsigned)(64 * (T - sp.Tdp))), dim3(256),
                        0, s, M, N, tiles_m, tiles_n, sp, ad, bd, c);
     return hipGetLastError();
 }

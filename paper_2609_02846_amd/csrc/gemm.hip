@@ -43,6 +43,8 @@ typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
 typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
 constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int kGemmThreads = 256;
@@ -414,6 +416,25 @@ __device__ __forceinline__ void mfma16(f32x16_t (&acc)[4][4], const Frags& f) {
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
 }
 
+// The same products issued as B x A^T: accumulator (i, j) then holds the
+// transposed 32 x 32 block, so that each lane owns runs of 4 adjacent output
+// columns (element e of lane l: row l%32, column 8(e/4) + 4(l/32) + e%4).
+__device__ __forceinline__ void mfma16_t(f32x16_t (&acc)[4][4], const Frags& f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
+}
+
+// Two floats to two bf16 (round to nearest even), packed low-first.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    typedef __attribute__((ext_vector_type(2))) float f32x2_t;
+    typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+    const f32x2_t v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
 typedef __attribute__((address_space(3))) void* lds_void_ptr;
 typedef __attribute__((address_space(1))) void* glb_void_ptr;
 
@@ -720,9 +741,35 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)p);
 }
 
-__device__ __forceinline__ void dma_x4(const uint8_t* g, uint32_t lds) {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-                 :: "v"(g), "s"(lds) : "memory", "m0");
+// Calls f(integral_constant<int, i>) for i in [I0, I1).
+template <int I0, int I1, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (I0 < I1) {
+        f(std::integral_constant<int, I0>{});
+        static_for<I0 + 1, I1>(f);
+    }
+}
+
+// Buffer resource of a raw byte range [base, base + bytes): loads whose
+// per-lane offset falls outside it are dropped by the hardware.
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4_t buffer_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t a = (uint64_t)(uintptr_t)base;
+    i32x4_t r;
+    r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));   // stride 0
+    r[2] = (int)bytes;
+    r[3] = 0x00020000;                                                   // 32-bit data format
+    return r;
+}
+
+// 16 bytes per lane from rsrc at voff + soff into LDS at lds + OFF + 16 lane
+// (the LDS offset is added inside the instruction sequence so that the
+// compiler does not keep one register per destination).
+template <int OFF>
+__device__ __forceinline__ void dma_buf_x4(i32x4_t rsrc, uint32_t voff, uint32_t soff, uint32_t lds) {
+    asm volatile("s_add_u32 m0, %3, %4\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+                 :: "v"(voff), "s"(rsrc), "s"(soff), "s"(lds), "i"(OFF) : "memory", "m0", "scc");
 }
 
 // vmcnt(n) with expcnt and lgkmcnt left at their maxima (n < 64).
@@ -732,40 +779,48 @@ __device__ __forceinline__ void wait_vmem() {
     __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | 0x0F70);
 }
 
+// Per-lane source of a wave's stage loads for one output tile: byte offsets
+// of the lane's first payload chunk and of its two scale rows.
+struct SupSrc {
+    uint32_t off0, so0, so1;
+};
+
 // A wave's share of the loads of one stage: payload loads i in [I0, I1)
 // (1 KB each: 8 stage rows of 128 B, lane l -> row 8i + l/8 of the wave's
 // 128, position l % 8) and, with SC, its two scale loads (64 rows x 16 B).
+// Payload rows past the matrix fall outside the buffer and are dropped (they
+// only feed discarded outputs); scale rows are clamped when the tile is set up.
 struct SupLoader {
-    const uint8_t* mat;      // payload matrix of this wave's rows (A or B)
-    int64_t row0, rmax;      // matrix row of the lane's first payload row, last valid row
-    int64_t rowb;            // payload row bytes
-    int chunk;               // source chunk of the lane (position ^ row & 7)
-    const uint8_t* sc[2];    // scale row pointers of the lane's two scale loads
+    i32x4_t pay, sca;        // payload and scale buffers of this wave's matrix (A or B)
+    uint32_t rows8;          // bytes of 8 payload rows
     uint32_t ldp, lds;       // this wave's LDS offsets inside a payload / scale stage
 
     template <int I0, int I1, bool SC>
-    __device__ __forceinline__ void issue(uint32_t P, uint32_t S, int64_t G) const {
-#pragma unroll
-        for (int i = I0; i < I1; ++i) {
-            const int64_t row = min(row0 + 8 * i, rmax);
-            dma_x4(mat + row * rowb + G * kSupRowBytes + chunk * 16, P + ldp + i * 1024);
-        }
+    __device__ __forceinline__ void issue(uint32_t P, uint32_t S, const SupSrc& src, int64_t G) const {
+        const uint32_t gp = (uint32_t)G * kSupRowBytes;
+        const uint32_t pl = P + ldp;
+        static_for<I0, I1>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            dma_buf_x4<i * 1024>(pay, src.off0 + i * rows8, gp, pl);
+        });
         if (SC) {
-#pragma unroll
-            for (int u = 0; u < 2; ++u) dma_x4(sc[u] + G * 16, S + lds + u * 1024);
+            const uint32_t gs = (uint32_t)G * 16;
+            const uint32_t sl = S + lds;
+            dma_buf_x4<0>(sca, src.so0, gs, sl);
+            dma_buf_x4<1024>(sca, src.so1, gs, sl);
         }
     }
 };
 
 // Split of the last, partial wave of tiles: with T tiles on P CUs, the first
-// Tdp = T - r tiles (whole waves) run one per workgroup; each of the r
-// leftover tiles runs as `parts` workgroups over equal ranges of its stages,
-// which write fp32 partial tiles; a second kernel adds each tile's partials
-// in part order (so the sum is deterministic) and stores it.
+// Tdp = T - r tiles (whole waves) are whole work items; each of the r
+// leftover tiles becomes `parts` items over equal ranges of its stages, which
+// write fp32 partial tiles; a second kernel adds each tile's partials in part
+// order (so the sum is deterministic) and stores it.
 struct SplitPlan {
-    int Tdp;                 // whole-tile workgroups
-    int parts;               // workgroups per leftover tile (1: no split)
-    float* part;             // [r][parts][4 waves][16 acc][16 e][64 lanes] fp32 partials
+    int Tdp;                 // whole-tile items
+    int parts;               // items per leftover tile (1: no split)
+    float* part;             // [r][parts][4 waves][16 acc (i, j)][4 runs][64 lanes][4] fp32 partials
 };
 
 // Origin of logical tile t: workgroups are dispatched round-robin over the
@@ -784,9 +839,42 @@ __device__ __forceinline__ void tile_origin(int t, int tiles_m, int tiles_n, int
     n0 = (int64_t)(rr / gm) * BN;
 }
 
+constexpr bool kStaggerSplit = true;
+
+// One work item: a whole tile (split_j < 0) or part `part` of leftover tile
+// split_j, over stages [g0, g1).  With an even stage count per tile, part
+// boundaries fall on even stages so every item has an even length.
+struct WorkItem {
+    int t, split_j, part, g0, g1;
+};
+
+__device__ __forceinline__ WorkItem work_item(int it, const SplitPlan& sp, int NG) {
+    WorkItem w;
+    if (it < sp.Tdp) {
+        w.t = it; w.split_j = -1; w.part = 0; w.g0 = 0; w.g1 = NG;
+        return w;
+    }
+    const int s = it - sp.Tdp;
+    w.split_j = s / sp.parts;
+    w.part = s - w.split_j * sp.parts;
+    w.t = sp.Tdp + w.split_j;
+    const int unit = (NG % 2 == 0) ? 2 : 1;
+    const int nu = NG / unit;
+    w.g0 = unit * ((nu * w.part) / sp.parts);
+    w.g1 = unit * ((nu * (w.part + 1)) / sp.parts);
+    return w;
+}
+
+// Register-decode GEMM, persistent: workgroup w runs items w, w + grid, ...
+// (whole tiles first, then split parts).  During the last two stages of an
+// item the next item's first two stages are loaded, so its epilogue and the
+// next item's start overlap those loads instead of waiting for them.  Items
+// must have an even number of stages when a workgroup runs more than one
+// (the stage buffers alternate and every item starts in buffer 0).  Sizes:
+// every operand, C and the partial workspace span less than 2^31 bytes.
 template <int BMODE, bool OUT_BF16>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
-    int64_t M, int64_t N, int64_t K, int tiles_m, int tiles_n, SplitPlan sp,
+    int M, int N, int K, int tiles_m, int tiles_n, int items, SplitPlan sp,
     const uint8_t* __restrict__ A, const uint8_t* __restrict__ As, const float* __restrict__ a_dec,
     const uint8_t* __restrict__ B, const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec,
     void* __restrict__ C) {
@@ -797,54 +885,41 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     const int r = lane & 31, hi = lane >> 5;
 
-    const int64_t kbt = K / 16;
-    const int64_t NG = K / (kSupK * BK);             // stages of a whole tile
+    const int kbt = K / 16;                          // scale bytes per row
+    const int NG = K / (kSupK * BK);                 // stages of a whole tile
 
-    // work of this workgroup: a whole tile, or one part of a leftover tile
-    int t = blockIdx.x, part_idx = 0, split_j = -1;
-    int64_t g0 = 0, g1 = NG;
-    if (t >= sp.Tdp) {
-        const int s = t - sp.Tdp;
-        split_j = s / sp.parts;
-        part_idx = s - split_j * sp.parts;
-        t = sp.Tdp + split_j;
-        g0 = (NG * part_idx) / sp.parts;
-        g1 = (NG * (part_idx + 1)) / sp.parts;
-    }
-
-    int64_t m0, n0;
-    tile_origin(t, tiles_m, tiles_n, m0, n0);
-
-    auto stage_of = [&](int64_t G) { return min(G, g1 - 1); };
-
-    // Loads: waves 0, 1 bring A stage rows 0..255, waves 2, 3 B rows 256..511
-    // (rows clamped into the matrix; clamped rows only feed discarded outputs).
+    // Loads: waves 0, 1 bring A stage rows 0..255, waves 2, 3 B rows 256..511.
+    const bool isA = wave < 2;
+    const int xw = 128 * (wave & 1);                 // first stage row of the wave within A or B
+    const int brows = BMODE == (int)BScale::Row ? N : (N + 15) / 16;   // rows of the B scale matrix
     SupLoader L;
-    {
-        const bool isA = wave < 2;
-        const int xw = 128 * (wave & 1);             // first stage row of the wave within A or B
-        L.mat = isA ? A : B;
-        L.rowb = kbt * 8;
-        L.row0 = (isA ? m0 : n0) + xw + (lane >> 3);
-        L.rmax = (isA ? M : N) - 1;
-        L.chunk = (lane & 7) ^ ((lane >> 3) & 7);
-        L.ldp = __builtin_amdgcn_readfirstlane((uint32_t)(128 * wave * kSupRowBytes));
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            const int64_t x = (isA ? m0 : n0) + xw + 64 * u + lane;
-            if (isA) {
-                L.sc[u] = As + min(x, M - 1) * kbt;
-            } else {
-                const int64_t n = min(x, N - 1);
-                L.sc[u] = Bs + (BMODE == (int)BScale::Row ? n : (n >> 4)) * kbt;
-            }
+    L.pay = isA ? buffer_rsrc(A, (uint32_t)M * kbt * 8) : buffer_rsrc(B, (uint32_t)N * kbt * 8);
+    L.sca = isA ? buffer_rsrc(As, (uint32_t)M * kbt) : buffer_rsrc(Bs, (uint32_t)brows * kbt);
+    L.rows8 = (uint32_t)(64 * kbt);
+    L.ldp = (uint32_t)(128 * wave * kSupRowBytes);
+    L.lds = (uint32_t)(128 * wave * kSupK * 4);
+    const uint32_t chunk16 = (uint32_t)(((lane & 7) ^ ((lane >> 3) & 7)) * 16);
+    auto src_of = [&](int t) {
+        int64_t m0, n0;
+        tile_origin(t, tiles_m, tiles_n, m0, n0);
+        const int x0 = (int)(isA ? m0 : n0) + xw;
+        SupSrc q;
+        q.off0 = (uint32_t)(x0 + (lane >> 3)) * (uint32_t)(kbt * 8) + chunk16;
+        const int xa = x0 + lane, xb = x0 + 64 + lane;
+        if (isA) {
+            q.so0 = (uint32_t)min(xa, M - 1) * kbt;
+            q.so1 = (uint32_t)min(xb, M - 1) * kbt;
+        } else {
+            const int na = min(xa, N - 1), nb = min(xb, N - 1);
+            q.so0 = (uint32_t)(BMODE == (int)BScale::Row ? na : (na >> 4)) * kbt;
+            q.so1 = (uint32_t)(BMODE == (int)BScale::Row ? nb : (nb >> 4)) * kbt;
         }
-        L.lds = __builtin_amdgcn_readfirstlane((uint32_t)(128 * wave * kSupK * 4));
-    }
+        return q;
+    };
     const uint32_t P0 = lds_addr(sP0), P1 = lds_addr(sP1), S0 = lds_addr(sC0), S1 = lds_addr(sC1);
 
     // Read offsets of the lane: first A / B stage rows and per-slice chunk.
@@ -855,167 +930,248 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
     const uint32_t sel = hi ? 0x0C030C02u : 0x0C010C00u;
 
     f32x16_t acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-
     RegSlice R0, R1;
     Frags F0, F1;
 
-    // prologue: stages 0 and 1 in flight; stage 0 complete everywhere; slice 0
-    // in registers and its k-step 0 decoded
-    L.issue<0, kSupPayLoads, true>(P0, S0, g0);
-    L.issue<0, kSupPayLoads, true>(P1, S1, stage_of(g0 + 1));
-    wait_vmem<kSupLoads>();
-    __syncthreads();
-    read_sup_slice<0>(R0, sP0, sC0, pa, pb, x0);
-    decode_kstep<0>(F0, R0, sel);
+    // Items of this workgroup: w, w + grid, ...  Odd workgroups whose last
+    // item is a split part run that part first, so that their tile
+    // boundaries fall between those of the even ones and the output stores
+    // of all CUs do not come in one burst.
+    const int grid = (int)gridDim.x;
+    const int nw = (items - (int)blockIdx.x + grid - 1) / grid;
+    const int last_it = (int)blockIdx.x + (nw - 1) * grid;
+    const bool rot = kStaggerSplit && (blockIdx.x & 1) && nw > 1 && last_it >= sp.Tdp;
+    auto item_at = [&](int k) {
+        return rot ? (k == 0 ? last_it : (int)blockIdx.x + (k - 1) * grid) : (int)blockIdx.x + k * grid;
+    };
 
-    // One slice.  Slices 0..2 of a stage read the next slice of the same
-    // stage; slice 3 first waits for the next stage (loaded during the
-    // previous stage), synchronizes, starts the loads of stage G+2 into the
-    // buffer just consumed, and reads slice 0 of the next stage.
-    auto slice = [&](auto SLc, int64_t G, const uint8_t* Pc, const uint8_t* Sc, const uint8_t* Pn,
-                     const uint8_t* Sn, uint32_t ldP, uint32_t ldS, RegSlice& Rc, RegSlice& Rn) {
-        constexpr int SL = decltype(SLc)::value;
-        decode_kstep<1>(F1, Rc, sel);
-        mfma16(acc, F0);
-        kstep_schedule<0, 0, 4>();
-        __builtin_amdgcn_sched_barrier(0);
-        if (SL == 3) {
-            wait_vmem<0>();
-            __syncthreads();
-            read_sup_slice<0>(Rn, Pn, Sn, pa, pb, x0);
-            L.issue<0, 6, false>(ldP, ldS, stage_of(G + 2));
-        } else {
-            read_sup_slice<SL + 1>(Rn, Pc, Sc, pa, pb, SL == 0 ? x1 : (SL == 1 ? x2 : x3));
-        }
-        decode_kstep<2>(F0, Rc, sel);
-        mfma16(acc, F1);
-        kstep_schedule<16, 0, 4>();
-        __builtin_amdgcn_sched_barrier(0);
-        if (SL == 3) L.issue<6, 12, false>(ldP, ldS, stage_of(G + 2));
-        decode_kstep<3>(F1, Rc, sel);
-        mfma16(acc, F0);
-        kstep_schedule<0, 0, 4>();
-        __builtin_amdgcn_sched_barrier(0);
-        if (SL == 3) L.issue<12, kSupPayLoads, true>(ldP, ldS, stage_of(G + 2));
-        decode_kstep<0>(F0, Rn, sel);
-        mfma16(acc, F1);
-        kstep_schedule<0, 0, 4>();
-        __builtin_amdgcn_sched_barrier(0);
-    };
-    using I0 = std::integral_constant<int, 0>;
-    using I1 = std::integral_constant<int, 1>;
-    using I2 = std::integral_constant<int, 2>;
-    using I3 = std::integral_constant<int, 3>;
-    auto stage = [&](int64_t G, const uint8_t* Pc, const uint8_t* Sc, const uint8_t* Pn,
-                     const uint8_t* Sn, uint32_t ldP, uint32_t ldS) {
-        slice(I0{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R0, R1);
-        slice(I1{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R1, R0);
-        slice(I2{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R0, R1);
-        slice(I3{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R1, R0);
-    };
-    int64_t G = g0;
-    for (; G + 1 < g1; G += 2) {
-        stage(G, sP0, sC0, sP1, sC1, P0, S0);
-        stage(G + 1, sP1, sC1, sP0, sC0, P1, S1);
+    // prologue: stages 0 and 1 of the first item in flight, stage 0 complete
+    // everywhere
+    {
+        const WorkItem w = work_item(item_at(0), sp, NG);
+        const SupSrc q = src_of(w.t);
+        L.issue<0, kSupPayLoads, true>(P0, S0, q, w.g0);
+        L.issue<0, kSupPayLoads, true>(P1, S1, q, min(w.g0 + 1, w.g1 - 1));
+        wait_vmem<kSupLoads>();
+        __syncthreads();
     }
-    if (G < g1) stage(G, sP0, sC0, sP1, sC1, P0, S0);   // odd stage count
-    wait_vmem<0>();                                // no load outlives the kernel's LDS
 
-    // ---- epilogue: C = alpha * value ----------------------------------------
-    // Element e of accumulator (i, j) is row 32i + 8(e/4) + 4(l/32) + e%4,
-    // column 32j + l%32 of the wave's 128 x 128 block.
-    const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;   // operands were scaled by 2^-3
-    const int64_t mw = m0 + wm * 128, nw = n0 + wn * 128;
-    auto store_tile = [&](auto value) {
+    // Only the item position is carried from one item to the next; everything
+    // else is rebuilt from it, which keeps the registers free for the
+    // epilogue.  The item's first stage is in buffer 0 and complete.
+    for (int k = 0;; ++k) {
+        const int it = item_at(k);
+        const WorkItem cur = work_item(it, sp, NG);
+        const SupSrc scur = src_of(cur.t);
+        const bool has_next = k + 1 < nw;
+        const WorkItem nxt = work_item(has_next ? item_at(k + 1) : it, sp, NG);
+        const SupSrc snxt = src_of(nxt.t);
+        read_sup_slice<0>(R0, sP0, sC0, pa, pb, x0);
+        decode_kstep<0>(F0, R0, sel);
+        // stage index of the load sequence -> (source, stage): this item's,
+        // the next item's first stages, or (no next item) this item's last
+        // again; chosen by selects so that the stage code stays branch-free
+        const int gshift = has_next ? nxt.g0 - cur.g1 : -1;
+        const int gclamp = has_next ? 0x7FFFFFFF : cur.g1 - 1;
+
+        auto issue_for = [&](auto I0c, auto I1c, auto SCc, uint32_t ldP, uint32_t ldS, int Gt) {
+            constexpr int I0v = decltype(I0c)::value, I1v = decltype(I1c)::value;
+            constexpr bool SCv = decltype(SCc)::value;
+            const bool in_cur = Gt < cur.g1;
+            const int Gl = in_cur ? Gt : min(Gt + gshift, gclamp);
+            SupSrc q;
+            q.off0 = in_cur ? scur.off0 : snxt.off0;
+            q.so0 = in_cur ? scur.so0 : snxt.so0;
+            q.so1 = in_cur ? scur.so1 : snxt.so1;
+            L.issue<I0v, I1v, SCv>(ldP, ldS, q, Gl);
+        };
+
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int64_t n = nw + j * 32 + r;
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int64_t m = mw + i * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-                    if (m < M && n < N) {
-                        const float v = alpha * value(i, j, e);
-                        if (OUT_BF16) {
-                            const uint32_t b = __float_as_uint(v);
-                            const uint32_t rb16 = (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
-                            reinterpret_cast<uint16_t*>(C)[m * N + n] = (uint16_t)rb16;
+                for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+        // One slice.  Slices 0..2 of a stage read the next slice of the same
+        // stage; slice 3 first waits for the next stage (loaded during the
+        // previous stage), synchronizes, starts the loads of stage G+2 into
+        // the buffer just consumed, and reads slice 0 of the next stage.
+        auto slice = [&](auto SLc, int G, const uint8_t* Pc, const uint8_t* Sc, const uint8_t* Pn,
+                         const uint8_t* Sn, uint32_t ldP, uint32_t ldS, RegSlice& Rc, RegSlice& Rn) {
+            constexpr int SL = decltype(SLc)::value;
+            using Z = std::integral_constant<int, 0>;
+            using C6 = std::integral_constant<int, 6>;
+            using C12 = std::integral_constant<int, 12>;
+            using CP = std::integral_constant<int, kSupPayLoads>;
+            using F = std::integral_constant<bool, false>;
+            using T = std::integral_constant<bool, true>;
+            decode_kstep<1>(F1, Rc, sel);
+            mfma16_t(acc, F0);
+            kstep_schedule<0, 0, 4>();
+            __builtin_amdgcn_sched_barrier(0);
+            if (SL == 3) {
+                wait_vmem<0>();
+                __syncthreads();
+                read_sup_slice<0>(Rn, Pn, Sn, pa, pb, x0);
+                issue_for(Z{}, C6{}, F{}, ldP, ldS, G + 2);
+            } else {
+                read_sup_slice<SL + 1>(Rn, Pc, Sc, pa, pb, SL == 0 ? x1 : (SL == 1 ? x2 : x3));
+            }
+            decode_kstep<2>(F0, Rc, sel);
+            mfma16_t(acc, F1);
+            kstep_schedule<16, 0, 4>();
+            __builtin_amdgcn_sched_barrier(0);
+            if (SL == 3) issue_for(C6{}, C12{}, F{}, ldP, ldS, G + 2);
+            decode_kstep<3>(F1, Rc, sel);
+            mfma16_t(acc, F0);
+            kstep_schedule<0, 0, 4>();
+            __builtin_amdgcn_sched_barrier(0);
+            if (SL == 3) issue_for(C12{}, CP{}, T{}, ldP, ldS, G + 2);
+            decode_kstep<0>(F0, Rn, sel);
+            mfma16_t(acc, F1);
+            kstep_schedule<0, 0, 4>();
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        using I0 = std::integral_constant<int, 0>;
+        using I1 = std::integral_constant<int, 1>;
+        using I2 = std::integral_constant<int, 2>;
+        using I3 = std::integral_constant<int, 3>;
+        auto stage = [&](int G, const uint8_t* Pc, const uint8_t* Sc, const uint8_t* Pn,
+                         const uint8_t* Sn, uint32_t ldP, uint32_t ldS) {
+            slice(I0{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R0, R1);
+            slice(I1{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R1, R0);
+            slice(I2{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R0, R1);
+            slice(I3{}, G, Pc, Sc, Pn, Sn, ldP, ldS, R1, R0);
+        };
+        int G = cur.g0;
+        for (; G + 1 < cur.g1; G += 2) {
+            stage(G, sP0, sC0, sP1, sC1, P0, S0);
+            stage(G + 1, sP1, sC1, sP0, sC0, P1, S1);
+        }
+        if (G < cur.g1) stage(G, sP0, sC0, sP1, sC1, P0, S0);   // odd stage count (single item)
+
+        // ---- epilogue --------------------------------------------------------
+        // Element e of accumulator (i, j) is row 32i + l%32, column
+        // 32j + 8(e/4) + 4(l/32) + e%4 of the wave's 128 x 128 block.  Stores
+        // go through buffer resources: an out-of-range offset drops the store,
+        // which masks rows and columns past C without branches.
+        if (cur.split_j >= 0) {
+            // one part of a leftover tile: fp32 partial, [acc (i, j)][run g]
+            // [lane][4] so that every store is 16 bytes per lane, 1 KB per wave
+            const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
+                sp.part + ((int64_t)cur.split_j * sp.parts + cur.part) * 65536, 0, 65536 * 4, 0x00020000);
+            const uint32_t vo = (uint32_t)(wave * 65536 + lane * 16);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const f32x4_t v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                                           acc[i][j][4 * g + 3]};
+                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), pr, vo,
+                                                               ((i * 4 + j) * 4 + g) * 1024, 0);
+                    }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
+            const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;   // operands were scaled by 2^-3
+            constexpr uint32_t esz = OUT_BF16 ? 2 : 4;
+            constexpr uint32_t kOff = 0x80000000u;               // past every buffer
+            const __amdgpu_buffer_rsrc_t cr =
+                __builtin_amdgcn_make_buffer_rsrc(C, 0, (int)((uint32_t)M * (uint32_t)N * esz), 0x00020000);
+            int64_t m0, n0;
+            tile_origin(cur.t, tiles_m, tiles_n, m0, n0);
+            const int mrow = (int)m0 + wm * 128 + r;
+            const int ncol = (int)n0 + wn * 128 + hi * 4;
+            const bool vec = (N & 3) == 0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int m = mrow + 32 * i;
+                const uint32_t rbase = ((uint32_t)m * (uint32_t)N + (uint32_t)ncol) * esz;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int n = ncol + 32 * j + 8 * g;
+                        const float v0 = alpha * acc[i][j][4 * g + 0], v1 = alpha * acc[i][j][4 * g + 1];
+                        const float v2 = alpha * acc[i][j][4 * g + 2], v3 = alpha * acc[i][j][4 * g + 3];
+                        const uint32_t imm = (uint32_t)(32 * j + 8 * g) * esz;
+                        if (vec) {
+                            // N % 4 == 0: a run is inside C or wholly past it
+                            const uint32_t vo = (m < M && n < N) ? rbase : kOff;
+                            if (OUT_BF16) {
+                                const u32x2_t d = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+                                __builtin_amdgcn_raw_buffer_store_b64(d, cr, vo + imm, 0, 0);
+                            } else {
+                                const f32x4_t d = {v0, v1, v2, v3};
+                                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, d), cr, vo + imm,
+                                                                       0, 0);
+                            }
                         } else {
-                            reinterpret_cast<float*>(C)[m * N + n] = v;
+                            const float vv[4] = {v0, v1, v2, v3};
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                const uint32_t vo = (m < M && n + q < N) ? rbase : kOff;
+                                if (OUT_BF16) {
+                                    __builtin_amdgcn_raw_buffer_store_b16(
+                                        (unsigned short)pack_bf16x2(vv[q], 0.0f), cr, vo + imm + q * esz, 0, 0);
+                                } else {
+                                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(vv[q]), cr,
+                                                                          vo + imm + q * esz, 0, 0);
+                                }
+                            }
                         }
                     }
-                }
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
-    };
-    if (split_j < 0) {
-        store_tile([&](int i, int j, int e) { return acc[i][j][e]; });
-        return;
+        if (!has_next) break;
     }
-    // one part of a leftover tile: fp32 partial, lane-major so that the
-    // stores coalesce
-    float* mine = sp.part + ((int64_t)split_j * sp.parts + part_idx) * 65536 + (int64_t)wave * 16384;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) mine[((i * 4 + j) * 16 + e) * 64 + lane] = acc[i][j][e];
+    wait_vmem<0>();                                  // no load outlives the kernel's LDS
 }
 
 // Sum of the partials of the split tiles, in part order, times alpha, into C.
-// Workgroup (tile j, block wv) covers the 128 x 128 block that wave wv of the
-// GEMM workgroups computed; thread t takes entries t + 256k of the block's
-// lane-major partial layout.
+// 64 workgroups per split tile, one per (wave block wv, accumulator (i, j)):
+// thread t covers row t/8 of that 32 x 32 block and its 4 columns 4(t%8)..+3,
+// so that 8 adjacent threads store 8 adjacent runs of one row.
 template <int BMODE, bool OUT_BF16>
 __global__ __launch_bounds__(256) void gemm_split_sum_kernel(
     int64_t M, int64_t N, int tiles_m, int tiles_n, SplitPlan sp, const float* __restrict__ a_dec,
     const float* __restrict__ b_dec, void* __restrict__ C) {
-    // 64 workgroups per split tile: (wave quarter wv, accumulator acc) pairs,
-    // 1024 partial floats each; a thread owns 4 consecutive lanes of one
-    // accumulator element, i.e. 4 adjacent output columns.
-    const int j = blockIdx.x >> 6, wv = (blockIdx.x >> 4) & 3, acc = blockIdx.x & 15;
+    const int j = blockIdx.x >> 6, wv = (blockIdx.x >> 4) & 3, ij = blockIdx.x & 15;
     int64_t m0, n0;
     tile_origin(sp.Tdp + j, tiles_m, tiles_n, m0, n0);
     const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;
-    const int o = acc * 1024 + threadIdx.x * 4;
-    const float* base = sp.part + (int64_t)j * sp.parts * 65536 + (int64_t)wv * 16384 + o;
+    const int row = threadIdx.x >> 3, c4 = threadIdx.x & 7;     // c4 = 2 g + lane half
+    const int lane = row + 32 * (c4 & 1), g = c4 >> 1;
+    const float* base = sp.part + (int64_t)j * sp.parts * 65536 + (int64_t)wv * 16384 +
+                        ((ij * 4 + g) * 64 + lane) * 4;
     float4 v = *reinterpret_cast<const float4*>(base);
     for (int p = 1; p < sp.parts; ++p) {
         const float4 u = *reinterpret_cast<const float4*>(base + (int64_t)p * 65536);
         v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
     }
-    const int lane = o & 63, e = (o >> 6) & 15;
-    const int64_t m = m0 + (wv >> 1) * 128 + (acc >> 2) * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-    const int64_t n = n0 + (wv & 1) * 128 + (acc & 3) * 32 + (lane & 31);
+    const int64_t m = m0 + (wv >> 1) * 128 + (ij >> 2) * 32 + row;
+    const int64_t n = n0 + (wv & 1) * 128 + (ij & 3) * 32 + 4 * c4;
     if (m >= M) return;
     const float r[4] = {alpha * v.x, alpha * v.y, alpha * v.z, alpha * v.w};
     if (OUT_BF16) {
-        uint16_t h[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const uint32_t b = __float_as_uint(r[q]);
-            h[q] = (uint16_t)((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
-        }
         uint16_t* dst = reinterpret_cast<uint16_t*>(C) + m * N + n;
         if ((N & 3) == 0 && n + 3 < N) {
-            *reinterpret_cast<uint2*>(dst) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+            *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
         } else {
-            for (int q = 0; q < 4; ++q) if (n + q < N) dst[q] = h[q];
+            for (int q = 0; q < 4; ++q)
+                if (n + q < N) dst[q] = (uint16_t)pack_bf16x2(r[q], 0.0f);
         }
     } else {
         float* dst = reinterpret_cast<float*>(C) + m * N + n;
         if ((N & 3) == 0 && n + 3 < N) {
             *reinterpret_cast<float4*>(dst) = make_float4(r[0], r[1], r[2], r[3]);
         } else {
-            for (int q = 0; q < 4; ++q) if (n + q < N) dst[q] = r[q];
+            for (int q = 0; q < 4; ++q)
+                if (n + q < N) dst[q] = r[q];
         }
     }
 }
@@ -1074,11 +1230,13 @@ hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
     // One workgroup per CU at a time (LDS-bound).  Split only a partial last
-    // wave of tiles that leaves at least 1 - 1/kSplitRemDiv of the CUs idle.
+    // wave of tiles that leaves at least 1 - 1/kSplitRemDiv of the CUs idle;
+    // parts cover whole stage pairs when the stage count is even.
+    const bool even = NG % 2 == 0;
     SplitPlan sp{T, 1, nullptr};
     const int rem = cus > 0 ? T % cus : 0;
     if (T > cus && rem > 0 && rem <= cus / kSplitRemDiv) {
-        const int parts = min(cus / rem, NG);
+        const int parts = min(cus / rem, even ? NG / 2 : NG);
         if (parts > 1) {
             sp.Tdp = T - rem;
             sp.parts = parts;
@@ -1086,9 +1244,12 @@ hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
             if (e != hipSuccess) return e;
         }
     }
-    const int grid = sp.Tdp + (T - sp.Tdp) * sp.parts;
+    const int items = sp.Tdp + (T - sp.Tdp) * sp.parts;
+    // persistent (one workgroup per CU walking the items) when every item has
+    // an even stage count, else one item per workgroup
+    const int grid = (even && cus > 0) ? min(items, cus) : items;
     hipLaunchKernelGGL((gemm_fp4_reg_kernel<BMODE, OUT_BF16>), dim3((unsigned)grid), dim3(kGemmThreads),
-                       0, s, M, N, K, tiles_m, tiles_n, sp, a, as, ad, b, bs, bd, c);
+                       0, s, (int)M, (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c);
     if ((e = hipGetLastError()) != hipSuccess || sp.parts == 1) return e;
     hipLaunchKernelGGL((gemm_split_sum_kernel<BMODE, OUT_BF16>), dim3((unsigned)(64 * (T - sp.Tdp))), dim3(256),
                        0, s, M, N, tiles_m, tiles_n, sp, ad, bd, c);
@@ -1119,7 +1280,9 @@ template <int BMODE>
 hipError_t launch_mode(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                        const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
                        void* c, bool c_bf16, hipStream_t s) {
-    if (K % (4 * BK) == 0 && K > 0)
+    // the register-decode kernel addresses operands and C with 32-bit offsets
+    const int64_t kLim = (int64_t)1 << 31;
+    if (K % (4 * BK) == 0 && K > 0 && M * (K / 2) < kLim && N * (K / 2) < kLim && M * N * 4 < kLim)
         return c_bf16 ? launch_reg<BMODE, true>(M, N, K, a, as, ad, b, bs, bd, c, s)
                       : launch_reg<BMODE, false>(M, N, K, a, as, ad, b, bs, bd, c, s);
     if (K % BK == 0 && K > 0)

@@ -80,8 +80,9 @@ def test_ragged_m_and_n():
         c = ue.gemm("nt", M, N, K, u8_to_dev(ar[0]), u8_to_dev(ar[1]), f32_scalar_dev(ar[2]),
                     u8_to_dev(wq[0]), u8_to_dev(wq[1]), f32_scalar_dev(wq[3]))
         gemm_check(host(c), ogemm.fprop(A, W, al), al, ogemm.abs_product(A, W), K, f"nt {M}x{N}x{K}")
-    # TN with N not a multiple of 16 (row-scaled B); K = 64 and K = 512
-    for T, Mo, No in [(64, 40, 24), (512, 300, 40)]:
+    # TN with N not a multiple of 16 (row-scaled B); K = 64 and K = 512; the
+    # last case has N % 4 == 2, so its output rows end inside a run of 4
+    for T, Mo, No in [(64, 40, 24), (512, 300, 40), (512, 300, 42)]:
         dy = synthetic.gradient(4, T, Mo, 1e-3, 1.0)
         x = synthetic.activation(4, T, No, 1e-2, 50.0)
         dc = oq.quantize_1d(dy, 0, osc.amax(dy), 448.0, "sr", 1, 2)
@@ -199,8 +200,9 @@ def test_ffn_up_projection_sampled():
 
 def test_split_tail_tiles():
     """A partial last wave of tiles: 16 x 17 = 272 tiles of 256 x 256 on 256
-    CUs leave 16 tiles, which run split along K (4 parts of 1 stage each)
-    and are summed by the second kernel.  Every output is compared."""
+    CUs leave 16 tiles, which run split along K (2 parts of 2 stages each)
+    and are summed by the second kernel; 32 workgroups run a whole tile and
+    then a part.  Every output is compared."""
     say("gemm split tail")
     M, N, K = 4096, 4352, 1024
     a = synthetic.activation(13, M, K, 1e-2, 50.0)
@@ -220,3 +222,27 @@ def test_split_tail_tiles():
                 c16 = c.float().cpu().numpy().astype(np.float64)
                 ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
                 assert np.all(np.abs(c16 - ref) <= ulp * 1.01 + 1e-30), rep
+
+
+def test_persistent_several_tiles_per_workgroup():
+    """19 x 24 = 456 tiles on 256 CUs: the leftover 200 tiles are too many to
+    split, so 200 workgroups run two whole tiles each, the second one's first
+    stages loaded during the first one's last.  Every output is compared."""
+    say("gemm persistent")
+    M, N, K = 4864, 6144, 512
+    a = synthetic.activation(17, M, K, 1e-2, 50.0)
+    w = synthetic.weight(17, N, K)
+    ar = oq.quantize_1d(a, 1, osc.amax(a))
+    wq = oq.quantize_2d(w, osc.amax(w))
+    A, W = oq.decoded_1d(ar[0], ar[1], 1), oq.decoded_2d(wq[0], wq[1])
+    al = ogemm.alpha(ar[2], wq[3])
+    ref, ap = ogemm.fprop(A, W, al), ogemm.abs_product(A, W)
+    for out_dtype in [torch.float32, torch.bfloat16]:
+        c = ue.gemm("nt", M, N, K, u8_to_dev(ar[0]), u8_to_dev(ar[1]), f32_scalar_dev(ar[2]),
+                    u8_to_dev(wq[0]), u8_to_dev(wq[1]), f32_scalar_dev(wq[3]), out_dtype=out_dtype)
+        if out_dtype == torch.float32:
+            gemm_check(host(c), ref, al, ap, K, "persistent nt fp32")
+        else:
+            c16 = c.float().cpu().numpy().astype(np.float64)
+            ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
+            assert np.all(np.abs(c16 - ref) <= ulp * 1.01 + 1e-30)

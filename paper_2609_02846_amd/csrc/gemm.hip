@@ -1086,6 +1086,35 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
             const int mrow = (int)m0 + wm * 128 + r;
             const int ncol = (int)n0 + wn * 128 + hi * 4;
             const bool vec = (N & 3) == 0;
+            if (OUT_BF16 && (N & 7) == 0) {
+                // bf16 with N % 8 == 0: lanes l and l + 32 hold the two halves
+                // of each run of 8 columns; one lane-half swap per pair of runs
+                // gives lane l runs 0 and 2 and lane l + 32 runs 1 and 3 whole,
+                // so every store is 16 bytes per lane (32 per row).
+                const int ncol8 = (int)n0 + wn * 128 + hi * 8;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int m = mrow + 32 * i;
+                    const uint32_t rbase = ((uint32_t)m * (uint32_t)N + (uint32_t)ncol8) * 2u;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+#pragma unroll
+                        for (int q = 0; q < 2; ++q) {
+                            const int g0 = 2 * q, g1 = 2 * q + 1;
+                            const uint32_t x0 = pack_bf16x2(alpha * acc[i][j][4 * g0], alpha * acc[i][j][4 * g0 + 1]);
+                            const uint32_t x1 = pack_bf16x2(alpha * acc[i][j][4 * g0 + 2], alpha * acc[i][j][4 * g0 + 3]);
+                            const uint32_t y0 = pack_bf16x2(alpha * acc[i][j][4 * g1], alpha * acc[i][j][4 * g1 + 1]);
+                            const uint32_t y1 = pack_bf16x2(alpha * acc[i][j][4 * g1 + 2], alpha * acc[i][j][4 * g1 + 3]);
+                            const auto s0 = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
+                            const auto s1 = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
+                            const u32x4_t d = {(uint32_t)s0[0], (uint32_t)s1[0], (uint32_t)s0[1], (uint32_t)s1[1]};
+                            const int n = ncol8 + 32 * j + 16 * q;
+                            const uint32_t vo = (m < M && n < N) ? rbase : kOff;
+                            __builtin_amdgcn_raw_buffer_store_b128(d, cr, vo + (uint32_t)(32 * j + 16 * q) * 2u, 0, 0);
+                        }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            } else {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int m = mrow + 32 * i;
@@ -1125,6 +1154,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
                         }
                     }
                 __builtin_amdgcn_sched_barrier(0);
+            }
             }
         }
         if (!has_next) break;

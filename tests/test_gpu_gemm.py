@@ -93,6 +93,20 @@ def test_ragged_m_and_n():
                     u8_to_dev(xc[0]), u8_to_dev(xc[1]), f32_scalar_dev(xc[2]))
         gemm_check(host(c), ogemm.wgrad(dYc, Xc, al), al, ogemm.abs_product(dYc.T, Xc.T), T,
                    f"tn ragged {Mo}x{No}x{T}")
+    # bf16 output with N % 8 == 4 and N % 4 == 2 (the narrower store paths)
+    for T, Mo, No in [(512, 300, 44), (512, 300, 42)]:
+        dy = synthetic.gradient(5, T, Mo, 1e-3, 1.0)
+        x = synthetic.activation(5, T, No, 1e-2, 50.0)
+        dc = oq.quantize_1d(dy, 0, osc.amax(dy), 448.0, "sr", 1, 2)
+        xc = oq.quantize_1d(x, 0, osc.amax(x))
+        dYc, Xc = oq.decoded_1d(dc[0], dc[1], 0), oq.decoded_1d(xc[0], xc[1], 0)
+        al = ogemm.alpha(dc[2], xc[2])
+        c = ue.gemm("tn", Mo, No, T, u8_to_dev(dc[0]), u8_to_dev(dc[1]), f32_scalar_dev(dc[2]),
+                    u8_to_dev(xc[0]), u8_to_dev(xc[1]), f32_scalar_dev(xc[2]), out_dtype=torch.bfloat16)
+        ref = ogemm.wgrad(dYc, Xc, al)
+        c16 = c.float().cpu().numpy().astype(np.float64)
+        ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
+        assert np.all(np.abs(c16 - ref) <= ulp * 1.01 + 1e-30), f"tn bf16 {Mo}x{No}x{T}"
 
 
 def test_k_zero_writes_zeros():

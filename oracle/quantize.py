@@ -31,6 +31,20 @@ dimension for activations and gradients, 2D 16x16 tiles for weights):
 
 SR words: element (r, c) of an R x C source uses ``philox.sr_words(seed,
 tensor_id, r * C + c)``, independent of the blocking.
+
+Comparison scale formats (``fmt``; Sec. 2, Table tab:formats):
+
+* ``"ue5m3"`` (default): the recipe above, blocks of 16.
+* ``"e4m3"``: the NVFP4 arrangement -- blocks of 16 with an E4M3 block scale
+  under the FP32 tensor scale.  Same steps with step 3 the nearest E4M3 code
+  (ties to even, saturating at 448) and the zero rule giving the E4M3 code
+  of 1.0 (0x38).
+* ``"e8m0"``: the MXFP4 arrangement -- blocks of 32, a power-of-two E8M0
+  block scale and no tensor scale (dec = 1).  The paper gives no exponent
+  rule; this oracle takes the OCP microscaling one: with a_B > 0,
+  E = clamp(floor(log2 a_B) - 2, -127, 127) (2 = exponent of E2M1's largest
+  value 6), code = E + 127, r_B = 2**-E, y_i = x_i * r_B (exact), so
+  |y| < 8 and E2M1 saturation clips (6, 8) to 6; a_B = 0 gives code 0.
 """
 
 import numpy as np
@@ -38,23 +52,62 @@ import numpy as np
 from . import formats, philox, scaling
 
 
-def _block_codes(xb, S, G, mode, words, chunk=1 << 16):
+FORMATS = ("ue5m3", "e4m3", "e8m0")
+
+
+def block_size(fmt):
+    """Elements per block (1D) for a scale format."""
+    if fmt not in FORMATS:
+        raise ValueError(fmt)
+    return 32 if fmt == "e8m0" else 16
+
+
+def scale_decode(fmt, code):
+    """Value of block-scale codes of a format (float64)."""
+    if fmt == "ue5m3":
+        return formats.ue5m3_decode(code)
+    if fmt == "e4m3":
+        return formats.e4m3_decode(code)
+    if fmt == "e8m0":
+        return formats.e8m0_decode(code)
+    raise ValueError(fmt)
+
+
+def _e8m0_codes(a_B):
+    """OCP microscaling exponent of each block maximum (module header)."""
+    a = np.asarray(a_B, dtype=np.float64)
+    _, e = np.frexp(a)                                      # a = m 2**e, m in [0.5, 1)
+    E = np.clip(e.astype(np.int64) - 1 - 2, -127, 127)
+    return np.where(a > 0, E + 127, 0).astype(np.uint8)
+
+
+def _block_codes(xb, S, G, mode, words, fmt="ue5m3", chunk=1 << 16):
     """xb: float32 [nb, B].  Returns (scale codes uint8 [nb], nibbles [nb, B]).
     Blocks are independent; large inputs are processed ``chunk`` blocks at a
     time only to bound memory."""
     xb = np.asarray(xb, dtype=np.float32)
     if xb.shape[0] > chunk:
         parts = [_block_codes(xb[i:i + chunk], S, G, mode,
-                              None if words is None else words[i:i + chunk], chunk)
+                              None if words is None else words[i:i + chunk], fmt, chunk)
                  for i in range(0, xb.shape[0], chunk)]
         return (np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts]))
     a_B = np.max(np.abs(xb), axis=1) if xb.shape[1] else np.zeros(xb.shape[0], np.float32)
     with np.errstate(over="ignore", invalid="ignore"):
-        u_B = (a_B * np.float32(S)).astype(np.float32)
-        code = formats.ue5m3_encode_rne_sat(u_B)
-        code = np.where(code == 0, formats.UE5M3_ONE, code).astype(np.uint8)
-        s_hat = formats.ue5m3_decode(code).astype(np.float32)
-        r_B = (np.float32(G) / s_hat).astype(np.float32)
+        if fmt == "e8m0":
+            code = _e8m0_codes(a_B)
+            r_B = np.ldexp(np.float32(1.0), 127 - code.astype(np.int32)).astype(np.float32)
+        else:
+            u_B = (a_B * np.float32(S)).astype(np.float32)
+            if fmt == "ue5m3":
+                code = formats.ue5m3_encode_rne_sat(u_B)
+                code = np.where(code == 0, formats.UE5M3_ONE, code).astype(np.uint8)
+            elif fmt == "e4m3":
+                code = formats.e4m3_encode_rne_sat(u_B)
+                code = np.where(code == 0, formats.E4M3_ONE, code).astype(np.uint8)
+            else:
+                raise ValueError(fmt)
+            s_hat = scale_decode(fmt, code).astype(np.float32)
+            r_B = (np.float32(G) / s_hat).astype(np.float32)
         y = (xb * r_B[:, None]).astype(np.float32)
     if mode == "rn":
         nib = formats.e2m1_encode_rne(y)
@@ -88,37 +141,46 @@ def _words_for(shape, seed, tensor_id, mode, elem_index):
     return philox.sr_words(seed, tensor_id, np.asarray(elem_index, np.int64))
 
 
-def quantize_1d(x_bits, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0, elem_index=None):
-    """1D block-16 quantization of a bf16 matrix.  Returns
-    (payload, scales, dec) in the layouts described in the module header.
-    ``elem_index`` (SR only) gives each element's row-major index in the
-    source tensor when ``x_bits`` is a sampled part of it (default: x itself
-    is the source)."""
+def quantize_1d(x_bits, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0, elem_index=None,
+                fmt="ue5m3"):
+    """1D block quantization of a bf16 matrix (blocks of 16, or 32 for
+    E8M0).  Returns (payload, scales, dec) in the layouts described in the
+    module header.  ``elem_index`` (SR only) gives each element's row-major
+    index in the source tensor when ``x_bits`` is a sampled part of it
+    (default: x itself is the source).  E8M0 ignores g and target (no tensor
+    scale) and returns dec = 1."""
     x = scaling.bf16_to_f32(x_bits)
     R, C = x.shape
-    S, G, dec = scaling.tensor_multipliers(g, target)
+    B = block_size(fmt)
+    if fmt == "e8m0":
+        S, G, dec = np.float32(1.0), np.float32(1.0), np.float32(1.0)
+    else:
+        S, G, dec = scaling.tensor_multipliers(g, target)
     words = _words_for((R, C), seed, tensor_id, mode, elem_index)
     if axis == 1:
-        if C % 16:
-            raise ValueError("cols must be a multiple of 16")
-        xb = x.reshape(R * (C // 16), 16)
-        wb = None if words is None else words.reshape(R * (C // 16), 16)
-        code, nib = _block_codes(xb, S, G, mode, wb)
-        return _pack_rows(nib.reshape(R, C)), code.reshape(R, C // 16), dec
+        if C % B:
+            raise ValueError(f"cols must be a multiple of {B}")
+        xb = x.reshape(R * (C // B), B)
+        wb = None if words is None else words.reshape(R * (C // B), B)
+        code, nib = _block_codes(xb, S, G, mode, wb, fmt)
+        return _pack_rows(nib.reshape(R, C)), code.reshape(R, C // B), dec
     if axis == 0:
-        if R % 16:
-            raise ValueError("rows must be a multiple of 16")
+        if R % B:
+            raise ValueError(f"rows must be a multiple of {B}")
         xt = np.ascontiguousarray(x.T)                     # [C, R]
-        xb = xt.reshape(C * (R // 16), 16)
-        wb = None if words is None else np.ascontiguousarray(words.T).reshape(C * (R // 16), 16)
-        code, nib = _block_codes(xb, S, G, mode, wb)
-        return _pack_rows(nib.reshape(C, R)), code.reshape(C, R // 16), dec
+        xb = xt.reshape(C * (R // B), B)
+        wb = None if words is None else np.ascontiguousarray(words.T).reshape(C * (R // B), B)
+        code, nib = _block_codes(xb, S, G, mode, wb, fmt)
+        return _pack_rows(nib.reshape(C, R)), code.reshape(C, R // B), dec
     raise ValueError("axis must be 0 or 1")
 
 
-def quantize_2d(x_bits, g, target=448.0, mode="rn", seed=0, tensor_id=0, elem_index=None):
-    """16x16 tile quantization.  Returns (payload [R, C/2], scales
-    [R/16, C/16], payload_t [C, R/2], dec)."""
+def quantize_2d(x_bits, g, target=448.0, mode="rn", seed=0, tensor_id=0, elem_index=None,
+                fmt="ue5m3"):
+    """16x16 tile quantization (UE5M3 or E4M3 scales).  Returns (payload
+    [R, C/2], scales [R/16, C/16], payload_t [C, R/2], dec)."""
+    if fmt not in ("ue5m3", "e4m3"):
+        raise ValueError("2D tiles take UE5M3 or E4M3 scales")
     x = scaling.bf16_to_f32(x_bits)
     R, C = x.shape
     if R % 16 or C % 16:
@@ -129,33 +191,33 @@ def quantize_2d(x_bits, g, target=448.0, mode="rn", seed=0, tensor_id=0, elem_in
     wt = None
     if words is not None:
         wt = words.reshape(R // 16, 16, C // 16, 16).transpose(0, 2, 1, 3).reshape(-1, 256)
-    code, nib = _block_codes(tiles, S, G, mode, wt)
+    code, nib = _block_codes(tiles, S, G, mode, wt, fmt)
     nib = nib.reshape(R // 16, C // 16, 16, 16).transpose(0, 2, 1, 3).reshape(R, C)
     return (_pack_rows(nib), code.reshape(R // 16, C // 16),
             _pack_rows(np.ascontiguousarray(nib.T)), dec)
 
 
 # ------------------------------------------------------ dequantization ----
-def decoded_1d(payload, scales, axis):
+def decoded_1d(payload, scales, axis, fmt="ue5m3"):
     """Decoded operand q * s_B (float64, exact) in the logical [R, C] shape
     of the tensor that ``quantize_1d`` consumed."""
     q = formats.e2m1_decode(_unpack_rows(payload))         # [rows_stored, L]
-    s = formats.ue5m3_decode(scales)
-    v = q * np.repeat(s, 16, axis=1)
+    s = scale_decode(fmt, scales)
+    v = q * np.repeat(s, block_size(fmt), axis=1)
     return v if axis == 1 else np.ascontiguousarray(v.T)
 
 
-def decoded_2d(payload, scales):
+def decoded_2d(payload, scales, fmt="ue5m3"):
     """Decoded weight q * s_tile (float64, exact), logical [R, C]."""
     q = formats.e2m1_decode(_unpack_rows(payload))
-    s = formats.ue5m3_decode(scales)
+    s = scale_decode(fmt, scales)
     return q * np.repeat(np.repeat(s, 16, axis=0), 16, axis=1)
 
 
-def decoded_2d_t(payload_t, scales):
+def decoded_2d_t(payload_t, scales, fmt="ue5m3"):
     """Decoded weight from the transposed payload, logical [R, C]."""
     q = formats.e2m1_decode(_unpack_rows(payload_t)).T
-    s = formats.ue5m3_decode(scales)
+    s = scale_decode(fmt, scales)
     return q * np.repeat(np.repeat(s, 16, axis=0), 16, axis=1)
 
 

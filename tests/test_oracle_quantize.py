@@ -185,3 +185,100 @@ def test_sr_deterministic_and_keyed():
     col = quantize.quantize_1d(bits, 0, g, 448.0, "sr", seed=1, tensor_id=1)
     rowT = quantize.quantize_1d(np.ascontiguousarray(bits.T), 1, g, 448.0, "sr", seed=1, tensor_id=1)
     assert np.array_equal(col[1], rowT[1])
+
+
+# ------------------------------------------ comparison scale formats ----
+def _format_blocks(golden_dir):
+    out = []
+    for line in open(os.path.join(golden_dir, "worked_blocks_formats.txt")):
+        if not line.strip() or line.startswith("#"):
+            continue
+        name, fmt, g, T, xs, sc, pay = [f.strip() for f in line.split("|")]
+        B = quantize.block_size(fmt)
+        x = np.zeros(B, np.float32)
+        vals = [float(v) for v in xs.split()]
+        x[:len(vals)] = vals
+        out.append((name, fmt, float(g), float(T), x, int(sc, 16),
+                    np.array([int(b, 16) for b in pay.split()], np.uint8)))
+    return out
+
+
+def test_worked_blocks_comparison_formats(golden_dir):
+    blocks = _format_blocks(golden_dir)
+    assert {b[1] for b in blocks} == {"e4m3", "e8m0"} and len(blocks) == 11
+    for name, fmt, g, T, x, sc, pay in blocks:
+        bits = synthetic.f32_to_bf16_bits(x)
+        assert np.array_equal(synthetic.bf16_bits_to_f32(bits).view(np.uint32), x.view(np.uint32)), name
+        p, s, dec = quantize.quantize_1d(bits[None, :], 1, np.float32(g), T, fmt=fmt)
+        assert s.shape == (1, 1) and s[0, 0] == sc, (name, hex(s[0, 0]))
+        assert np.array_equal(p[0], pay), (name, p[0])
+        if fmt == "e8m0":
+            assert dec == 1.0
+        pc, scc, _ = quantize.quantize_1d(bits[:, None], 0, np.float32(g), T, fmt=fmt)
+        assert scc[0, 0] == sc and np.array_equal(pc[0], pay), name
+        if fmt == "e4m3":
+            tile = np.zeros((16, 16), np.uint16)
+            tile[3] = bits
+            p2, s2, pt2, _ = quantize.quantize_2d(tile, np.float32(g), T, fmt=fmt)
+            assert s2[0, 0] == sc and np.array_equal(p2[3], pay), name
+
+
+def test_e4m3_pipeline_differs_from_ue5m3_only_in_the_scale_code():
+    # Inside E4M3's range the two 3-fraction-bit scales pick the same value,
+    # so payloads agree; they part only where E4M3 saturates (448) or
+    # underflows (2^-9) and UE5M3 does not (Sec. 3, Table 2).
+    rng = np.random.default_rng(5)
+    x = (rng.standard_normal((64, 256)) * np.exp(rng.uniform(-3, 3, (64, 1)))).astype(np.float32)
+    bits = synthetic.f32_to_bf16_bits(x)
+    g = scaling.amax(bits)
+    pu, su, du = quantize.quantize_1d(bits, 1, g, 448.0)
+    pe, se, de = quantize.quantize_1d(bits, 1, g, 448.0, fmt="e4m3")
+    vu, ve = formats.ue5m3_decode(su), formats.e4m3_decode(se)
+    inside = (vu >= 2.0 ** -6) & (vu <= 448.0)          # both normal, E4M3 not saturated
+    assert inside.mean() > 0.5
+    assert np.array_equal(vu[inside], ve[inside]) and du == de
+    rows = np.all(inside, axis=1)
+    assert np.array_equal(pu[rows], pe[rows])
+
+
+def test_e8m0_exponent_rule_properties():
+    # OCP microscaling exponent: 2^(E+2) <= a_B < 2^(E+3) (unclamped), the
+    # scaled block maximum lies in [4, 8), and y = x * 2^-E is exact.
+    rng = np.random.default_rng(6)
+    x = (rng.standard_normal((128, 64)) * np.exp2(rng.integers(-40, 40, (128, 1)))).astype(np.float32)
+    x[5] = 0.0
+    bits = synthetic.f32_to_bf16_bits(x)
+    xf = synthetic.bf16_bits_to_f32(bits).astype(np.float64)
+    p, s, dec = quantize.quantize_1d(bits, 1, np.float32(0), 0.0, fmt="e8m0")
+    assert s.shape == (128, 2) and dec == 1.0
+    a = np.abs(xf).reshape(128, 2, 32).max(axis=2)
+    E = s.astype(np.int64) - 127
+    nz = a > 0
+    assert np.all(np.exp2(E[nz] + 2.0) <= a[nz]) and np.all(a[nz] < np.exp2(E[nz] + 3.0))
+    assert np.all(s[~nz] == 0)
+    q = formats.e2m1_decode(quantize._unpack_rows(p)).reshape(128, 2, 32)
+    y = xf.reshape(128, 2, 32) * np.exp2(-E)[:, :, None]
+    # RN error: each nibble is a nearest E2M1 value of y (saturating at 6)
+    err = np.abs(np.clip(y, -6, 6) - q)
+    step = np.where(np.abs(y) < 2, 0.5, np.where(np.abs(y) < 4, 1.0, 2.0))
+    assert np.all(err <= step / 2 + 1e-12)
+    # decoded operand = q * 2^E
+    dec_v = quantize.decoded_1d(p, s, 1, fmt="e8m0")
+    assert np.array_equal(dec_v.reshape(128, 2, 32), q * np.exp2(E)[:, :, None])
+
+
+def test_e8m0_sr_uses_the_element_words():
+    # SR under E8M0 draws the same per-element words as under UE5M3
+    rng = np.random.default_rng(7)
+    x = rng.standard_normal((32, 64)).astype(np.float32)
+    bits = synthetic.f32_to_bf16_bits(x)
+    p1, s1, _ = quantize.quantize_1d(bits, 1, np.float32(0), 0.0, mode="sr", seed=9, tensor_id=4, fmt="e8m0")
+    p2, s2, _ = quantize.quantize_1d(bits, 1, np.float32(0), 0.0, mode="sr", seed=9, tensor_id=4, fmt="e8m0")
+    p3, _, _ = quantize.quantize_1d(bits, 1, np.float32(0), 0.0, mode="sr", seed=10, tensor_id=4, fmt="e8m0")
+    assert np.array_equal(p1, p2) and not np.array_equal(p1, p3)
+    xf = synthetic.bf16_bits_to_f32(bits).astype(np.float64)
+    E = s1.astype(np.int64) - 127
+    y = xf.reshape(32, 2, 32) * np.exp2(-E)[:, :, None]
+    q = formats.e2m1_decode(quantize._unpack_rows(p1)).reshape(32, 2, 32)
+    # SR lands on one of the two E2M1 neighbours of y (6 at or above 6)
+    assert np.all(np.abs(np.abs(q) - np.minimum(np.abs(y), 6.0)) <= np.where(np.abs(y) < 2, 0.5, 2.0))

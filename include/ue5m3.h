@@ -188,6 +188,80 @@ ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K
                           const uint8_t* b, const uint8_t* b_scales, const float* b_dec,
                           void* c, ue5m3_out_t c_type, hipStream_t stream);
 
+/*
+ * Comparison block-scale formats (Sec. 2, Table tab:formats: the MXFP4 and
+ * NVFP4 arrangements of the same E2M1 payload).
+ *   UE5M3_SCALE_UE5M3  the recipe: blocks of 16, UE5M3 scales, tensor scale
+ *                      (the calls above).
+ *   UE5M3_SCALE_E4M3   blocks of 16 with an E4M3 block scale (OCP E4M3FN:
+ *                      bias 7, largest 448 = 0x7E, smallest subnormal 2^-9)
+ *                      under the same FP32 tensor scale: the per-block
+ *                      arithmetic of ue5m3_quantize_1d with s = E4M3(u)
+ *                      (nearest, ties to even, saturating above 448) and
+ *                      the zero code replaced by 0x38 (1.0).
+ *   UE5M3_SCALE_E8M0   blocks of 32 with a power-of-two E8M0 scale (value
+ *                      2^(code - 127)) and no tensor scale: for a block
+ *                      maximum a > 0, E = clamp(floor(log2 a) - 2, -127, 127)
+ *                      (the OCP microscaling rule; 2 is the exponent of the
+ *                      largest E2M1 value), code = E + 127, y_i = x_i * 2^-E
+ *                      (exact); a = 0 gives code 0.  amax_dev and target
+ *                      are ignored (amax_dev may be null) and dec_out
+ *                      receives 1.
+ */
+typedef enum {
+    UE5M3_SCALE_UE5M3 = 0,
+    UE5M3_SCALE_E4M3 = 1,
+    UE5M3_SCALE_E8M0 = 2
+} ue5m3_scale_kind_t;
+
+/*
+ * ue5m3_quantize_1d with a scale format.  Blocks are `block` elements long:
+ * 16 for UE5M3 and E4M3, 32 for E8M0 (EINVAL otherwise).  Layouts as in
+ * ue5m3_quantize_1d with 16 replaced by `block` (axis 1: cols % block == 0,
+ * scales [rows, cols/block]; axis 0: rows % block == 0, cols % 2 == 0,
+ * transposed payload [cols, rows/2] and scales [cols, rows/block]).
+ */
+ue5m3_status_t ue5m3_quantize_1d_ex(const void* x_bf16, int64_t rows, int64_t cols,
+                                    int32_t axis, const float* amax_dev, float target,
+                                    ue5m3_round_t mode, uint64_t seed, uint32_t tensor_id,
+                                    ue5m3_scale_kind_t scale_kind, int32_t block,
+                                    uint8_t* payload, uint8_t* scales, float* dec_out,
+                                    hipStream_t stream);
+
+/*
+ * ue5m3_quantize_2d with a scale format: UE5M3 or E4M3 (block 16); E8M0
+ * weights are quantized in 1D blocks of 32 along each GEMM's contraction
+ * dimension instead (ue5m3_quantize_1d_ex on W, axis 1 for fprop and axis 0
+ * for dgrad), so E8M0 here is EINVAL.
+ */
+ue5m3_status_t ue5m3_quantize_2d_ex(const void* w_bf16, int64_t rows, int64_t cols,
+                                    const float* amax_dev, float target,
+                                    ue5m3_round_t mode, uint64_t seed, uint32_t tensor_id,
+                                    ue5m3_scale_kind_t scale_kind,
+                                    uint8_t* payload, uint8_t* scales, uint8_t* payload_t,
+                                    uint8_t* scales_t, float* dec_out, hipStream_t stream);
+
+/*
+ * ue5m3_gemm with a scale format; both operands use it.
+ *   UE5M3, E4M3: operands and requirements exactly as for ue5m3_gemm.
+ *   E8M0: every layout takes A as [M, K/2] payload with [M, K/32] scales and
+ *         B as [N, K/2] payload with [N, K/32] scales, both blocked along the
+ *         contraction:
+ *           NT fprop: a = quantize_1d_ex(X, axis 1), b = quantize_1d_ex(W, axis 1)
+ *           NN dgrad: a = quantize_1d_ex(dY, axis 1), b = quantize_1d_ex(W, axis 0)
+ *           TN wgrad: a = quantize_1d_ex(dY, axis 0), b = quantize_1d_ex(X, axis 0)
+ *         The products run on the gfx950 scaled FP4 matrix instructions,
+ *         which apply the E8M0 powers of two themselves.  Requires
+ *         K % 256 == 0, and M*K/2, N*K/2 and 4*M*N each below 2^31 (ESHAPE
+ *         otherwise); a_dec and b_dec hold the decode multipliers (1 from the
+ *         E8M0 quantizers).  Workspace as for ue5m3_gemm.
+ */
+ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
+                             const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
+                             const uint8_t* b, const uint8_t* b_scales, const float* b_dec,
+                             void* c, ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind,
+                             hipStream_t stream);
+
 /* Static description of a status code. */
 const char* ue5m3_status_string(ue5m3_status_t status);
 

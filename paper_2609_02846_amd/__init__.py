@@ -23,10 +23,14 @@ NT, NN, TN = 0, 1, 2
 OUT_F32, OUT_BF16 = 0, 1
 _MODES = {"rn": RN, "sr": SR}
 _LAYOUTS = {"nt": NT, "nn": NN, "tn": TN}
+SCALE_UE5M3, SCALE_E4M3, SCALE_E8M0 = 0, 1, 2
+_FORMATS = {"ue5m3": SCALE_UE5M3, "e4m3": SCALE_E4M3, "e8m0": SCALE_E8M0}
+BLOCK = {"ue5m3": 16, "e4m3": 16, "e8m0": 32}
 
 EXPORTED_SYMBOLS = (
     "ue5m3_amax_state_init", "ue5m3_amax_state_reset", "ue5m3_amax_sample",
     "ue5m3_quantize_1d", "ue5m3_quantize_2d", "ue5m3_gemm",
+    "ue5m3_quantize_1d_ex", "ue5m3_quantize_2d_ex", "ue5m3_gemm_ex",
     "ue5m3_status_string", "ue5m3_version",
 )
 
@@ -70,6 +74,14 @@ def load_library(path=LIB_PATH):
     lib.ue5m3_quantize_2d.restype = i32
     lib.ue5m3_gemm.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, vp]
     lib.ue5m3_gemm.restype = i32
+    lib.ue5m3_quantize_1d_ex.argtypes = [vp, i64, i64, i32, vp, f32, i32, u64, u32, i32, i32,
+                                         vp, vp, vp, vp]
+    lib.ue5m3_quantize_1d_ex.restype = i32
+    lib.ue5m3_quantize_2d_ex.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, i32,
+                                         vp, vp, vp, vp, vp, vp]
+    lib.ue5m3_quantize_2d_ex.restype = i32
+    lib.ue5m3_gemm_ex.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp]
+    lib.ue5m3_gemm_ex.restype = i32
     lib.ue5m3_status_string.argtypes = [i32]
     lib.ue5m3_status_string.restype = ctypes.c_char_p
     lib.ue5m3_version.argtypes = []
@@ -143,33 +155,40 @@ def amax_sample(state, x, step, stream=None):
 
 
 def quantize_1d(x, axis, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0,
-                payload=None, scales=None, dec_out=None, stream=None):
-    """1D block-16 quantization (see ue5m3_quantize_1d).  Returns
-    (payload, scales, dec_out); axis 0 outputs are stored transposed."""
+                payload=None, scales=None, dec_out=None, stream=None, fmt="ue5m3"):
+    """1D block quantization (see ue5m3_quantize_1d and, for ``fmt`` "e4m3"
+    or "e8m0", ue5m3_quantize_1d_ex).  Returns (payload, scales, dec_out);
+    axis 0 outputs are stored transposed.  E8M0 takes no amax (None)."""
     _bf16_2d(x, "x")
     R, C = x.shape
+    B = BLOCK[fmt]
     if axis == 1:
-        pshape, sshape = (R, C // 2), (R, C // 16)
+        pshape, sshape = (R, C // 2), (R, C // B)
     else:
-        pshape, sshape = (C, R // 2), (C, R // 16)
+        pshape, sshape = (C, R // 2), (C, R // B)
     payload = _u8(pshape, x) if payload is None else payload
     scales = _u8(sshape, x) if scales is None else scales
     if dec_out is None:
         dec_out = torch.empty(1, dtype=torch.float32, device=x.device)
-    _check(load_library().ue5m3_quantize_1d(_ptr(x), R, C, int(axis), _ptr(amax_dev),
-                                            float(target), _MODES[mode], int(seed) & (2**64 - 1),
-                                            int(tensor_id) & 0xFFFFFFFF, _ptr(payload),
-                                            _ptr(scales), _ptr(dec_out), _stream(stream)),
-           "ue5m3_quantize_1d")
+    lib = load_library()
+    common = (_ptr(x), R, C, int(axis), _ptr(amax_dev), float(target), _MODES[mode],
+              int(seed) & (2**64 - 1), int(tensor_id) & 0xFFFFFFFF)
+    if fmt == "ue5m3":
+        st = lib.ue5m3_quantize_1d(*common, _ptr(payload), _ptr(scales), _ptr(dec_out), _stream(stream))
+    else:
+        st = lib.ue5m3_quantize_1d_ex(*common, _FORMATS[fmt], B, _ptr(payload), _ptr(scales),
+                                      _ptr(dec_out), _stream(stream))
+    _check(st, "ue5m3_quantize_1d")
     return payload, scales, dec_out
 
 
 def quantize_2d(w, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0, transposed=True,
                 payload=None, scales=None, payload_t=None, dec_out=None, scales_t=None,
-                stream=None):
-    """16x16 tile quantization (see ue5m3_quantize_2d).  Returns
-    (payload, scales, payload_t or None, dec_out, scales_t or None); the
-    transposed payload and scales are the dgrad operand."""
+                stream=None, fmt="ue5m3"):
+    """16x16 tile quantization (see ue5m3_quantize_2d; ``fmt`` "e4m3" uses
+    ue5m3_quantize_2d_ex).  Returns (payload, scales, payload_t or None,
+    dec_out, scales_t or None); the transposed payload and scales are the
+    dgrad operand."""
     _bf16_2d(w, "w")
     R, C = w.shape
     payload = _u8((R, C // 2), w) if payload is None else payload
@@ -180,27 +199,35 @@ def quantize_2d(w, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0, trans
         scales_t = _u8((C // 16, R // 16), w)
     if dec_out is None:
         dec_out = torch.empty(1, dtype=torch.float32, device=w.device)
-    _check(load_library().ue5m3_quantize_2d(_ptr(w), R, C, _ptr(amax_dev), float(target),
-                                            _MODES[mode], int(seed) & (2**64 - 1),
-                                            int(tensor_id) & 0xFFFFFFFF, _ptr(payload),
-                                            _ptr(scales), _ptr(payload_t), _ptr(scales_t),
-                                            _ptr(dec_out), _stream(stream)),
-           "ue5m3_quantize_2d")
+    lib = load_library()
+    common = (_ptr(w), R, C, _ptr(amax_dev), float(target), _MODES[mode], int(seed) & (2**64 - 1),
+              int(tensor_id) & 0xFFFFFFFF)
+    outs = (_ptr(payload), _ptr(scales), _ptr(payload_t), _ptr(scales_t), _ptr(dec_out), _stream(stream))
+    if fmt == "ue5m3":
+        st = lib.ue5m3_quantize_2d(*common, *outs)
+    else:
+        st = lib.ue5m3_quantize_2d_ex(*common, _FORMATS[fmt], *outs)
+    _check(st, "ue5m3_quantize_2d")
     return payload, scales, payload_t, dec_out, scales_t
 
 
 def gemm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
-         out_dtype=torch.float32, stream=None):
-    """Decoded-operand FP4 GEMM (see ue5m3_gemm); layout is "nt" (fprop),
-    "nn" (dgrad) or "tn" (wgrad).  Returns the [M, N] output tensor."""
+         out_dtype=torch.float32, stream=None, fmt="ue5m3"):
+    """Decoded-operand FP4 GEMM (see ue5m3_gemm and, for ``fmt`` "e4m3" or
+    "e8m0", ue5m3_gemm_ex); layout is "nt" (fprop), "nn" (dgrad) or "tn"
+    (wgrad).  Returns the [M, N] output tensor."""
     lay = _LAYOUTS[layout] if isinstance(layout, str) else int(layout)
     if out is None:
         out = torch.empty((M, N), dtype=out_dtype, device=a.device)
     ctype = OUT_BF16 if out.dtype == torch.bfloat16 else OUT_F32
     if out.dtype not in (torch.float32, torch.bfloat16) or not out.is_contiguous():
         raise ValueError("out must be a contiguous fp32 or bf16 tensor")
-    _check(load_library().ue5m3_gemm(lay, int(M), int(N), int(K), _ptr(a), _ptr(a_scales),
-                                     _ptr(a_dec), _ptr(b), _ptr(b_scales), _ptr(b_dec),
-                                     _ptr(out), ctype, _stream(stream)),
-           "ue5m3_gemm")
+    lib = load_library()
+    args = (lay, int(M), int(N), int(K), _ptr(a), _ptr(a_scales), _ptr(a_dec), _ptr(b), _ptr(b_scales),
+            _ptr(b_dec), _ptr(out), ctype)
+    if fmt == "ue5m3":
+        st = lib.ue5m3_gemm(*args, _stream(stream))
+    else:
+        st = lib.ue5m3_gemm_ex(*args, _FORMATS[fmt], _stream(stream))
+    _check(st, "ue5m3_gemm")
     return out

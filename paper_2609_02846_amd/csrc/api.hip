@@ -67,37 +67,54 @@ ue5m3_status_t ue5m3_amax_sample(ue5m3_amax_state_t* st, const void* x_bf16, int
     return UE5M3_OK;
 }
 
-ue5m3_status_t ue5m3_quantize_1d(const void* x_bf16, int64_t rows, int64_t cols, int32_t axis,
-                                 const float* amax_dev, float target, ue5m3_round_t mode,
-                                 uint64_t seed, uint32_t tensor_id, uint8_t* payload,
-                                 uint8_t* scales, float* dec_out, hipStream_t stream) {
+ue5m3_status_t ue5m3_quantize_1d_ex(const void* x_bf16, int64_t rows, int64_t cols, int32_t axis,
+                                    const float* amax_dev, float target, ue5m3_round_t mode,
+                                    uint64_t seed, uint32_t tensor_id, ue5m3_scale_kind_t scale_kind,
+                                    int32_t block, uint8_t* payload, uint8_t* scales, float* dec_out,
+                                    hipStream_t stream) {
     if (axis != 0 && axis != 1) return UE5M3_EINVAL;
     if (mode != UE5M3_RN && mode != UE5M3_SR) return UE5M3_EINVAL;
-    if (amax_dev == nullptr || !valid_target(target)) return UE5M3_EINVAL;
+    if (scale_kind != UE5M3_SCALE_UE5M3 && scale_kind != UE5M3_SCALE_E4M3 &&
+        scale_kind != UE5M3_SCALE_E8M0)
+        return UE5M3_EINVAL;
+    const bool e8 = scale_kind == UE5M3_SCALE_E8M0;
+    if (block != (e8 ? 32 : 16)) return UE5M3_EINVAL;
+    if (!e8 && (amax_dev == nullptr || !valid_target(target))) return UE5M3_EINVAL;
     if (rows < 0 || cols < 0) return UE5M3_ESHAPE;
-    if (axis == 1 && cols % 16 != 0) return UE5M3_ESHAPE;
-    if (axis == 0 && (rows % 16 != 0 || cols % 2 != 0)) return UE5M3_ESHAPE;
-    if (!aligned4(amax_dev) || (dec_out != nullptr && !aligned4(dec_out))) return UE5M3_EALIGN;
+    if (axis == 1 && cols % block != 0) return UE5M3_ESHAPE;
+    if (axis == 0 && (rows % block != 0 || cols % 2 != 0)) return UE5M3_ESHAPE;
+    if ((amax_dev != nullptr && !aligned4(amax_dev)) || (dec_out != nullptr && !aligned4(dec_out)))
+        return UE5M3_EALIGN;
     if (rows == 0 || cols == 0) return UE5M3_OK;
     if (x_bf16 == nullptr || payload == nullptr || scales == nullptr) return UE5M3_EINVAL;
     if (!aligned16(x_bf16) || !aligned16(payload) || !aligned16(scales)) return UE5M3_EALIGN;
     const bool sr = mode == UE5M3_SR;
+    const ue5m3::ScaleKind fmt = static_cast<ue5m3::ScaleKind>(scale_kind);
     hipError_t e;
     if (axis == 1)
-        e = ue5m3::launch_quant_rows(x_bf16, rows, cols, amax_dev, target, sr, seed, tensor_id,
+        e = ue5m3::launch_quant_rows(fmt, x_bf16, rows, cols, amax_dev, target, sr, seed, tensor_id,
                                      payload, scales, dec_out, stream);
     else
-        e = ue5m3::launch_quant_cols(x_bf16, rows, cols, amax_dev, target, sr, seed, tensor_id,
+        e = ue5m3::launch_quant_cols(fmt, x_bf16, rows, cols, amax_dev, target, sr, seed, tensor_id,
                                      payload, scales, dec_out, stream);
     return hip_status(e);
 }
 
-ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
+ue5m3_status_t ue5m3_quantize_1d(const void* x_bf16, int64_t rows, int64_t cols, int32_t axis,
                                  const float* amax_dev, float target, ue5m3_round_t mode,
                                  uint64_t seed, uint32_t tensor_id, uint8_t* payload,
-                                 uint8_t* scales, uint8_t* payload_t, uint8_t* scales_t,
-                                 float* dec_out, hipStream_t stream) {
+                                 uint8_t* scales, float* dec_out, hipStream_t stream) {
+    return ue5m3_quantize_1d_ex(x_bf16, rows, cols, axis, amax_dev, target, mode, seed, tensor_id,
+                                UE5M3_SCALE_UE5M3, 16, payload, scales, dec_out, stream);
+}
+
+ue5m3_status_t ue5m3_quantize_2d_ex(const void* w_bf16, int64_t rows, int64_t cols,
+                                    const float* amax_dev, float target, ue5m3_round_t mode,
+                                    uint64_t seed, uint32_t tensor_id, ue5m3_scale_kind_t scale_kind,
+                                    uint8_t* payload, uint8_t* scales, uint8_t* payload_t,
+                                    uint8_t* scales_t, float* dec_out, hipStream_t stream) {
     if (mode != UE5M3_RN && mode != UE5M3_SR) return UE5M3_EINVAL;
+    if (scale_kind != UE5M3_SCALE_UE5M3 && scale_kind != UE5M3_SCALE_E4M3) return UE5M3_EINVAL;
     if (amax_dev == nullptr || !valid_target(target)) return UE5M3_EINVAL;
     if (rows < 0 || cols < 0 || rows % 16 != 0 || cols % 16 != 0) return UE5M3_ESHAPE;
     if (!aligned4(amax_dev) || (dec_out != nullptr && !aligned4(dec_out))) return UE5M3_EALIGN;
@@ -107,15 +124,26 @@ ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
         (payload_t != nullptr && !aligned16(payload_t)) ||
         (scales_t != nullptr && !aligned16(scales_t)))
         return UE5M3_EALIGN;
-    return hip_status(ue5m3::launch_quant_tiles(w_bf16, rows, cols, amax_dev, target,
-                                                mode == UE5M3_SR, seed, tensor_id, payload,
-                                                scales, payload_t, scales_t, dec_out, stream));
+    return hip_status(ue5m3::launch_quant_tiles(static_cast<ue5m3::ScaleKind>(scale_kind), w_bf16, rows,
+                                                cols, amax_dev, target, mode == UE5M3_SR, seed,
+                                                tensor_id, payload, scales, payload_t, scales_t,
+                                                dec_out, stream));
 }
 
-ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
-                          const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
-                          const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,
-                          ue5m3_out_t c_type, hipStream_t stream) {
+ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
+                                 const float* amax_dev, float target, ue5m3_round_t mode,
+                                 uint64_t seed, uint32_t tensor_id, uint8_t* payload,
+                                 uint8_t* scales, uint8_t* payload_t, uint8_t* scales_t,
+                                 float* dec_out, hipStream_t stream) {
+    return ue5m3_quantize_2d_ex(w_bf16, rows, cols, amax_dev, target, mode, seed, tensor_id,
+                                UE5M3_SCALE_UE5M3, payload, scales, payload_t, scales_t, dec_out,
+                                stream);
+}
+
+ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
+                             const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
+                             const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,
+                             ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind, hipStream_t stream) {
     ue5m3::BScale bmode;
     switch (layout) {
         case UE5M3_NT: bmode = ue5m3::BScale::Tile; break;
@@ -123,9 +151,18 @@ ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K
         case UE5M3_TN: bmode = ue5m3::BScale::Row; break;
         default: return UE5M3_ELAYOUT;
     }
+    if (scale_kind != UE5M3_SCALE_UE5M3 && scale_kind != UE5M3_SCALE_E4M3 &&
+        scale_kind != UE5M3_SCALE_E8M0)
+        return UE5M3_EINVAL;
+    const bool e8 = scale_kind == UE5M3_SCALE_E8M0;
     if (c_type != UE5M3_OUT_F32 && c_type != UE5M3_OUT_BF16) return UE5M3_EINVAL;
     if (M < 0 || N < 0 || K < 0 || K % 16 != 0) return UE5M3_ESHAPE;
-    if (layout != UE5M3_TN && N % 16 != 0) return UE5M3_ESHAPE;
+    if (!e8 && layout != UE5M3_TN && N % 16 != 0) return UE5M3_ESHAPE;
+    if (e8) {
+        const int64_t lim = (int64_t)1 << 31;
+        if (K % 256 != 0 || M * (K / 2) >= lim || N * (K / 2) >= lim || 4 * M * N >= lim)
+            return UE5M3_ESHAPE;
+    }
     if (M == 0 || N == 0) return UE5M3_OK;
     if (c == nullptr || a_dec == nullptr || b_dec == nullptr) return UE5M3_EINVAL;
     if (K > 0 && (a == nullptr || a_scales == nullptr || b == nullptr || b_scales == nullptr))
@@ -133,8 +170,27 @@ ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K
     if (!aligned16(c) || !aligned4(a_dec) || !aligned4(b_dec)) return UE5M3_EALIGN;
     if (K > 0 && (!aligned16(a) || !aligned16(b) || !aligned16(a_scales) || !aligned16(b_scales)))
         return UE5M3_EALIGN;
-    return hip_status(ue5m3::launch_gemm(bmode, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c,
-                                         c_type == UE5M3_OUT_BF16, stream));
+    const bool bf = c_type == UE5M3_OUT_BF16;
+    if (e8) {
+        if (K == 0)   // no products: zeros, through the general kernel
+            return hip_status(ue5m3::launch_gemm(ue5m3::BScale::Row, 1.0f, M, N, K, a, a_scales, a_dec,
+                                                 b, b_scales, b_dec, c, bf, stream));
+        return hip_status(ue5m3::launch_gemm_mx(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, bf,
+                                                stream));
+    }
+    // UE5M3 codes decode with the operands scaled by 2^-3 (alpha * 2^6); E4M3
+    // codes read as UE5M3 are value / 2^8, so alpha * 2^22.
+    const float amul = scale_kind == UE5M3_SCALE_E4M3 ? 4194304.0f : 64.0f;
+    return hip_status(ue5m3::launch_gemm(bmode, amul, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c,
+                                         bf, stream));
+}
+
+ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
+                          const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
+                          const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,
+                          ue5m3_out_t c_type, hipStream_t stream) {
+    return ue5m3_gemm_ex(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_type,
+                         UE5M3_SCALE_UE5M3, stream);
 }
 
 }  // extern "C"

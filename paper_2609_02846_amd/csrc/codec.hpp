@@ -63,6 +63,49 @@ __device__ __forceinline__ float ue5m3_decode(uint32_t c) {
     return e ? nrm : sub;
 }
 
+// ---- comparison block-scale formats (Sec. 2, Table tab:formats) ----------
+// E4M3 (OCP E4M3FN: bias 7, largest finite 448 = 0x7E, 0x7F NaN, smallest
+// subnormal 2^-9) encode of a non-negative binary32 u: nearest code, ties to
+// the even code, every u above 448 saturating to 0x7E.
+constexpr float kE4M3Max = 448.0f;
+constexpr uint32_t kE4M3CodeMax = 0x7Eu;
+constexpr uint32_t kE4M3CodeOne = 0x38u;
+__device__ __forceinline__ uint32_t e4m3_encode(float u) {
+    // subnormal band [0, 2^-6): codes 0..8 are m * 2^-9
+    const uint32_t sub = (uint32_t)__builtin_rintf(u * 0x1p9f);
+    // normal band: fraction rounded to 3 bits (nearest-even), exponent
+    // rebased from 127 to 7; a carry lands on the next code
+    uint32_t b = __float_as_uint(u);
+    b += 0x7FFFFu + ((b >> 20) & 1u);
+    const uint32_t nrm = (b >> 20) - ((127u - 7u) << 3);
+    const uint32_t c = (u < 0x1p-6f) ? sub : nrm;
+    return (u <= kE4M3Max) ? c : kE4M3CodeMax;
+}
+
+// E4M3 decode of a finite non-negative code (0x00..0x7E), exact in binary32.
+__device__ __forceinline__ float e4m3_decode(uint32_t c) {
+    const uint32_t e = c >> 3, m = c & 7u;
+    const float sub = (float)m * 0x1p-9f;
+    const float nrm = __uint_as_float(((e + 120u) << 23) | (m << 20));
+    return e ? nrm : sub;
+}
+
+// E8M0 block exponent of a 32-element block from the bf16 bits of its
+// largest magnitude (15-bit pattern): the OCP microscaling rule
+// E = clamp(floor(log2 a) - 2, -127, 127) gives code = E + 127 =
+// max(exponent field - 2, 0) for every finite bf16 a (a subnormal or zero a
+// has exponent field 0 and takes code 0; the upper clamp is never reached).
+__device__ __forceinline__ uint32_t e8m0_code_of_amax(uint32_t amax_bits15) {
+    const int ef = (int)(amax_bits15 >> 7);
+    return (uint32_t)max(ef - 2, 0);
+}
+
+// 2^-E for an E8M0 code (E = code - 127), exact: binary32 exponent field
+// 254 - code, within 2..254 for every code the encoder produces (0..252).
+__device__ __forceinline__ float e8m0_reciprocal(uint32_t code) {
+    return __uint_as_float((254u - code) << 23);
+}
+
 // E2M1 nibble of y by stochastic rounding with the uniform 32-bit word w
 // (eq:sr): between adjacent magnitudes q_lo <= |y| < q_hi round up iff
 // w < ceil((|y| - q_lo) / (q_hi - q_lo) * 2^32).  |y| >= 6 gives code 7.

@@ -212,7 +212,7 @@ template <int BMODE, bool OUT_BF16, bool FULLK>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_kernel(
     int64_t M, int64_t N, int64_t K, int tiles_m, int tiles_n, const uint8_t* __restrict__ A,
     const uint8_t* __restrict__ As, const float* __restrict__ a_dec, const uint8_t* __restrict__ B,
-    const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec, void* __restrict__ C) {
+    const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec, void* __restrict__ C, float amul) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     uint16_t* stage0 = reinterpret_cast<uint16_t*>(smem);
     uint16_t* stage1 = stage0 + kStageElems;
@@ -329,7 +329,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_kernel(
     // 32x32 accumulator layout: lane l, register r holds
     // row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
     // operands were decoded as A_hat * 2^-3 and B_hat * 2^-3
-    const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;
+    const float alpha = (a_dec[0] * b_dec[0]) * amul;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -458,7 +458,7 @@ template <int BMODE, bool OUT_BF16>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_dma_kernel(
     int64_t M, int64_t N, int64_t K, int tiles_m, int tiles_n, const uint8_t* __restrict__ A,
     const uint8_t* __restrict__ As, const float* __restrict__ a_dec, const uint8_t* __restrict__ B,
-    const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec, void* __restrict__ C) {
+    const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec, void* __restrict__ C, float amul) {
     __shared__ __attribute__((aligned(16))) uint16_t sF0[(BM + BN) * kFRow];
     __shared__ __attribute__((aligned(16))) uint16_t sF1[(BM + BN) * kFRow];
     __shared__ __attribute__((aligned(16))) uint8_t sP0[(BM + BN) * kPRow];
@@ -600,7 +600,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_dma_kernel(
     wait_vmem_all();                              // no load outlives the kernel's LDS
 
     // ---- epilogue: C = alpha * acc ------------------------------------------
-    const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;   // operands were scaled by 2^-3
+    const float alpha = (a_dec[0] * b_dec[0]) * amul;   // operands were scaled by 2^-3
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -627,11 +627,11 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_dma_kernel(
 template <int BMODE, bool OUT_BF16>
 hipError_t launch_dma(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                       const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
-                      void* c, hipStream_t s) {
+                      void* c, float amul, hipStream_t s) {
     const int tiles_m = (int)((M + BM - 1) / BM);
     const int tiles_n = (int)((N + BN - 1) / BN);
     hipLaunchKernelGGL((gemm_fp4_dma_kernel<BMODE, OUT_BF16>), dim3((unsigned)(tiles_m * tiles_n)),
-                       dim3(kGemmThreads), 0, s, M, N, K, tiles_m, tiles_n, a, as, ad, b, bs, bd, c);
+                       dim3(kGemmThreads), 0, s, M, N, K, tiles_m, tiles_n, a, as, ad, b, bs, bd, c, amul);
     return hipGetLastError();
 }
 
@@ -865,6 +865,120 @@ __device__ __forceinline__ WorkItem work_item(int it, const SplitPlan& sp, int N
     return w;
 }
 
+// Epilogue of one work item.  Element e of accumulator (i, j) is row
+// 32i + l%32, column 32j + 8(e/4) + 4(l/32) + e%4 of the wave's 128 x 128
+// block (the products are issued as B x A^T).  A split part stores its fp32
+// partial; a whole tile stores alpha * value through a buffer resource over
+// C, where an out-of-range offset drops the store, which masks rows and
+// columns past C without branches.
+template <bool OUT_BF16>
+__device__ __forceinline__ void store_item(const f32x16_t (&acc)[4][4], const WorkItem& cur,
+                                           const SplitPlan& sp, int M, int N, int tiles_m, int tiles_n,
+                                           int wave, int lane, float alpha, void* __restrict__ C) {
+    const int wm = wave >> 1, wn = wave & 1;
+    const int r = lane & 31, hi = lane >> 5;
+    if (cur.split_j >= 0) {
+        // one part of a leftover tile: fp32 partial, [acc (i, j)][run g]
+        // [lane][4] so that every store is 16 bytes per lane, 1 KB per wave
+        const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
+            sp.part + ((int64_t)cur.split_j * sp.parts + cur.part) * 65536, 0, 65536 * 4, 0x00020000);
+        const uint32_t vo = (uint32_t)(wave * 65536 + lane * 16);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const f32x4_t v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                                       acc[i][j][4 * g + 3]};
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), pr, vo,
+                                                           ((i * 4 + j) * 4 + g) * 1024, 0);
+                }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    } else {
+            constexpr uint32_t esz = OUT_BF16 ? 2 : 4;
+        constexpr uint32_t kOff = 0x80000000u;               // past every buffer
+        const __amdgpu_buffer_rsrc_t cr =
+            __builtin_amdgcn_make_buffer_rsrc(C, 0, (int)((uint32_t)M * (uint32_t)N * esz), 0x00020000);
+        int64_t m0, n0;
+        tile_origin(cur.t, tiles_m, tiles_n, m0, n0);
+        const int mrow = (int)m0 + wm * 128 + r;
+        const int ncol = (int)n0 + wn * 128 + hi * 4;
+        const bool vec = (N & 3) == 0;
+        if (OUT_BF16 && (N & 7) == 0) {
+            // bf16 with N % 8 == 0: lanes l and l + 32 hold the two halves
+            // of each run of 8 columns; one lane-half swap per pair of runs
+            // gives lane l runs 0 and 2 and lane l + 32 runs 1 and 3 whole,
+            // so every store is 16 bytes per lane (32 per row).
+            const int ncol8 = (int)n0 + wn * 128 + hi * 8;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int m = mrow + 32 * i;
+                const uint32_t rbase = ((uint32_t)m * (uint32_t)N + (uint32_t)ncol8) * 2u;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int q = 0; q < 2; ++q) {
+                        const int g0 = 2 * q, g1 = 2 * q + 1;
+                        const uint32_t x0 = pack_bf16x2(alpha * acc[i][j][4 * g0], alpha * acc[i][j][4 * g0 + 1]);
+                        const uint32_t x1 = pack_bf16x2(alpha * acc[i][j][4 * g0 + 2], alpha * acc[i][j][4 * g0 + 3]);
+                        const uint32_t y0 = pack_bf16x2(alpha * acc[i][j][4 * g1], alpha * acc[i][j][4 * g1 + 1]);
+                        const uint32_t y1 = pack_bf16x2(alpha * acc[i][j][4 * g1 + 2], alpha * acc[i][j][4 * g1 + 3]);
+                        const auto s0 = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
+                        const auto s1 = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
+                        const u32x4_t d = {(uint32_t)s0[0], (uint32_t)s1[0], (uint32_t)s0[1], (uint32_t)s1[1]};
+                        const int n = ncol8 + 32 * j + 16 * q;
+                        const uint32_t vo = (m < M && n < N) ? rbase : kOff;
+                        __builtin_amdgcn_raw_buffer_store_b128(d, cr, vo + (uint32_t)(32 * j + 16 * q) * 2u, 0, 0);
+                    }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int m = mrow + 32 * i;
+            const uint32_t rbase = ((uint32_t)m * (uint32_t)N + (uint32_t)ncol) * esz;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int n = ncol + 32 * j + 8 * g;
+                    const float v0 = alpha * acc[i][j][4 * g + 0], v1 = alpha * acc[i][j][4 * g + 1];
+                    const float v2 = alpha * acc[i][j][4 * g + 2], v3 = alpha * acc[i][j][4 * g + 3];
+                    const uint32_t imm = (uint32_t)(32 * j + 8 * g) * esz;
+                    if (vec) {
+                        // N % 4 == 0: a run is inside C or wholly past it
+                        const uint32_t vo = (m < M && n < N) ? rbase : kOff;
+                        if (OUT_BF16) {
+                            const u32x2_t d = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+                            __builtin_amdgcn_raw_buffer_store_b64(d, cr, vo + imm, 0, 0);
+                        } else {
+                            const f32x4_t d = {v0, v1, v2, v3};
+                            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, d), cr, vo + imm,
+                                                                   0, 0);
+                        }
+                    } else {
+                        const float vv[4] = {v0, v1, v2, v3};
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const uint32_t vo = (m < M && n + q < N) ? rbase : kOff;
+                            if (OUT_BF16) {
+                                __builtin_amdgcn_raw_buffer_store_b16(
+                                    (unsigned short)pack_bf16x2(vv[q], 0.0f), cr, vo + imm + q * esz, 0, 0);
+                            } else {
+                                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(vv[q]), cr,
+                                                                      vo + imm + q * esz, 0, 0);
+                            }
+                        }
+                    }
+                }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        }
+    }
+}
+
 // Register-decode GEMM, persistent: workgroup w runs items w, w + grid, ...
 // (whole tiles first, then split parts).  During the last two stages of an
 // item the next item's first two stages are loaded, so its epilogue and the
@@ -877,7 +991,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
     int M, int N, int K, int tiles_m, int tiles_n, int items, SplitPlan sp,
     const uint8_t* __restrict__ A, const uint8_t* __restrict__ As, const float* __restrict__ a_dec,
     const uint8_t* __restrict__ B, const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec,
-    void* __restrict__ C) {
+    void* __restrict__ C, float amul) {
     __shared__ __attribute__((aligned(16))) uint8_t sP0[kSupPayload];
     __shared__ __attribute__((aligned(16))) uint8_t sP1[kSupPayload];
     __shared__ __attribute__((aligned(16))) uint8_t sC0[kSupScales];
@@ -1051,112 +1165,292 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
         }
         if (G < cur.g1) stage(G, sP0, sC0, sP1, sC1, P0, S0);   // odd stage count (single item)
 
-        // ---- epilogue --------------------------------------------------------
-        // Element e of accumulator (i, j) is row 32i + l%32, column
-        // 32j + 8(e/4) + 4(l/32) + e%4 of the wave's 128 x 128 block.  Stores
-        // go through buffer resources: an out-of-range offset drops the store,
-        // which masks rows and columns past C without branches.
-        if (cur.split_j >= 0) {
-            // one part of a leftover tile: fp32 partial, [acc (i, j)][run g]
-            // [lane][4] so that every store is 16 bytes per lane, 1 KB per wave
-            const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
-                sp.part + ((int64_t)cur.split_j * sp.parts + cur.part) * 65536, 0, 65536 * 4, 0x00020000);
-            const uint32_t vo = (uint32_t)(wave * 65536 + lane * 16);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-#pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        const f32x4_t v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
-                                           acc[i][j][4 * g + 3]};
-                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), pr, vo,
-                                                               ((i * 4 + j) * 4 + g) * 1024, 0);
-                    }
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        } else {
-            const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;   // operands were scaled by 2^-3
-            constexpr uint32_t esz = OUT_BF16 ? 2 : 4;
-            constexpr uint32_t kOff = 0x80000000u;               // past every buffer
-            const __amdgpu_buffer_rsrc_t cr =
-                __builtin_amdgcn_make_buffer_rsrc(C, 0, (int)((uint32_t)M * (uint32_t)N * esz), 0x00020000);
-            int64_t m0, n0;
-            tile_origin(cur.t, tiles_m, tiles_n, m0, n0);
-            const int mrow = (int)m0 + wm * 128 + r;
-            const int ncol = (int)n0 + wn * 128 + hi * 4;
-            const bool vec = (N & 3) == 0;
-            if (OUT_BF16 && (N & 7) == 0) {
-                // bf16 with N % 8 == 0: lanes l and l + 32 hold the two halves
-                // of each run of 8 columns; one lane-half swap per pair of runs
-                // gives lane l runs 0 and 2 and lane l + 32 runs 1 and 3 whole,
-                // so every store is 16 bytes per lane (32 per row).
-                const int ncol8 = (int)n0 + wn * 128 + hi * 8;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int m = mrow + 32 * i;
-                    const uint32_t rbase = ((uint32_t)m * (uint32_t)N + (uint32_t)ncol8) * 2u;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-#pragma unroll
-                        for (int q = 0; q < 2; ++q) {
-                            const int g0 = 2 * q, g1 = 2 * q + 1;
-                            const uint32_t x0 = pack_bf16x2(alpha * acc[i][j][4 * g0], alpha * acc[i][j][4 * g0 + 1]);
-                            const uint32_t x1 = pack_bf16x2(alpha * acc[i][j][4 * g0 + 2], alpha * acc[i][j][4 * g0 + 3]);
-                            const uint32_t y0 = pack_bf16x2(alpha * acc[i][j][4 * g1], alpha * acc[i][j][4 * g1 + 1]);
-                            const uint32_t y1 = pack_bf16x2(alpha * acc[i][j][4 * g1 + 2], alpha * acc[i][j][4 * g1 + 3]);
-                            const auto s0 = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
-                            const auto s1 = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
-                            const u32x4_t d = {(uint32_t)s0[0], (uint32_t)s1[0], (uint32_t)s0[1], (uint32_t)s1[1]};
-                            const int n = ncol8 + 32 * j + 16 * q;
-                            const uint32_t vo = (m < M && n < N) ? rbase : kOff;
-                            __builtin_amdgcn_raw_buffer_store_b128(d, cr, vo + (uint32_t)(32 * j + 16 * q) * 2u, 0, 0);
-                        }
-                    __builtin_amdgcn_sched_barrier(0);
-                }
-            } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int m = mrow + 32 * i;
-                const uint32_t rbase = ((uint32_t)m * (uint32_t)N + (uint32_t)ncol) * esz;
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-#pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        const int n = ncol + 32 * j + 8 * g;
-                        const float v0 = alpha * acc[i][j][4 * g + 0], v1 = alpha * acc[i][j][4 * g + 1];
-                        const float v2 = alpha * acc[i][j][4 * g + 2], v3 = alpha * acc[i][j][4 * g + 3];
-                        const uint32_t imm = (uint32_t)(32 * j + 8 * g) * esz;
-                        if (vec) {
-                            // N % 4 == 0: a run is inside C or wholly past it
-                            const uint32_t vo = (m < M && n < N) ? rbase : kOff;
-                            if (OUT_BF16) {
-                                const u32x2_t d = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-                                __builtin_amdgcn_raw_buffer_store_b64(d, cr, vo + imm, 0, 0);
-                            } else {
-                                const f32x4_t d = {v0, v1, v2, v3};
-                                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, d), cr, vo + imm,
-                                                                       0, 0);
-                            }
-                        } else {
-                            const float vv[4] = {v0, v1, v2, v3};
-#pragma unroll
-                            for (int q = 0; q < 4; ++q) {
-                                const uint32_t vo = (m < M && n + q < N) ? rbase : kOff;
-                                if (OUT_BF16) {
-                                    __builtin_amdgcn_raw_buffer_store_b16(
-                                        (unsigned short)pack_bf16x2(vv[q], 0.0f), cr, vo + imm + q * esz, 0, 0);
-                                } else {
-                                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(vv[q]), cr,
-                                                                          vo + imm + q * esz, 0, 0);
-                                }
-                            }
-                        }
-                    }
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            }
+        store_item<OUT_BF16>(acc, cur, sp, M, N, tiles_m, tiles_n, wave, lane,
+                             (a_dec[0] * b_dec[0]) * amul, C);   // operands were scaled by 2^-3
+        if (!has_next) break;
+    }
+    wait_vmem<0>();                                  // no load outlives the kernel's LDS
+}
+
+// ===================================================================== //
+// E8M0 blocks of 32 (MXFP4 arrangement): the gfx950 scaled FP4 matrix    //
+// instruction multiplies E2M1 payloads and applies the per-32 power-of-  //
+// two scales itself, so nothing is decoded.                              //
+// ===================================================================== //
+// v_mfma_scale_f32_32x32x64_f8f6f4 with both formats E2M1: lane l supplies
+// row l%32 and k = 32(l/32) .. +31 as 16 payload bytes (the stored order),
+// plus the E8M0 byte of that row and k-half; the product of the two scale
+// powers is exact and the accumulation is binary32.  Same tiles, stages,
+// persistent items and epilogue as the register-decode kernel; a stage row
+// holds 128 payload bytes and 8 scale bytes (256 k).
+constexpr int kMxScaleStage = kSupRows * 8;               // 4 KB of scales per stage
+constexpr int kMxScLoads = 4;                             // 4 x 256 B per wave
+constexpr int kMxLoads = kSupPayLoads + kMxScLoads;
+
+// 4 bytes per lane from rsrc at voff + soff into LDS at lds + OFF + 4 lane.
+template <int OFF>
+__device__ __forceinline__ void dma_buf_x1(i32x4_t rsrc, uint32_t voff, uint32_t soff, uint32_t lds) {
+    asm volatile("s_add_u32 m0, %3, %4\n\ts_nop 0\n\tbuffer_load_dword %0, %1, %2 offen lds"
+                 :: "v"(voff), "s"(rsrc), "s"(soff), "s"(lds), "i"(OFF) : "memory", "m0", "scc");
+}
+
+// Per-lane load sources of one tile: first payload chunk; the scale bytes
+// of rows x0 + 32u + l/2 (dword l%2 of their 8 stage bytes), u = 0..3.
+struct MxSrc {
+    uint32_t off0;
+    uint32_t so[4];
+};
+
+struct MxLoader {
+    i32x4_t pay, sca;
+    uint32_t rows8;          // bytes of 8 payload rows
+    uint32_t ldp, lds;       // this wave's LDS offsets inside a payload / scale stage
+
+    template <int I0, int I1, bool SC>
+    __device__ __forceinline__ void issue(uint32_t P, uint32_t S, const MxSrc& src, int G) const {
+        const uint32_t gp = (uint32_t)G * kSupRowBytes;
+        const uint32_t pl = P + ldp;
+        static_for<I0, I1>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            dma_buf_x4<i * 1024>(pay, src.off0 + i * rows8, gp, pl);
+        });
+        if (SC) {
+            const uint32_t gs = (uint32_t)G * 8;
+            const uint32_t sl = S + lds;
+            dma_buf_x1<0>(sca, src.so[0], gs, sl);
+            dma_buf_x1<256>(sca, src.so[1], gs, sl);
+            dma_buf_x1<512>(sca, src.so[2], gs, sl);
+            dma_buf_x1<768>(sca, src.so[3], gs, sl);
         }
+    }
+};
+
+// One slice of a lane's operands: 16 payload bytes of each of its 4 A and 4
+// B rows (groups 0..3 = A rows 32i + l%32, 4..7 = B rows 32j + l%32).
+struct MxSlice {
+    uint32_t w[8][4];
+};
+
+template <int SL>
+__device__ __forceinline__ void read_mx_slice(MxSlice& R, const uint8_t* P, int pa, int pb, int xo) {
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+        const int row_off = (g < 4 ? pa : pb) + (g & 3) * 32 * kSupRowBytes;
+        const uint4 v = *reinterpret_cast<const uint4*>(P + row_off + xo);
+        R.w[g][0] = v.x; R.w[g][1] = v.y; R.w[g][2] = v.z; R.w[g][3] = v.w;
+    }
+}
+
+// The 8 scale bytes (256 k) of each of the lane's 8 rows, shifted right by
+// one byte in the upper lane half so that, for slice SL, the lane's byte
+// (2 SL + l/32) sits at byte 2 (SL % 2) of dword SL / 2.
+__device__ __forceinline__ void read_mx_scales(uint32_t (&sc)[8][2], const uint8_t* S, int ra, int rb,
+                                               int hi) {
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+        const int row = (g < 4 ? ra : rb) + (g & 3) * 32;
+        const uint2 v = *reinterpret_cast<const uint2*>(S + row * 8);
+        sc[g][0] = v.x >> (8 * hi);
+        sc[g][1] = v.y >> (8 * hi);
+    }
+}
+
+// One scaled FP4 product accumulated in place.  Written as an instruction
+// with a read-write accumulator operand: the compiler's builtin for it has no
+// accumulate-in-place form, and its register allocator then moves every
+// accumulator through a temporary around each product.  SEL picks byte SEL
+// of both scale registers.
+typedef int i32x4v_t __attribute__((ext_vector_type(4)));
+template <int SEL>
+__device__ __forceinline__ void mfma_mx(f32x16_t& acc, const i32x4v_t& a, const i32x4v_t& b, uint32_t sa,
+                                        uint32_t sb) {
+    static_assert(SEL == 0 || SEL == 2, "scale byte 0 or 2");
+    // volatile: kept in program order with the waits placed after them
+    if (SEL == 0)
+        asm volatile("v_mfma_scale_f32_32x32x64_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:4 blgp:4"
+                     : "+a"(acc) : "v"(a), "v"(b), "v"(sa), "v"(sb));
+    else
+        asm volatile("v_mfma_scale_f32_32x32x64_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[1,1,0] cbsz:4 blgp:4"
+                     : "+a"(acc) : "v"(a), "v"(b), "v"(sa), "v"(sb));
+}
+
+template <int SL>
+__device__ __forceinline__ void mfma_mx16(f32x16_t (&acc)[4][4], const MxSlice& R, const uint32_t (&sc)[8][2]) {
+    constexpr int d = SL / 2, sel = 2 * (SL % 2);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const i32x4v_t a = {(int)R.w[4 + j][0], (int)R.w[4 + j][1], (int)R.w[4 + j][2], (int)R.w[4 + j][3]};
+            const i32x4v_t b = {(int)R.w[i][0], (int)R.w[i][1], (int)R.w[i][2], (int)R.w[i][3]};
+            // products issued as B x A^T (see store_item)
+            mfma_mx<sel>(acc[i][j], a, b, sc[4 + j][d], sc[i][d]);
+        }
+}
+
+template <bool OUT_BF16>
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_mx_kernel(
+    int M, int N, int K, int tiles_m, int tiles_n, int items, SplitPlan sp,
+    const uint8_t* __restrict__ A, const uint8_t* __restrict__ As, const float* __restrict__ a_dec,
+    const uint8_t* __restrict__ B, const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec,
+    void* __restrict__ C) {
+    __shared__ __attribute__((aligned(16))) uint8_t sP0[kSupPayload];
+    __shared__ __attribute__((aligned(16))) uint8_t sP1[kSupPayload];
+    __shared__ __attribute__((aligned(16))) uint8_t sC0[kMxScaleStage];
+    __shared__ __attribute__((aligned(16))) uint8_t sC1[kMxScaleStage];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+    const int r = lane & 31, hi = lane >> 5;
+
+    const int kb32 = K / 32;                         // scale bytes per row
+    const int NG = K / (kSupK * BK);                 // stages of a whole tile
+
+    // Loads: waves 0, 1 bring A stage rows 0..255, waves 2, 3 B rows 256..511.
+    const bool isA = wave < 2;
+    const int xw = 128 * (wave & 1);
+    MxLoader L;
+    L.pay = isA ? buffer_rsrc(A, (uint32_t)M * (uint32_t)(K / 2)) : buffer_rsrc(B, (uint32_t)N * (uint32_t)(K / 2));
+    L.sca = isA ? buffer_rsrc(As, (uint32_t)M * kb32) : buffer_rsrc(Bs, (uint32_t)N * kb32);
+    L.rows8 = (uint32_t)(8 * (K / 2));
+    L.ldp = (uint32_t)(128 * wave * kSupRowBytes);
+    L.lds = (uint32_t)(128 * wave * 8);
+    const uint32_t chunk16 = (uint32_t)(((lane & 7) ^ ((lane >> 3) & 7)) * 16);
+    const int rmax = (isA ? M : N) - 1;
+    auto src_of = [&](int t) {
+        int64_t m0, n0;
+        tile_origin(t, tiles_m, tiles_n, m0, n0);
+        const int x0 = (int)(isA ? m0 : n0) + xw;
+        MxSrc q;
+        q.off0 = (uint32_t)(x0 + (lane >> 3)) * (uint32_t)(K / 2) + chunk16;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            q.so[u] = (uint32_t)min(x0 + 32 * u + (lane >> 1), rmax) * (uint32_t)kb32 + 4u * (lane & 1);
+        return q;
+    };
+    const uint32_t P0 = lds_addr(sP0), P1 = lds_addr(sP1), S0 = lds_addr(sC0), S1 = lds_addr(sC1);
+
+    // Read offsets of the lane: first A / B stage rows and per-slice chunk.
+    const int ra = wm * 128 + r, rb = BM + wn * 128 + r;
+    const int pa = ra * kSupRowBytes, pb = rb * kSupRowBytes;
+    const int x0 = ((0 + hi) ^ (r & 7)) * 16, x1 = ((2 + hi) ^ (r & 7)) * 16;
+    const int x2 = ((4 + hi) ^ (r & 7)) * 16, x3 = ((6 + hi) ^ (r & 7)) * 16;
+
+    f32x16_t acc[4][4];
+    MxSlice R0, R1;
+    uint32_t SC0[8][2], SC1[8][2];
+
+    const int grid = (int)gridDim.x;
+    const int nw = (items - (int)blockIdx.x + grid - 1) / grid;
+    const int last_it = (int)blockIdx.x + (nw - 1) * grid;
+    const bool rot = kStaggerSplit && (blockIdx.x & 1) && nw > 1 && last_it >= sp.Tdp;
+    auto item_at = [&](int k) {
+        return rot ? (k == 0 ? last_it : (int)blockIdx.x + (k - 1) * grid) : (int)blockIdx.x + k * grid;
+    };
+
+    {
+        const WorkItem w = work_item(item_at(0), sp, NG);
+        const MxSrc q = src_of(w.t);
+        L.issue<0, kSupPayLoads, true>(P0, S0, q, w.g0);
+        L.issue<0, kSupPayLoads, true>(P1, S1, q, min(w.g0 + 1, w.g1 - 1));
+        wait_vmem<kMxLoads>();
+        __syncthreads();
+    }
+
+    for (int k = 0;; ++k) {
+        const int it = item_at(k);
+        const WorkItem cur = work_item(it, sp, NG);
+        const MxSrc scur = src_of(cur.t);
+        const bool has_next = k + 1 < nw;
+        const WorkItem nxt = work_item(has_next ? item_at(k + 1) : it, sp, NG);
+        const MxSrc snxt = src_of(nxt.t);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+        read_mx_slice<0>(R0, sP0, pa, pb, x0);
+        read_mx_scales(SC0, sC0, ra, rb, hi);
+        // the products are instructions the compiler does not model: keep
+        // the accumulator and scale writes above clear of the first ones
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_nop 4" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        const int gshift = has_next ? nxt.g0 - cur.g1 : -1;
+        const int gclamp = has_next ? 0x7FFFFFFF : cur.g1 - 1;
+
+        auto issue_for = [&](auto I0c, auto I1c, auto SCk, uint32_t ldP, uint32_t ldS, int Gt) {
+            constexpr int I0v = decltype(I0c)::value, I1v = decltype(I1c)::value;
+            constexpr bool SCv = decltype(SCk)::value;
+            const bool in_cur = Gt < cur.g1;
+            const int Gl = in_cur ? Gt : min(Gt + gshift, gclamp);
+            MxSrc q;
+            q.off0 = in_cur ? scur.off0 : snxt.off0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) q.so[u] = in_cur ? scur.so[u] : snxt.so[u];
+            L.issue<I0v, I1v, SCv>(ldP, ldS, q, Gl);
+        };
+
+        // One slice: 16 products on the current slice while the next slice
+        // (or, at slice 3, after the stage barrier, the next stage's slice 0
+        // and scales) is read and, at slice 3, the loads of stage G+2 go out.
+        auto slice = [&](auto SLc, int G, const uint8_t* Pc, const uint8_t* Pn, const uint8_t* Sn,
+                         uint32_t ldP, uint32_t ldS, MxSlice& Rc, MxSlice& Rn, uint32_t (&SCc)[8][2],
+                         uint32_t (&SCn)[8][2]) {
+            constexpr int SL = decltype(SLc)::value;
+            using Z = std::integral_constant<int, 0>;
+            using C8 = std::integral_constant<int, 8>;
+            using CP = std::integral_constant<int, kSupPayLoads>;
+            using F = std::integral_constant<bool, false>;
+            using T = std::integral_constant<bool, true>;
+            if (SL == 3) {
+                wait_vmem<0>();
+                __syncthreads();
+                read_mx_slice<0>(Rn, Pn, pa, pb, x0);
+                read_mx_scales(SCn, Sn, ra, rb, hi);
+                issue_for(Z{}, C8{}, F{}, ldP, ldS, G + 2);
+            } else {
+                read_mx_slice<SL + 1>(Rn, Pc, pa, pb, SL == 0 ? x1 : (SL == 1 ? x2 : x3));
+            }
+            mfma_mx16<SL>(acc, Rc, SCc);
+            if (SL == 3) {
+                issue_for(C8{}, CP{}, T{}, ldP, ldS, G + 2);
+                // The products are instructions the compiler does not model:
+                // whatever it places after a stage (spills of accumulators,
+                // the epilogue) must not read them before the last ones have
+                // landed.  The wait overlaps the queued products.
+                asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 15" ::: "memory");
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        using I0 = std::integral_constant<int, 0>;
+        using I1 = std::integral_constant<int, 1>;
+        using I2 = std::integral_constant<int, 2>;
+        using I3 = std::integral_constant<int, 3>;
+        // stage scales alternate between SC0 (even stages) and SC1 (odd)
+        auto stage = [&](int G, const uint8_t* Pc, const uint8_t* Pn, const uint8_t* Sn, uint32_t ldP,
+                         uint32_t ldS, uint32_t (&SCc)[8][2], uint32_t (&SCn)[8][2]) {
+            slice(I0{}, G, Pc, Pn, Sn, ldP, ldS, R0, R1, SCc, SCn);
+            slice(I1{}, G, Pc, Pn, Sn, ldP, ldS, R1, R0, SCc, SCn);
+            slice(I2{}, G, Pc, Pn, Sn, ldP, ldS, R0, R1, SCc, SCn);
+            slice(I3{}, G, Pc, Pn, Sn, ldP, ldS, R1, R0, SCc, SCn);
+        };
+        int G = cur.g0;
+        for (; G + 1 < cur.g1; G += 2) {
+            stage(G, sP0, sP1, sC1, P0, S0, SC0, SC1);
+            stage(G + 1, sP1, sP0, sC0, P1, S1, SC1, SC0);
+        }
+        if (G < cur.g1) stage(G, sP0, sP1, sC1, P0, S0, SC0, SC1);   // odd stage count (single item)
+
+        // the products above are instructions the compiler does not model:
+        // give the last ones time to land before their results are read
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 15" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        store_item<OUT_BF16>(acc, cur, sp, M, N, tiles_m, tiles_n, wave, lane, a_dec[0] * b_dec[0], C);
         if (!has_next) break;
     }
     wait_vmem<0>();                                  // no load outlives the kernel's LDS
@@ -1169,11 +1463,11 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
 template <int BMODE, bool OUT_BF16>
 __global__ __launch_bounds__(256) void gemm_split_sum_kernel(
     int64_t M, int64_t N, int tiles_m, int tiles_n, SplitPlan sp, const float* __restrict__ a_dec,
-    const float* __restrict__ b_dec, void* __restrict__ C) {
+    const float* __restrict__ b_dec, void* __restrict__ C, float amul) {
     const int j = blockIdx.x >> 6, wv = (blockIdx.x >> 4) & 3, ij = blockIdx.x & 15;
     int64_t m0, n0;
     tile_origin(sp.Tdp + j, tiles_m, tiles_n, m0, n0);
-    const float alpha = (a_dec[0] * b_dec[0]) * 64.0f;
+    const float alpha = (a_dec[0] * b_dec[0]) * amul;
     const int row = threadIdx.x >> 3, c4 = threadIdx.x & 7;     // c4 = 2 g + lane half
     const int lane = row + 32 * (c4 & 1), g = c4 >> 1;
     const float* base = sp.part + (int64_t)j * sp.parts * 65536 + (int64_t)wv * 16384 +
@@ -1250,7 +1544,7 @@ constexpr int kSplitRemDiv = 2;
 template <int BMODE, bool OUT_BF16>
 hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                       const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
-                      void* c, hipStream_t s) {
+                      void* c, float amul, hipStream_t s) {
     const int tiles_m = (int)((M + BM - 1) / BM);
     const int tiles_n = (int)((N + BN - 1) / BN);
     const int T = tiles_m * tiles_n;
@@ -1279,17 +1573,51 @@ hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
     // an even stage count, else one item per workgroup
     const int grid = (even && cus > 0) ? min(items, cus) : items;
     hipLaunchKernelGGL((gemm_fp4_reg_kernel<BMODE, OUT_BF16>), dim3((unsigned)grid), dim3(kGemmThreads),
-                       0, s, (int)M, (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c);
+                       0, s, (int)M, (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c, amul);
     if ((e = hipGetLastError()) != hipSuccess || sp.parts == 1) return e;
     hipLaunchKernelGGL((gemm_split_sum_kernel<BMODE, OUT_BF16>), dim3((unsigned)(64 * (T - sp.Tdp))), dim3(256),
-                       0, s, M, N, tiles_m, tiles_n, sp, ad, bd, c);
+                       0, s, M, N, tiles_m, tiles_n, sp, ad, bd, c, amul);
+    return hipGetLastError();
+}
+
+template <bool OUT_BF16>
+hipError_t launch_mx(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
+                     const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
+                     void* c, hipStream_t s) {
+    const int tiles_m = (int)((M + BM - 1) / BM);
+    const int tiles_n = (int)((N + BN - 1) / BN);
+    const int T = tiles_m * tiles_n;
+    const int NG = (int)(K / (kSupK * BK));
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    const bool even = NG % 2 == 0;
+    SplitPlan sp{T, 1, nullptr};
+    const int rem = cus > 0 ? T % cus : 0;
+    if (T > cus && rem > 0 && rem <= cus / kSplitRemDiv) {
+        const int parts = min(cus / rem, even ? NG / 2 : NG);
+        if (parts > 1) {
+            sp.Tdp = T - rem;
+            sp.parts = parts;
+            e = split_workspace(s, (size_t)rem * parts * 65536, &sp.part);
+            if (e != hipSuccess) return e;
+        }
+    }
+    const int items = sp.Tdp + (T - sp.Tdp) * sp.parts;
+    const int grid = (even && cus > 0) ? min(items, cus) : items;
+    hipLaunchKernelGGL((gemm_mx_kernel<OUT_BF16>), dim3((unsigned)grid), dim3(kGemmThreads), 0, s, (int)M,
+                       (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c);
+    if ((e = hipGetLastError()) != hipSuccess || sp.parts == 1) return e;
+    hipLaunchKernelGGL((gemm_split_sum_kernel<(int)BScale::Row, OUT_BF16>), dim3((unsigned)(64 * (T - sp.Tdp))),
+                       dim3(256), 0, s, M, N, tiles_m, tiles_n, sp, ad, bd, c, 1.0f);
     return hipGetLastError();
 }
 
 template <int BMODE, bool OUT_BF16, bool FULLK>
 hipError_t launch_one(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                       const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
-                      void* c, hipStream_t s) {
+                      void* c, float amul, hipStream_t s) {
     static bool attr_set = false;
     if (!attr_set) {
         const hipError_t e = hipFuncSetAttribute(
@@ -1302,42 +1630,50 @@ hipError_t launch_one(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
     const int tiles_n = (int)((N + BN - 1) / BN);
     hipLaunchKernelGGL((gemm_fp4_kernel<BMODE, OUT_BF16, FULLK>),
                        dim3((unsigned)(tiles_m * tiles_n)), dim3(kGemmThreads), kSmemBytes, s, M,
-                       N, K, tiles_m, tiles_n, a, as, ad, b, bs, bd, c);
+                       N, K, tiles_m, tiles_n, a, as, ad, b, bs, bd, c, amul);
     return hipGetLastError();
 }
 
 template <int BMODE>
 hipError_t launch_mode(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                        const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
-                       void* c, bool c_bf16, hipStream_t s) {
+                       void* c, bool c_bf16, float amul, hipStream_t s) {
     // the register-decode kernel addresses operands and C with 32-bit offsets
     const int64_t kLim = (int64_t)1 << 31;
     if (K % (4 * BK) == 0 && K > 0 && M * (K / 2) < kLim && N * (K / 2) < kLim && M * N * 4 < kLim)
-        return c_bf16 ? launch_reg<BMODE, true>(M, N, K, a, as, ad, b, bs, bd, c, s)
-                      : launch_reg<BMODE, false>(M, N, K, a, as, ad, b, bs, bd, c, s);
+        return c_bf16 ? launch_reg<BMODE, true>(M, N, K, a, as, ad, b, bs, bd, c, amul, s)
+                      : launch_reg<BMODE, false>(M, N, K, a, as, ad, b, bs, bd, c, amul, s);
     if (K % BK == 0 && K > 0)
-        return c_bf16 ? launch_dma<BMODE, true>(M, N, K, a, as, ad, b, bs, bd, c, s)
-                      : launch_dma<BMODE, false>(M, N, K, a, as, ad, b, bs, bd, c, s);
-    return c_bf16 ? launch_one<BMODE, true, false>(M, N, K, a, as, ad, b, bs, bd, c, s)
-                  : launch_one<BMODE, false, false>(M, N, K, a, as, ad, b, bs, bd, c, s);
+        return c_bf16 ? launch_dma<BMODE, true>(M, N, K, a, as, ad, b, bs, bd, c, amul, s)
+                      : launch_dma<BMODE, false>(M, N, K, a, as, ad, b, bs, bd, c, amul, s);
+    return c_bf16 ? launch_one<BMODE, true, false>(M, N, K, a, as, ad, b, bs, bd, c, amul, s)
+                  : launch_one<BMODE, false, false>(M, N, K, a, as, ad, b, bs, bd, c, amul, s);
 }
 
 }  // namespace
 
-hipError_t launch_gemm(BScale bmode, int64_t M, int64_t N, int64_t K, const uint8_t* a,
+hipError_t launch_gemm(BScale bmode, float amul, int64_t M, int64_t N, int64_t K, const uint8_t* a,
                        const uint8_t* a_scales, const float* a_dec, const uint8_t* b,
                        const uint8_t* b_scales, const float* b_dec, void* c, bool c_bf16,
                        hipStream_t s) {
     if (M == 0 || N == 0) return hipSuccess;
     switch (bmode) {
         case BScale::Row:
-            return launch_mode<(int)BScale::Row>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, s);
+            return launch_mode<(int)BScale::Row>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, amul, s);
         case BScale::Tile:
-            return launch_mode<(int)BScale::Tile>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, s);
+            return launch_mode<(int)BScale::Tile>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, amul, s);
         case BScale::TileDgrad:
-            return launch_mode<(int)BScale::TileDgrad>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, s);
+            return launch_mode<(int)BScale::TileDgrad>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, amul, s);
     }
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_mx(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* a_scales,
+                          const float* a_dec, const uint8_t* b, const uint8_t* b_scales,
+                          const float* b_dec, void* c, bool c_bf16, hipStream_t s) {
+    if (M == 0 || N == 0) return hipSuccess;
+    return c_bf16 ? launch_mx<true>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, s)
+                  : launch_mx<false>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, s);
 }
 
 }  // namespace ue5m3

@@ -13,27 +13,39 @@ namespace ue5m3 {
 // that profiles tell the fprop and dgrad launches apart.
 enum class BScale : int { Row = 0, Tile = 1, TileDgrad = 2 };
 
+// Block-scale format: UE5M3 (blocks of 16, the recipe), E4M3 (blocks of 16,
+// NVFP4-style) or E8M0 (blocks of 32, MXFP4-style, no tensor scale).
+enum class ScaleKind : int { UE5M3 = 0, E4M3 = 1, E8M0 = 2 };
+
 hipError_t launch_amax(const void* x_bf16, int64_t numel, float* amax_dev, hipStream_t s);
 
-hipError_t launch_quant_rows(const void* x_bf16, int64_t rows, int64_t cols,
+hipError_t launch_quant_rows(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
                              const float* amax_dev, float target, bool sr, uint64_t seed,
                              uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
                              float* dec_out, hipStream_t s);
 
-hipError_t launch_quant_cols(const void* x_bf16, int64_t rows, int64_t cols,
+hipError_t launch_quant_cols(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
                              const float* amax_dev, float target, bool sr, uint64_t seed,
                              uint32_t tensor_id, uint8_t* payload_t, uint8_t* scales_t,
                              float* dec_out, hipStream_t s);
 
-hipError_t launch_quant_tiles(const void* w_bf16, int64_t rows, int64_t cols,
+hipError_t launch_quant_tiles(ScaleKind fmt, const void* w_bf16, int64_t rows, int64_t cols,
                               const float* amax_dev, float target, bool sr, uint64_t seed,
                               uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
                               uint8_t* payload_t, uint8_t* scales_t, float* dec_out,
                               hipStream_t s);
 
-hipError_t launch_gemm(BScale bmode, int64_t M, int64_t N, int64_t K,
+// amul: power of two folded into alpha for the decode's operand scaling
+// (2^6 for UE5M3 codes; 2^22 for E4M3 codes, decoded as UE5M3 = value / 2^8).
+hipError_t launch_gemm(BScale bmode, float amul, int64_t M, int64_t N, int64_t K,
                        const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
                        const uint8_t* b, const uint8_t* b_scales, const float* b_dec,
                        void* c, bool c_bf16, hipStream_t s);
+
+// E8M0 blocks of 32 on the gfx950 scaled FP4 matrix instructions: A [M, K]
+// and B [N, K] rows, one E8M0 byte per 32 k of each row.
+hipError_t launch_gemm_mx(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* a_scales,
+                          const float* a_dec, const uint8_t* b, const uint8_t* b_scales,
+                          const float* b_dec, void* c, bool c_bf16, hipStream_t s);
 
 }  // namespace ue5m3

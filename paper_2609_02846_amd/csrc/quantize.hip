@@ -30,14 +30,39 @@ struct BlockScale {
     float r;
 };
 
+// Block scale and reciprocal of a block from the bf16 bits of its largest
+// magnitude.  UE5M3 and E4M3: code = nearest code of a * S (zero code ->
+// code of 1.0), r = G / value(code).  E8M0: the power-of-two exponent of the
+// OCP microscaling rule and r = 2^-E (no tensor scale).
+template <int FMT>
 __device__ __forceinline__ BlockScale block_scale(uint32_t amax_bits15, const Multipliers& m) {
-    const float a = __uint_as_float(amax_bits15 << 16);
-    uint32_t code = ue5m3_encode(a * m.S);
-    code = code ? code : kCodeOne;
     BlockScale bs;
+    if (FMT == (int)ScaleKind::E8M0) {
+        bs.code = e8m0_code_of_amax(amax_bits15);
+        bs.r = e8m0_reciprocal(bs.code);
+        return bs;
+    }
+    const float a = __uint_as_float(amax_bits15 << 16);
+    const bool e4 = FMT == (int)ScaleKind::E4M3;
+    uint32_t code = e4 ? e4m3_encode(a * m.S) : ue5m3_encode(a * m.S);
+    code = code ? code : (e4 ? kE4M3CodeOne : kCodeOne);
     bs.code = code;
-    bs.r = m.G / ue5m3_decode(code);
+    bs.r = m.G / (e4 ? e4m3_decode(code) : ue5m3_decode(code));
     return bs;
+}
+
+// Tensor multipliers of a quantizer launch (E8M0 has no tensor scale: the
+// held amax is not read and the decode multiplier is 1).
+template <int FMT>
+__device__ __forceinline__ Multipliers kernel_multipliers(const float* amax_dev, float T) {
+    if (FMT == (int)ScaleKind::E8M0) {
+        Multipliers m;
+        m.S = 1.0f;
+        m.G = 1.0f;
+        m.dec = 1.0f;
+        return m;
+    }
+    return tensor_multipliers(*amax_dev, T);
 }
 
 // E2M1 round-to-nearest-even of y0, y1 into byte SEL of p (y0 in the low
@@ -172,46 +197,55 @@ __device__ __forceinline__ void words4(uint64_t e0, uint32_t tid, uint32_t k0, u
 }
 
 // ------------------------------------------------------------ rows (1D) --
-// The flat tensor is a sequence of 16-element blocks (cols % 16 == 0).  One
-// lane per block: two 16-byte loads, 8 bytes of payload and 1 byte of scale,
-// so one wave instruction stores 512 contiguous payload bytes and 64 scale
-// bytes.  Persistent grid: a lane walks blocks b, b + stride, ..., loading
-// the next block before quantizing the current one.
-template <bool SR>
+// The flat tensor is a sequence of blocks of 16 (32 for E8M0) elements.  One
+// lane per block: two (four) 16-byte loads, 8 (16) bytes of payload and 1
+// byte of scale, so one wave instruction stores 512 (1024) contiguous payload
+// bytes and 64 scale bytes.  Persistent grid: a lane walks blocks b,
+// b + stride, ..., loading the next block before quantizing the current one.
+template <bool SR, int FMT>
 __global__ __launch_bounds__(kThreads) void quant_rows_kernel(
     const uint4* __restrict__ x, int64_t nblocks, const float* __restrict__ amax_dev, float T,
     uint32_t key0, uint32_t key1, uint32_t tid, uint2* __restrict__ payload,
     uint8_t* __restrict__ scales, float* __restrict__ dec_out) {
-    const Multipliers m = tensor_multipliers(*amax_dev, T);
+    constexpr int H = FMT == (int)ScaleKind::E8M0 ? 2 : 1;    // 16-element halves per block
+    const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    uint4 c0, c1;
+    uint4 c[2 * H];
     if (b < nblocks) {
-        c0 = x[2 * b];
-        c1 = x[2 * b + 1];
+#pragma unroll
+        for (int i = 0; i < 2 * H; ++i) c[i] = x[2 * H * b + i];
     }
     for (; b < nblocks; b += stride) {
         const int64_t bn = b + stride;
-        uint4 n0 = make_uint4(0u, 0u, 0u, 0u), n1 = n0;
-        if (bn < nblocks) {
-            n0 = x[2 * bn];
-            n1 = x[2 * bn + 1];
-        }
-        const BlockScale bs = block_scale(max(amax8(c0), amax8(c1)), m);
-        uint32_t w[16];
-        if (SR) {
-            // elements 16b .. 16b+15: Philox blocks 4b .. 4b+3
+        uint4 n[2 * H];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint4 q = sr_words4((uint64_t)b * 4 + i, tid, key0, key1);
-                w[4 * i] = q.x; w[4 * i + 1] = q.y; w[4 * i + 2] = q.z; w[4 * i + 3] = q.w;
-            }
+        for (int i = 0; i < 2 * H; ++i) n[i] = make_uint4(0u, 0u, 0u, 0u);
+        if (bn < nblocks) {
+#pragma unroll
+            for (int i = 0; i < 2 * H; ++i) n[i] = x[2 * H * bn + i];
         }
-        payload[b] = make_uint2(quant8<SR>(c0, bs.r, w), quant8<SR>(c1, bs.r, w + 8));
+        uint32_t mx = 0u;
+#pragma unroll
+        for (int i = 0; i < 2 * H; ++i) mx = max(mx, amax8(c[i]));
+        const BlockScale bs = block_scale<FMT>(mx, m);
+#pragma unroll
+        for (int h = 0; h < H; ++h) {
+            uint32_t w[16];
+            if (SR) {
+                // elements 16(Hb + h) .. +15: Philox blocks 4(Hb + h) .. +3
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint4 q = sr_words4((uint64_t)(H * b + h) * 4 + i, tid, key0, key1);
+                    w[4 * i] = q.x; w[4 * i + 1] = q.y; w[4 * i + 2] = q.z; w[4 * i + 3] = q.w;
+                }
+            }
+            payload[H * b + h] = make_uint2(quant8<SR>(c[2 * h], bs.r, w), quant8<SR>(c[2 * h + 1], bs.r, w + 8));
+        }
         scales[b] = (uint8_t)bs.code;
-        c0 = n0;
-        c1 = n1;
+#pragma unroll
+        for (int i = 0; i < 2 * H; ++i) c[i] = n[i];
     }
 }
 
@@ -290,7 +324,7 @@ __device__ __forceinline__ void sr_cols16x4(const uint32_t (&lo)[16], const uint
         for (int h = 0; h < 2; ++h) pk[j][h] = (aL[j][h] & 0x0F0F0F0Fu) | (aH[j][h] & 0xF0F0F0F0u);
 }
 
-template <bool SR>
+template <bool SR, int FMT>
 __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
     const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t rows_per_item, int64_t gx,
     int64_t nitems, const float* __restrict__ amax_dev, float T, uint32_t key0, uint32_t key1,
@@ -298,12 +332,15 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
     float* __restrict__ dec_out) {
     __shared__ __attribute__((aligned(16))) uint8_t stP[kColCols][kColGroupRB * 8];
     __shared__ __attribute__((aligned(16))) uint8_t stS[kColCols][kColGroupRB * kColScaleGroups];
-    const Multipliers m = tensor_multipliers(*amax_dev, T);
+    // E8M0 blocks are 32 rows: the two 16-row blocks of a wave (lanes l and
+    // l + 32) form one block and share its maximum and scale byte.
+    constexpr int H = FMT == (int)ScaleKind::E8M0 ? 2 : 1;
+    const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
     const int t = threadIdx.x;
     const int q = t & 31, rbl = t >> 5;
     const bool vec8 = (cols & 3) == 0;
-    const int64_t nrb = rows / 16;
+    const int64_t nrb = rows / (16 * H);                        // scale bytes per column
     const int64_t ldo = rows / 2;                               // payload_t row stride (bytes)
 
     // 16 rows x 4 columns of this lane's row block of group g of item ci:
@@ -357,9 +394,13 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
                 mx[2] = max(mx[2], hi[r] & 0x7FFFu);
                 mx[3] = max(mx[3], (hi[r] >> 16) & 0x7FFFu);
             }
+            if (H == 2) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) mx[j] = max(mx[j], (uint32_t)__shfl_xor((int)mx[j], 32));
+            }
             BlockScale bs[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) bs[j] = block_scale(mx[j], m);
+            for (int j = 0; j < 4; ++j) bs[j] = block_scale<FMT>(mx[j], m);
             uint32_t pk[4][2];
             if (SR) {
                 if (vec8)
@@ -382,7 +423,8 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 *reinterpret_cast<uint2*>(&stP[4 * q + j][rbl * 8]) = make_uint2(pk[j][0], pk[j][1]);
-                stS[4 * q + j][sg * kColGroupRB + rbl] = (uint8_t)bs[j].code;
+                if (H == 1 || (rbl & 1) == 0)
+                    stS[4 * q + j][(sg * kColGroupRB + rbl) / H] = (uint8_t)bs[j].code;
             }
         }
         __syncthreads();
@@ -406,17 +448,20 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
                                 *reinterpret_cast<const uint2*>(s + (k - half * 4) * 8);
                 }
             }
-            // scales: at the end of the item (or of a full 64-block chunk)
+            // scales: at the end of the item (or of a full 64-block chunk);
+            // SB bytes per column for a full chunk, half of them per lane
             if (sg == kColScaleGroups - 1 || g == ci.ngroups - 1) {
-                const int64_t rbs = rb0 - (int64_t)sg * kColGroupRB;
-                const int ns = (int)(rb0 + nvalid - rbs);
+                constexpr int SB = kColGroupRB * kColScaleGroups / H;
+                const int64_t rbs = (rb0 - (int64_t)sg * kColGroupRB) / H;
+                const int ns = (int)((rb0 + nvalid) / H - rbs);
                 if (gc < cols) {
-                    uint8_t* dst = scales_t + gc * nrb + rbs + half * 32;
-                    const uint8_t* s = &stS[col][half * 32];
-                    const int lo_k = half * 32, hi_k = min(ns, half * 32 + 32);
-                    if (hi_k - lo_k == 32 && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
-                        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(s);
-                        *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(s + 16);
+                    uint8_t* dst = scales_t + gc * nrb + rbs + half * (SB / 2);
+                    const uint8_t* s = &stS[col][half * (SB / 2)];
+                    const int lo_k = half * (SB / 2), hi_k = min(ns, (half + 1) * (SB / 2));
+                    if (hi_k - lo_k == SB / 2 && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
+#pragma unroll
+                        for (int v = 0; v < SB / 32; ++v)
+                            reinterpret_cast<uint4*>(dst)[v] = reinterpret_cast<const uint4*>(s)[v];
                     } else {
                         for (int k = lo_k; k < hi_k; ++k) dst[k - lo_k] = s[k - lo_k];
                     }
@@ -446,14 +491,15 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
 constexpr int kTileCols = 128;
 constexpr int kTileRowTiles = 8;
 
-template <bool SR>
+template <bool SR, int FMT>
 __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
     const uint16_t* __restrict__ w, int64_t rows, int64_t cols, const float* __restrict__ amax_dev,
     float T, uint32_t key0, uint32_t key1, uint32_t tid, uint8_t* __restrict__ payload,
     uint8_t* __restrict__ scales, uint8_t* __restrict__ payload_t, uint8_t* __restrict__ scales_t,
     float* __restrict__ dec_out) {
     __shared__ __attribute__((aligned(16))) uint8_t stT[kTileCols][kTileRowTiles * 8];
-    const Multipliers m = tensor_multipliers(*amax_dev, T);
+    static_assert(FMT != (int)ScaleKind::E8M0, "2D tiles take UE5M3 or E4M3 scales");
+    const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *dec_out = m.dec;
     const int t = threadIdx.x;
     const int q = t & 31, trl = t >> 5;
@@ -476,7 +522,7 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
         for (int r = 0; r < 16; ++r) mx = max(mx, max(bf16_abs_max_pair(lo[r]), bf16_abs_max_pair(hi[r])));
         mx = max(mx, (uint32_t)__shfl_xor((int)mx, 1));
         mx = max(mx, (uint32_t)__shfl_xor((int)mx, 2));
-        const BlockScale bs = block_scale(mx, m);
+        const BlockScale bs = block_scale<FMT>(mx, m);
         uint32_t colpk[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
         if (SR) {
 #pragma unroll
@@ -564,13 +610,12 @@ inline void seed_key(uint64_t seed, uint32_t& k0, uint32_t& k1) {
 // Resident workgroups to aim for: 8 per CU on the 256 CUs of an MI355X.
 constexpr int64_t kPersistentWGs = 256 * 8;
 
-}  // namespace
-
-hipError_t launch_quant_rows(const void* x_bf16, int64_t rows, int64_t cols,
-                             const float* amax_dev, float target, bool sr, uint64_t seed,
-                             uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
-                             float* dec_out, hipStream_t s) {
-    const int64_t nblocks = rows * cols / 16;
+template <int FMT>
+hipError_t launch_rows_fmt(const void* x_bf16, int64_t rows, int64_t cols, const float* amax_dev,
+                           float target, bool sr, uint64_t seed, uint32_t tensor_id,
+                           uint8_t* payload, uint8_t* scales, float* dec_out, hipStream_t s) {
+    constexpr int64_t BE = FMT == (int)ScaleKind::E8M0 ? 32 : 16;
+    const int64_t nblocks = rows * cols / BE;
     uint32_t k0, k1;
     seed_key(seed, k0, k1);
     int64_t wgs = (nblocks + kThreads - 1) / kThreads;
@@ -579,10 +624,10 @@ hipError_t launch_quant_rows(const void* x_bf16, int64_t rows, int64_t cols,
     const uint4* x = reinterpret_cast<const uint4*>(x_bf16);
     uint2* p = reinterpret_cast<uint2*>(payload);
     if (sr)
-        hipLaunchKernelGGL(quant_rows_kernel<true>, dim3((unsigned)wgs), dim3(kThreads), 0, s, x,
+        hipLaunchKernelGGL((quant_rows_kernel<true, FMT>), dim3((unsigned)wgs), dim3(kThreads), 0, s, x,
                            nblocks, amax_dev, target, k0, k1, tensor_id, p, scales, dec_out);
     else
-        hipLaunchKernelGGL(quant_rows_kernel<false>, dim3((unsigned)wgs), dim3(kThreads), 0, s, x,
+        hipLaunchKernelGGL((quant_rows_kernel<false, FMT>), dim3((unsigned)wgs), dim3(kThreads), 0, s, x,
                            nblocks, amax_dev, target, k0, k1, tensor_id, p, scales, dec_out);
     return hipGetLastError();
 }
@@ -590,7 +635,7 @@ hipError_t launch_quant_rows(const void* x_bf16, int64_t rows, int64_t cols,
 // Resident workgroups of a kernel on the current device (cached per device).
 template <typename K>
 int64_t resident_wgs(K kernel, int slot) {
-    static int64_t cache[16][4] = {};
+    static int64_t cache[16][8] = {};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return kPersistentWGs;
     if (cache[dev][slot] == 0) {
@@ -605,15 +650,15 @@ int64_t resident_wgs(K kernel, int slot) {
     return cache[dev][slot];
 }
 
-hipError_t launch_quant_cols(const void* x_bf16, int64_t rows, int64_t cols,
-                             const float* amax_dev, float target, bool sr, uint64_t seed,
-                             uint32_t tensor_id, uint8_t* payload_t, uint8_t* scales_t,
-                             float* dec_out, hipStream_t s) {
+template <int FMT>
+hipError_t launch_cols_fmt(const void* x_bf16, int64_t rows, int64_t cols, const float* amax_dev,
+                           float target, bool sr, uint64_t seed, uint32_t tensor_id,
+                           uint8_t* payload_t, uint8_t* scales_t, float* dec_out, hipStream_t s) {
     uint32_t k0, k1;
     seed_key(seed, k0, k1);
     const int64_t gx = (cols + kColCols - 1) / kColCols;
-    const int64_t resident = sr ? resident_wgs(quant_cols_kernel<true>, 0)
-                                : resident_wgs(quant_cols_kernel<false>, 1);
+    const int64_t resident = sr ? resident_wgs(quant_cols_kernel<true, FMT>, 2 * FMT)
+                                : resident_wgs(quant_cols_kernel<false, FMT>, 2 * FMT + 1);
     // Items of up to 64 row blocks (whole 64-byte scale runs); shorter when
     // that leaves fewer than 2 items per resident workgroup.
     int64_t rows_per_item = (int64_t)kColGroupRB * kColScaleGroups * 16;     // 1024 rows
@@ -624,35 +669,85 @@ hipError_t launch_quant_cols(const void* x_bf16, int64_t rows, int64_t cols,
     const int64_t grid = min(nitems, resident);
     const uint16_t* x = reinterpret_cast<const uint16_t*>(x_bf16);
     if (sr)
-        hipLaunchKernelGGL(quant_cols_kernel<true>, dim3((unsigned)grid), dim3(kThreads), 0, s, x, rows,
-                           cols, rows_per_item, gx, nitems, amax_dev, target, k0, k1, tensor_id,
+        hipLaunchKernelGGL((quant_cols_kernel<true, FMT>), dim3((unsigned)grid), dim3(kThreads), 0, s, x,
+                           rows, cols, rows_per_item, gx, nitems, amax_dev, target, k0, k1, tensor_id,
                            payload_t, scales_t, dec_out);
     else
-        hipLaunchKernelGGL(quant_cols_kernel<false>, dim3((unsigned)grid), dim3(kThreads), 0, s, x, rows,
-                           cols, rows_per_item, gx, nitems, amax_dev, target, k0, k1, tensor_id,
+        hipLaunchKernelGGL((quant_cols_kernel<false, FMT>), dim3((unsigned)grid), dim3(kThreads), 0, s, x,
+                           rows, cols, rows_per_item, gx, nitems, amax_dev, target, k0, k1, tensor_id,
                            payload_t, scales_t, dec_out);
     return hipGetLastError();
 }
 
-hipError_t launch_quant_tiles(const void* w_bf16, int64_t rows, int64_t cols,
-                              const float* amax_dev, float target, bool sr, uint64_t seed,
-                              uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
-                              uint8_t* payload_t, uint8_t* scales_t, float* dec_out,
-                              hipStream_t s) {
+template <int FMT>
+hipError_t launch_tiles_fmt(const void* w_bf16, int64_t rows, int64_t cols, const float* amax_dev,
+                            float target, bool sr, uint64_t seed, uint32_t tensor_id,
+                            uint8_t* payload, uint8_t* scales, uint8_t* payload_t, uint8_t* scales_t,
+                            float* dec_out, hipStream_t s) {
     uint32_t k0, k1;
     seed_key(seed, k0, k1);
     const int64_t gx = (cols + kTileCols - 1) / kTileCols;
     const int64_t gy = (rows / 16 + kTileRowTiles - 1) / kTileRowTiles;
     const uint16_t* w = reinterpret_cast<const uint16_t*>(w_bf16);
     if (sr)
-        hipLaunchKernelGGL(quant_tiles_kernel<true>, dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
+        hipLaunchKernelGGL((quant_tiles_kernel<true, FMT>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
                            0, s, w, rows, cols, amax_dev, target, k0, k1, tensor_id, payload, scales,
                            payload_t, scales_t, dec_out);
     else
-        hipLaunchKernelGGL(quant_tiles_kernel<false>, dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
+        hipLaunchKernelGGL((quant_tiles_kernel<false, FMT>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
                            0, s, w, rows, cols, amax_dev, target, k0, k1, tensor_id, payload, scales,
                            payload_t, scales_t, dec_out);
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_quant_rows(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
+                             const float* amax_dev, float target, bool sr, uint64_t seed,
+                             uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
+                             float* dec_out, hipStream_t s) {
+    switch (fmt) {
+        case ScaleKind::E4M3:
+            return launch_rows_fmt<(int)ScaleKind::E4M3>(x_bf16, rows, cols, amax_dev, target, sr, seed,
+                                                         tensor_id, payload, scales, dec_out, s);
+        case ScaleKind::E8M0:
+            return launch_rows_fmt<(int)ScaleKind::E8M0>(x_bf16, rows, cols, amax_dev, target, sr, seed,
+                                                         tensor_id, payload, scales, dec_out, s);
+        default:
+            return launch_rows_fmt<(int)ScaleKind::UE5M3>(x_bf16, rows, cols, amax_dev, target, sr, seed,
+                                                          tensor_id, payload, scales, dec_out, s);
+    }
+}
+
+hipError_t launch_quant_cols(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
+                             const float* amax_dev, float target, bool sr, uint64_t seed,
+                             uint32_t tensor_id, uint8_t* payload_t, uint8_t* scales_t,
+                             float* dec_out, hipStream_t s) {
+    switch (fmt) {
+        case ScaleKind::E4M3:
+            return launch_cols_fmt<(int)ScaleKind::E4M3>(x_bf16, rows, cols, amax_dev, target, sr, seed,
+                                                         tensor_id, payload_t, scales_t, dec_out, s);
+        case ScaleKind::E8M0:
+            return launch_cols_fmt<(int)ScaleKind::E8M0>(x_bf16, rows, cols, amax_dev, target, sr, seed,
+                                                         tensor_id, payload_t, scales_t, dec_out, s);
+        default:
+            return launch_cols_fmt<(int)ScaleKind::UE5M3>(x_bf16, rows, cols, amax_dev, target, sr, seed,
+                                                          tensor_id, payload_t, scales_t, dec_out, s);
+    }
+}
+
+hipError_t launch_quant_tiles(ScaleKind fmt, const void* w_bf16, int64_t rows, int64_t cols,
+                              const float* amax_dev, float target, bool sr, uint64_t seed,
+                              uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
+                              uint8_t* payload_t, uint8_t* scales_t, float* dec_out,
+                              hipStream_t s) {
+    if (fmt == ScaleKind::E4M3)
+        return launch_tiles_fmt<(int)ScaleKind::E4M3>(w_bf16, rows, cols, amax_dev, target, sr, seed,
+                                                      tensor_id, payload, scales, payload_t, scales_t,
+                                                      dec_out, s);
+    return launch_tiles_fmt<(int)ScaleKind::UE5M3>(w_bf16, rows, cols, amax_dev, target, sr, seed,
+                                                   tensor_id, payload, scales, payload_t, scales_t,
+                                                   dec_out, s);
 }
 
 }  // namespace ue5m3

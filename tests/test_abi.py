@@ -122,3 +122,32 @@ def test_amax_state_host_logic(lib):
     lib.ue5m3_amax_state_reset(ctypes.byref(st))
     assert st.has_cache == 0
     lib.ue5m3_amax_state_reset(None)
+
+
+def test_format_entry_points_validation(lib):
+    """_ex calls: scale kind, block length, E8M0 without amax, 2D E8M0 and
+    the E8M0 GEMM's K % 256 requirement are checked on the host."""
+    q = lib.ue5m3_quantize_1d_ex
+
+    def call(kind=1, block=16, amax=FAKE, rows=32, cols=32, axis=1):
+        return q(FAKE, rows, cols, axis, amax, 448.0, 0, 0, 0, kind, block, FAKE, FAKE, NULL, NULL)
+    assert call(kind=3) == ue.UE5M3_EINVAL
+    assert call(kind=1, block=32) == ue.UE5M3_EINVAL          # E4M3 blocks are 16
+    assert call(kind=2, block=16) == ue.UE5M3_EINVAL          # E8M0 blocks are 32
+    assert call(kind=1, amax=NULL) == ue.UE5M3_EINVAL         # E4M3 needs the held amax
+    assert call(kind=2, block=32, amax=NULL, rows=0) == ue.UE5M3_OK   # E8M0 does not
+    assert call(kind=2, block=32, cols=48) == ue.UE5M3_ESHAPE
+    assert call(kind=2, block=32, axis=0, rows=48) == ue.UE5M3_ESHAPE
+    q2 = lib.ue5m3_quantize_2d_ex
+    assert q2(FAKE, 32, 32, FAKE, 448.0, 0, 0, 0, 2, FAKE, FAKE, NULL, NULL, NULL, NULL) == ue.UE5M3_EINVAL
+    assert q2(FAKE, 0, 32, FAKE, 448.0, 0, 0, 0, 1, FAKE, FAKE, NULL, NULL, NULL, NULL) == ue.UE5M3_OK
+    g = lib.ue5m3_gemm_ex
+
+    def gcall(kind=2, M=32, N=32, K=256, layout=0):
+        return g(layout, M, N, K, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, kind, NULL)
+    assert gcall(kind=5) == ue.UE5M3_EINVAL
+    assert gcall(K=128) == ue.UE5M3_ESHAPE                    # E8M0 needs K % 256
+    assert gcall(kind=1, K=128, N=40) == ue.UE5M3_ESHAPE      # E4M3 NT: N % 16
+    assert gcall(layout=3) == ue.UE5M3_ELAYOUT
+    assert gcall(M=0) == ue.UE5M3_OK
+    assert gcall(M=1 << 20, N=1 << 20) == ue.UE5M3_ESHAPE     # 32-bit offsets

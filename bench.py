@@ -45,6 +45,10 @@ def parse():
     p.add_argument("--kernel", default=None,
                    help="profiling aid: after setup run only this step kernel (e.g. gemm_fprop) "
                         "--steps times and exit without a JSON line")
+    p.add_argument("--formats", action="store_true",
+                   help="scale-format comparison instead of the headline step: UE5M3 (delayed "
+                        "amax), E4M3 (current amax) and E8M0 (blocks of 32) on the QKV workload "
+                        "X [16384, 4096], W [6144, 4096], dY [16384, 6144]; one JSON line")
     p.add_argument("--copy-ref", type=int, default=0, metavar="BYTES",
                    help="profiling aid: time a plain device copy of BYTES bytes (the reference "
                         "that scales the HBM byte counters) and exit")
@@ -110,12 +114,109 @@ def cpu_baseline(wl, T, K, N, target_s=12.0):
                        f"{t_step:.1f} s")}
 
 
+def _decode_rows(payload, scales, fmt):
+    """Host decode of sampled quantized rows (measurement only): E2M1 value
+    times its block scale, float64."""
+    mag = np.array([0, .5, 1, 1.5, 2, 3, 4, 6], np.float64)
+    p = payload.astype(np.uint8)
+    nib = np.empty((p.shape[0], p.shape[1] * 2), np.uint8)
+    nib[:, 0::2], nib[:, 1::2] = p & 15, p >> 4
+    q = np.where(nib & 8, -1.0, 1.0) * mag[nib & 7]
+    c = scales.astype(np.int64)
+    if fmt == "e8m0":
+        s = np.exp2(c - 127.0)
+    else:
+        bias, sub = (15, 2.0 ** -17) if fmt == "ue5m3" else (7, 2.0 ** -9)
+        e, m = c >> 3, c & 7
+        s = np.where(e == 0, m * sub, (1 + m / 8.0) * np.exp2(e - float(bias)))
+    return q * np.repeat(s, q.shape[1] // s.shape[1], axis=1)
+
+
+def formats_bench(args):
+    """Config-5 comparison: per encoding, the step time of the quantizers and
+    the three GEMMs, and the quantization error on sampled rows."""
+    import torch
+    import paper_2609_02846_amd as ue
+    import synthetic
+    T, K, N = 16384, 4096, 6144
+    dev = torch.device("cuda:0")
+    wl = synthetic.qkv_formats(0, T, K, N)
+    up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+    x, w, dy = up(wl["x"]), up(wl["w"]), up(wl["dy"])
+    flop = 3 * 2.0 * T * N * K
+    rows = np.random.default_rng(0).choice(T, 256, replace=False)
+    res = {}
+    for fmt in ["ue5m3", "e4m3", "e8m0"]:
+        period = 50 if fmt == "ue5m3" else 1
+        st = {n: ue.AmaxState(period) for n in "xwd"}
+        y = torch.empty(T, N, dtype=torch.float32, device=dev)
+        dx = torch.empty(T, K, dtype=torch.bfloat16, device=dev)
+        dw = torch.empty(N, K, dtype=torch.float32, device=dev)
+        out = {}
+
+        def step(t):
+            if fmt != "e8m0":
+                ue.amax_sample(st["x"], x, t)
+                ue.amax_sample(st["w"], w, t)
+                ue.amax_sample(st["d"], dy, t)
+            a = (lambda n: None) if fmt == "e8m0" else (lambda n: st[n].amax)
+            out["xr"] = ue.quantize_1d(x, 1, a("x"), fmt=fmt)
+            out["xc"] = ue.quantize_1d(x, 0, a("x"), fmt=fmt)
+            out["dr"] = ue.quantize_1d(dy, 1, a("d"), 448.0, "sr", 1000 + t, 1, fmt=fmt)
+            out["dc"] = ue.quantize_1d(dy, 0, a("d"), 448.0, "sr", 1000 + t, 2, fmt=fmt)
+            if fmt == "e8m0":
+                wr = ue.quantize_1d(w, 1, None, fmt=fmt)
+                wc = ue.quantize_1d(w, 0, None, fmt=fmt)
+                out["bf"], out["bd"] = (wr[0], wr[1], wr[2]), (wc[0], wc[1], wc[2])
+            else:
+                wq = ue.quantize_2d(w, a("w"), fmt=fmt)
+                out["bf"], out["bd"] = (wq[0], wq[1], wq[3]), (wq[2], wq[4], wq[3])
+            ue.gemm("nt", T, N, K, *out["xr"], *out["bf"], out=y, fmt=fmt)
+            ue.gemm("nn", T, K, N, *out["dr"], *out["bd"], out=dx, fmt=fmt)
+            ue.gemm("tn", N, K, T, *out["dc"], *out["xc"], out=dw, fmt=fmt)
+
+        for t in range(args.warmup):
+            step(t)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for t in range(args.warmup, args.warmup + args.steps):
+            step(t)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        # quantization error on 256 sampled rows (X, dY rows) and the fprop
+        # output against fp32 products of the bf16 inputs
+        xs = torch.from_numpy(synthetic.bf16_bits_to_f32(wl["x"][rows])).double().numpy()
+        ds = torch.from_numpy(synthetic.bf16_bits_to_f32(wl["dy"][rows])).double().numpy()
+        dec = lambda r, sel: _decode_rows(r[0].cpu().numpy()[sel], r[1].cpu().numpy()[sel], fmt) * \
+            float(r[2].item())
+        xq, dq = dec(out["xr"], rows), dec(out["dr"], rows)
+        rel = lambda a, b: float(np.sqrt(np.mean((a - b) ** 2)) / np.sqrt(np.mean(b ** 2)))
+        wf = synthetic.bf16_bits_to_f32(wl["w"])
+        yref = (torch.from_numpy(synthetic.bf16_bits_to_f32(wl["x"][rows])).to(dev) @
+                torch.from_numpy(wf).to(dev).t()).double().cpu().numpy()
+        res[fmt] = {"ms_per_step": round(ms, 4), "gemm_TFLOPs_step": round(flop / ms / 1e9, 1),
+                    "rel_rmse_x": round(rel(xq, xs), 5), "rel_rmse_dy": round(rel(dq, ds), 5),
+                    "rel_rmse_y": round(rel(y[torch.from_numpy(rows).to(dev)].double().cpu().numpy(), yref), 5),
+                    "amax_period": period if fmt != "e8m0" else None,
+                    "blocks": 32 if fmt == "e8m0" else 16}
+    print(json.dumps({"metric": "scale-format comparison (QKV workload)", "unit": "TFLOP/s",
+                      "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "data": "synthetic",
+                      "dtype": "fp4-e2m1 operands, fp32 accumulate",
+                      "config": {"workload": "QKV projection T=16384 K=4096 N=6144, SR dY"},
+                      "formats": res}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this build has no "
               "multi-GPU path; see DESIGN.md for how the step would shard.", file=sys.stderr)
         sys.exit(2)
+    if args.formats:
+        formats_bench(args)
+        return
     import torch
     import paper_2609_02846_amd as ue
     import synthetic

@@ -103,3 +103,12 @@ def ffn_step(seed=0, tokens=8192, k=4096, n=21504):
     return {"x": activation(seed, tokens, k, 1e-3, 100.0),
             "w": weight(seed, n, k),
             "dy": gradient(seed, tokens, n, 1e-5)}
+
+
+def qkv_formats(seed=0, tokens=16384, k=4096, n=6144):
+    """The scale-format comparison workload (a QKV projection): X [T, K]
+    N(0,1) with 0.1% x100 outliers, W [N, K] N(0, 0.02), dY [T, N]
+    N(0, 1e-4) with a lognormal per-row scale (sigma 2)."""
+    return {"x": activation(seed, tokens, k, 1e-3, 100.0),
+            "w": weight(seed, n, k),
+            "dy": gradient(seed, tokens, n, 1e-4, 2.0)}

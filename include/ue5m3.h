@@ -189,6 +189,25 @@ ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K
                           void* c, ue5m3_out_t c_type, hipStream_t stream);
 
 /*
+ * Both 1D blockings of one bf16 tensor x [rows, cols] from a single read:
+ * the axis-1 result (payload_r [rows, cols/2], scales_r [rows, cols/16]) and
+ * the axis-0 result stored transposed (payload_c [cols, rows/2], scales_c
+ * [cols, rows/16]), each identical to what ue5m3_quantize_1d_ex writes for
+ * that axis -- with SR words keyed on tensor_id_r for the row blocking and
+ * tensor_id_c for the column blocking.  These are the two backward operands
+ * of dY (dgrad and wgrad) or the fprop and wgrad operands of X.
+ * scale_kind UE5M3 or E4M3 (blocks of 16; EINVAL otherwise).  Requires
+ * rows % 16 == 0 and cols % 16 == 0.  dec_out (nullable) as in
+ * ue5m3_quantize_1d.
+ */
+ue5m3_status_t ue5m3_quantize_dual(const void* x_bf16, int64_t rows, int64_t cols,
+                                   const float* amax_dev, float target, ue5m3_round_t mode,
+                                   uint64_t seed, uint32_t tensor_id_r, uint32_t tensor_id_c,
+                                   int32_t scale_kind, uint8_t* payload_r, uint8_t* scales_r,
+                                   uint8_t* payload_c, uint8_t* scales_c, float* dec_out,
+                                   hipStream_t stream);
+
+/*
  * Comparison block-scale formats (Sec. 2, Table tab:formats: the MXFP4 and
  * NVFP4 arrangements of the same E2M1 payload).
  *   UE5M3_SCALE_UE5M3  the recipe: blocks of 16, UE5M3 scales, tensor scale

@@ -30,7 +30,7 @@ BLOCK = {"ue5m3": 16, "e4m3": 16, "e8m0": 32}
 EXPORTED_SYMBOLS = (
     "ue5m3_amax_state_init", "ue5m3_amax_state_reset", "ue5m3_amax_sample",
     "ue5m3_quantize_1d", "ue5m3_quantize_2d", "ue5m3_gemm",
-    "ue5m3_quantize_1d_ex", "ue5m3_quantize_2d_ex", "ue5m3_gemm_ex",
+    "ue5m3_quantize_1d_ex", "ue5m3_quantize_2d_ex", "ue5m3_gemm_ex", "ue5m3_quantize_dual",
     "ue5m3_status_string", "ue5m3_version",
 )
 
@@ -82,6 +82,9 @@ def load_library(path=LIB_PATH):
     lib.ue5m3_quantize_2d_ex.restype = i32
     lib.ue5m3_gemm_ex.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp]
     lib.ue5m3_gemm_ex.restype = i32
+    lib.ue5m3_quantize_dual.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, u32, i32,
+                                        vp, vp, vp, vp, vp, vp]
+    lib.ue5m3_quantize_dual.restype = i32
     lib.ue5m3_status_string.argtypes = [i32]
     lib.ue5m3_status_string.restype = ctypes.c_char_p
     lib.ue5m3_version.argtypes = []
@@ -180,6 +183,24 @@ def quantize_1d(x, axis, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0,
                                       _ptr(dec_out), _stream(stream))
     _check(st, "ue5m3_quantize_1d")
     return payload, scales, dec_out
+
+
+def quantize_dual(x, amax_dev, target=448.0, mode="rn", seed=0, tensor_id_r=0, tensor_id_c=0,
+                  rows_out=None, cols_out=None, dec_out=None, stream=None, fmt="ue5m3"):
+    """Both 1D blockings of ``x`` from one read (see ue5m3_quantize_dual).
+    Returns ((payload_r, scales_r, dec), (payload_c, scales_c, dec)) laid out
+    exactly as quantize_1d's axis-1 and axis-0 results."""
+    _bf16_2d(x, "x")
+    R, C = x.shape
+    pr, sr_ = rows_out if rows_out is not None else (_u8((R, C // 2), x), _u8((R, C // 16), x))
+    pc, sc = cols_out if cols_out is not None else (_u8((C, R // 2), x), _u8((C, R // 16), x))
+    if dec_out is None:
+        dec_out = torch.empty(1, dtype=torch.float32, device=x.device)
+    _check(load_library().ue5m3_quantize_dual(
+        _ptr(x), R, C, _ptr(amax_dev), float(target), _MODES[mode], int(seed) & (2**64 - 1),
+        int(tensor_id_r) & 0xFFFFFFFF, int(tensor_id_c) & 0xFFFFFFFF, _FORMATS[fmt], _ptr(pr),
+        _ptr(sr_), _ptr(pc), _ptr(sc), _ptr(dec_out), _stream(stream)), "ue5m3_quantize_dual")
+    return (pr, sr_, dec_out), (pc, sc, dec_out)
 
 
 def quantize_2d(w, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0, transposed=True,

@@ -140,6 +140,30 @@ ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
                                 stream);
 }
 
+ue5m3_status_t ue5m3_quantize_dual(const void* x_bf16, int64_t rows, int64_t cols,
+                                   const float* amax_dev, float target, ue5m3_round_t mode,
+                                   uint64_t seed, uint32_t tensor_id_r, uint32_t tensor_id_c,
+                                   int32_t scale_kind, uint8_t* payload_r, uint8_t* scales_r,
+                                   uint8_t* payload_c, uint8_t* scales_c, float* dec_out,
+                                   hipStream_t stream) {
+    if (mode != UE5M3_RN && mode != UE5M3_SR) return UE5M3_EINVAL;
+    if (scale_kind != UE5M3_SCALE_UE5M3 && scale_kind != UE5M3_SCALE_E4M3) return UE5M3_EINVAL;
+    if (amax_dev == nullptr || !valid_target(target)) return UE5M3_EINVAL;
+    if (rows < 0 || cols < 0 || rows % 16 != 0 || cols % 16 != 0) return UE5M3_ESHAPE;
+    if (!aligned4(amax_dev) || (dec_out != nullptr && !aligned4(dec_out))) return UE5M3_EALIGN;
+    if (rows == 0 || cols == 0) return UE5M3_OK;
+    if (x_bf16 == nullptr || payload_r == nullptr || scales_r == nullptr || payload_c == nullptr ||
+        scales_c == nullptr)
+        return UE5M3_EINVAL;
+    if (!aligned16(x_bf16) || !aligned16(payload_r) || !aligned16(scales_r) || !aligned16(payload_c) ||
+        !aligned16(scales_c))
+        return UE5M3_EALIGN;
+    return hip_status(ue5m3::launch_quant_dual(static_cast<ue5m3::ScaleKind>(scale_kind), x_bf16, rows, cols,
+                                               amax_dev, target, mode == UE5M3_SR, seed, tensor_id_r,
+                                               tensor_id_c, payload_r, scales_r, payload_c, scales_c,
+                                               dec_out, stream));
+}
+
 ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
                              const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
                              const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,

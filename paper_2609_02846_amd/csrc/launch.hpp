@@ -35,6 +35,12 @@ hipError_t launch_quant_tiles(ScaleKind fmt, const void* w_bf16, int64_t rows, i
                               uint8_t* payload_t, uint8_t* scales_t, float* dec_out,
                               hipStream_t s);
 
+// Row and column blockings of one tensor from one read (blocks of 16).
+hipError_t launch_quant_dual(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
+                             const float* amax_dev, float target, bool sr, uint64_t seed,
+                             uint32_t tid_r, uint32_t tid_c, uint8_t* payload_r, uint8_t* scales_r,
+                             uint8_t* payload_c, uint8_t* scales_c, float* dec_out, hipStream_t s);
+
 // amul: power of two folded into alpha for the decode's operand scaling
 // (2^6 for UE5M3 codes; 2^22 for E4M3 codes, decoded as UE5M3 = value / 2^8).
 hipError_t launch_gemm(BScale bmode, float amul, int64_t M, int64_t N, int64_t K,

@@ -128,6 +128,21 @@ __device__ __forceinline__ uint32_t sr8(const float (&y)[8], const uint32_t* w) 
     return p;
 }
 
+// 4 values y (element e -> nibble e of the low 16 bits) by SR with words w.
+__device__ __forceinline__ uint32_t sr4(const float (&y)[4], const uint32_t* w) {
+    uint32_t lo = 0u, hi = 0u;
+    const v2f_t v0 = {y[0], y[1]}, v1 = {y[2], y[3]};
+    lo = sr_pair<0>(lo, v0, ~w[0]);
+    hi = sr_pair<0>(hi, v0, __builtin_amdgcn_alignbit(~w[1], ~w[1], 1));
+    lo = sr_pair<1>(lo, v1, ~w[2]);
+    hi = sr_pair<1>(hi, v1, __builtin_amdgcn_alignbit(~w[3], ~w[3], 1));
+    uint32_t p = (lo & 0x0F0Fu) | (hi & 0xF0F0u);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        if (sr_check(y[e], w[e])) p = (p & ~(0xFu << (4 * e))) | (e2m1_sr(y[e], w[e]) << (4 * e));
+    return p;
+}
+
 // Quantize the 8 bf16 values held in v (element e in half e&1 of word e>>1)
 // with reciprocal r; returns 8 nibbles packed little-endian.  For SR, w holds
 // the 8 Philox words of the elements.
@@ -602,6 +617,168 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
     }
 }
 
+// ------------------------------------------------- both axes in one pass --
+// The row blocking (blocks of 16 along each row) and the column blocking
+// (blocks of 16 down each column, stored transposed) of one tensor from a
+// single read of it -- the two operands of a backward pass (dY: dgrad and
+// wgrad) or of X (fprop and wgrad).  A workgroup covers 128 rows (8 tile
+// rows; thread t handles tile row t / 32) x 128 columns (lane q = t % 32
+// holds columns 4q .. 4q+3), i.e. a 16 x 4 piece per lane: its 4 column
+// blocks are in-lane, each row block spans the 4 lanes 4k .. 4k+3 (maxima
+// combined by two lane swaps).  Row payloads go out straight from registers
+// (32 lanes x 2 bytes = 64 contiguous bytes per row); the transposed payload
+// and both scale arrays are assembled in LDS.  SR words use tensor id
+// tid_r for the row blocking and tid_c for the column blocking.
+template <bool SR, int FMT>
+__global__ __launch_bounds__(kThreads) void quant_dual_kernel(
+    const uint16_t* __restrict__ x, int64_t rows, int64_t cols, const float* __restrict__ amax_dev,
+    float T, uint32_t key0, uint32_t key1, uint32_t tid_r, uint32_t tid_c,
+    uint8_t* __restrict__ payload_r, uint8_t* __restrict__ scales_r, uint8_t* __restrict__ payload_c,
+    uint8_t* __restrict__ scales_c, float* __restrict__ dec_out) {
+    __shared__ __attribute__((aligned(16))) uint8_t stP[kTileCols][kTileRowTiles * 8];
+    __shared__ __attribute__((aligned(16))) uint8_t stSR[kTileRowTiles * 16][kTileCols / 16];
+    __shared__ __attribute__((aligned(16))) uint8_t stSC[kTileCols][kTileRowTiles];
+    static_assert(FMT != (int)ScaleKind::E8M0, "blocks of 16");
+    const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
+    if (dec_out != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *dec_out = m.dec;
+    const int t = threadIdx.x;
+    const int q = t & 31, trl = t >> 5;
+    const int64_t cw = (int64_t)blockIdx.x * kTileCols;
+    const int64_t c = cw + 4 * q;
+    const int64_t tr = (int64_t)blockIdx.y * kTileRowTiles + trl;     // tile row
+    const int64_t ntr = rows / 16;
+    const bool active = (c < cols) && (tr < ntr);                     // cols % 16 == 0
+    if (active) {
+        const uint16_t* src = x + (tr * 16) * cols + c;
+        uint32_t lo[16], hi[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const uint2 v = *reinterpret_cast<const uint2*>(src + r * cols);
+            lo[r] = v.x;
+            hi[r] = v.y;
+        }
+        // column blocks: in-lane maxima of the 4 columns
+        uint32_t mc[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            mc[0] = max(mc[0], lo[r] & 0x7FFFu);
+            mc[1] = max(mc[1], (lo[r] >> 16) & 0x7FFFu);
+            mc[2] = max(mc[2], hi[r] & 0x7FFFu);
+            mc[3] = max(mc[3], (hi[r] >> 16) & 0x7FFFu);
+        }
+        BlockScale bc[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) bc[j] = block_scale<FMT>(mc[j], m);
+        uint32_t pk[4][2];
+        if (SR) {
+            sr_cols16x4<true>(lo, hi, bc, (uint64_t)(tr * 16) * (uint64_t)cols + (uint64_t)c,
+                              (uint64_t)cols, tid_c, key0, key1, pk);
+        } else {
+            const uint32_t nw[16] = {};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                float xv[16];
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    xv[r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
+                quant_col16<false>(xv, bc[j].r, nw, pk[j][0], pk[j][1]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            *reinterpret_cast<uint2*>(&stP[4 * q + j][trl * 8]) = make_uint2(pk[j][0], pk[j][1]);
+            stSC[4 * q + j][trl] = (uint8_t)bc[j].code;
+        }
+        // row blocks: one per row over the lane quad 4k .. 4k+3.  Maxima
+        // are combined by quad permutations; lane k of the quad derives the
+        // scales of rows k, k+4, k+8, k+12 and the others take them by a
+        // quad broadcast, so each block scale is computed once.
+        uint32_t mrow[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            uint32_t mr = max(bf16_abs_max_pair(lo[r]), bf16_abs_max_pair(hi[r]));
+            mr = max(mr, (uint32_t)__builtin_amdgcn_mov_dpp((int)mr, 0xB1, 0xF, 0xF, false));   // quad xor 1
+            mr = max(mr, (uint32_t)__builtin_amdgcn_mov_dpp((int)mr, 0x4E, 0xF, 0xF, false));   // quad xor 2
+            mrow[r] = mr;
+        }
+        const int qk = q & 3;
+        BlockScale own[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            // row 4u + qk of this lane's quad position
+            const uint32_t mo = qk == 0 ? mrow[4 * u] : qk == 1 ? mrow[4 * u + 1] : qk == 2 ? mrow[4 * u + 2] : mrow[4 * u + 3];
+            own[u] = block_scale<FMT>(mo, m);
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            // broadcast of quad lane r % 4 (its own[r / 4])
+            BlockScale br;
+            const int ov = __float_as_int(own[r >> 2].r);
+            const int src = r & 3;
+            br.r = __int_as_float(src == 0 ? __builtin_amdgcn_mov_dpp(ov, 0x00, 0xF, 0xF, false)
+                                  : src == 1 ? __builtin_amdgcn_mov_dpp(ov, 0x55, 0xF, 0xF, false)
+                                  : src == 2 ? __builtin_amdgcn_mov_dpp(ov, 0xAA, 0xF, 0xF, false)
+                                             : __builtin_amdgcn_mov_dpp(ov, 0xFF, 0xF, 0xF, false));
+            br.code = own[r >> 2].code;                  // valid in quad lane r % 4, which stores it
+            const float y[4] = {bf16_lo(lo[r]) * br.r, bf16_hi(lo[r]) * br.r, bf16_lo(hi[r]) * br.r,
+                                bf16_hi(hi[r]) * br.r};
+            uint32_t p;
+            if (SR) {
+                uint32_t wd[4];
+                words4<true>((uint64_t)(tr * 16 + r) * (uint64_t)cols + (uint64_t)c, tid_r, key0, key1, wd);
+                p = sr4(y, wd);
+            } else {
+                p = 0u;
+                p = rn_pair<0>(p, y[0], y[1]);
+                p = rn_pair<1>(p, y[2], y[3]);
+            }
+            *reinterpret_cast<uint16_t*>(payload_r + (tr * 16 + r) * (cols / 2) + c / 2) = (uint16_t)p;
+            if (qk == (r & 3)) stSR[trl * 16 + r][q >> 2] = (uint8_t)br.code;
+            // one row at a time: keeps the live Philox words to 4
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    __syncthreads();
+    const int64_t tr0 = (int64_t)blockIdx.y * kTileRowTiles;
+    const int nvalid = (int)min((int64_t)kTileRowTiles, ntr - tr0);
+    // transposed payload: 2 lanes per column, 32 bytes each
+    {
+        const int col = t >> 1, half = t & 1;
+        const int64_t gc = cw + col;
+        if (gc < cols) {
+            uint8_t* dst = payload_c + gc * (rows / 2) + tr0 * 8 + half * 32;
+            const uint8_t* sp = &stP[col][half * 32];
+            if (nvalid == kTileRowTiles && ((rows / 2) & 15) == 0) {
+                *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(sp);
+                *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(sp + 16);
+            } else {
+                for (int k = half * 4; k < half * 4 + 4; ++k)
+                    if (k < nvalid)
+                        *reinterpret_cast<uint2*>(dst + (k - half * 4) * 8) =
+                            *reinterpret_cast<const uint2*>(sp + (k - half * 4) * 8);
+            }
+        }
+    }
+    // column scales [cols, rows/16]: up to 8 bytes per column
+    if (t < kTileCols) {
+        const int64_t gc = cw + t;
+        if (gc < cols) {
+            uint8_t* dst = scales_c + gc * ntr + tr0;
+            for (int k = 0; k < nvalid; ++k) dst[k] = stSC[t][k];
+        }
+    }
+    // row scales [rows, cols/16]: up to 8 bytes per row
+    {
+        const int row = t >> 1;
+        const int64_t gr = tr0 * 16 + row;
+        if (row < nvalid * 16 && (t & 1) == 0) {
+            const int64_t nb = min((int64_t)(kTileCols / 16), (cols - cw) / 16);
+            uint8_t* dst = scales_r + gr * (cols / 16) + cw / 16;
+            for (int k = 0; k < nb; ++k) dst[k] = stSR[row][k];
+        }
+    }
+}
+
 inline void seed_key(uint64_t seed, uint32_t& k0, uint32_t& k1) {
     k0 = (uint32_t)seed;
     k1 = (uint32_t)(seed >> 32);
@@ -700,6 +877,27 @@ hipError_t launch_tiles_fmt(const void* w_bf16, int64_t rows, int64_t cols, cons
     return hipGetLastError();
 }
 
+template <int FMT>
+hipError_t launch_dual_fmt(const void* x_bf16, int64_t rows, int64_t cols, const float* amax_dev,
+                           float target, bool sr, uint64_t seed, uint32_t tid_r, uint32_t tid_c,
+                           uint8_t* payload_r, uint8_t* scales_r, uint8_t* payload_c, uint8_t* scales_c,
+                           float* dec_out, hipStream_t s) {
+    uint32_t k0, k1;
+    seed_key(seed, k0, k1);
+    const int64_t gx = (cols + kTileCols - 1) / kTileCols;
+    const int64_t gy = (rows / 16 + kTileRowTiles - 1) / kTileRowTiles;
+    const uint16_t* x = reinterpret_cast<const uint16_t*>(x_bf16);
+    if (sr)
+        hipLaunchKernelGGL((quant_dual_kernel<true, FMT>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads), 0,
+                           s, x, rows, cols, amax_dev, target, k0, k1, tid_r, tid_c, payload_r, scales_r,
+                           payload_c, scales_c, dec_out);
+    else
+        hipLaunchKernelGGL((quant_dual_kernel<false, FMT>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads), 0,
+                           s, x, rows, cols, amax_dev, target, k0, k1, tid_r, tid_c, payload_r, scales_r,
+                           payload_c, scales_c, dec_out);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_quant_rows(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
@@ -748,6 +946,19 @@ hipError_t launch_quant_tiles(ScaleKind fmt, const void* w_bf16, int64_t rows, i
     return launch_tiles_fmt<(int)ScaleKind::UE5M3>(w_bf16, rows, cols, amax_dev, target, sr, seed,
                                                    tensor_id, payload, scales, payload_t, scales_t,
                                                    dec_out, s);
+}
+
+hipError_t launch_quant_dual(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
+                             const float* amax_dev, float target, bool sr, uint64_t seed,
+                             uint32_t tid_r, uint32_t tid_c, uint8_t* payload_r, uint8_t* scales_r,
+                             uint8_t* payload_c, uint8_t* scales_c, float* dec_out, hipStream_t s) {
+    if (fmt == ScaleKind::E4M3)
+        return launch_dual_fmt<(int)ScaleKind::E4M3>(x_bf16, rows, cols, amax_dev, target, sr, seed, tid_r,
+                                                     tid_c, payload_r, scales_r, payload_c, scales_c,
+                                                     dec_out, s);
+    return launch_dual_fmt<(int)ScaleKind::UE5M3>(x_bf16, rows, cols, amax_dev, target, sr, seed, tid_r,
+                                                  tid_c, payload_r, scales_r, payload_c, scales_c, dec_out,
+                                                  s);
 }
 
 }  // namespace ue5m3

@@ -151,3 +151,16 @@ def test_format_entry_points_validation(lib):
     assert gcall(layout=3) == ue.UE5M3_ELAYOUT
     assert gcall(M=0) == ue.UE5M3_OK
     assert gcall(M=1 << 20, N=1 << 20) == ue.UE5M3_ESHAPE     # 32-bit offsets
+
+
+def test_dual_quantizer_validation(lib):
+    d = lib.ue5m3_quantize_dual
+
+    def call(rows=32, cols=32, kind=0, mode=0, amax=FAKE):
+        return d(FAKE, rows, cols, amax, 448.0, mode, 0, 1, 2, kind, FAKE, FAKE, FAKE, FAKE, NULL, NULL)
+    assert call(kind=2) == ue.UE5M3_EINVAL          # E8M0 blocks are 32
+    assert call(mode=3) == ue.UE5M3_EINVAL
+    assert call(amax=NULL) == ue.UE5M3_EINVAL
+    assert call(rows=24) == ue.UE5M3_ESHAPE
+    assert call(cols=40) == ue.UE5M3_ESHAPE
+    assert call(rows=0) == ue.UE5M3_OK

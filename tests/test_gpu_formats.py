@@ -206,3 +206,40 @@ def test_quantizers_feed_gemm_end_to_end():
         c = ue.gemm("nt", T, N, K, xr[0], xr[1], xr[2], *b, fmt=fmt)
         al = ogemm.alpha(xo[2], dw)
         gemm_check(host(c), ogemm.fprop(X, W, al), al, ogemm.abs_product(X, W), K, f"{fmt} end to end")
+
+
+# ------------------------------------------------ both axes in one pass ----
+@pytest.mark.parametrize("fmt", ["ue5m3", "e4m3"])
+@pytest.mark.parametrize("mode", ["rn", "sr"])
+def test_quantize_dual_equals_both_axes(fmt, mode):
+    """ue5m3_quantize_dual writes exactly the axis-1 result (words keyed on
+    tensor_id_r) and the transposed axis-0 result (tensor_id_c)."""
+    for shape in [(16, 16), (48, 80), (128, 128), (256, 512), (208, 4096), (400, 1040)]:
+        say("dual", fmt, mode, shape)
+        bits = synthetic.gradient(12, *shape, 1e-4, 2.0) if mode == "sr" else \
+            synthetic.activation(12, *shape, 0.01, 50.0)
+        xd = to_dev(bits)
+        g = osc.amax(bits)
+        (pr, sr_, d), (pc, sc, _) = ue.quantize_dual(xd, _amax_dev(bits), 448.0, mode, seed=5,
+                                                     tensor_id_r=1, tensor_id_c=2, fmt=fmt)
+        por, sor, do = oq.quantize_1d(bits, 1, g, 448.0, mode, 5, 1, fmt=fmt)
+        poc, soc, _ = oq.quantize_1d(bits, 0, g, 448.0, mode, 5, 2, fmt=fmt)
+        assert np.array_equal(host(sr_), sor) and np.array_equal(host(pr), por), (shape, "rows")
+        assert np.array_equal(host(sc), soc) and np.array_equal(host(pc), poc), (shape, "cols")
+        assert np.float32(d.item()) == do
+
+
+@pytest.mark.parametrize("mode", ["rn", "sr"])
+def test_quantize_dual_every_bf16_value(mode):
+    say("dual every bf16 value", mode)
+    bits = _all_bf16(256, 512, 29)
+    xd = to_dev(bits)
+    for g in [1.0, 3.0e4, 2.0 ** -20]:
+        amax = torch.zeros(1, dtype=torch.float32, device="cuda")
+        set_amax(amax, g)
+        (pr, sr_, _), (pc, sc, _) = ue.quantize_dual(xd, amax, 448.0, mode, seed=17, tensor_id_r=3,
+                                                     tensor_id_c=4)
+        por, sor, _ = oq.quantize_1d(bits, 1, np.float32(g), 448.0, mode, 17, 3)
+        poc, soc, _ = oq.quantize_1d(bits, 0, np.float32(g), 448.0, mode, 17, 4)
+        assert np.array_equal(host(sr_), sor) and np.array_equal(host(pr), por), g
+        assert np.array_equal(host(sc), soc) and np.array_equal(host(pc), poc), g

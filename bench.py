@@ -4,8 +4,9 @@
 A step is the whole per-linear hot path on the Nemotron-H-8B FFN
 up-projection (T = 8192 tokens, K = 4096, N = 21504):
   sample-and-hold amax (D = 50; a refresh launches the amax kernels),
-  X rows RN, X columns RN (re-blocked along tokens), W 16x16 tiles RN (+ the
-  transposed payload), dY rows SR, dY columns SR,
+  X rows and columns RN (re-blocked along tokens) from one read, W 16x16
+  tiles RN (+ the transposed payload), dY rows SR, dY columns SR (two
+  kernels: SR is VALU-bound, and the one-read form is no faster there),
   fprop Y = X W^T (bf16 out), dgrad dX = dY W (bf16 out),
   wgrad dW = dY^T X (fp32 out).
 Inputs are seeded synthetic bf16 tensors resident in HBM before timing.
@@ -57,6 +58,10 @@ def parse():
 
 def quant_bytes_1d(rows, cols):
     return rows * cols * 2 + rows * cols // 2 + rows * cols // 16
+
+
+def quant_bytes_dual(rows, cols):
+    return rows * cols * 2 + 2 * (rows * cols // 2 + rows * cols // 16)
 
 
 def quant_bytes_2d(rows, cols, transposed):
@@ -250,8 +255,17 @@ def main():
     dw = torch.empty(N, K, dtype=torch.float32, device=dev)
     sx, sw, sd = ue.AmaxState(args.period), ue.AmaxState(args.period), ue.AmaxState(args.period)
 
-    names = ["amax", "quant_x_rows", "quant_x_cols", "quant_w_tiles", "quant_dy_rows",
-             "quant_dy_cols", "gemm_fprop", "gemm_dgrad", "gemm_wgrad"]
+    names = ["amax", "quant_x_dual", "quant_w_tiles", "quant_dy_rows", "quant_dy_cols", "gemm_fprop",
+             "gemm_dgrad", "gemm_wgrad"]
+
+    def quant_x():
+        ue.quantize_dual(x, sx.amax, 448.0, "rn", 0, 0, 0, bufs["xr"][:2], bufs["xc"][:2], bufs["xr"][2])
+
+    def quant_dy_rows(seed):
+        ue.quantize_1d(dy, 1, sd.amax, 448.0, "sr", seed, 1, *bufs["dr"])
+
+    def quant_dy_cols(seed):
+        ue.quantize_1d(dy, 0, sd.amax, 448.0, "sr", seed, 2, *bufs["dc"])
 
     def step(t, ev=None):
         def mark(i):
@@ -262,40 +276,40 @@ def main():
         ue.amax_sample(sw, w, t)
         ue.amax_sample(sd, dy, t)
         mark(1)
-        ue.quantize_1d(x, 1, sx.amax, 448.0, "rn", 0, 0, *bufs["xr"])
+        quant_x()
         mark(2)
-        ue.quantize_1d(x, 0, sx.amax, 448.0, "rn", 0, 0, *bufs["xc"])
-        mark(3)
         pw, sw_, pwt, dw_, swt = bufs["w"]
         ue.quantize_2d(w, sw.amax, 448.0, "rn", 0, 0, True, pw, sw_, pwt, dw_, swt)
+        mark(3)
+        quant_dy_rows(1000 + t)
         mark(4)
-        ue.quantize_1d(dy, 1, sd.amax, 448.0, "sr", 1000 + t, 1, *bufs["dr"])
+        quant_dy_cols(1000 + t)
         mark(5)
-        ue.quantize_1d(dy, 0, sd.amax, 448.0, "sr", 1000 + t, 2, *bufs["dc"])
-        mark(6)
         xr, xc, dr, dc = bufs["xr"], bufs["xc"], bufs["dr"], bufs["dc"]
         ue.gemm("nt", T, N, K, xr[0], xr[1], xr[2], pw, sw_, dw_, out=y)
-        mark(7)
+        mark(6)
         ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], pwt, swt, dw_, out=dx)
+        mark(7)
+        ue.gemm("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xr[2], out=dw)
         mark(8)
-        ue.gemm("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xc[2], out=dw)
-        mark(9)
 
     for t in range(args.warmup):
         step(t)
     torch.cuda.synchronize()
     if args.kernel is not None:
         single = {
-            "quant_x_rows": lambda: ue.quantize_1d(x, 1, sx.amax, 448.0, "rn", 0, 0, *bufs["xr"]),
-            "quant_x_cols": lambda: ue.quantize_1d(x, 0, sx.amax, 448.0, "rn", 0, 0, *bufs["xc"]),
+            "quant_x_dual": quant_x,
             "quant_w_tiles": lambda: ue.quantize_2d(w, sw.amax, 448.0, "rn", 0, 0, True, *bufs["w"]),
-            "quant_dy_rows": lambda: ue.quantize_1d(dy, 1, sd.amax, 448.0, "sr", 7, 1, *bufs["dr"]),
-            "quant_dy_cols": lambda: ue.quantize_1d(dy, 0, sd.amax, 448.0, "sr", 7, 2, *bufs["dc"]),
+            "quant_dy_rows": lambda: quant_dy_rows(7),
+            "quant_dy_cols": lambda: quant_dy_cols(7),
+            "quant_dy_dual": lambda: ue.quantize_dual(dy, sd.amax, 448.0, "sr", 7, 1, 2, bufs["dr"][:2],
+                                                      bufs["dc"][:2], bufs["dr"][2]),
             "gemm_fprop": lambda: ue.gemm("nt", T, N, K, *bufs["xr"], bufs["w"][0], bufs["w"][1],
                                           bufs["w"][3], out=y),
-            "gemm_dgrad": lambda: ue.gemm("nn", T, K, N, *bufs["dr"], bufs["w"][2], bufs["w"][4],
-                                          bufs["w"][3], out=dx),
-            "gemm_wgrad": lambda: ue.gemm("tn", N, K, T, *bufs["dc"], *bufs["xc"], out=dw),
+            "gemm_dgrad": lambda: ue.gemm("nn", T, K, N, bufs["dr"][0], bufs["dr"][1], bufs["dr"][2],
+                                          bufs["w"][2], bufs["w"][4], bufs["w"][3], out=dx),
+            "gemm_wgrad": lambda: ue.gemm("tn", N, K, T, *bufs["dc"], bufs["xc"][0], bufs["xc"][1],
+                                          bufs["xr"][2], out=dw),
         }[args.kernel]
         for _ in range(args.steps):
             single()
@@ -314,7 +328,7 @@ def main():
     # --- per-kernel durations (HIP events between launches, same stream) ---
     per = {n: [] for n in names}
     nprof = min(args.steps, 20)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(10)] for _ in range(nprof)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(nprof)]
     for i in range(nprof):
         step(args.warmup + args.steps + i, evs[i])
     torch.cuda.synchronize()
@@ -324,9 +338,8 @@ def main():
     avg = {n: float(np.mean(v)) for n, v in per.items()}
 
     flop_gemm = 2.0 * T * N * K
-    qbytes = {"quant_x_rows": quant_bytes_1d(T, K), "quant_x_cols": quant_bytes_1d(T, K),
-              "quant_w_tiles": quant_bytes_2d(N, K, True), "quant_dy_rows": quant_bytes_1d(T, N),
-              "quant_dy_cols": quant_bytes_1d(T, N)}
+    qbytes = {"quant_x_dual": quant_bytes_dual(T, K), "quant_w_tiles": quant_bytes_2d(N, K, True),
+              "quant_dy_rows": quant_bytes_1d(T, N), "quant_dy_cols": quant_bytes_1d(T, N)}
     kernels = {}
     for n, b in qbytes.items():
         gbs = b / (avg[n] * 1e-3) / 1e9

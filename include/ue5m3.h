@@ -63,7 +63,9 @@ typedef enum { UE5M3_OUT_F32 = 0, UE5M3_OUT_BF16 = 1 } ue5m3_out_t;
  *                 max |x|); read by the quantizers.
  *   last_refresh  optimizer step of the last refresh (tau).
  *   period        refresh period D in optimizer steps (50 in the paper's
- *                 recipe; 1 = current scaling).
+ *                 recipe; 1 = current scaling; 0 = measure once, then hold
+ *                 until reset: the inference policy for loaded weights, Sec.
+ *                 "Inference with delayed scaling").
  *   has_cache     0 until the first refresh; reset to 0 on resume (the
  *                 paper's caches are not checkpointed).
  */
@@ -75,7 +77,7 @@ typedef struct {
 } ue5m3_amax_state_t;
 
 /* Initialise `st` with an empty cache.  EINVAL if st or amax_dev is null or
- * period < 1; EALIGN if amax_dev is not 4-byte aligned. */
+ * period < 0; EALIGN if amax_dev is not 4-byte aligned. */
 ue5m3_status_t ue5m3_amax_state_init(ue5m3_amax_state_t* st, float* amax_dev,
                                      int32_t period);
 
@@ -83,9 +85,28 @@ ue5m3_status_t ue5m3_amax_state_init(ue5m3_amax_state_t* st, float* amax_dev,
  * process restart / resume).  A null st is ignored. */
 void ue5m3_amax_state_reset(ue5m3_amax_state_t* st);
 
+/* Hold the reference now in *st->amax_dev for good: has_cache = 1 and
+ * period = 0, so ue5m3_amax_sample refreshes again only after a reset (the
+ * calibrated-frozen inference policy, Table tab:inference-scale-summary).
+ * The caller has filled *amax_dev first, e.g. with ue5m3_amax_accumulate
+ * over calibration batches.  A null st is ignored. */
+void ue5m3_amax_state_freeze(ue5m3_amax_state_t* st);
+
+/*
+ * Running tensor amax for calibration (App. "Inference-Scale Sensitivity":
+ * the largest activation amax over calibration data).  Enqueues
+ * *amax_dev = max(clear ? 0 : *amax_dev, max_i |x_i|) for the bf16 tensor x
+ * (numel elements).  With clear = 0, *amax_dev must already hold a
+ * non-negative finite float (from an earlier call with clear = 1).
+ * EINVAL: null amax_dev, null x with numel > 0, clear not 0 or 1;
+ * ESHAPE: numel < 0; EALIGN: x not 16-byte or amax_dev not 4-byte aligned.
+ */
+ue5m3_status_t ue5m3_amax_accumulate(const void* x_bf16, int64_t numel, float* amax_dev,
+                                     int32_t clear, hipStream_t stream);
+
 /*
  * eq:delayed-amax.  At optimizer step `step`, if the cache is empty or
- * step - last_refresh >= period, enqueue the tensor amax a = max_i |x_i| of
+ * period > 0 and step - last_refresh >= period, enqueue the tensor amax a = max_i |x_i| of
  * the bf16 tensor x (numel elements) into *st->amax_dev, set last_refresh =
  * step, has_cache = 1 and *refreshed = 1; otherwise enqueue nothing and set
  * *refreshed = 0.  The decision uses host integers only (no device read).

@@ -6,6 +6,12 @@
   t - tau >= D (tau = step of the last refresh), otherwise the cached value;
   the cache starts empty and is reset (not restored) on resume; D = 50 with
   multiplicative factor 1 in the paper's recipe, D = 1 is current scaling.
+* Inference-scale policies (Sec. "Inference with delayed scaling", Table
+  tab:inference-scale-summary, App. "Inference-Scale Sensitivity"): a
+  loaded weight's amax is measured once and then held (read here as period
+  D = 0: refresh only while the cache is empty); activations either follow
+  D = 50 from an empty cache, D = 1, or a calibrated reference -- the
+  largest amax seen over calibration batches -- held fixed (``freeze``).
 * Tensor multipliers (Sec. 4.2, eq:scale-target): with F = 6 and target T
   (448 by default, 2048 for the wgrad-dY override), G = T F / g and the ideal
   block-scale code of a block with maximum a_B is u_B = a_B T / g.
@@ -59,12 +65,22 @@ def tensor_multipliers(g, target):
     return S, G, dec
 
 
+def calibrated_amax(batches):
+    """Calibrated-frozen reference: the largest tensor amax over a sequence
+    of calibration batches (bf16 bit arrays); 0 for no batches."""
+    g = np.float32(0.0)
+    for b in batches:
+        g = max(g, amax(b))
+    return np.float32(g)
+
+
 class AmaxState:
-    """One operand's sample-and-hold cache (eq:delayed-amax)."""
+    """One operand's sample-and-hold cache (eq:delayed-amax).  ``period`` 0
+    holds the first measurement until ``reset``."""
 
     def __init__(self, period=50):
-        if period < 1:
-            raise ValueError("period must be >= 1")
+        if period < 0:
+            raise ValueError("period must be >= 0")
         self.period = int(period)
         self.reset()
 
@@ -76,7 +92,15 @@ class AmaxState:
         self.g = np.float32(0.0)
 
     def needs_refresh(self, step):
-        return (not self.has_cache) or (step - self.last_refresh >= self.period)
+        if not self.has_cache:
+            return True
+        return self.period > 0 and step - self.last_refresh >= self.period
+
+    def freeze(self, g):
+        """Hold the given reference from now on (calibrated-frozen policy)."""
+        self.g = np.float32(g)
+        self.has_cache = True
+        self.period = 0
 
     def observe(self, x_bf16_bits, step):
         """Reference amax for optimizer step ``step``; returns (g, refreshed)."""

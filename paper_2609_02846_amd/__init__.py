@@ -29,6 +29,7 @@ BLOCK = {"ue5m3": 16, "e4m3": 16, "e8m0": 32}
 
 EXPORTED_SYMBOLS = (
     "ue5m3_amax_state_init", "ue5m3_amax_state_reset", "ue5m3_amax_sample",
+    "ue5m3_amax_state_freeze", "ue5m3_amax_accumulate",
     "ue5m3_quantize_1d", "ue5m3_quantize_2d", "ue5m3_gemm",
     "ue5m3_quantize_1d_ex", "ue5m3_quantize_2d_ex", "ue5m3_gemm_ex", "ue5m3_quantize_dual",
     "ue5m3_status_string", "ue5m3_version",
@@ -68,6 +69,10 @@ def load_library(path=LIB_PATH):
     lib.ue5m3_amax_sample.argtypes = [ctypes.POINTER(AmaxStateC), vp, i64, i64,
                                       ctypes.POINTER(ctypes.c_int32), vp]
     lib.ue5m3_amax_sample.restype = i32
+    lib.ue5m3_amax_state_freeze.argtypes = [ctypes.POINTER(AmaxStateC)]
+    lib.ue5m3_amax_state_freeze.restype = None
+    lib.ue5m3_amax_accumulate.argtypes = [vp, i64, vp, i32, vp]
+    lib.ue5m3_amax_accumulate.restype = i32
     lib.ue5m3_quantize_1d.argtypes = [vp, i64, i64, i32, vp, f32, i32, u64, u32, vp, vp, vp, vp]
     lib.ue5m3_quantize_1d.restype = i32
     lib.ue5m3_quantize_2d.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, vp, vp, vp, vp, vp, vp]
@@ -121,19 +126,59 @@ def _u8(shape, like):
     return torch.empty(shape, dtype=torch.uint8, device=like.device)
 
 
+def _numel(shape):
+    n = 1
+    for d in shape:
+        n *= int(d)
+    return n
+
+
+def _dev_buf(t, dtype, numel, name):
+    """The library takes bare pointers: check that a buffer it reads or
+    writes is a contiguous device tensor of the dtype with room for
+    ``numel`` elements."""
+    if not isinstance(t, torch.Tensor) or t.dtype != dtype or not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} CUDA/HIP tensor")
+    if t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, {numel} needed")
+    return t
+
+
+def _u8_out(t, shape, name):
+    return _dev_buf(t, torch.uint8, _numel(shape), name)
+
+
+def _f32_out(t, name):
+    return _dev_buf(t, torch.float32, 1, name)
+
+
 # ------------------------------------------------------------------ API ---
 class AmaxState:
     """One operand's sample-and-hold cache (eq:delayed-amax): host integers
-    plus a device float holding the sampled amax."""
+    plus a device float holding the sampled amax.  ``period`` 50 is the
+    training recipe, 1 current scaling, 0 measure-once-and-hold."""
 
     def __init__(self, period=50, device="cuda"):
         self.amax = torch.zeros(1, dtype=torch.float32, device=device)
         self.c = AmaxStateC()
+        self.set_period(period)
+
+    def set_period(self, period):
+        """Re-initialise with another period; the cache is emptied."""
         _check(load_library().ue5m3_amax_state_init(ctypes.byref(self.c), _ptr(self.amax),
                                                      int(period)), "ue5m3_amax_state_init")
 
     def reset(self):
         load_library().ue5m3_amax_state_reset(ctypes.byref(self.c))
+
+    def freeze(self):
+        """Hold the reference now in ``amax`` until reset (calibrated-frozen
+        policy; fill ``amax`` with ``amax_accumulate`` first)."""
+        load_library().ue5m3_amax_state_freeze(ctypes.byref(self.c))
+
+    @property
+    def period(self):
+        return int(self.c.period)
 
     @property
     def has_cache(self):
@@ -157,6 +202,17 @@ def amax_sample(state, x, step, stream=None):
     return bool(flag.value)
 
 
+def amax_accumulate(x, amax_dev, clear=False, stream=None):
+    """Enqueue amax_dev = max(0 if clear else amax_dev, max |x|) (see
+    ue5m3_amax_accumulate): the running maximum over calibration batches."""
+    if x.dtype != torch.bfloat16 or not x.is_contiguous() or not x.is_cuda:
+        raise ValueError("x must be a contiguous bf16 CUDA/HIP tensor")
+    _f32_out(amax_dev, "amax_dev")
+    _check(load_library().ue5m3_amax_accumulate(_ptr(x), x.numel(), _ptr(amax_dev), int(bool(clear)),
+                                                _stream(stream)), "ue5m3_amax_accumulate")
+    return amax_dev
+
+
 def quantize_1d(x, axis, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0,
                 payload=None, scales=None, dec_out=None, stream=None, fmt="ue5m3"):
     """1D block quantization (see ue5m3_quantize_1d and, for ``fmt`` "e4m3"
@@ -167,12 +223,17 @@ def quantize_1d(x, axis, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0,
     B = BLOCK[fmt]
     if axis == 1:
         pshape, sshape = (R, C // 2), (R, C // B)
-    else:
+    elif axis == 0:
         pshape, sshape = (C, R // 2), (C, R // B)
-    payload = _u8(pshape, x) if payload is None else payload
-    scales = _u8(sshape, x) if scales is None else scales
+    else:
+        raise ValueError("axis must be 0 or 1")
+    payload = _u8(pshape, x) if payload is None else _u8_out(payload, pshape, "payload")
+    scales = _u8(sshape, x) if scales is None else _u8_out(scales, sshape, "scales")
     if dec_out is None:
         dec_out = torch.empty(1, dtype=torch.float32, device=x.device)
+    _f32_out(dec_out, "dec_out")
+    if fmt != "e8m0":
+        _f32_out(amax_dev, "amax_dev")
     lib = load_library()
     common = (_ptr(x), R, C, int(axis), _ptr(amax_dev), float(target), _MODES[mode],
               int(seed) & (2**64 - 1), int(tensor_id) & 0xFFFFFFFF)
@@ -194,8 +255,14 @@ def quantize_dual(x, amax_dev, target=448.0, mode="rn", seed=0, tensor_id_r=0, t
     R, C = x.shape
     pr, sr_ = rows_out if rows_out is not None else (_u8((R, C // 2), x), _u8((R, C // 16), x))
     pc, sc = cols_out if cols_out is not None else (_u8((C, R // 2), x), _u8((C, R // 16), x))
+    _u8_out(pr, (R, C // 2), "payload_r")
+    _u8_out(sr_, (R, C // 16), "scales_r")
+    _u8_out(pc, (C, R // 2), "payload_c")
+    _u8_out(sc, (C, R // 16), "scales_c")
     if dec_out is None:
         dec_out = torch.empty(1, dtype=torch.float32, device=x.device)
+    _f32_out(dec_out, "dec_out")
+    _f32_out(amax_dev, "amax_dev")
     _check(load_library().ue5m3_quantize_dual(
         _ptr(x), R, C, _ptr(amax_dev), float(target), _MODES[mode], int(seed) & (2**64 - 1),
         int(tensor_id_r) & 0xFFFFFFFF, int(tensor_id_c) & 0xFFFFFFFF, _FORMATS[fmt], _ptr(pr),
@@ -212,14 +279,20 @@ def quantize_2d(w, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0, trans
     dgrad operand."""
     _bf16_2d(w, "w")
     R, C = w.shape
-    payload = _u8((R, C // 2), w) if payload is None else payload
-    scales = _u8((R // 16, C // 16), w) if scales is None else scales
+    payload = _u8((R, C // 2), w) if payload is None else _u8_out(payload, (R, C // 2), "payload")
+    scales = _u8((R // 16, C // 16), w) if scales is None else _u8_out(scales, (R // 16, C // 16), "scales")
     if transposed and payload_t is None:
         payload_t = _u8((C, R // 2), w)
     if transposed and scales_t is None:
         scales_t = _u8((C // 16, R // 16), w)
+    if payload_t is not None:
+        _u8_out(payload_t, (C, R // 2), "payload_t")
+    if scales_t is not None:
+        _u8_out(scales_t, (C // 16, R // 16), "scales_t")
     if dec_out is None:
         dec_out = torch.empty(1, dtype=torch.float32, device=w.device)
+    _f32_out(dec_out, "dec_out")
+    _f32_out(amax_dev, "amax_dev")
     lib = load_library()
     common = (_ptr(w), R, C, _ptr(amax_dev), float(target), _MODES[mode], int(seed) & (2**64 - 1),
               int(tensor_id) & 0xFFFFFFFF)
@@ -243,6 +316,17 @@ def gemm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
     ctype = OUT_BF16 if out.dtype == torch.bfloat16 else OUT_F32
     if out.dtype not in (torch.float32, torch.bfloat16) or not out.is_contiguous():
         raise ValueError("out must be a contiguous fp32 or bf16 tensor")
+    _dev_buf(out, out.dtype, int(M) * int(N), "out")
+    if M > 0 and N > 0 and K > 0:
+        Bk = BLOCK[fmt]
+        tiled = fmt != "e8m0" and lay in (NT, NN)
+        _u8_out(a, (M, K // 2), "a")
+        _u8_out(a_scales, (M, K // Bk), "a_scales")
+        _u8_out(b, (N, K // 2), "b")
+        _u8_out(b_scales, ((N + 15) // 16, K // 16) if tiled else (N, K // Bk), "b_scales")
+    if M > 0 and N > 0:
+        _f32_out(a_dec, "a_dec")
+        _f32_out(b_dec, "b_dec")
     lib = load_library()
     args = (lay, int(M), int(N), int(K), _ptr(a), _ptr(a_scales), _ptr(a_dec), _ptr(b), _ptr(b_scales),
             _ptr(b_dec), _ptr(out), ctype)

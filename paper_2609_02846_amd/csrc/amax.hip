@@ -1,5 +1,7 @@
 // Tensor amax of a bf16 tensor (paper Sec. 4.1: a_t = max_i |x_{t,i}|),
-// launched only on refresh steps of the sample-and-hold rule.
+// launched only on refresh steps of the sample-and-hold rule, or without the
+// clear as a running maximum over calibration batches (the calibrated-frozen
+// inference reference).
 //
 // The maximum is exact: |x| of a bf16 is its 15 low bits, and the integer
 // order of those bits is the numeric order of non-negative finite values, so
@@ -58,9 +60,10 @@ __global__ __launch_bounds__(kAmaxThreads) void amax_bf16_kernel(
 
 }  // namespace
 
-hipError_t launch_amax(const void* x_bf16, int64_t numel, float* amax_dev, hipStream_t s) {
+hipError_t launch_amax(const void* x_bf16, int64_t numel, float* amax_dev, bool clear,
+                       hipStream_t s) {
     uint32_t* out = reinterpret_cast<uint32_t*>(amax_dev);
-    hipLaunchKernelGGL(amax_clear_kernel, dim3(1), dim3(64), 0, s, out);
+    if (clear) hipLaunchKernelGGL(amax_clear_kernel, dim3(1), dim3(64), 0, s, out);
     if (numel <= 0) return hipGetLastError();
     const int64_t nvec = numel / 8;
     const int tail_n = (int)(numel - nvec * 8);

@@ -34,7 +34,7 @@ const char* ue5m3_status_string(ue5m3_status_t s) {
 }
 
 ue5m3_status_t ue5m3_amax_state_init(ue5m3_amax_state_t* st, float* amax_dev, int32_t period) {
-    if (st == nullptr || amax_dev == nullptr || period < 1) return UE5M3_EINVAL;
+    if (st == nullptr || amax_dev == nullptr || period < 0) return UE5M3_EINVAL;
     if (!aligned4(amax_dev)) return UE5M3_EALIGN;
     st->amax_dev = amax_dev;
     st->last_refresh = 0;
@@ -52,19 +52,37 @@ void ue5m3_amax_state_reset(ue5m3_amax_state_t* st) {
 
 ue5m3_status_t ue5m3_amax_sample(ue5m3_amax_state_t* st, const void* x_bf16, int64_t numel,
                                  int64_t step, int32_t* refreshed, hipStream_t stream) {
-    if (st == nullptr || st->amax_dev == nullptr || st->period < 1) return UE5M3_EINVAL;
+    if (st == nullptr || st->amax_dev == nullptr || st->period < 0) return UE5M3_EINVAL;
     if (numel < 0) return UE5M3_ESHAPE;
     if (numel > 0 && x_bf16 == nullptr) return UE5M3_EINVAL;
     if (numel > 0 && !aligned16(x_bf16)) return UE5M3_EALIGN;
     if (!aligned4(st->amax_dev)) return UE5M3_EALIGN;
-    const bool refresh = !st->has_cache || (step - st->last_refresh >= (int64_t)st->period);
+    const bool refresh = !st->has_cache ||
+                         (st->period > 0 && step - st->last_refresh >= (int64_t)st->period);
     if (refreshed != nullptr) *refreshed = refresh ? 1 : 0;
     if (!refresh) return UE5M3_OK;
-    const hipError_t e = ue5m3::launch_amax(x_bf16, numel, st->amax_dev, stream);
+    const hipError_t e = ue5m3::launch_amax(x_bf16, numel, st->amax_dev, true, stream);
     if (e != hipSuccess) return UE5M3_EHIP;
     st->has_cache = 1;
     st->last_refresh = step;
     return UE5M3_OK;
+}
+
+void ue5m3_amax_state_freeze(ue5m3_amax_state_t* st) {
+    if (st != nullptr) {
+        st->has_cache = 1;
+        st->period = 0;
+    }
+}
+
+ue5m3_status_t ue5m3_amax_accumulate(const void* x_bf16, int64_t numel, float* amax_dev,
+                                     int32_t clear, hipStream_t stream) {
+    if (amax_dev == nullptr || (clear != 0 && clear != 1)) return UE5M3_EINVAL;
+    if (numel < 0) return UE5M3_ESHAPE;
+    if (numel > 0 && x_bf16 == nullptr) return UE5M3_EINVAL;
+    if (numel > 0 && !aligned16(x_bf16)) return UE5M3_EALIGN;
+    if (!aligned4(amax_dev)) return UE5M3_EALIGN;
+    return hip_status(ue5m3::launch_amax(x_bf16, numel, amax_dev, clear == 1, stream));
 }
 
 ue5m3_status_t ue5m3_quantize_1d_ex(const void* x_bf16, int64_t rows, int64_t cols, int32_t axis,

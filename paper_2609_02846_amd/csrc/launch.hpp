@@ -17,7 +17,10 @@ enum class BScale : int { Row = 0, Tile = 1, TileDgrad = 2 };
 // NVFP4-style) or E8M0 (blocks of 32, MXFP4-style, no tensor scale).
 enum class ScaleKind : int { UE5M3 = 0, E4M3 = 1, E8M0 = 2 };
 
-hipError_t launch_amax(const void* x_bf16, int64_t numel, float* amax_dev, hipStream_t s);
+// *amax_dev = max(clear ? 0 : *amax_dev, max |x|); a kept value must be a
+// non-negative finite float (the kernel takes an integer max of its bits).
+hipError_t launch_amax(const void* x_bf16, int64_t numel, float* amax_dev, bool clear,
+                       hipStream_t s);
 
 hipError_t launch_quant_rows(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
                              const float* amax_dev, float target, bool sr, uint64_t seed,

@@ -109,7 +109,7 @@ def test_amax_state_host_logic(lib):
     the period enqueue nothing (eq:delayed-amax)."""
     st = ue.AmaxStateC()
     assert lib.ue5m3_amax_state_init(ctypes.byref(st), NULL, 50) == ue.UE5M3_EINVAL
-    assert lib.ue5m3_amax_state_init(ctypes.byref(st), FAKE, 0) == ue.UE5M3_EINVAL
+    assert lib.ue5m3_amax_state_init(ctypes.byref(st), FAKE, -1) == ue.UE5M3_EINVAL
     assert lib.ue5m3_amax_state_init(ctypes.byref(st), FAKE, 50) == ue.UE5M3_OK
     assert st.has_cache == 0 and st.period == 50
     st.has_cache, st.last_refresh = 1, 100
@@ -122,6 +122,37 @@ def test_amax_state_host_logic(lib):
     lib.ue5m3_amax_state_reset(ctypes.byref(st))
     assert st.has_cache == 0
     lib.ue5m3_amax_state_reset(None)
+
+
+def test_amax_hold_and_freeze_host_logic(lib):
+    """Period 0 holds the first measurement until reset; freeze holds the
+    reference already in amax_dev (inference policies, Table
+    tab:inference-scale-summary).  Only host integers are involved."""
+    st = ue.AmaxStateC()
+    assert lib.ue5m3_amax_state_init(ctypes.byref(st), FAKE, 0) == ue.UE5M3_OK
+    st.has_cache, st.last_refresh = 1, 3           # as after the first refresh
+    flag = ctypes.c_int32(-1)
+    for step in [3, 53, 10**15]:
+        assert lib.ue5m3_amax_sample(ctypes.byref(st), FAKE, 64, step, ctypes.byref(flag), NULL) == 0
+        assert flag.value == 0 and st.last_refresh == 3
+    assert lib.ue5m3_amax_state_init(ctypes.byref(st), FAKE, 50) == ue.UE5M3_OK
+    lib.ue5m3_amax_state_freeze(ctypes.byref(st))
+    assert st.has_cache == 1 and st.period == 0
+    assert lib.ue5m3_amax_sample(ctypes.byref(st), FAKE, 64, 500, ctypes.byref(flag), NULL) == 0
+    assert flag.value == 0
+    lib.ue5m3_amax_state_freeze(None)
+    st.period = -2
+    assert lib.ue5m3_amax_sample(ctypes.byref(st), FAKE, 64, 0, ctypes.byref(flag), NULL) == ue.UE5M3_EINVAL
+
+
+def test_amax_accumulate_validation(lib):
+    acc = lib.ue5m3_amax_accumulate
+    assert acc(FAKE, 64, NULL, 1, NULL) == ue.UE5M3_EINVAL
+    assert acc(NULL, 64, FAKE, 1, NULL) == ue.UE5M3_EINVAL
+    assert acc(FAKE, 64, FAKE, 2, NULL) == ue.UE5M3_EINVAL
+    assert acc(FAKE, -1, FAKE, 0, NULL) == ue.UE5M3_ESHAPE
+    assert acc(FAKE_MIS, 64, FAKE, 0, NULL) == ue.UE5M3_EALIGN
+    assert acc(FAKE, 64, ctypes.c_void_p(0x100002), 0, NULL) == ue.UE5M3_EALIGN
 
 
 def test_format_entry_points_validation(lib):

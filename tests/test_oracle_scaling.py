@@ -59,7 +59,26 @@ def test_sample_and_hold_irregular_steps_reset_and_current():
     cur = scaling.AmaxState(period=1)            # D = 1 is current scaling
     assert all(cur.observe(_bits([[float(t)]]), t)[1] for t in range(5))
     with pytest.raises(ValueError):
-        scaling.AmaxState(period=0)
+        scaling.AmaxState(period=-1)
+
+
+def test_inference_policies():
+    """Inference-scale policies (Table tab:inference-scale-summary): a held
+    weight reference is measured on the first batch only, even across a
+    huge step gap; a calibrated reference is the largest calibration amax
+    and never refreshes; reset empties a held cache."""
+    held = scaling.AmaxState(period=0)
+    got = [held.observe(_bits([[float(v)]]), t) for t, v in [(0, 3.0), (1, 9.0), (10**12, 20.0)]]
+    assert [(float(g), r) for g, r in got] == [(3.0, True), (3.0, False), (3.0, False)]
+    held.reset()
+    assert held.observe(_bits([[5.0]]), 10**12 + 1) == (5.0, True)
+    cal = [_bits([[1.0, -4.5]]), _bits([[-7.0, 2.0]]), _bits([[6.0]])]
+    assert scaling.calibrated_amax(cal) == np.float32(7.0)
+    assert scaling.calibrated_amax([]) == 0.0
+    st = scaling.AmaxState(period=50)
+    st.observe(_bits([[100.0]]), 0)
+    st.freeze(scaling.calibrated_amax(cal))
+    assert all(st.observe(_bits([[1e3]]), t) == (7.0, False) for t in (0, 50, 500))
 
 
 def test_multipliers_table3_example(golden_dir):

@@ -19,6 +19,9 @@ Language Model Pretraining" (arXiv 2609.02846):
   eq:sr, Table 5) and dequantization.
 * ``gemm``     -- the decoded-operand GEMM model (Sec. 5.1) for the fprop,
   dgrad and wgrad products of Sec. 4.3.
+* ``accumulate`` -- the probe-matched output model (eq:issue-partial,
+  eq:issue-rz, eq:final-grid, eq:grid-denominator): 64-product RNE
+  partials, toward-zero cross-group adds, optional 1/d product-lattice snap.
 
 Floating point: every decision that yields a code (block-scale byte, payload
 nibble) is taken in IEEE binary32 with round-to-nearest-even, one rounding
@@ -32,4 +35,4 @@ does not fix ("parity unpinned" against the paper for that choice; the
 worked blocks in ``tests/golden`` pin it against hand derivation).
 """
 
-from . import formats, philox, scaling, quantize, gemm  # noqa: F401
+from . import formats, philox, scaling, quantize, gemm, accumulate  # noqa: F401

@@ -28,6 +28,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12   # 32-bit (and binary64 add) VALU lane ops/s
+PM_VALU_PER_GROUP = 9          # probe-matched VALU ops per output per 64-product group
 METRIC = "quantize GB/s + emulated FP4 GEMM TFLOP/s (fprop+dgrad+wgrad), % roofline"
 
 
@@ -46,6 +48,9 @@ def parse():
     p.add_argument("--kernel", default=None,
                    help="profiling aid: after setup run only this step kernel (e.g. gemm_fprop) "
                         "--steps times and exit without a JSON line")
+    p.add_argument("--pm", type=int, default=None, metavar="GRID",
+                   help="run the step with the probe-matched GEMMs (64-product RNE partials, "
+                        "toward-zero cross-group adds, 1/GRID snap; 0 = no snap)")
     p.add_argument("--formats", action="store_true",
                    help="scale-format comparison instead of the headline step: UE5M3 (delayed "
                         "amax), E4M3 (current amax) and E8M0 (blocks of 32) on the QKV workload "
@@ -267,6 +272,12 @@ def main():
     def quant_dy_cols(seed):
         ue.quantize_1d(dy, 0, sd.amax, 448.0, "sr", seed, 2, *bufs["dc"])
 
+    if args.pm is None:
+        G = ue.gemm
+    else:
+        def G(*a, **kw):
+            return ue.gemm_pm(*a, grid=args.pm, **kw)
+
     def step(t, ev=None):
         def mark(i):
             if ev is not None:
@@ -286,11 +297,11 @@ def main():
         quant_dy_cols(1000 + t)
         mark(5)
         xr, xc, dr, dc = bufs["xr"], bufs["xc"], bufs["dr"], bufs["dc"]
-        ue.gemm("nt", T, N, K, xr[0], xr[1], xr[2], pw, sw_, dw_, out=y)
+        G("nt", T, N, K, xr[0], xr[1], xr[2], pw, sw_, dw_, out=y)
         mark(6)
-        ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], pwt, swt, dw_, out=dx)
+        G("nn", T, K, N, dr[0], dr[1], dr[2], pwt, swt, dw_, out=dx)
         mark(7)
-        ue.gemm("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xr[2], out=dw)
+        G("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xr[2], out=dw)
         mark(8)
 
     for t in range(args.warmup):
@@ -304,12 +315,12 @@ def main():
             "quant_dy_cols": lambda: quant_dy_cols(7),
             "quant_dy_dual": lambda: ue.quantize_dual(dy, sd.amax, 448.0, "sr", 7, 1, 2, bufs["dr"][:2],
                                                       bufs["dc"][:2], bufs["dr"][2]),
-            "gemm_fprop": lambda: ue.gemm("nt", T, N, K, *bufs["xr"], bufs["w"][0], bufs["w"][1],
-                                          bufs["w"][3], out=y),
-            "gemm_dgrad": lambda: ue.gemm("nn", T, K, N, bufs["dr"][0], bufs["dr"][1], bufs["dr"][2],
-                                          bufs["w"][2], bufs["w"][4], bufs["w"][3], out=dx),
-            "gemm_wgrad": lambda: ue.gemm("tn", N, K, T, *bufs["dc"], bufs["xc"][0], bufs["xc"][1],
-                                          bufs["xr"][2], out=dw),
+            "gemm_fprop": lambda: G("nt", T, N, K, *bufs["xr"], bufs["w"][0], bufs["w"][1],
+                                    bufs["w"][3], out=y),
+            "gemm_dgrad": lambda: G("nn", T, K, N, bufs["dr"][0], bufs["dr"][1], bufs["dr"][2],
+                                    bufs["w"][2], bufs["w"][4], bufs["w"][3], out=dx),
+            "gemm_wgrad": lambda: G("tn", N, K, T, *bufs["dc"], bufs["xc"][0], bufs["xc"][1],
+                                    bufs["xr"][2], out=dw),
         }[args.kernel]
         for _ in range(args.steps):
             single()
@@ -371,6 +382,15 @@ def main():
     roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": traffic}
+    if args.pm is not None:
+        # probe-matched GEMM: bound by the per-output VALU work of each
+        # 64-product group (4 widenings, 3 binary64 adds, 1 narrowing, 1
+        # toward-zero add), against 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+        ops = PM_VALU_PER_GROUP * T * N * ((K + 63) // 64)
+        ach = ops / (avg[dom] * 1e-3) / 1e12
+        roofline = {"bound": "alu", "kernel": dom + " (probe-matched)", "achieved": round(ach, 2),
+                    "peak": VALU_PEAK_TOPS, "unit": "Tops/s (VALU lane ops)",
+                    "frac": round(ach / VALU_PEAK_TOPS, 4), "traffic": None}
 
     value = 3 * flop_gemm / (ms * 1e-3) / 1e12
     out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
@@ -379,11 +399,13 @@ def main():
            "data": "synthetic",
            "config": {"workload": f"FFN up-projection linear training step T={T} K={K} N={N}",
                       "tokens": T, "k": K, "n": N, "refresh_period": args.period,
-                      "target": 448.0},
+                      "target": 448.0,
+                      "gemm": ("decoded-operand, fp32 accumulation" if args.pm is None else
+                               f"probe-matched, grid 1/{args.pm}" if args.pm else "probe-matched, no snap")},
            "quantize_GBps": round(quant_gbs, 1), "quantize_frac_hbm": round(quant_gbs / HBM_PEAK_GBS, 4),
            "gemm_TFLOPs": round(gemm_tf, 1), "gemm_frac_bf16": round(gemm_tf / BF16_PEAK_TFLOPS, 4),
            "kernels": kernels, "roofline": roofline}
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.pm is None:
         out["cpu_baseline"] = cpu_baseline(wl, T, K, N)
     print(json.dumps(out), flush=True)
 

@@ -32,6 +32,7 @@ EXPORTED_SYMBOLS = (
     "ue5m3_amax_state_freeze", "ue5m3_amax_accumulate",
     "ue5m3_quantize_1d", "ue5m3_quantize_2d", "ue5m3_gemm",
     "ue5m3_quantize_1d_ex", "ue5m3_quantize_2d_ex", "ue5m3_gemm_ex", "ue5m3_quantize_dual",
+    "ue5m3_gemm_pm",
     "ue5m3_status_string", "ue5m3_version",
 )
 
@@ -87,6 +88,8 @@ def load_library(path=LIB_PATH):
     lib.ue5m3_quantize_2d_ex.restype = i32
     lib.ue5m3_gemm_ex.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp]
     lib.ue5m3_gemm_ex.restype = i32
+    lib.ue5m3_gemm_pm.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp]
+    lib.ue5m3_gemm_pm.restype = i32
     lib.ue5m3_quantize_dual.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, u32, i32,
                                         vp, vp, vp, vp, vp, vp]
     lib.ue5m3_quantize_dual.restype = i32
@@ -305,11 +308,7 @@ def quantize_2d(w, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0, trans
     return payload, scales, payload_t, dec_out, scales_t
 
 
-def gemm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
-         out_dtype=torch.float32, stream=None, fmt="ue5m3"):
-    """Decoded-operand FP4 GEMM (see ue5m3_gemm and, for ``fmt`` "e4m3" or
-    "e8m0", ue5m3_gemm_ex); layout is "nt" (fprop), "nn" (dgrad) or "tn"
-    (wgrad).  Returns the [M, N] output tensor."""
+def _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt):
     lay = _LAYOUTS[layout] if isinstance(layout, str) else int(layout)
     if out is None:
         out = torch.empty((M, N), dtype=out_dtype, device=a.device)
@@ -327,9 +326,30 @@ def gemm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
     if M > 0 and N > 0:
         _f32_out(a_dec, "a_dec")
         _f32_out(b_dec, "b_dec")
-    lib = load_library()
     args = (lay, int(M), int(N), int(K), _ptr(a), _ptr(a_scales), _ptr(a_dec), _ptr(b), _ptr(b_scales),
             _ptr(b_dec), _ptr(out), ctype)
+    return out, args
+
+
+def gemm_pm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
+            out_dtype=torch.float32, grid=1024, stream=None, fmt="ue5m3"):
+    """Probe-matched GEMM (see ue5m3_gemm_pm): 64-product RNE partials,
+    toward-zero cross-group adds, snap of the encoded accumulator to the
+    1/``grid`` lattice (0: none), then alpha.  Operands as ``gemm``."""
+    if fmt not in ("ue5m3", "e4m3"):
+        raise ValueError("the probe-matched GEMM takes UE5M3 or E4M3 scales")
+    out, args = _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt)
+    _check(load_library().ue5m3_gemm_pm(*args, _FORMATS[fmt], int(grid), _stream(stream)), "ue5m3_gemm_pm")
+    return out
+
+
+def gemm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
+         out_dtype=torch.float32, stream=None, fmt="ue5m3"):
+    """Decoded-operand FP4 GEMM (see ue5m3_gemm and, for ``fmt`` "e4m3" or
+    "e8m0", ue5m3_gemm_ex); layout is "nt" (fprop), "nn" (dgrad) or "tn"
+    (wgrad).  Returns the [M, N] output tensor."""
+    out, args = _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt)
+    lib = load_library()
     if fmt == "ue5m3":
         st = lib.ue5m3_gemm(*args, _stream(stream))
     else:

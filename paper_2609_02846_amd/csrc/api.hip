@@ -227,6 +227,35 @@ ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
                                          bf, stream));
 }
 
+ue5m3_status_t ue5m3_gemm_pm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
+                             const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
+                             const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,
+                             ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind, int32_t grid_d,
+                             hipStream_t stream) {
+    ue5m3::BScale bmode;
+    switch (layout) {
+        case UE5M3_NT: bmode = ue5m3::BScale::Tile; break;
+        case UE5M3_NN: bmode = ue5m3::BScale::TileDgrad; break;
+        case UE5M3_TN: bmode = ue5m3::BScale::Row; break;
+        default: return UE5M3_ELAYOUT;
+    }
+    if (scale_kind != UE5M3_SCALE_UE5M3 && scale_kind != UE5M3_SCALE_E4M3) return UE5M3_EINVAL;
+    if (c_type != UE5M3_OUT_F32 && c_type != UE5M3_OUT_BF16) return UE5M3_EINVAL;
+    if (grid_d < 0 || grid_d > (1 << 30) || (grid_d & (grid_d - 1)) != 0) return UE5M3_EINVAL;
+    if (M < 0 || N < 0 || K < 0 || K % 16 != 0) return UE5M3_ESHAPE;
+    if (layout != UE5M3_TN && N % 16 != 0) return UE5M3_ESHAPE;
+    if (M == 0 || N == 0) return UE5M3_OK;
+    if (c == nullptr || a_dec == nullptr || b_dec == nullptr) return UE5M3_EINVAL;
+    if (K > 0 && (a == nullptr || a_scales == nullptr || b == nullptr || b_scales == nullptr))
+        return UE5M3_EINVAL;
+    if (!aligned16(c) || !aligned4(a_dec) || !aligned4(b_dec)) return UE5M3_EALIGN;
+    if (K > 0 && (!aligned16(a) || !aligned16(b) || !aligned16(a_scales) || !aligned16(b_scales)))
+        return UE5M3_EALIGN;
+    const float amul = scale_kind == UE5M3_SCALE_E4M3 ? 4194304.0f : 64.0f;
+    return hip_status(ue5m3::launch_gemm_pm(bmode, amul, (float)grid_d, M, N, K, a, a_scales, a_dec, b,
+                                            b_scales, b_dec, c, c_type == UE5M3_OUT_BF16, stream));
+}
+
 ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
                           const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
                           const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,

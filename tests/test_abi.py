@@ -195,3 +195,20 @@ def test_dual_quantizer_validation(lib):
     assert call(rows=24) == ue.UE5M3_ESHAPE
     assert call(cols=40) == ue.UE5M3_ESHAPE
     assert call(rows=0) == ue.UE5M3_OK
+
+
+def test_gemm_pm_validation(lib):
+    g = lib.ue5m3_gemm_pm
+
+    def call(layout=0, M=32, N=32, K=64, kind=0, grid=1024, ctype=0, a=FAKE, c=FAKE):
+        return g(layout, M, N, K, a, FAKE, FAKE, FAKE, FAKE, FAKE, c, ctype, kind, grid, NULL)
+    assert call(layout=3) == ue.UE5M3_ELAYOUT
+    assert call(kind=2) == ue.UE5M3_EINVAL                 # E8M0 has no probe-matched path
+    for bad in (-1, 1000, 3, (1 << 31) - 1):
+        assert call(grid=bad) == ue.UE5M3_EINVAL
+    assert call(K=40) == ue.UE5M3_ESHAPE
+    assert call(N=40) == ue.UE5M3_ESHAPE and call(layout=1, N=40) == ue.UE5M3_ESHAPE
+    assert call(ctype=3) == ue.UE5M3_EINVAL
+    assert call(c=NULL) == ue.UE5M3_EINVAL
+    assert call(a=FAKE_MIS) == ue.UE5M3_EALIGN
+    assert call(M=0) == ue.UE5M3_OK and call(N=0) == ue.UE5M3_OK

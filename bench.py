@@ -51,6 +51,9 @@ def parse():
     p.add_argument("--pm", type=int, default=None, metavar="GRID",
                    help="run the step with the probe-matched GEMMs (64-product RNE partials, "
                         "toward-zero cross-group adds, 1/GRID snap; 0 = no snap)")
+    p.add_argument("--control", action="store_true",
+                   help="teacher-student regression control: BF16 vs FP4 (probe-matched GEMM) final-eval MSE "
+                        "and grid invariance over seeds 41-43, RN and SR gradients")
     p.add_argument("--formats", action="store_true",
                    help="scale-format comparison instead of the headline step: UE5M3 (delayed "
                         "amax), E4M3 (current amax) and E8M0 (blocks of 32) on the QKV workload "
@@ -142,6 +145,41 @@ def _decode_rows(payload, scales, fmt):
     return q * np.repeat(s, q.shape[1] // s.shape[1], axis=1)
 
 
+def control_bench(args):
+    """Table tab:grid-regression structure: per gradient rounding, the mean
+    BF16 and FP4 (d = 1024) final-eval MSE over seeds 41-43, and how many of
+    the 15 (seed, nonzero d) runs reproduce the d = 0 run exactly (records:
+    every loss, gradient norm and zero-gradient rate; states: final
+    weights)."""
+    from paper_2609_02846_amd import control
+    grids = (256, 512, 1024, 2048, 4096)
+    res = {}
+    t0 = time.time()
+    bf = {s: control.run(s, "bf16") for s in (41, 42, 43)}
+    for rnd in ("rn", "sr"):
+        mse_q, rec, st = [], 0, 0
+        for s in (41, 42, 43):
+            base = control.run(s, "fp4", rnd, grid=0)
+            for d in grids:
+                r = control.run(s, "fp4", rnd, grid=d)
+                a, b = control.same_trajectory(base, r)
+                rec += int(a)
+                st += int(b)
+                if d == 1024:
+                    mse_q.append(r["eval_mse"])
+            print(f"control {rnd} seed {s} done ({time.time() - t0:.0f} s)", flush=True)
+        res[rnd] = {"bf16_eval_mse": round(float(np.mean([bf[s]["eval_mse"] for s in bf])), 6),
+                    "fp4_eval_mse": round(float(np.mean(mse_q)), 6),
+                    "exact_records": f"{rec}/15", "exact_states": f"{st}/15"}
+    print(json.dumps({"metric": "teacher-student regression control (256-256-64, 500 AdamW steps)",
+                      "unit": "final-eval MSE", "seeds": [41, 42, 43], "grids": list(grids),
+                      "results": res, "paper": {"rn": {"bf16_eval_mse": 0.001956, "fp4_eval_mse": 0.027130,
+                                                        "exact_records": "15/15", "exact_states": "15/15"},
+                                                 "sr": {"bf16_eval_mse": 0.001956, "fp4_eval_mse": 0.027578,
+                                                        "exact_records": "15/15", "exact_states": "15/15"}},
+                      "seconds": round(time.time() - t0, 1)}), flush=True)
+
+
 def formats_bench(args):
     """Config-5 comparison: per encoding, the step time of the quantizers and
     the three GEMMs, and the quantization error on sampled rows."""
@@ -221,9 +259,12 @@ def formats_bench(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this build has no "
-              "multi-GPU path; see DESIGN.md for how the step would shard.", file=sys.stderr)
+        print(f"bench.py measures one GPU (got --gpus {args.gpus}): the step has no multi-GPU path.",
+              file=sys.stderr)
         sys.exit(2)
+    if args.control:
+        control_bench(args)
+        return
     if args.formats:
         formats_bench(args)
         return

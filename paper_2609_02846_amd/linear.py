@@ -11,7 +11,8 @@ forward (Sec. 2.3, Table 5; eq:delayed-amax)
   * W 16x16 tiles RN, plus the transposed payload when X needs a gradient;
   * fprop GEMM, bf16 Y.
 
-backward (eq:sr: stochastic rounding on the upstream gradient only)
+backward (eq:sr: stochastic rounding on the upstream gradient only; RN on
+request)
   * sample-and-hold amax of dY;
   * dY row blocks SR -> dgrad GEMM dX = dY W (bf16);
   * dY column blocks SR -> wgrad GEMM dW = dY^T X (in the weight's dtype).
@@ -39,7 +40,8 @@ Weights are bf16.  There is no bias term.
 
 import torch
 
-from . import AmaxState, amax_accumulate, amax_sample, gemm, quantize_1d, quantize_2d, quantize_dual
+from . import (AmaxState, amax_accumulate, amax_sample, gemm, gemm_pm, quantize_1d, quantize_2d,
+               quantize_dual)
 
 
 class _FP4LinearFn(torch.autograd.Function):
@@ -59,7 +61,7 @@ class _FP4LinearFn(torch.autograd.Function):
             xr, sxr, dec_x = quantize_1d(x2d, 1, layer.amax_x.amax, tx, "rn")
             xc = sxc = None
         pw, sw, pwt, dec_w, swt = quantize_2d(weight, layer.amax_w.amax, tx, "rn", transposed=need_dx)
-        y = gemm("nt", T, N, K, xr, sxr, dec_x, pw, sw, dec_w, out_dtype=torch.bfloat16)
+        y = layer._gemm("nt", T, N, K, xr, sxr, dec_x, pw, sw, dec_w, out_dtype=torch.bfloat16)
         ctx.layer = layer
         ctx.step = step
         ctx.shape = (T, K, N)
@@ -76,13 +78,14 @@ class _FP4LinearFn(torch.autograd.Function):
         amax_sample(layer.amax_dy, dy, ctx.step)
         seed = layer._next_sr_seed()
         dx = dw = None
+        mode = layer.grad_rounding
         if ctx.needs_input_grad[0]:
-            dr = quantize_1d(dy, 1, layer.amax_dy.amax, layer.target, "sr", seed, 2 * layer.layer_id + 1)
-            dx = gemm("nn", T, K, N, *dr, pwt, swt, dec_w, out_dtype=torch.bfloat16)
+            dr = quantize_1d(dy, 1, layer.amax_dy.amax, layer.target, mode, seed, 2 * layer.layer_id + 1)
+            dx = layer._gemm("nn", T, K, N, *dr, pwt, swt, dec_w, out_dtype=torch.bfloat16)
         if ctx.needs_input_grad[1]:
-            dc = quantize_1d(dy, 0, layer.amax_dy.amax, layer.target_dy_wgrad, "sr", seed,
+            dc = quantize_1d(dy, 0, layer.amax_dy.amax, layer.target_dy_wgrad, mode, seed,
                              2 * layer.layer_id + 2)
-            dw = gemm("tn", N, K, T, *dc, xc, sxc, dec_x, out_dtype=ctx.wdtype)
+            dw = layer._gemm("tn", N, K, T, *dc, xc, sxc, dec_x, out_dtype=ctx.wdtype)
         return dx, dw, None, None, None
 
 
@@ -92,11 +95,18 @@ class Linear(torch.nn.Module):
     ``period``: sample-and-hold period D in optimizer steps (50 in the
     recipe).  ``target``: scale target T (448); ``target_dy_wgrad``: T of the
     wgrad dY operand (448, or 2048 for the paper's override).  The weight is
-    bf16 and so is its gradient (the wgrad GEMM writes it directly)."""
+    bf16 and so is its gradient (the wgrad GEMM writes it directly).
+    ``grad_rounding``: "sr" (the recipe) or "rn" for the dY quantizers.
+    ``pm_grid``: None runs the decoded-operand GEMMs (fp32 accumulation);
+    an integer d runs all three products through the probe-matched output
+    model with final-grid denominator d (0 = no snap, the paper's 1024)."""
 
     def __init__(self, in_features, out_features, period=50, target=448.0, target_dy_wgrad=448.0,
-                 seed=0, layer_id=0, device="cuda"):
+                 seed=0, layer_id=0, device="cuda", grad_rounding="sr", pm_grid=None):
         super().__init__()
+        if grad_rounding not in ("sr", "rn"):
+            raise ValueError("grad_rounding must be 'sr' or 'rn'")
+        self.grad_rounding, self.pm_grid = grad_rounding, pm_grid
         if in_features % 16 or out_features % 16 or in_features <= 0 or out_features <= 0:
             raise ValueError("in_features and out_features must be positive multiples of 16")
         self.in_features, self.out_features = int(in_features), int(out_features)
@@ -146,6 +156,11 @@ class Linear(torch.nn.Module):
         return self
 
     # -- internals ------------------------------------------------------
+    def _gemm(self, *args, **kw):
+        if self.pm_grid is None:
+            return gemm(*args, **kw)
+        return gemm_pm(*args, grid=self.pm_grid, **kw)
+
     def _forward_step(self):
         if self.policy is None:
             return self.step

@@ -19,6 +19,9 @@ Language Model Pretraining" (arXiv 2609.02846):
   eq:sr, Table 5) and dequantization.
 * ``gemm``     -- the decoded-operand GEMM model (Sec. 5.1) for the fprop,
   dgrad and wgrad products of Sec. 4.3.
+* ``rht``      -- the 16-point randomized Hadamard transform of the wgrad
+  operands (the "UE5M3 with Transformer Engine settings" recipe) and the
+  quantizer on transformed values.
 * ``accumulate`` -- the probe-matched output model (eq:issue-partial,
   eq:issue-rz, eq:final-grid, eq:grid-denominator): 64-product RNE
   partials, toward-zero cross-group adds, optional 1/d product-lattice snap.
@@ -35,4 +38,4 @@ does not fix ("parity unpinned" against the paper for that choice; the
 worked blocks in ``tests/golden`` pin it against hand derivation).
 """
 
-from . import formats, philox, scaling, quantize, gemm, accumulate  # noqa: F401
+from . import formats, philox, scaling, quantize, gemm, accumulate, rht  # noqa: F401

@@ -149,7 +149,15 @@ def quantize_1d(x_bits, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0, e
     index in the source tensor when ``x_bits`` is a sampled part of it
     (default: x itself is the source).  E8M0 ignores g and target (no tensor
     scale) and returns dec = 1."""
-    x = scaling.bf16_to_f32(x_bits)
+    return quantize_1d_values(scaling.bf16_to_f32(x_bits), axis, g, target, mode, seed, tensor_id,
+                              elem_index, fmt)
+
+
+def quantize_1d_values(x, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0, elem_index=None,
+                       fmt="ue5m3"):
+    """``quantize_1d`` of a float32 matrix (values already widened, or a
+    transformed operand)."""
+    x = np.asarray(x, dtype=np.float32)
     R, C = x.shape
     B = block_size(fmt)
     if fmt == "e8m0":

@@ -51,6 +51,9 @@ def parse():
     p.add_argument("--pm", type=int, default=None, metavar="GRID",
                    help="run the step with the probe-matched GEMMs (64-product RNE partials, "
                         "toward-zero cross-group adds, 1/GRID snap; 0 = no snap)")
+    p.add_argument("--rht", action="store_true",
+                   help="quantize the wgrad operands (X and dY blocked along tokens) after the 16-point "
+                        "randomized Hadamard transform, each with its transformed amax")
     p.add_argument("--control", action="store_true",
                    help="teacher-student regression control: BF16 vs FP4 (probe-matched GEMM) final-eval MSE "
                         "and grid invariance over seeds 41-43, RN and SR gradients")
@@ -304,14 +307,25 @@ def main():
     names = ["amax", "quant_x_dual", "quant_w_tiles", "quant_dy_rows", "quant_dy_cols", "gemm_fprop",
              "gemm_dgrad", "gemm_wgrad"]
 
+    sxt, sdt = ue.AmaxState(args.period), ue.AmaxState(args.period)   # transformed wgrad operands
+    MASK = 0x3C5A
+    xc_dec = bufs["xc"][2] if args.rht else bufs["xr"][2]     # one-read X quantizer: one decode factor
+
     def quant_x():
-        ue.quantize_dual(x, sx.amax, 448.0, "rn", 0, 0, 0, bufs["xr"][:2], bufs["xc"][:2], bufs["xr"][2])
+        if args.rht:
+            ue.quantize_1d(x, 1, sx.amax, 448.0, "rn", 0, 0, *bufs["xr"])
+            ue.quantize_cols_rht(x, sxt.amax, MASK, 448.0, "rn", 0, 0, *bufs["xc"])
+        else:
+            ue.quantize_dual(x, sx.amax, 448.0, "rn", 0, 0, 0, bufs["xr"][:2], bufs["xc"][:2], bufs["xr"][2])
 
     def quant_dy_rows(seed):
         ue.quantize_1d(dy, 1, sd.amax, 448.0, "sr", seed, 1, *bufs["dr"])
 
     def quant_dy_cols(seed):
-        ue.quantize_1d(dy, 0, sd.amax, 448.0, "sr", seed, 2, *bufs["dc"])
+        if args.rht:
+            ue.quantize_cols_rht(dy, sdt.amax, MASK, 448.0, "sr", seed, 2, *bufs["dc"])
+        else:
+            ue.quantize_1d(dy, 0, sd.amax, 448.0, "sr", seed, 2, *bufs["dc"])
 
     if args.pm is None:
         G = ue.gemm
@@ -327,6 +341,9 @@ def main():
         ue.amax_sample(sx, x, t)
         ue.amax_sample(sw, w, t)
         ue.amax_sample(sd, dy, t)
+        if args.rht:
+            ue.amax_sample_rht(sxt, x, MASK, t)
+            ue.amax_sample_rht(sdt, dy, MASK, t)
         mark(1)
         quant_x()
         mark(2)
@@ -342,7 +359,7 @@ def main():
         mark(6)
         G("nn", T, K, N, dr[0], dr[1], dr[2], pwt, swt, dw_, out=dx)
         mark(7)
-        G("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xr[2], out=dw)
+        G("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xc_dec, out=dw)
         mark(8)
 
     for t in range(args.warmup):
@@ -360,8 +377,7 @@ def main():
                                     bufs["w"][3], out=y),
             "gemm_dgrad": lambda: G("nn", T, K, N, bufs["dr"][0], bufs["dr"][1], bufs["dr"][2],
                                     bufs["w"][2], bufs["w"][4], bufs["w"][3], out=dx),
-            "gemm_wgrad": lambda: G("tn", N, K, T, *bufs["dc"], bufs["xc"][0], bufs["xc"][1],
-                                    bufs["xr"][2], out=dw),
+            "gemm_wgrad": lambda: G("tn", N, K, T, *bufs["dc"], bufs["xc"][0], bufs["xc"][1], xc_dec, out=dw),
         }[args.kernel]
         for _ in range(args.steps):
             single()
@@ -390,7 +406,8 @@ def main():
     avg = {n: float(np.mean(v)) for n, v in per.items()}
 
     flop_gemm = 2.0 * T * N * K
-    qbytes = {"quant_x_dual": quant_bytes_dual(T, K), "quant_w_tiles": quant_bytes_2d(N, K, True),
+    qbytes = {"quant_x_dual": 2 * quant_bytes_1d(T, K) if args.rht else quant_bytes_dual(T, K),
+              "quant_w_tiles": quant_bytes_2d(N, K, True),
               "quant_dy_rows": quant_bytes_1d(T, N), "quant_dy_cols": quant_bytes_1d(T, N)}
     kernels = {}
     for n, b in qbytes.items():
@@ -413,8 +430,10 @@ def main():
         try:
             import hashlib
             tr = json.load(open(args.traffic))
-            src = open(os.path.join(ROOT, "paper_2609_02846_amd", "csrc", "gemm.hip"), "rb").read()
-            fresh = hashlib.sha256(src).hexdigest()[:16] == tr.get("source_sha256_16")
+            h = hashlib.sha256()
+            for f in ("gemm.hip", "fp4_decode.hpp"):
+                h.update(open(os.path.join(ROOT, "paper_2609_02846_amd", "csrc", f), "rb").read())
+            fresh = h.hexdigest()[:16] == tr.get("source_sha256_16")
             if fresh and tr.get("kernel") == dom and tr.get("config") == [T, K, N]:
                 traffic = round(float(tr["bytes_per_launch"]))
         except Exception:
@@ -440,13 +459,13 @@ def main():
            "data": "synthetic",
            "config": {"workload": f"FFN up-projection linear training step T={T} K={K} N={N}",
                       "tokens": T, "k": K, "n": N, "refresh_period": args.period,
-                      "target": 448.0,
+                      "target": 448.0, "wgrad_operand_rht": bool(args.rht),
                       "gemm": ("decoded-operand, fp32 accumulation" if args.pm is None else
                                f"probe-matched, grid 1/{args.pm}" if args.pm else "probe-matched, no snap")},
            "quantize_GBps": round(quant_gbs, 1), "quantize_frac_hbm": round(quant_gbs / HBM_PEAK_GBS, 4),
            "gemm_TFLOPs": round(gemm_tf, 1), "gemm_frac_bf16": round(gemm_tf / BF16_PEAK_TFLOPS, 4),
            "kernels": kernels, "roofline": roofline}
-    if not args.no_cpu_baseline and args.pm is None:
+    if not args.no_cpu_baseline and args.pm is None and not args.rht:
         out["cpu_baseline"] = cpu_baseline(wl, T, K, N)
     print(json.dumps(out), flush=True)
 

@@ -105,6 +105,41 @@ ue5m3_status_t ue5m3_amax_accumulate(const void* x_bf16, int64_t numel, float* a
                                      int32_t clear, hipStream_t stream);
 
 /*
+ * Randomized Hadamard transform of the weight-gradient operands (the "UE5M3
+ * with Transformer Engine settings" recipe: paper Table 6, Sec. 2).  The
+ * transform replaces every block of 16 consecutive rows (tokens) of each
+ * column of a bf16 matrix x [rows, cols] by y = (1/4) H16 diag(s) x_block,
+ * H16[i][j] = (-1)^popcount(i & j), s_i = -1 where bit i of sign_mask is set,
+ * evaluated in binary32 as sign flips, butterfly stages h = 1, 2, 4, 8
+ * ((u_i, u_{i+h}) <- (u_i + u_{i+h}, u_i - u_{i+h}) for i with bit h clear,
+ * one rounding each) and an exact 1/4 scaling.  The same sign_mask must be
+ * used for both operands of one weight-gradient product (X and dY), which
+ * leaves dY^T X unchanged in exact arithmetic.  The paper fixes neither the
+ * size nor the signs; the caller draws the mask.
+ *
+ * ue5m3_amax_sample_rht: ue5m3_amax_sample for the transformed tensor (its
+ * amax is the reference of the transformed operand).  Requires rows % 16 ==
+ * 0 and cols % 2 == 0 (ESHAPE), sign_mask < 2^16 (EINVAL).
+ */
+ue5m3_status_t ue5m3_amax_sample_rht(ue5m3_amax_state_t* st, const void* x_bf16, int64_t rows,
+                                     int64_t cols, uint32_t sign_mask, int64_t step, int32_t* refreshed,
+                                     hipStream_t stream);
+
+/*
+ * COL16 quantization (UE5M3, as ue5m3_quantize_1d with axis 0: payload_t
+ * [cols][rows/2], scales_t [cols][rows/16]) of the transformed tensor
+ * described at ue5m3_amax_sample_rht, with the held reference *amax_dev of
+ * the transformed tensor.  SR words follow each element's position (r, c)
+ * in x.  Same status codes as ue5m3_quantize_1d, plus EINVAL for
+ * sign_mask >= 2^16.
+ */
+ue5m3_status_t ue5m3_quantize_cols_rht(const void* x_bf16, int64_t rows, int64_t cols,
+                                       const float* amax_dev, float target, ue5m3_round_t mode,
+                                       uint64_t seed, uint32_t tensor_id, uint32_t sign_mask,
+                                       uint8_t* payload_t, uint8_t* scales_t, float* dec_out,
+                                       hipStream_t stream);
+
+/*
  * eq:delayed-amax.  At optimizer step `step`, if the cache is empty or
  * period > 0 and step - last_refresh >= period, enqueue the tensor amax a = max_i |x_i| of
  * the bf16 tensor x (numel elements) into *st->amax_dev, set last_refresh =

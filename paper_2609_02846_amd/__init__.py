@@ -32,7 +32,7 @@ EXPORTED_SYMBOLS = (
     "ue5m3_amax_state_freeze", "ue5m3_amax_accumulate",
     "ue5m3_quantize_1d", "ue5m3_quantize_2d", "ue5m3_gemm",
     "ue5m3_quantize_1d_ex", "ue5m3_quantize_2d_ex", "ue5m3_gemm_ex", "ue5m3_quantize_dual",
-    "ue5m3_gemm_pm",
+    "ue5m3_gemm_pm", "ue5m3_amax_sample_rht", "ue5m3_quantize_cols_rht",
     "ue5m3_status_string", "ue5m3_version",
 )
 
@@ -88,6 +88,11 @@ def load_library(path=LIB_PATH):
     lib.ue5m3_quantize_2d_ex.restype = i32
     lib.ue5m3_gemm_ex.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp]
     lib.ue5m3_gemm_ex.restype = i32
+    lib.ue5m3_amax_sample_rht.argtypes = [ctypes.POINTER(AmaxStateC), vp, i64, i64, u32, i64,
+                                          ctypes.POINTER(ctypes.c_int32), vp]
+    lib.ue5m3_amax_sample_rht.restype = i32
+    lib.ue5m3_quantize_cols_rht.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, u32, vp, vp, vp, vp]
+    lib.ue5m3_quantize_cols_rht.restype = i32
     lib.ue5m3_gemm_pm.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp]
     lib.ue5m3_gemm_pm.restype = i32
     lib.ue5m3_quantize_dual.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, u32, i32,
@@ -214,6 +219,36 @@ def amax_accumulate(x, amax_dev, clear=False, stream=None):
     _check(load_library().ue5m3_amax_accumulate(_ptr(x), x.numel(), _ptr(amax_dev), int(bool(clear)),
                                                 _stream(stream)), "ue5m3_amax_accumulate")
     return amax_dev
+
+
+def amax_sample_rht(state, x, sign_mask, step, stream=None):
+    """amax_sample for the randomized Hadamard transform of x's 16-row
+    column blocks (see ue5m3_amax_sample_rht)."""
+    _bf16_2d(x, "x")
+    flag = ctypes.c_int32(0)
+    _check(load_library().ue5m3_amax_sample_rht(ctypes.byref(state.c), _ptr(x), x.shape[0], x.shape[1],
+                                                int(sign_mask), int(step), ctypes.byref(flag),
+                                                _stream(stream)), "ue5m3_amax_sample_rht")
+    return bool(flag.value)
+
+
+def quantize_cols_rht(x, amax_dev, sign_mask, target=448.0, mode="rn", seed=0, tensor_id=0,
+                      payload_t=None, scales_t=None, dec_out=None, stream=None):
+    """COL16 quantization of the transformed x (see ue5m3_quantize_cols_rht).
+    Returns (payload_t [C, R/2], scales_t [C, R/16], dec_out)."""
+    _bf16_2d(x, "x")
+    R, C = x.shape
+    payload_t = _u8((C, R // 2), x) if payload_t is None else _u8_out(payload_t, (C, R // 2), "payload_t")
+    scales_t = _u8((C, R // 16), x) if scales_t is None else _u8_out(scales_t, (C, R // 16), "scales_t")
+    if dec_out is None:
+        dec_out = torch.empty(1, dtype=torch.float32, device=x.device)
+    _f32_out(dec_out, "dec_out")
+    _f32_out(amax_dev, "amax_dev")
+    _check(load_library().ue5m3_quantize_cols_rht(
+        _ptr(x), R, C, _ptr(amax_dev), float(target), _MODES[mode], int(seed) & (2**64 - 1),
+        int(tensor_id) & 0xFFFFFFFF, int(sign_mask), _ptr(payload_t), _ptr(scales_t), _ptr(dec_out),
+        _stream(stream)), "ue5m3_quantize_cols_rht")
+    return payload_t, scales_t, dec_out
 
 
 def quantize_1d(x, axis, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0,

@@ -118,6 +118,43 @@ ue5m3_status_t ue5m3_quantize_1d_ex(const void* x_bf16, int64_t rows, int64_t co
     return hip_status(e);
 }
 
+ue5m3_status_t ue5m3_amax_sample_rht(ue5m3_amax_state_t* st, const void* x_bf16, int64_t rows,
+                                     int64_t cols, uint32_t sign_mask, int64_t step, int32_t* refreshed,
+                                     hipStream_t stream) {
+    if (st == nullptr || st->amax_dev == nullptr || st->period < 0 || sign_mask > 0xFFFFu)
+        return UE5M3_EINVAL;
+    if (rows < 0 || cols < 0 || rows % 16 != 0 || cols % 2 != 0) return UE5M3_ESHAPE;
+    const bool empty = rows == 0 || cols == 0;
+    if (!empty && x_bf16 == nullptr) return UE5M3_EINVAL;
+    if ((!empty && !aligned16(x_bf16)) || !aligned4(st->amax_dev)) return UE5M3_EALIGN;
+    const bool refresh = !st->has_cache ||
+                         (st->period > 0 && step - st->last_refresh >= (int64_t)st->period);
+    if (refreshed != nullptr) *refreshed = refresh ? 1 : 0;
+    if (!refresh) return UE5M3_OK;
+    const hipError_t e = ue5m3::launch_amax_rht(x_bf16, rows, cols, sign_mask, st->amax_dev, stream);
+    if (e != hipSuccess) return UE5M3_EHIP;
+    st->has_cache = 1;
+    st->last_refresh = step;
+    return UE5M3_OK;
+}
+
+ue5m3_status_t ue5m3_quantize_cols_rht(const void* x_bf16, int64_t rows, int64_t cols,
+                                       const float* amax_dev, float target, ue5m3_round_t mode,
+                                       uint64_t seed, uint32_t tensor_id, uint32_t sign_mask,
+                                       uint8_t* payload_t, uint8_t* scales_t, float* dec_out,
+                                       hipStream_t stream) {
+    if (mode != UE5M3_RN && mode != UE5M3_SR) return UE5M3_EINVAL;
+    if (amax_dev == nullptr || !valid_target(target) || sign_mask > 0xFFFFu) return UE5M3_EINVAL;
+    if (rows < 0 || cols < 0 || rows % 16 != 0 || cols % 2 != 0) return UE5M3_ESHAPE;
+    if (!aligned4(amax_dev) || (dec_out != nullptr && !aligned4(dec_out))) return UE5M3_EALIGN;
+    if (rows == 0 || cols == 0) return UE5M3_OK;
+    if (x_bf16 == nullptr || payload_t == nullptr || scales_t == nullptr) return UE5M3_EINVAL;
+    if (!aligned16(x_bf16) || !aligned16(payload_t) || !aligned16(scales_t)) return UE5M3_EALIGN;
+    return hip_status(ue5m3::launch_quant_cols_rht(x_bf16, rows, cols, amax_dev, target, mode == UE5M3_SR,
+                                                   seed, tensor_id, sign_mask, payload_t, scales_t,
+                                                   dec_out, stream));
+}
+
 ue5m3_status_t ue5m3_quantize_1d(const void* x_bf16, int64_t rows, int64_t cols, int32_t axis,
                                  const float* amax_dev, float target, ue5m3_round_t mode,
                                  uint64_t seed, uint32_t tensor_id, uint8_t* payload,

@@ -22,6 +22,18 @@ enum class ScaleKind : int { UE5M3 = 0, E4M3 = 1, E8M0 = 2 };
 hipError_t launch_amax(const void* x_bf16, int64_t numel, float* amax_dev, bool clear,
                        hipStream_t s);
 
+// Amax of the 16-point randomized Hadamard transform of every 16-row block
+// of each column (rows % 16 == 0, cols % 2 == 0) into *amax_dev.
+hipError_t launch_amax_rht(const void* x_bf16, int64_t rows, int64_t cols, uint32_t sign_mask,
+                           float* amax_dev, hipStream_t s);
+
+// COL16 quantization (UE5M3) of the transformed tensor, layout as
+// launch_quant_cols.
+hipError_t launch_quant_cols_rht(const void* x_bf16, int64_t rows, int64_t cols, const float* amax_dev,
+                                 float target, bool sr, uint64_t seed, uint32_t tensor_id,
+                                 uint32_t sign_mask, uint8_t* payload_t, uint8_t* scales_t,
+                                 float* dec_out, hipStream_t s);
+
 hipError_t launch_quant_rows(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
                              const float* amax_dev, float target, bool sr, uint64_t seed,
                              uint32_t tensor_id, uint8_t* payload, uint8_t* scales,

@@ -19,6 +19,7 @@
 // assembled in LDS first.
 #include "codec.hpp"
 #include "launch.hpp"
+#include "rht.hpp"
 
 namespace ue5m3 {
 namespace {
@@ -34,6 +35,19 @@ struct BlockScale {
 // magnitude.  UE5M3 and E4M3: code = nearest code of a * S (zero code ->
 // code of 1.0), r = G / value(code).  E8M0: the power-of-two exponent of the
 // OCP microscaling rule and r = 2^-E (no tensor scale).
+// UE5M3 / E4M3 block scale of a block whose largest magnitude is a (any
+// binary32 value, e.g. of a transformed block).
+template <int FMT>
+__device__ __forceinline__ BlockScale block_scale_value(float a, const Multipliers& m) {
+    BlockScale bs;
+    const bool e4 = FMT == (int)ScaleKind::E4M3;
+    uint32_t code = e4 ? e4m3_encode(a * m.S) : ue5m3_encode(a * m.S);
+    code = code ? code : (e4 ? kE4M3CodeOne : kCodeOne);
+    bs.code = code;
+    bs.r = m.G / (e4 ? e4m3_decode(code) : ue5m3_decode(code));
+    return bs;
+}
+
 template <int FMT>
 __device__ __forceinline__ BlockScale block_scale(uint32_t amax_bits15, const Multipliers& m) {
     BlockScale bs;
@@ -298,11 +312,12 @@ __device__ __forceinline__ ColItem col_item(int64_t it, int64_t gx, int64_t rows
 // SR of 16 rows x 4 columns (row pairs 2k, 2k+1 per conversion) into the
 // column-wise payload words pk[j][0..1]; Philox words are made per row pair.
 // A flagged pair (see sr_check) has its two nibbles redone in software.
-template <bool ALIGNED>
-__device__ __forceinline__ void sr_cols16x4(const uint32_t (&lo)[16], const uint32_t (&hi)[16],
-                                            const BlockScale (&bs)[4], uint64_t e_row0, uint64_t cols,
-                                            uint32_t tid, uint32_t k0, uint32_t k1,
-                                            uint32_t (&pk)[4][2]) {
+// get(j, r): value of row r, column j of the 16 x 4 block (compile-time
+// indices after unrolling).
+template <bool ALIGNED, typename Get>
+__device__ __forceinline__ void sr_cols16x4_v(Get get, const BlockScale (&bs)[4], uint64_t e_row0,
+                                              uint64_t cols, uint32_t tid, uint32_t k0, uint32_t k1,
+                                              uint32_t (&pk)[4][2]) {
     uint32_t aL[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
     uint32_t aH[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
 #pragma unroll
@@ -312,9 +327,8 @@ __device__ __forceinline__ void sr_cols16x4(const uint32_t (&lo)[16], const uint
         words4<ALIGNED>(e_row0 + (uint64_t)(2 * k + 1) * cols, tid, k0, k1, w1);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const uint32_t a0 = j < 2 ? lo[2 * k] : hi[2 * k], a1 = j < 2 ? lo[2 * k + 1] : hi[2 * k + 1];
-            const float y0 = ((j & 1) ? bf16_hi(a0) : bf16_lo(a0)) * bs[j].r;
-            const float y1 = ((j & 1) ? bf16_hi(a1) : bf16_lo(a1)) * bs[j].r;
+            const float y0 = get(j, 2 * k) * bs[j].r;
+            const float y1 = get(j, 2 * k + 1) * bs[j].r;
             const v2f_t v = {y0, y1};
             const uint32_t r0 = ~w0[j];
             const uint32_t r1 = __builtin_amdgcn_alignbit(~w1[j], ~w1[j], 1);
@@ -339,12 +353,30 @@ __device__ __forceinline__ void sr_cols16x4(const uint32_t (&lo)[16], const uint
         for (int h = 0; h < 2; ++h) pk[j][h] = (aL[j][h] & 0x0F0F0F0Fu) | (aH[j][h] & 0xF0F0F0F0u);
 }
 
-template <bool SR, int FMT>
+// The 16 x 4 block held as bf16 pairs: columns (c, c+1) in lo, (c+2, c+3) in hi.
+template <bool ALIGNED>
+__device__ __forceinline__ void sr_cols16x4(const uint32_t (&lo)[16], const uint32_t (&hi)[16],
+                                            const BlockScale (&bs)[4], uint64_t e_row0, uint64_t cols,
+                                            uint32_t tid, uint32_t k0, uint32_t k1,
+                                            uint32_t (&pk)[4][2]) {
+    sr_cols16x4_v<ALIGNED>(
+        [&](int j, int r) -> float {
+            const uint32_t a = j < 2 ? lo[r] : hi[r];
+            return (j & 1) ? bf16_hi(a) : bf16_lo(a);
+        },
+        bs, e_row0, cols, tid, k0, k1, pk);
+}
+
+// RHT: every 16-row block of each column is first replaced by its 16-point
+// randomized Hadamard transform (rht16, sign mask rht_mask) and quantized as
+// binary32 values (UE5M3 / E4M3 only).
+template <bool SR, int FMT, bool RHT = false>
 __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
     const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t rows_per_item, int64_t gx,
     int64_t nitems, const float* __restrict__ amax_dev, float T, uint32_t key0, uint32_t key1,
     uint32_t tid, uint8_t* __restrict__ payload_t, uint8_t* __restrict__ scales_t,
-    float* __restrict__ dec_out) {
+    float* __restrict__ dec_out, uint32_t rht_mask) {
+    static_assert(!RHT || FMT != (int)ScaleKind::E8M0, "no transformed E8M0 operands");
     __shared__ __attribute__((aligned(16))) uint8_t stP[kColCols][kColGroupRB * 8];
     __shared__ __attribute__((aligned(16))) uint8_t stS[kColCols][kColGroupRB * kColScaleGroups];
     // E8M0 blocks are 32 rows: the two 16-row blocks of a wave (lanes l and
@@ -400,7 +432,40 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
         const int64_t c = ci.cw + 4 * q;
         const int64_t r0 = ci.r_begin + g * (kColGroupRB * 16) + rbl * 16;
         const int sg = (int)(g % kColScaleGroups);
-        if (r0 < ci.r_end && c < cols) {
+        if (RHT && r0 < ci.r_end && c < cols) {
+            float v[4][16];
+            BlockScale bs[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    v[j][r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
+                rht16(v[j], rht_mask);
+                uint32_t mb = 0u;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) mb = max(mb, __float_as_uint(v[j][r]) & 0x7FFFFFFFu);
+                bs[j] = block_scale_value<FMT>(__uint_as_float(mb), m);
+            }
+            uint32_t pk[4][2];
+            if (SR) {
+                auto get = [&](int j, int r) -> float { return v[j][r]; };
+                if (vec8)
+                    sr_cols16x4_v<true>(get, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c, (uint64_t)cols,
+                                        tid, key0, key1, pk);
+                else
+                    sr_cols16x4_v<false>(get, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c, (uint64_t)cols,
+                                         tid, key0, key1, pk);
+            } else {
+                const uint32_t nw[16] = {};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) quant_col16<false>(v[j], bs[j].r, nw, pk[j][0], pk[j][1]);
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                *reinterpret_cast<uint2*>(&stP[4 * q + j][rbl * 8]) = make_uint2(pk[j][0], pk[j][1]);
+                stS[4 * q + j][sg * kColGroupRB + rbl] = (uint8_t)bs[j].code;
+            }
+        } else if (!RHT && r0 < ci.r_end && c < cols) {
             uint32_t mx[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
@@ -827,15 +892,17 @@ int64_t resident_wgs(K kernel, int slot) {
     return cache[dev][slot];
 }
 
-template <int FMT>
+template <int FMT, bool RHT = false>
 hipError_t launch_cols_fmt(const void* x_bf16, int64_t rows, int64_t cols, const float* amax_dev,
                            float target, bool sr, uint64_t seed, uint32_t tensor_id,
-                           uint8_t* payload_t, uint8_t* scales_t, float* dec_out, hipStream_t s) {
+                           uint8_t* payload_t, uint8_t* scales_t, float* dec_out, hipStream_t s,
+                           uint32_t rht_mask = 0u) {
     uint32_t k0, k1;
     seed_key(seed, k0, k1);
     const int64_t gx = (cols + kColCols - 1) / kColCols;
-    const int64_t resident = sr ? resident_wgs(quant_cols_kernel<true, FMT>, 2 * FMT)
-                                : resident_wgs(quant_cols_kernel<false, FMT>, 2 * FMT + 1);
+    const int slot = 2 * FMT + (RHT ? 6 : 0);
+    const int64_t resident = sr ? resident_wgs(quant_cols_kernel<true, FMT, RHT>, slot)
+                                : resident_wgs(quant_cols_kernel<false, FMT, RHT>, slot + 1);
     // Items of up to 64 row blocks (whole 64-byte scale runs); shorter when
     // that leaves fewer than 2 items per resident workgroup.
     int64_t rows_per_item = (int64_t)kColGroupRB * kColScaleGroups * 16;     // 1024 rows
@@ -846,13 +913,13 @@ hipError_t launch_cols_fmt(const void* x_bf16, int64_t rows, int64_t cols, const
     const int64_t grid = min(nitems, resident);
     const uint16_t* x = reinterpret_cast<const uint16_t*>(x_bf16);
     if (sr)
-        hipLaunchKernelGGL((quant_cols_kernel<true, FMT>), dim3((unsigned)grid), dim3(kThreads), 0, s, x,
+        hipLaunchKernelGGL((quant_cols_kernel<true, FMT, RHT>), dim3((unsigned)grid), dim3(kThreads), 0, s, x,
                            rows, cols, rows_per_item, gx, nitems, amax_dev, target, k0, k1, tensor_id,
-                           payload_t, scales_t, dec_out);
+                           payload_t, scales_t, dec_out, rht_mask);
     else
-        hipLaunchKernelGGL((quant_cols_kernel<false, FMT>), dim3((unsigned)grid), dim3(kThreads), 0, s, x,
+        hipLaunchKernelGGL((quant_cols_kernel<false, FMT, RHT>), dim3((unsigned)grid), dim3(kThreads), 0, s, x,
                            rows, cols, rows_per_item, gx, nitems, amax_dev, target, k0, k1, tensor_id,
-                           payload_t, scales_t, dec_out);
+                           payload_t, scales_t, dec_out, rht_mask);
     return hipGetLastError();
 }
 
@@ -932,6 +999,15 @@ hipError_t launch_quant_cols(ScaleKind fmt, const void* x_bf16, int64_t rows, in
             return launch_cols_fmt<(int)ScaleKind::UE5M3>(x_bf16, rows, cols, amax_dev, target, sr, seed,
                                                           tensor_id, payload_t, scales_t, dec_out, s);
     }
+}
+
+hipError_t launch_quant_cols_rht(const void* x_bf16, int64_t rows, int64_t cols, const float* amax_dev,
+                                 float target, bool sr, uint64_t seed, uint32_t tensor_id,
+                                 uint32_t sign_mask, uint8_t* payload_t, uint8_t* scales_t,
+                                 float* dec_out, hipStream_t s) {
+    return launch_cols_fmt<(int)ScaleKind::UE5M3, true>(x_bf16, rows, cols, amax_dev, target, sr, seed,
+                                                        tensor_id, payload_t, scales_t, dec_out, s,
+                                                        sign_mask);
 }
 
 hipError_t launch_quant_tiles(ScaleKind fmt, const void* w_bf16, int64_t rows, int64_t cols,

@@ -40,8 +40,8 @@ Weights are bf16.  There is no bias term.
 
 import torch
 
-from . import (AmaxState, amax_accumulate, amax_sample, gemm, gemm_pm, quantize_1d, quantize_2d,
-               quantize_dual)
+from . import (AmaxState, amax_accumulate, amax_sample, amax_sample_rht, gemm, gemm_pm, quantize_1d,
+               quantize_2d, quantize_cols_rht, quantize_dual)
 
 
 class _FP4LinearFn(torch.autograd.Function):
@@ -55,8 +55,14 @@ class _FP4LinearFn(torch.autograd.Function):
         amax_sample(layer.amax_x, x2d, step)
         amax_sample(layer.amax_w, weight, step)
         tx = layer.target
-        if need_dw:
+        dec_xc = None
+        if need_dw and layer.rht_wgrad:
+            xr, sxr, dec_x = quantize_1d(x2d, 1, layer.amax_x.amax, tx, "rn")
+            amax_sample_rht(layer.amax_xt, x2d, layer.rht_mask, step)
+            xc, sxc, dec_xc = quantize_cols_rht(x2d, layer.amax_xt.amax, layer.rht_mask, tx, "rn")
+        elif need_dw:
             (xr, sxr, dec_x), (xc, sxc, _) = quantize_dual(x2d, layer.amax_x.amax, tx, "rn")
+            dec_xc = dec_x
         else:
             xr, sxr, dec_x = quantize_1d(x2d, 1, layer.amax_x.amax, tx, "rn")
             xc = sxc = None
@@ -66,14 +72,14 @@ class _FP4LinearFn(torch.autograd.Function):
         ctx.step = step
         ctx.shape = (T, K, N)
         ctx.wdtype = weight.dtype
-        ctx.save_for_backward(xc, sxc, dec_x, pwt, swt, dec_w)
+        ctx.save_for_backward(xc, sxc, dec_xc, pwt, swt, dec_w)
         return y
 
     @staticmethod
     def backward(ctx, dy):
         layer = ctx.layer
         T, K, N = ctx.shape
-        xc, sxc, dec_x, pwt, swt, dec_w = ctx.saved_tensors
+        xc, sxc, dec_xc, pwt, swt, dec_w = ctx.saved_tensors
         dy = dy.to(torch.bfloat16).contiguous()
         amax_sample(layer.amax_dy, dy, ctx.step)
         seed = layer._next_sr_seed()
@@ -83,9 +89,14 @@ class _FP4LinearFn(torch.autograd.Function):
             dr = quantize_1d(dy, 1, layer.amax_dy.amax, layer.target, mode, seed, 2 * layer.layer_id + 1)
             dx = layer._gemm("nn", T, K, N, *dr, pwt, swt, dec_w, out_dtype=torch.bfloat16)
         if ctx.needs_input_grad[1]:
-            dc = quantize_1d(dy, 0, layer.amax_dy.amax, layer.target_dy_wgrad, mode, seed,
-                             2 * layer.layer_id + 2)
-            dw = layer._gemm("tn", N, K, T, *dc, xc, sxc, dec_x, out_dtype=ctx.wdtype)
+            tid = 2 * layer.layer_id + 2
+            if layer.rht_wgrad:
+                amax_sample_rht(layer.amax_dyt, dy, layer.rht_mask, ctx.step)
+                dc = quantize_cols_rht(dy, layer.amax_dyt.amax, layer.rht_mask, layer.target_dy_wgrad, mode,
+                                       seed, tid)
+            else:
+                dc = quantize_1d(dy, 0, layer.amax_dy.amax, layer.target_dy_wgrad, mode, seed, tid)
+            dw = layer._gemm("tn", N, K, T, *dc, xc, sxc, dec_xc, out_dtype=ctx.wdtype)
         return dx, dw, None, None, None
 
 
@@ -99,14 +110,21 @@ class Linear(torch.nn.Module):
     ``grad_rounding``: "sr" (the recipe) or "rn" for the dY quantizers.
     ``pm_grid``: None runs the decoded-operand GEMMs (fp32 accumulation);
     an integer d runs all three products through the probe-matched output
-    model with final-grid denominator d (0 = no snap, the paper's 1024)."""
+    model with final-grid denominator d (0 = no snap, the paper's 1024).
+    ``rht_wgrad``: quantize the two wgrad operands (X and dY blocked along
+    tokens) after a 16-point randomized Hadamard transform with one sign mask
+    per layer (drawn from ``seed``), each with the amax of its transformed
+    tensor as reference (the "UE5M3 with Transformer Engine settings"
+    recipe, with ``period`` 1 and ``pm_grid`` 1024)."""
 
     def __init__(self, in_features, out_features, period=50, target=448.0, target_dy_wgrad=448.0,
-                 seed=0, layer_id=0, device="cuda", grad_rounding="sr", pm_grid=None):
+                 seed=0, layer_id=0, device="cuda", grad_rounding="sr", pm_grid=None, rht_wgrad=False):
         super().__init__()
         if grad_rounding not in ("sr", "rn"):
             raise ValueError("grad_rounding must be 'sr' or 'rn'")
         self.grad_rounding, self.pm_grid = grad_rounding, pm_grid
+        self.rht_wgrad = bool(rht_wgrad)
+        self.rht_mask = (((int(seed) * 0x9E3779B97F4A7C15 + 0x632BE59BD9B4E019) % 2 ** 64) >> 48) & 0xFFFF
         if in_features % 16 or out_features % 16 or in_features <= 0 or out_features <= 0:
             raise ValueError("in_features and out_features must be positive multiples of 16")
         self.in_features, self.out_features = int(in_features), int(out_features)
@@ -118,6 +136,8 @@ class Linear(torch.nn.Module):
         self.amax_x = AmaxState(period, device)
         self.amax_w = AmaxState(period, device)
         self.amax_dy = AmaxState(period, device)
+        self.amax_xt = AmaxState(period, device)     # transformed wgrad operands
+        self.amax_dyt = AmaxState(period, device)
         self.step = 0               # optimizer-step index, set by the training loop
         self.sr_calls = 0           # backward calls so far (SR key offset)
         self.batches = 0            # forward calls under an inference policy
@@ -150,7 +170,7 @@ class Linear(torch.nn.Module):
     def training_policy(self, period=50):
         """Back to training: every operand refreshes every ``period`` steps,
         from empty caches."""
-        for st in (self.amax_x, self.amax_w, self.amax_dy):
+        for st in (self.amax_x, self.amax_w, self.amax_dy, self.amax_xt, self.amax_dyt):
             st.set_period(period)
         self.policy = None
         return self

@@ -212,3 +212,28 @@ def test_gemm_pm_validation(lib):
     assert call(c=NULL) == ue.UE5M3_EINVAL
     assert call(a=FAKE_MIS) == ue.UE5M3_EALIGN
     assert call(M=0) == ue.UE5M3_OK and call(N=0) == ue.UE5M3_OK
+
+
+def test_rht_entry_points_validation(lib):
+    st = ue.AmaxStateC()
+    assert lib.ue5m3_amax_state_init(ctypes.byref(st), FAKE, 1) == ue.UE5M3_OK
+    smp = lib.ue5m3_amax_sample_rht
+    flag = ctypes.c_int32(-1)
+    assert smp(ctypes.byref(st), FAKE, 24, 8, 0, 0, ctypes.byref(flag), NULL) == ue.UE5M3_ESHAPE
+    assert smp(ctypes.byref(st), FAKE, 32, 7, 0, 0, ctypes.byref(flag), NULL) == ue.UE5M3_ESHAPE
+    assert smp(ctypes.byref(st), FAKE, 32, 8, 1 << 16, 0, ctypes.byref(flag), NULL) == ue.UE5M3_EINVAL
+    assert smp(ctypes.byref(st), FAKE_MIS, 32, 8, 0, 0, ctypes.byref(flag), NULL) == ue.UE5M3_EALIGN
+    st.has_cache, st.last_refresh = 1, 5
+    assert smp(ctypes.byref(st), FAKE, 32, 8, 0, 5, ctypes.byref(flag), NULL) == 0 and flag.value == 0
+    q = lib.ue5m3_quantize_cols_rht
+
+    def call(rows=32, cols=8, amax=FAKE, T=448.0, mode=0, mask=0x1234, x=FAKE, p=FAKE):
+        return q(x, rows, cols, amax, T, mode, 0, 0, mask, p, FAKE, NULL, NULL)
+    assert call(mode=2) == ue.UE5M3_EINVAL
+    assert call(amax=NULL) == ue.UE5M3_EINVAL
+    assert call(T=0.0) == ue.UE5M3_EINVAL
+    assert call(mask=1 << 16) == ue.UE5M3_EINVAL
+    assert call(rows=24) == ue.UE5M3_ESHAPE and call(cols=9) == ue.UE5M3_ESHAPE
+    assert call(x=NULL) == ue.UE5M3_EINVAL and call(p=NULL) == ue.UE5M3_EINVAL
+    assert call(x=FAKE_MIS) == ue.UE5M3_EALIGN
+    assert call(rows=0) == ue.UE5M3_OK

@@ -104,8 +104,13 @@ class AmaxState:
 
     def observe(self, x_bf16_bits, step):
         """Reference amax for optimizer step ``step``; returns (g, refreshed)."""
+        return self.observe_amax(lambda: amax(x_bf16_bits), step)
+
+    def observe_amax(self, amax_of, step):
+        """``observe`` with the tensor amax supplied by ``amax_of()`` (called
+        only on a refresh)."""
         if self.needs_refresh(step):
-            self.g = amax(x_bf16_bits)
+            self.g = np.float32(amax_of())
             self.last_refresh = int(step)
             self.has_cache = True
             return self.g, True

@@ -16,7 +16,7 @@ given (seed, role) always yields the same bytes on every machine.
 
 import numpy as np
 
-ROLE_X, ROLE_W, ROLE_DY, ROLE_OUTLIER, ROLE_ROWSCALE, ROLE_MISC = range(6)
+ROLE_X, ROLE_W, ROLE_DY, ROLE_OUTLIER, ROLE_ROWSCALE, ROLE_MISC, ROLE_DRIFT = range(7)
 
 
 def rng_for(seed, role):
@@ -112,3 +112,26 @@ def qkv_formats(seed=0, tokens=16384, k=4096, n=6144):
     return {"x": activation(seed, tokens, k, 1e-3, 100.0),
             "w": weight(seed, n, k),
             "dy": gradient(seed, tokens, n, 1e-4, 2.0)}
+
+
+def drift_factors(seed=0, steps=120, sigma=0.05, spike_prob=0.05, spike=20.0):
+    """Per-step magnitude factors of the X, W and dY operands ([steps, 3]
+    float32): a lognormal random walk (log step N(0, sigma)) per operand,
+    times ``spike`` on steps drawn with probability ``spike_prob`` (a
+    one-step spike).  Used to drive held tensor scales through drift,
+    spikes and refreshes."""
+    rng = rng_for(seed, ROLE_DRIFT)
+    walk = np.exp(np.cumsum(rng.normal(0.0, sigma, (steps, 3)), axis=0))
+    spikes = np.where(rng.random((steps, 3)) < spike_prob, spike, 1.0)
+    walk[0] = 1.0
+    return (walk * spikes).astype(np.float32)
+
+
+def ffn_down_drift(seed=0, tokens=8192, k=21504, n=4096):
+    """Base operands of the FFN down-projection drift workload: X [T, K]
+    (the FFN activations) N(0,1) with 0.1% x100 outliers, W [N, K]
+    N(0, 0.02), dY [T, N] N(0, 1e-5); each step multiplies them by
+    ``drift_factors``."""
+    return {"x": activation(seed, tokens, k, 1e-3, 100.0),
+            "w": weight(seed, n, k),
+            "dy": gradient(seed, tokens, n, 1e-5)}

@@ -1,0 +1,124 @@
+"""FFN down-projection (T = 8192, K = 21504, N = 4096) over 120 optimizer
+steps with the 50-step sample-and-hold reference (eq:delayed-amax) while the
+operand magnitudes drift (lognormal walk, sigma 0.05 per step) and spike
+(x20 on random steps): every step checks the refresh decisions and held
+references of X, W and dY against the oracle's trace; at the refresh steps,
+the spike steps between refreshes and the last step, sampled rows of the
+quantized operands are bit-exact and sampled GEMM outputs meet the GEMM bar.
+
+The operand of step t is bf16(base * f_t) (binary32 product, RNE), formed on
+the device; the oracle forms the same bits for the rows it samples.  The
+tensor amax of bf16(base * f) is bf16(max|base| * f) because both roundings
+are monotone, which gives the oracle its references without materialising
+each step's tensors on the host."""
+
+import numpy as np
+import pytest
+import torch
+
+import synthetic
+from oracle import gemm as ogemm
+from oracle import quantize as oq
+from oracle import scaling as osc
+import paper_2609_02846_amd as ue
+from tests.gpu_util import gemm_check, host, row_elem_index, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+STEPS, PERIOD = 120, 50
+
+
+def _scaled_bits(bits, f):
+    return synthetic.f32_to_bf16_bits(synthetic.bf16_bits_to_f32(bits) * np.float32(f))
+
+
+def _amax_scaled(base_max, f):
+    return osc.amax(synthetic.f32_to_bf16_bits(np.array([[base_max * np.float32(f)]], np.float32)))
+
+
+def test_down_projection_drift_120_steps():
+    T, K, N = 8192, 21504, 4096
+    say("down-projection drift", T, K, N, STEPS, "steps")
+    wl = synthetic.ffn_down_drift(0, T, K, N)
+    x0b, w0b, d0b = wl["x"], wl["w"], wl["dy"]
+    fac = synthetic.drift_factors(0, STEPS)
+    bmax = [np.float32(np.max(np.abs(synthetic.bf16_bits_to_f32(b)))) for b in (x0b, w0b, d0b)]
+    x0, w0, d0 = (to_dev(b).float() for b in (x0b, w0b, d0b))
+    states = [ue.AmaxState(PERIOD) for _ in range(3)]
+    ost = [osc.AmaxState(PERIOD) for _ in range(3)]
+    spikes = {int(t) for t, j in np.argwhere(fac > 5.0)}
+    refresh_steps = set(range(0, STEPS, PERIOD))
+    checks = sorted((refresh_steps | {t for t in spikes if t % PERIOD}) | {STEPS - 1})
+    rng = np.random.default_rng(3)
+    rows = np.sort(np.concatenate([[0, T - 1], rng.choice(T, 4, replace=False)]))
+    rdev = torch.from_numpy(rows).cuda()
+    sat = 0
+    for t in range(STEPS):
+        f = fac[t]
+        xt = (x0 * float(f[0])).to(torch.bfloat16)
+        wt = (w0 * float(f[1])).to(torch.bfloat16)
+        dt = (d0 * float(f[2])).to(torch.bfloat16)
+        for j, (st, tens) in enumerate(zip(states, (xt, wt, dt))):
+            r = ue.amax_sample(st, tens, t)
+            g_o, r_o = ost[j].observe_amax(lambda: _amax_scaled(bmax[j], f[j]), t)
+            assert r == r_o, (t, j)
+        torch.cuda.synchronize()
+        for j in range(3):
+            assert np.float32(states[j].amax.item()) == ost[j].g, (t, j)
+        if t not in checks:
+            continue
+        say("drift check step", t, "factors", f.tolist())
+        gx, gw, gd = (ost[j].g for j in range(3))
+        xr = ue.quantize_1d(xt, 1, states[0].amax)
+        xc = ue.quantize_1d(xt, 0, states[0].amax)
+        wq = ue.quantize_2d(wt, states[1].amax)
+        dr = ue.quantize_1d(dt, 1, states[2].amax, 448.0, "sr", 500 + t, 1)
+        dc = ue.quantize_1d(dt, 0, states[2].amax, 448.0, "sr", 500 + t, 2)
+        y = ue.gemm("nt", T, N, K, *xr, wq[0], wq[1], wq[3], out_dtype=torch.bfloat16)
+        dx = ue.gemm("nn", T, K, N, *dr, wq[2], wq[4], wq[3], out_dtype=torch.bfloat16)
+        dw = ue.gemm("tn", N, K, T, *dc, xc[0], xc[1], xc[2])
+        torch.cuda.synchronize()
+        # quantized rows of X and dY, bit-exact
+        xs = _scaled_bits(x0b[rows], f[0])
+        ds = _scaled_bits(d0b[rows], f[2])
+        xo = oq.quantize_1d(xs, 1, gx)
+        do = oq.quantize_1d(ds, 1, gd, 448.0, "sr", 500 + t, 1, elem_index=row_elem_index(rows, N))
+        assert np.array_equal(host(xr[0][rdev]), xo[0]) and np.array_equal(host(xr[1][rdev]), xo[1]), t
+        assert np.array_equal(host(dr[0][rdev]), do[0]) and np.array_equal(host(dr[1][rdev]), do[1]), t
+        sat += int(np.sum(xo[1] == 0xF7)) + int(np.sum(do[1] == 0xF7))
+        # fprop: sampled rows x one weight tile row (16 outputs each)
+        wt16 = _scaled_bits(w0b[16 * 7:16 * 8], f[1])
+        wo = oq.quantize_2d(wt16, gw)
+        X, W = oq.decoded_1d(xo[0], xo[1], 1), oq.decoded_2d(wo[0], wo[1])
+        al = ogemm.alpha(xo[2], wo[3])
+        ref = ogemm.fprop(X, W, al)
+        c16 = host(y[rdev][:, 16 * 7:16 * 8].float()).astype(np.float64)
+        e = float(al) * K * 2.0 ** -23 * ogemm.abs_product(X, W)
+        ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref) + e, 1e-30))) - 7)
+        assert np.all(np.abs(c16 - ref) <= e + 1.01 * ulp + 1e-30), ("fprop", t)
+        # dgrad: sampled rows x one 16-column weight tile column (all of N)
+        wcol = _scaled_bits(np.ascontiguousarray(w0b[:, 16 * 3:16 * 4]), f[1])
+        wco = oq.quantize_2d(wcol, gw)
+        dY = oq.decoded_1d(do[0], do[1], 1)
+        Wc = oq.decoded_2d(wco[0], wco[1])
+        al = ogemm.alpha(do[2], wco[3])
+        ref = ogemm.dgrad(dY, Wc, al)
+        c16 = host(dx[rdev][:, 16 * 3:16 * 4].float()).astype(np.float64)
+        e = float(al) * N * 2.0 ** -23 * ogemm.abs_product(dY, np.ascontiguousarray(Wc.T))
+        ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref) + e, 1e-30))) - 7)
+        assert np.all(np.abs(c16 - ref) <= e + 1.01 * ulp + 1e-30), ("dgrad", t)
+        # wgrad: two dY columns x three X columns
+        nc, kc = np.array([5, N - 1]), np.array([0, 999, K - 1])
+        dsub = _scaled_bits(np.ascontiguousarray(d0b[:, nc]), f[2])
+        xsub = _scaled_bits(np.ascontiguousarray(x0b[:, kc]), f[0])
+        dco = oq.quantize_1d(dsub, 0, gd, 448.0, "sr", 500 + t, 2,
+                             elem_index=row_elem_index(np.arange(T), N, nc))
+        xco = oq.quantize_1d(xsub, 0, gx)
+        A = oq.decoded_1d(dco[0], dco[1], 0).T
+        B = oq.decoded_1d(xco[0], xco[1], 0).T
+        al = ogemm.alpha(dco[2], xco[2])
+        ref = ogemm.fprop(A, B, al)
+        got = host(dw)[np.ix_(nc, kc)]
+        gemm_check(got, ref, al, ogemm.abs_product(A, B), T, f"wgrad step {t}")
+    print("saturated block codes seen in the sampled rows:", sat)
+

@@ -121,9 +121,12 @@ def cpu_baseline(wl, T, K, N, target_s=12.0):
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         blas_threads = None
-    cores = len(os.sched_getaffinity(0))
+    # NumPy elementwise work (the quantizers) runs on one thread; the BLAS
+    # product of the GEMM sample on blas_threads
+    cores = blas_threads or 1
     return {"value": flop_step / t_step / 1e12, "unit": "TFLOP/s", "cores": cores,
-            "blas_threads": blas_threads, "kind": "oracle",
+            "blas_threads": blas_threads, "quantizer_threads": 1,
+            "host_cpus": len(os.sched_getaffinity(0)), "kind": "oracle",
             "sample": (f"oracle quantizers on 1/{f} row slices of X, W, dY (x{quant_scale:.0f}) "
                        f"+ float64 decoded-operand fprop on {X.shape[0]}x{W.shape[0]}x{K} "
                        f"(x{flop_step / flop_sample:.0f} flops); projected step "

@@ -34,7 +34,9 @@ tensor_id, r * C + c)``, independent of the blocking.
 
 Comparison scale formats (``fmt``; Sec. 2, Table tab:formats):
 
-* ``"ue5m3"`` (default): the recipe above, blocks of 16.
+* ``"ue5m3"`` (default): the recipe above, blocks of 16 (``block=32`` and
+  ``tile=32``: the block-size control, 1D blocks of 32 and 32x32 weight
+  tiles, same arithmetic on the larger blocks).
 * ``"e4m3"``: the NVFP4 arrangement -- blocks of 16 with an E4M3 block scale
   under the FP32 tensor scale.  Same steps with step 3 the nearest E4M3 code
   (ties to even, saturating at 448) and the zero rule giving the E4M3 code
@@ -55,11 +57,18 @@ from . import formats, philox, scaling
 FORMATS = ("ue5m3", "e4m3", "e8m0")
 
 
-def block_size(fmt):
-    """Elements per block (1D) for a scale format."""
+def block_size(fmt, block=None):
+    """Elements per block (1D) for a scale format: E8M0 32; UE5M3 and E4M3
+    16, or 32 for the block-size control (``block=32``)."""
     if fmt not in FORMATS:
         raise ValueError(fmt)
-    return 32 if fmt == "e8m0" else 16
+    if fmt == "e8m0":
+        if block not in (None, 32):
+            raise ValueError("E8M0 blocks are 32")
+        return 32
+    if block not in (None, 16, 32):
+        raise ValueError("block must be 16 or 32")
+    return block or 16
 
 
 def scale_decode(fmt, code):
@@ -142,7 +151,7 @@ def _words_for(shape, seed, tensor_id, mode, elem_index):
 
 
 def quantize_1d(x_bits, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0, elem_index=None,
-                fmt="ue5m3"):
+                fmt="ue5m3", block=None):
     """1D block quantization of a bf16 matrix (blocks of 16, or 32 for
     E8M0).  Returns (payload, scales, dec) in the layouts described in the
     module header.  ``elem_index`` (SR only) gives each element's row-major
@@ -150,16 +159,16 @@ def quantize_1d(x_bits, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0, e
     (default: x itself is the source).  E8M0 ignores g and target (no tensor
     scale) and returns dec = 1."""
     return quantize_1d_values(scaling.bf16_to_f32(x_bits), axis, g, target, mode, seed, tensor_id,
-                              elem_index, fmt)
+                              elem_index, fmt, block)
 
 
 def quantize_1d_values(x, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0, elem_index=None,
-                       fmt="ue5m3"):
+                       fmt="ue5m3", block=None):
     """``quantize_1d`` of a float32 matrix (values already widened, or a
     transformed operand)."""
     x = np.asarray(x, dtype=np.float32)
     R, C = x.shape
-    B = block_size(fmt)
+    B = block_size(fmt, block)
     if fmt == "e8m0":
         S, G, dec = np.float32(1.0), np.float32(1.0), np.float32(1.0)
     else:
@@ -184,49 +193,53 @@ def quantize_1d_values(x, axis, g, target=448.0, mode="rn", seed=0, tensor_id=0,
 
 
 def quantize_2d(x_bits, g, target=448.0, mode="rn", seed=0, tensor_id=0, elem_index=None,
-                fmt="ue5m3"):
-    """16x16 tile quantization (UE5M3 or E4M3 scales).  Returns (payload
-    [R, C/2], scales [R/16, C/16], payload_t [C, R/2], dec)."""
+                fmt="ue5m3", tile=16):
+    """tile x tile quantization (UE5M3 or E4M3 scales; 16, or 32 for the
+    block-size control).  Returns (payload [R, C/2], scales [R/tile,
+    C/tile], payload_t [C, R/2], dec)."""
     if fmt not in ("ue5m3", "e4m3"):
         raise ValueError("2D tiles take UE5M3 or E4M3 scales")
+    if tile not in (16, 32):
+        raise ValueError("tile must be 16 or 32")
     x = scaling.bf16_to_f32(x_bits)
     R, C = x.shape
-    if R % 16 or C % 16:
-        raise ValueError("rows and cols must be multiples of 16")
+    B = tile
+    if R % B or C % B:
+        raise ValueError(f"rows and cols must be multiples of {B}")
     S, G, dec = scaling.tensor_multipliers(g, target)
     words = _words_for((R, C), seed, tensor_id, mode, elem_index)
-    tiles = x.reshape(R // 16, 16, C // 16, 16).transpose(0, 2, 1, 3).reshape(-1, 256)
+    tiles = x.reshape(R // B, B, C // B, B).transpose(0, 2, 1, 3).reshape(-1, B * B)
     wt = None
     if words is not None:
-        wt = words.reshape(R // 16, 16, C // 16, 16).transpose(0, 2, 1, 3).reshape(-1, 256)
+        wt = words.reshape(R // B, B, C // B, B).transpose(0, 2, 1, 3).reshape(-1, B * B)
     code, nib = _block_codes(tiles, S, G, mode, wt, fmt)
-    nib = nib.reshape(R // 16, C // 16, 16, 16).transpose(0, 2, 1, 3).reshape(R, C)
-    return (_pack_rows(nib), code.reshape(R // 16, C // 16),
+    nib = nib.reshape(R // B, C // B, B, B).transpose(0, 2, 1, 3).reshape(R, C)
+    return (_pack_rows(nib), code.reshape(R // B, C // B),
             _pack_rows(np.ascontiguousarray(nib.T)), dec)
 
 
 # ------------------------------------------------------ dequantization ----
-def decoded_1d(payload, scales, axis, fmt="ue5m3"):
+def decoded_1d(payload, scales, axis, fmt="ue5m3", block=None):
     """Decoded operand q * s_B (float64, exact) in the logical [R, C] shape
     of the tensor that ``quantize_1d`` consumed."""
     q = formats.e2m1_decode(_unpack_rows(payload))         # [rows_stored, L]
     s = scale_decode(fmt, scales)
-    v = q * np.repeat(s, block_size(fmt), axis=1)
+    v = q * np.repeat(s, block_size(fmt, block), axis=1)
     return v if axis == 1 else np.ascontiguousarray(v.T)
 
 
-def decoded_2d(payload, scales, fmt="ue5m3"):
+def decoded_2d(payload, scales, fmt="ue5m3", tile=16):
     """Decoded weight q * s_tile (float64, exact), logical [R, C]."""
     q = formats.e2m1_decode(_unpack_rows(payload))
     s = scale_decode(fmt, scales)
-    return q * np.repeat(np.repeat(s, 16, axis=0), 16, axis=1)
+    return q * np.repeat(np.repeat(s, tile, axis=0), tile, axis=1)
 
 
-def decoded_2d_t(payload_t, scales, fmt="ue5m3"):
+def decoded_2d_t(payload_t, scales, fmt="ue5m3", tile=16):
     """Decoded weight from the transposed payload, logical [R, C]."""
     q = formats.e2m1_decode(_unpack_rows(payload_t)).T
     s = scale_decode(fmt, scales)
-    return q * np.repeat(np.repeat(s, 16, axis=0), 16, axis=1)
+    return q * np.repeat(np.repeat(s, tile, axis=0), tile, axis=1)
 
 
 def dequantize(decoded, dec):

@@ -282,3 +282,53 @@ def test_e8m0_sr_uses_the_element_words():
     q = formats.e2m1_decode(quantize._unpack_rows(p1)).reshape(32, 2, 32)
     # SR lands on one of the two E2M1 neighbours of y (6 at or above 6)
     assert np.all(np.abs(np.abs(q) - np.minimum(np.abs(y), 6.0)) <= np.where(np.abs(y) < 2, 0.5, 2.0))
+
+
+# ------------------------------------------------ block-size-32 control --
+def _b(vals):
+    return synthetic.f32_to_bf16_bits(np.asarray(vals, np.float32))
+
+
+def test_block32_hand_worked_and_halves():
+    """Block-size control (blocks of 32): the worked block A (g = 100,
+    T = 448, scale 0xBE) followed by a half whose largest magnitude is also
+    100 keeps A's scale and nibbles; the second half (-100, 0, ...) gives
+    -6 -> nibble 0xF.  A half with a larger maximum changes the shared
+    scale."""
+    a = [100, -37.5, 12, 0.25, 0, -0.0, 50, 25, -60, 8.5, 3, -1, 90, 75, 5.25, -16.5]
+    x = _b([a + [-100] + [0] * 15])
+    p, s, _ = quantize.quantize_1d(x, 1, 100.0, 448.0, block=32)
+    assert s.tolist() == [[0xBE]]
+    assert p[0, :8].tobytes() == bytes.fromhex("C7018035 1E8067A1".replace(" ", ""))
+    assert p[0, 8:].tolist() == [0x0F] + [0] * 7
+    x2 = _b([a + [400] + [0] * 15])
+    p2, s2, _ = quantize.quantize_1d(x2, 1, 100.0, 448.0, block=32)
+    assert s2[0, 0] != 0xBE
+
+
+def test_block32_equals_block16_when_halves_share_maxima():
+    """When both 16-element halves of every 32-block have the same maximum,
+    blocks of 32 give the blocks of 16 result (RN and SR, rows and
+    columns), and 32x32 tiles give the 16x16 result when the four sub-tiles
+    share their maximum."""
+    rng = np.random.default_rng(4)
+    v = rng.standard_normal((64, 128)).astype(np.float32)
+    v[:, ::16] = 5.0                                   # every 16-block (rows) peaks at 5
+    v[::16, :] = 5.0                                   # every 16-block (columns) peaks at 5
+    x = _b(v)
+    for axis in (0, 1):
+        for mode in ("rn", "sr"):
+            p16, s16, d16 = quantize.quantize_1d(x, axis, 5.0, 448.0, mode, 3, 7)
+            p32, s32, d32 = quantize.quantize_1d(x, axis, 5.0, 448.0, mode, 3, 7, block=32)
+            assert np.array_equal(p16, p32) and d16 == d32
+            assert np.array_equal(s16[:, ::2], s32) and np.array_equal(s16[:, 1::2], s32)
+    t16 = quantize.quantize_2d(x, 5.0)
+    t32 = quantize.quantize_2d(x, 5.0, tile=32)
+    assert np.array_equal(t16[0], t32[0]) and np.array_equal(t16[2], t32[2])
+    assert np.array_equal(t16[1][::2, ::2], t32[1]) and np.array_equal(t16[1][1::2, 1::2], t32[1])
+    # decoded operands agree too
+    assert np.array_equal(quantize.decoded_2d(t32[0], t32[1], tile=32), quantize.decoded_2d(t16[0], t16[1]))
+    with pytest.raises(ValueError):
+        quantize.quantize_1d(x, 1, 5.0, block=64)
+    with pytest.raises(ValueError):
+        quantize.quantize_2d(_b(np.zeros((48, 64))), 1.0, tile=32)

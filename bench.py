@@ -59,7 +59,8 @@ def parse():
                         "and grid invariance over seeds 41-43, RN and SR gradients")
     p.add_argument("--formats", action="store_true",
                    help="scale-format comparison instead of the headline step: UE5M3 (delayed "
-                        "amax), E4M3 (current amax) and E8M0 (blocks of 32) on the QKV workload "
+                        "amax; blocks of 16 and the block-32 control), E4M3 (current amax) and "
+                        "E8M0 (blocks of 32) on the QKV workload "
                         "X [16384, 4096], W [6144, 4096], dY [16384, 6144]; one JSON line")
     p.add_argument("--copy-ref", type=int, default=0, metavar="BYTES",
                    help="profiling aid: time a plain device copy of BYTES bytes (the reference "
@@ -200,8 +201,10 @@ def formats_bench(args):
     flop = 3 * 2.0 * T * N * K
     rows = np.random.default_rng(0).choice(T, 256, replace=False)
     res = {}
-    for fmt in ["ue5m3", "e4m3", "e8m0"]:
+    for name, fmt, B in [("ue5m3", "ue5m3", 16), ("ue5m3_b32", "ue5m3", 32), ("e4m3", "e4m3", 16),
+                         ("e8m0", "e8m0", 32)]:
         period = 50 if fmt == "ue5m3" else 1
+        kb = {} if fmt == "e8m0" else {"block": B}
         st = {n: ue.AmaxState(period) for n in "xwd"}
         y = torch.empty(T, N, dtype=torch.float32, device=dev)
         dx = torch.empty(T, K, dtype=torch.bfloat16, device=dev)
@@ -214,20 +217,20 @@ def formats_bench(args):
                 ue.amax_sample(st["w"], w, t)
                 ue.amax_sample(st["d"], dy, t)
             a = (lambda n: None) if fmt == "e8m0" else (lambda n: st[n].amax)
-            out["xr"] = ue.quantize_1d(x, 1, a("x"), fmt=fmt)
-            out["xc"] = ue.quantize_1d(x, 0, a("x"), fmt=fmt)
-            out["dr"] = ue.quantize_1d(dy, 1, a("d"), 448.0, "sr", 1000 + t, 1, fmt=fmt)
-            out["dc"] = ue.quantize_1d(dy, 0, a("d"), 448.0, "sr", 1000 + t, 2, fmt=fmt)
+            out["xr"] = ue.quantize_1d(x, 1, a("x"), fmt=fmt, **kb)
+            out["xc"] = ue.quantize_1d(x, 0, a("x"), fmt=fmt, **kb)
+            out["dr"] = ue.quantize_1d(dy, 1, a("d"), 448.0, "sr", 1000 + t, 1, fmt=fmt, **kb)
+            out["dc"] = ue.quantize_1d(dy, 0, a("d"), 448.0, "sr", 1000 + t, 2, fmt=fmt, **kb)
             if fmt == "e8m0":
                 wr = ue.quantize_1d(w, 1, None, fmt=fmt)
                 wc = ue.quantize_1d(w, 0, None, fmt=fmt)
                 out["bf"], out["bd"] = (wr[0], wr[1], wr[2]), (wc[0], wc[1], wc[2])
             else:
-                wq = ue.quantize_2d(w, a("w"), fmt=fmt)
+                wq = ue.quantize_2d(w, a("w"), fmt=fmt, tile=B)
                 out["bf"], out["bd"] = (wq[0], wq[1], wq[3]), (wq[2], wq[4], wq[3])
-            ue.gemm("nt", T, N, K, *out["xr"], *out["bf"], out=y, fmt=fmt)
-            ue.gemm("nn", T, K, N, *out["dr"], *out["bd"], out=dx, fmt=fmt)
-            ue.gemm("tn", N, K, T, *out["dc"], *out["xc"], out=dw, fmt=fmt)
+            ue.gemm("nt", T, N, K, *out["xr"], *out["bf"], out=y, fmt=fmt, **kb)
+            ue.gemm("nn", T, K, N, *out["dr"], *out["bd"], out=dx, fmt=fmt, **kb)
+            ue.gemm("tn", N, K, T, *out["dc"], *out["xc"], out=dw, fmt=fmt, **kb)
 
         for t in range(args.warmup):
             step(t)
@@ -250,11 +253,11 @@ def formats_bench(args):
         wf = synthetic.bf16_bits_to_f32(wl["w"])
         yref = (torch.from_numpy(synthetic.bf16_bits_to_f32(wl["x"][rows])).to(dev) @
                 torch.from_numpy(wf).to(dev).t()).double().cpu().numpy()
-        res[fmt] = {"ms_per_step": round(ms, 4), "gemm_TFLOPs_step": round(flop / ms / 1e9, 1),
-                    "rel_rmse_x": round(rel(xq, xs), 5), "rel_rmse_dy": round(rel(dq, ds), 5),
-                    "rel_rmse_y": round(rel(y[torch.from_numpy(rows).to(dev)].double().cpu().numpy(), yref), 5),
-                    "amax_period": period if fmt != "e8m0" else None,
-                    "blocks": 32 if fmt == "e8m0" else 16}
+        res[name] = {"ms_per_step": round(ms, 4), "gemm_TFLOPs_step": round(flop / ms / 1e9, 1),
+                     "rel_rmse_x": round(rel(xq, xs), 5), "rel_rmse_dy": round(rel(dq, ds), 5),
+                     "rel_rmse_y": round(rel(y[torch.from_numpy(rows).to(dev)].double().cpu().numpy(), yref), 5),
+                     "amax_period": period if fmt != "e8m0" else None,
+                     "blocks": B}
     print(json.dumps({"metric": "scale-format comparison (QKV workload)", "unit": "TFLOP/s",
                       "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "data": "synthetic",
                       "dtype": "fp4-e2m1 operands, fp32 accumulate",

@@ -291,7 +291,9 @@ typedef enum {
 
 /*
  * ue5m3_quantize_1d with a scale format.  Blocks are `block` elements long:
- * 16 for UE5M3 and E4M3, 32 for E8M0 (EINVAL otherwise).  Layouts as in
+ * 16 or 32 for UE5M3 and E4M3 (32 is the block-size control of Sec.
+ * "Recipe comparison" and Table tab:results: the same per-block arithmetic
+ * over 32 elements, one scale code per 32), 32 for E8M0; EINVAL otherwise.  Layouts as in
  * ue5m3_quantize_1d with 16 replaced by `block` (axis 1: cols % block == 0,
  * scales [rows, cols/block]; axis 0: rows % block == 0, cols % 2 == 0,
  * transposed payload [cols, rows/2] and scales [cols, rows/block]).
@@ -304,21 +306,36 @@ ue5m3_status_t ue5m3_quantize_1d_ex(const void* x_bf16, int64_t rows, int64_t co
                                     hipStream_t stream);
 
 /*
- * ue5m3_quantize_2d with a scale format: UE5M3 or E4M3 (block 16); E8M0
+ * ue5m3_quantize_2d with a scale format and tile size: UE5M3 or E4M3 with
+ * square tiles of `tile` = 16 or 32 (32: the block-size control; one scale
+ * code per 32 x 32 tile).  Layouts as in ue5m3_quantize_2d with 16
+ * replaced by `tile` (rows % tile == 0, cols % tile == 0; scales and
+ * scales_t [rows/tile, cols/tile] and [cols/tile, rows/tile]).  E8M0
  * weights are quantized in 1D blocks of 32 along each GEMM's contraction
  * dimension instead (ue5m3_quantize_1d_ex on W, axis 1 for fprop and axis 0
- * for dgrad), so E8M0 here is EINVAL.
+ * for dgrad), so E8M0 here is EINVAL, as is any other tile size.
  */
 ue5m3_status_t ue5m3_quantize_2d_ex(const void* w_bf16, int64_t rows, int64_t cols,
                                     const float* amax_dev, float target,
                                     ue5m3_round_t mode, uint64_t seed, uint32_t tensor_id,
-                                    ue5m3_scale_kind_t scale_kind,
+                                    ue5m3_scale_kind_t scale_kind, int32_t tile,
                                     uint8_t* payload, uint8_t* scales, uint8_t* payload_t,
                                     uint8_t* scales_t, float* dec_out, hipStream_t stream);
 
 /*
- * ue5m3_gemm with a scale format; both operands use it.
- *   UE5M3, E4M3: operands and requirements exactly as for ue5m3_gemm.
+ * ue5m3_gemm with a scale format and block size; both operands use them.
+ *   UE5M3, E4M3, block 16: operands and requirements exactly as for
+ *         ue5m3_gemm.
+ *   UE5M3, E4M3, block 32 (the block-size control): as for block 16 with
+ *         16 replaced by 32 -- A scales [M, K/32] in every layout, B scales
+ *         [N, K/32] for TN or [N/32, K/32] for NT and NN (32 x 32 tiles;
+ *         scales_t of ue5m3_quantize_2d_ex for NN) -- and K % 32 == 0,
+ *         N % 32 == 0 for NT and NN.  The block scales are expanded to one code per
+ *         16 elements (per 16 x 16 tile) in a workspace owned by the
+ *         library (one per stream, grown on demand and kept until the
+ *         process ends; calls on one stream run in order) and the block-16
+ *         kernels run, so the results obey the ue5m3_gemm bound.
+ *   block: 16 or 32 for UE5M3 and E4M3, 32 for E8M0; EINVAL otherwise.
  *   E8M0: every layout takes A as [M, K/2] payload with [M, K/32] scales and
  *         B as [N, K/2] payload with [N, K/32] scales, both blocked along the
  *         contraction:
@@ -335,7 +352,7 @@ ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
                              const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
                              const uint8_t* b, const uint8_t* b_scales, const float* b_dec,
                              void* c, ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind,
-                             hipStream_t stream);
+                             int32_t block, hipStream_t stream);
 
 /*
  * Probe-matched GEMM: the paper's output model of the native FP4 GEMM (Sec.
@@ -352,9 +369,11 @@ ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
  *         binary32 rounding, then RNE to bf16 for UE5M3_OUT_BF16.
  * Results are exact to this definition for every input (no accumulation
  * tolerance).  grid_d: 0 (no snap) or a power of two up to 2^30 (the paper
- * uses 1024), else EINVAL.  scale_kind: UE5M3 or E4M3 (E8M0: EINVAL).
- * Layouts, operand shapes, alignment and the other status codes as
- * ue5m3_gemm_ex.  The K loop runs in one workgroup per output tile in
+ * uses 1024), else EINVAL.  scale_kind: UE5M3 or E4M3 (E8M0: EINVAL);
+ * block 16 or 32 (EINVAL otherwise; a scale code's value is the same in
+ * every 16-element group it covers, so the 64-product groups and the result
+ * are defined as for block 16).  Layouts, operand shapes, alignment, the
+ * block-32 workspace and the other status codes as ue5m3_gemm_ex.  The K loop runs in one workgroup per output tile in
  * ascending k (the toward-zero chain is order dependent), so this call is
  * several times slower than ue5m3_gemm.
  */
@@ -362,7 +381,7 @@ ue5m3_status_t ue5m3_gemm_pm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
                              const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
                              const uint8_t* b, const uint8_t* b_scales, const float* b_dec,
                              void* c, ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind,
-                             int32_t grid_d, hipStream_t stream);
+                             int32_t block, int32_t grid_d, hipStream_t stream);
 
 /* Static description of a status code. */
 const char* ue5m3_status_string(ue5m3_status_t status);

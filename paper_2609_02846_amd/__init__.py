@@ -83,17 +83,17 @@ def load_library(path=LIB_PATH):
     lib.ue5m3_quantize_1d_ex.argtypes = [vp, i64, i64, i32, vp, f32, i32, u64, u32, i32, i32,
                                          vp, vp, vp, vp]
     lib.ue5m3_quantize_1d_ex.restype = i32
-    lib.ue5m3_quantize_2d_ex.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, i32,
+    lib.ue5m3_quantize_2d_ex.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, i32, i32,
                                          vp, vp, vp, vp, vp, vp]
     lib.ue5m3_quantize_2d_ex.restype = i32
-    lib.ue5m3_gemm_ex.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp]
+    lib.ue5m3_gemm_ex.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp]
     lib.ue5m3_gemm_ex.restype = i32
     lib.ue5m3_amax_sample_rht.argtypes = [ctypes.POINTER(AmaxStateC), vp, i64, i64, u32, i64,
                                           ctypes.POINTER(ctypes.c_int32), vp]
     lib.ue5m3_amax_sample_rht.restype = i32
     lib.ue5m3_quantize_cols_rht.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, u32, vp, vp, vp, vp]
     lib.ue5m3_quantize_cols_rht.restype = i32
-    lib.ue5m3_gemm_pm.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp]
+    lib.ue5m3_gemm_pm.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp]
     lib.ue5m3_gemm_pm.restype = i32
     lib.ue5m3_quantize_dual.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, u32, i32,
                                         vp, vp, vp, vp, vp, vp]
@@ -252,13 +252,14 @@ def quantize_cols_rht(x, amax_dev, sign_mask, target=448.0, mode="rn", seed=0, t
 
 
 def quantize_1d(x, axis, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0,
-                payload=None, scales=None, dec_out=None, stream=None, fmt="ue5m3"):
+                payload=None, scales=None, dec_out=None, stream=None, fmt="ue5m3", block=None):
     """1D block quantization (see ue5m3_quantize_1d and, for ``fmt`` "e4m3"
-    or "e8m0", ue5m3_quantize_1d_ex).  Returns (payload, scales, dec_out);
-    axis 0 outputs are stored transposed.  E8M0 takes no amax (None)."""
+    or "e8m0" or ``block`` 32, ue5m3_quantize_1d_ex).  Returns (payload,
+    scales, dec_out); axis 0 outputs are stored transposed.  E8M0 takes no
+    amax (None)."""
     _bf16_2d(x, "x")
     R, C = x.shape
-    B = BLOCK[fmt]
+    B = BLOCK[fmt] if block is None else int(block)
     if axis == 1:
         pshape, sshape = (R, C // 2), (R, C // B)
     elif axis == 0:
@@ -275,7 +276,7 @@ def quantize_1d(x, axis, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0,
     lib = load_library()
     common = (_ptr(x), R, C, int(axis), _ptr(amax_dev), float(target), _MODES[mode],
               int(seed) & (2**64 - 1), int(tensor_id) & 0xFFFFFFFF)
-    if fmt == "ue5m3":
+    if fmt == "ue5m3" and B == 16:
         st = lib.ue5m3_quantize_1d(*common, _ptr(payload), _ptr(scales), _ptr(dec_out), _stream(stream))
     else:
         st = lib.ue5m3_quantize_1d_ex(*common, _FORMATS[fmt], B, _ptr(payload), _ptr(scales),
@@ -310,23 +311,24 @@ def quantize_dual(x, amax_dev, target=448.0, mode="rn", seed=0, tensor_id_r=0, t
 
 def quantize_2d(w, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0, transposed=True,
                 payload=None, scales=None, payload_t=None, dec_out=None, scales_t=None,
-                stream=None, fmt="ue5m3"):
-    """16x16 tile quantization (see ue5m3_quantize_2d; ``fmt`` "e4m3" uses
-    ue5m3_quantize_2d_ex).  Returns (payload, scales, payload_t or None,
-    dec_out, scales_t or None); the transposed payload and scales are the
-    dgrad operand."""
+                stream=None, fmt="ue5m3", tile=16):
+    """Square-tile quantization, tiles of 16 x 16 (see ue5m3_quantize_2d) or,
+    with ``tile`` 32 or ``fmt`` "e4m3", ue5m3_quantize_2d_ex.  Returns
+    (payload, scales, payload_t or None, dec_out, scales_t or None); the
+    transposed payload and scales are the dgrad operand."""
     _bf16_2d(w, "w")
     R, C = w.shape
+    T = int(tile)
     payload = _u8((R, C // 2), w) if payload is None else _u8_out(payload, (R, C // 2), "payload")
-    scales = _u8((R // 16, C // 16), w) if scales is None else _u8_out(scales, (R // 16, C // 16), "scales")
+    scales = _u8((R // T, C // T), w) if scales is None else _u8_out(scales, (R // T, C // T), "scales")
     if transposed and payload_t is None:
         payload_t = _u8((C, R // 2), w)
     if transposed and scales_t is None:
-        scales_t = _u8((C // 16, R // 16), w)
+        scales_t = _u8((C // T, R // T), w)
     if payload_t is not None:
         _u8_out(payload_t, (C, R // 2), "payload_t")
     if scales_t is not None:
-        _u8_out(scales_t, (C // 16, R // 16), "scales_t")
+        _u8_out(scales_t, (C // T, R // T), "scales_t")
     if dec_out is None:
         dec_out = torch.empty(1, dtype=torch.float32, device=w.device)
     _f32_out(dec_out, "dec_out")
@@ -335,15 +337,15 @@ def quantize_2d(w, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0, trans
     common = (_ptr(w), R, C, _ptr(amax_dev), float(target), _MODES[mode], int(seed) & (2**64 - 1),
               int(tensor_id) & 0xFFFFFFFF)
     outs = (_ptr(payload), _ptr(scales), _ptr(payload_t), _ptr(scales_t), _ptr(dec_out), _stream(stream))
-    if fmt == "ue5m3":
+    if fmt == "ue5m3" and T == 16:
         st = lib.ue5m3_quantize_2d(*common, *outs)
     else:
-        st = lib.ue5m3_quantize_2d_ex(*common, _FORMATS[fmt], *outs)
+        st = lib.ue5m3_quantize_2d_ex(*common, _FORMATS[fmt], T, *outs)
     _check(st, "ue5m3_quantize_2d")
     return payload, scales, payload_t, dec_out, scales_t
 
 
-def _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt):
+def _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt, Bk):
     lay = _LAYOUTS[layout] if isinstance(layout, str) else int(layout)
     if out is None:
         out = torch.empty((M, N), dtype=out_dtype, device=a.device)
@@ -352,12 +354,11 @@ def _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out
         raise ValueError("out must be a contiguous fp32 or bf16 tensor")
     _dev_buf(out, out.dtype, int(M) * int(N), "out")
     if M > 0 and N > 0 and K > 0:
-        Bk = BLOCK[fmt]
         tiled = fmt != "e8m0" and lay in (NT, NN)
         _u8_out(a, (M, K // 2), "a")
         _u8_out(a_scales, (M, K // Bk), "a_scales")
         _u8_out(b, (N, K // 2), "b")
-        _u8_out(b_scales, ((N + 15) // 16, K // 16) if tiled else (N, K // Bk), "b_scales")
+        _u8_out(b_scales, ((N + Bk - 1) // Bk, K // Bk) if tiled else (N, K // Bk), "b_scales")
     if M > 0 and N > 0:
         _f32_out(a_dec, "a_dec")
         _f32_out(b_dec, "b_dec")
@@ -367,27 +368,30 @@ def _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out
 
 
 def gemm_pm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
-            out_dtype=torch.float32, grid=1024, stream=None, fmt="ue5m3"):
+            out_dtype=torch.float32, grid=1024, stream=None, fmt="ue5m3", block=16):
     """Probe-matched GEMM (see ue5m3_gemm_pm): 64-product RNE partials,
     toward-zero cross-group adds, snap of the encoded accumulator to the
     1/``grid`` lattice (0: none), then alpha.  Operands as ``gemm``."""
     if fmt not in ("ue5m3", "e4m3"):
         raise ValueError("the probe-matched GEMM takes UE5M3 or E4M3 scales")
-    out, args = _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt)
-    _check(load_library().ue5m3_gemm_pm(*args, _FORMATS[fmt], int(grid), _stream(stream)), "ue5m3_gemm_pm")
+    out, args = _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt,
+                           int(block))
+    _check(load_library().ue5m3_gemm_pm(*args, _FORMATS[fmt], int(block), int(grid), _stream(stream)),
+           "ue5m3_gemm_pm")
     return out
 
 
 def gemm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
-         out_dtype=torch.float32, stream=None, fmt="ue5m3"):
+         out_dtype=torch.float32, stream=None, fmt="ue5m3", block=None):
     """Decoded-operand FP4 GEMM (see ue5m3_gemm and, for ``fmt`` "e4m3" or
-    "e8m0", ue5m3_gemm_ex); layout is "nt" (fprop), "nn" (dgrad) or "tn"
-    (wgrad).  Returns the [M, N] output tensor."""
-    out, args = _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt)
+    "e8m0" or ``block`` 32, ue5m3_gemm_ex); layout is "nt" (fprop), "nn"
+    (dgrad) or "tn" (wgrad).  Returns the [M, N] output tensor."""
+    Bk = BLOCK[fmt] if block is None else int(block)
+    out, args = _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt, Bk)
     lib = load_library()
-    if fmt == "ue5m3":
+    if fmt == "ue5m3" and Bk == 16:
         st = lib.ue5m3_gemm(*args, _stream(stream))
     else:
-        st = lib.ue5m3_gemm_ex(*args, _FORMATS[fmt], _stream(stream))
+        st = lib.ue5m3_gemm_ex(*args, _FORMATS[fmt], Bk, _stream(stream))
     _check(st, "ue5m3_gemm")
     return out

@@ -96,7 +96,7 @@ ue5m3_status_t ue5m3_quantize_1d_ex(const void* x_bf16, int64_t rows, int64_t co
         scale_kind != UE5M3_SCALE_E8M0)
         return UE5M3_EINVAL;
     const bool e8 = scale_kind == UE5M3_SCALE_E8M0;
-    if (block != (e8 ? 32 : 16)) return UE5M3_EINVAL;
+    if (e8 ? block != 32 : (block != 16 && block != 32)) return UE5M3_EINVAL;
     if (!e8 && (amax_dev == nullptr || !valid_target(target))) return UE5M3_EINVAL;
     if (rows < 0 || cols < 0) return UE5M3_ESHAPE;
     if (axis == 1 && cols % block != 0) return UE5M3_ESHAPE;
@@ -110,10 +110,10 @@ ue5m3_status_t ue5m3_quantize_1d_ex(const void* x_bf16, int64_t rows, int64_t co
     const ue5m3::ScaleKind fmt = static_cast<ue5m3::ScaleKind>(scale_kind);
     hipError_t e;
     if (axis == 1)
-        e = ue5m3::launch_quant_rows(fmt, x_bf16, rows, cols, amax_dev, target, sr, seed, tensor_id,
+        e = ue5m3::launch_quant_rows(fmt, block, x_bf16, rows, cols, amax_dev, target, sr, seed, tensor_id,
                                      payload, scales, dec_out, stream);
     else
-        e = ue5m3::launch_quant_cols(fmt, x_bf16, rows, cols, amax_dev, target, sr, seed, tensor_id,
+        e = ue5m3::launch_quant_cols(fmt, block, x_bf16, rows, cols, amax_dev, target, sr, seed, tensor_id,
                                      payload, scales, dec_out, stream);
     return hip_status(e);
 }
@@ -166,12 +166,13 @@ ue5m3_status_t ue5m3_quantize_1d(const void* x_bf16, int64_t rows, int64_t cols,
 ue5m3_status_t ue5m3_quantize_2d_ex(const void* w_bf16, int64_t rows, int64_t cols,
                                     const float* amax_dev, float target, ue5m3_round_t mode,
                                     uint64_t seed, uint32_t tensor_id, ue5m3_scale_kind_t scale_kind,
-                                    uint8_t* payload, uint8_t* scales, uint8_t* payload_t,
+                                    int32_t block, uint8_t* payload, uint8_t* scales, uint8_t* payload_t,
                                     uint8_t* scales_t, float* dec_out, hipStream_t stream) {
     if (mode != UE5M3_RN && mode != UE5M3_SR) return UE5M3_EINVAL;
     if (scale_kind != UE5M3_SCALE_UE5M3 && scale_kind != UE5M3_SCALE_E4M3) return UE5M3_EINVAL;
+    if (block != 16 && block != 32) return UE5M3_EINVAL;
     if (amax_dev == nullptr || !valid_target(target)) return UE5M3_EINVAL;
-    if (rows < 0 || cols < 0 || rows % 16 != 0 || cols % 16 != 0) return UE5M3_ESHAPE;
+    if (rows < 0 || cols < 0 || rows % block != 0 || cols % block != 0) return UE5M3_ESHAPE;
     if (!aligned4(amax_dev) || (dec_out != nullptr && !aligned4(dec_out))) return UE5M3_EALIGN;
     if (rows == 0 || cols == 0) return UE5M3_OK;
     if (w_bf16 == nullptr || payload == nullptr || scales == nullptr) return UE5M3_EINVAL;
@@ -179,7 +180,7 @@ ue5m3_status_t ue5m3_quantize_2d_ex(const void* w_bf16, int64_t rows, int64_t co
         (payload_t != nullptr && !aligned16(payload_t)) ||
         (scales_t != nullptr && !aligned16(scales_t)))
         return UE5M3_EALIGN;
-    return hip_status(ue5m3::launch_quant_tiles(static_cast<ue5m3::ScaleKind>(scale_kind), w_bf16, rows,
+    return hip_status(ue5m3::launch_quant_tiles(static_cast<ue5m3::ScaleKind>(scale_kind), block, w_bf16, rows,
                                                 cols, amax_dev, target, mode == UE5M3_SR, seed,
                                                 tensor_id, payload, scales, payload_t, scales_t,
                                                 dec_out, stream));
@@ -191,7 +192,7 @@ ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
                                  uint8_t* scales, uint8_t* payload_t, uint8_t* scales_t,
                                  float* dec_out, hipStream_t stream) {
     return ue5m3_quantize_2d_ex(w_bf16, rows, cols, amax_dev, target, mode, seed, tensor_id,
-                                UE5M3_SCALE_UE5M3, payload, scales, payload_t, scales_t, dec_out,
+                                UE5M3_SCALE_UE5M3, 16, payload, scales, payload_t, scales_t, dec_out,
                                 stream);
 }
 
@@ -222,7 +223,8 @@ ue5m3_status_t ue5m3_quantize_dual(const void* x_bf16, int64_t rows, int64_t col
 ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
                              const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
                              const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,
-                             ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind, hipStream_t stream) {
+                             ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind, int32_t block,
+                             hipStream_t stream) {
     ue5m3::BScale bmode;
     switch (layout) {
         case UE5M3_NT: bmode = ue5m3::BScale::Tile; break;
@@ -234,9 +236,10 @@ ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
         scale_kind != UE5M3_SCALE_E8M0)
         return UE5M3_EINVAL;
     const bool e8 = scale_kind == UE5M3_SCALE_E8M0;
+    if (e8 ? block != 32 : (block != 16 && block != 32)) return UE5M3_EINVAL;
     if (c_type != UE5M3_OUT_F32 && c_type != UE5M3_OUT_BF16) return UE5M3_EINVAL;
-    if (M < 0 || N < 0 || K < 0 || K % 16 != 0) return UE5M3_ESHAPE;
-    if (!e8 && layout != UE5M3_TN && N % 16 != 0) return UE5M3_ESHAPE;
+    if (M < 0 || N < 0 || K < 0 || K % block != 0) return UE5M3_ESHAPE;
+    if (!e8 && layout != UE5M3_TN && N % block != 0) return UE5M3_ESHAPE;
     if (e8) {
         const int64_t lim = (int64_t)1 << 31;
         if (K % 256 != 0 || M * (K / 2) >= lim || N * (K / 2) >= lim || 4 * M * N >= lim)
@@ -260,6 +263,9 @@ ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
     // UE5M3 codes decode with the operands scaled by 2^-3 (alpha * 2^6); E4M3
     // codes read as UE5M3 are value / 2^8, so alpha * 2^22.
     const float amul = scale_kind == UE5M3_SCALE_E4M3 ? 4194304.0f : 64.0f;
+    if (block == 32)
+        return hip_status(ue5m3::launch_gemm_b32(bmode, amul, false, 0.0f, M, N, K, a, a_scales, a_dec, b,
+                                                 b_scales, b_dec, c, bf, stream));
     return hip_status(ue5m3::launch_gemm(bmode, amul, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c,
                                          bf, stream));
 }
@@ -267,8 +273,8 @@ ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
 ue5m3_status_t ue5m3_gemm_pm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
                              const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
                              const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,
-                             ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind, int32_t grid_d,
-                             hipStream_t stream) {
+                             ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind, int32_t block,
+                             int32_t grid_d, hipStream_t stream) {
     ue5m3::BScale bmode;
     switch (layout) {
         case UE5M3_NT: bmode = ue5m3::BScale::Tile; break;
@@ -279,8 +285,9 @@ ue5m3_status_t ue5m3_gemm_pm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
     if (scale_kind != UE5M3_SCALE_UE5M3 && scale_kind != UE5M3_SCALE_E4M3) return UE5M3_EINVAL;
     if (c_type != UE5M3_OUT_F32 && c_type != UE5M3_OUT_BF16) return UE5M3_EINVAL;
     if (grid_d < 0 || grid_d > (1 << 30) || (grid_d & (grid_d - 1)) != 0) return UE5M3_EINVAL;
-    if (M < 0 || N < 0 || K < 0 || K % 16 != 0) return UE5M3_ESHAPE;
-    if (layout != UE5M3_TN && N % 16 != 0) return UE5M3_ESHAPE;
+    if (block != 16 && block != 32) return UE5M3_EINVAL;
+    if (M < 0 || N < 0 || K < 0 || K % block != 0) return UE5M3_ESHAPE;
+    if (layout != UE5M3_TN && N % block != 0) return UE5M3_ESHAPE;
     if (M == 0 || N == 0) return UE5M3_OK;
     if (c == nullptr || a_dec == nullptr || b_dec == nullptr) return UE5M3_EINVAL;
     if (K > 0 && (a == nullptr || a_scales == nullptr || b == nullptr || b_scales == nullptr))
@@ -289,8 +296,12 @@ ue5m3_status_t ue5m3_gemm_pm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
     if (K > 0 && (!aligned16(a) || !aligned16(b) || !aligned16(a_scales) || !aligned16(b_scales)))
         return UE5M3_EALIGN;
     const float amul = scale_kind == UE5M3_SCALE_E4M3 ? 4194304.0f : 64.0f;
+    const bool bf = c_type == UE5M3_OUT_BF16;
+    if (block == 32)
+        return hip_status(ue5m3::launch_gemm_b32(bmode, amul, true, (float)grid_d, M, N, K, a, a_scales, a_dec,
+                                                 b, b_scales, b_dec, c, bf, stream));
     return hip_status(ue5m3::launch_gemm_pm(bmode, amul, (float)grid_d, M, N, K, a, a_scales, a_dec, b,
-                                            b_scales, b_dec, c, c_type == UE5M3_OUT_BF16, stream));
+                                            b_scales, b_dec, c, bf, stream));
 }
 
 ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
@@ -298,7 +309,7 @@ ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K
                           const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,
                           ue5m3_out_t c_type, hipStream_t stream) {
     return ue5m3_gemm_ex(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_type,
-                         UE5M3_SCALE_UE5M3, stream);
+                         UE5M3_SCALE_UE5M3, 16, stream);
 }
 
 }  // extern "C"

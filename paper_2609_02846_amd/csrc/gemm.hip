@@ -1402,40 +1402,74 @@ __global__ __launch_bounds__(256) void gemm_split_sum_kernel(
 // Per-device, per-stream workspace for the fp32 partials of split tiles,
 // grown on demand.  Launches on one stream are ordered, so one workspace per
 // (device, stream) suffices.
-struct SplitWorkspace {
+// Library workspaces, one per (kind, device, stream), grown on demand and
+// kept until the process ends.  Kind 0: split-tile partials; kind 1:
+// block-32 scales expanded to the block-16 layout.  Uses on one stream are
+// ordered by the stream, so a buffer can be reused by the next call.
+struct StreamWorkspace {
     int dev = -1;
     hipStream_t stream = nullptr;
-    float* part = nullptr;
-    size_t part_floats = 0;
+    void* ptr = nullptr;
+    size_t bytes = 0;
 };
 
-hipError_t split_workspace(hipStream_t s, size_t part_floats, float** part) {
+hipError_t stream_workspace(int kind, hipStream_t s, size_t bytes, void** out) {
     static std::mutex mu;
-    static SplitWorkspace ws[64];
+    static StreamWorkspace ws[2][64];
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     std::lock_guard<std::mutex> lock(mu);
-    SplitWorkspace* slot = nullptr;
-    for (auto& x : ws)
+    StreamWorkspace* slot = nullptr;
+    for (auto& x : ws[kind])
         if (x.dev == dev && x.stream == s) { slot = &x; break; }
     if (slot == nullptr)
-        for (auto& x : ws)
+        for (auto& x : ws[kind])
             if (x.dev < 0) { slot = &x; slot->dev = dev; slot->stream = s; break; }
     if (slot == nullptr) return hipErrorOutOfMemory;       // more than 64 (device, stream) pairs
-    if (slot->part_floats < part_floats) {
-        if (slot->part) {
+    if (slot->bytes < bytes) {
+        if (slot->ptr) {
             // a launch still queued on this stream may use the old buffer
             if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
-            (void)hipFree(slot->part);
+            (void)hipFree(slot->ptr);
         }
-        slot->part = nullptr;
-        slot->part_floats = 0;
-        if ((e = hipMalloc(&slot->part, part_floats * sizeof(float))) != hipSuccess) return e;
-        slot->part_floats = part_floats;
+        slot->ptr = nullptr;
+        slot->bytes = 0;
+        if ((e = hipMalloc(&slot->ptr, bytes)) != hipSuccess) return e;
+        slot->bytes = bytes;
     }
-    *part = slot->part;
+    *out = slot->ptr;
     return hipSuccess;
+}
+
+hipError_t split_workspace(hipStream_t s, size_t part_floats, float** part) {
+    void* p = nullptr;
+    const hipError_t e = stream_workspace(0, s, part_floats * sizeof(float), &p);
+    *part = static_cast<float*>(p);
+    return e;
+}
+
+// Block-32 scale codes to the block-16 layout the decode kernels read:
+// out[r][j] = in[r / rrep][j / 2] (rrep 2 for 32 x 32 tile scales, whose
+// tile rows cover two 16-row tile rows).
+__global__ __launch_bounds__(256) void expand_scales_kernel(const uint8_t* __restrict__ in, int64_t cols_in,
+                                                            int rrep, uint8_t* __restrict__ out,
+                                                            int64_t rows_out, int64_t cols_out) {
+    const int64_t n = rows_out * cols_out;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+        const int64_t r = i / cols_out, j = i - r * cols_out;
+        out[i] = in[(r / rrep) * cols_in + j / 2];
+    }
+}
+
+hipError_t expand_scales(const uint8_t* in, int64_t cols_in, int rrep, uint8_t* out, int64_t rows_out,
+                         int64_t cols_out, hipStream_t s) {
+    const int64_t n = rows_out * cols_out;
+    if (n <= 0) return hipSuccess;
+    const int64_t blocks = min((n + 255) / 256, (int64_t)4096);
+    hipLaunchKernelGGL(expand_scales_kernel, dim3((unsigned)blocks), dim3(256), 0, s, in, cols_in, rrep, out,
+                       rows_out, cols_out);
+    return hipGetLastError();
 }
 
 constexpr int kSplitRemDiv = 2;
@@ -1565,6 +1599,31 @@ hipError_t launch_gemm(BScale bmode, float amul, int64_t M, int64_t N, int64_t K
             return launch_mode<(int)BScale::TileDgrad>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, amul, s);
     }
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_b32(BScale bmode, float amul, bool pm, float grid_d, int64_t M, int64_t N, int64_t K,
+                           const uint8_t* a, const uint8_t* a_scales, const float* a_dec, const uint8_t* b,
+                           const uint8_t* b_scales, const float* b_dec, void* c, bool c_bf16, hipStream_t s) {
+    const uint8_t* as16 = a_scales;
+    const uint8_t* bs16 = b_scales;
+    if (M > 0 && N > 0 && K > 0) {
+        const bool tiled = bmode != BScale::Row;
+        const int64_t kb16 = K / 16, kb32 = K / 32;
+        const int64_t brows16 = tiled ? N / 16 : N;
+        const size_t abytes = (size_t)((M * kb16 + 255) / 256 * 256);
+        const size_t bbytes = (size_t)(brows16 * kb16);
+        void* ws = nullptr;
+        hipError_t e = stream_workspace(1, s, abytes + bbytes, &ws);
+        if (e != hipSuccess) return e;
+        uint8_t* wa = static_cast<uint8_t*>(ws);
+        uint8_t* wb = wa + abytes;
+        if ((e = expand_scales(a_scales, kb32, 1, wa, M, kb16, s)) != hipSuccess) return e;
+        if ((e = expand_scales(b_scales, kb32, tiled ? 2 : 1, wb, brows16, kb16, s)) != hipSuccess) return e;
+        as16 = wa;
+        bs16 = wb;
+    }
+    return pm ? launch_gemm_pm(bmode, amul, grid_d, M, N, K, a, as16, a_dec, b, bs16, b_dec, c, c_bf16, s)
+              : launch_gemm(bmode, amul, M, N, K, a, as16, a_dec, b, bs16, b_dec, c, c_bf16, s);
 }
 
 hipError_t launch_gemm_mx(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* a_scales,

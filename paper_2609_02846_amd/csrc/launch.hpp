@@ -34,17 +34,19 @@ hipError_t launch_quant_cols_rht(const void* x_bf16, int64_t rows, int64_t cols,
                                  uint32_t sign_mask, uint8_t* payload_t, uint8_t* scales_t,
                                  float* dec_out, hipStream_t s);
 
-hipError_t launch_quant_rows(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
+// block: 16, or 32 (E8M0 always; UE5M3 / E4M3 for the block-size control).
+hipError_t launch_quant_rows(ScaleKind fmt, int block, const void* x_bf16, int64_t rows, int64_t cols,
                              const float* amax_dev, float target, bool sr, uint64_t seed,
                              uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
                              float* dec_out, hipStream_t s);
 
-hipError_t launch_quant_cols(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
+hipError_t launch_quant_cols(ScaleKind fmt, int block, const void* x_bf16, int64_t rows, int64_t cols,
                              const float* amax_dev, float target, bool sr, uint64_t seed,
                              uint32_t tensor_id, uint8_t* payload_t, uint8_t* scales_t,
                              float* dec_out, hipStream_t s);
 
-hipError_t launch_quant_tiles(ScaleKind fmt, const void* w_bf16, int64_t rows, int64_t cols,
+// tile: 16 or 32 (the block-size control).
+hipError_t launch_quant_tiles(ScaleKind fmt, int tile, const void* w_bf16, int64_t rows, int64_t cols,
                               const float* amax_dev, float target, bool sr, uint64_t seed,
                               uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
                               uint8_t* payload_t, uint8_t* scales_t, float* dec_out,
@@ -70,6 +72,14 @@ hipError_t launch_gemm(BScale bmode, float amul, int64_t M, int64_t N, int64_t K
 hipError_t launch_gemm_pm(BScale bmode, float amul, float grid_d, int64_t M, int64_t N, int64_t K,
                           const uint8_t* a, const uint8_t* a_scales, const float* a_dec, const uint8_t* b,
                           const uint8_t* b_scales, const float* b_dec, void* c, bool c_bf16, hipStream_t s);
+
+// UE5M3 / E4M3 blocks of 32 (the block-size control): A scales [M, K/32],
+// B scales [N, K/32] (Row) or 32 x 32 tile scales [N/32, K/32]; expanded to
+// the block-16 layout in a library workspace (one per device and stream),
+// then launch_gemm (pm false) or launch_gemm_pm (pm true, grid_d).
+hipError_t launch_gemm_b32(BScale bmode, float amul, bool pm, float grid_d, int64_t M, int64_t N, int64_t K,
+                           const uint8_t* a, const uint8_t* a_scales, const float* a_dec, const uint8_t* b,
+                           const uint8_t* b_scales, const float* b_dec, void* c, bool c_bf16, hipStream_t s);
 
 // E8M0 blocks of 32 on the gfx950 scaled FP4 matrix instructions: A [M, K]
 // and B [N, K] rows, one E8M0 byte per 32 k of each row.

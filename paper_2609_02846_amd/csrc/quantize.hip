@@ -226,17 +226,20 @@ __device__ __forceinline__ void words4(uint64_t e0, uint32_t tid, uint32_t k0, u
 }
 
 // ------------------------------------------------------------ rows (1D) --
-// The flat tensor is a sequence of blocks of 16 (32 for E8M0) elements.  One
+// The flat tensor is a sequence of blocks of 16 (32: E8M0, block-size-32
+// control) elements.  One
 // lane per block: two (four) 16-byte loads, 8 (16) bytes of payload and 1
 // byte of scale, so one wave instruction stores 512 (1024) contiguous payload
 // bytes and 64 scale bytes.  Persistent grid: a lane walks blocks b,
 // b + stride, ..., loading the next block before quantizing the current one.
-template <bool SR, int FMT>
+// H: 16-element halves per block (2 for E8M0 and for the block-size-32
+// control of UE5M3 / E4M3).
+template <bool SR, int FMT, int H>
 __global__ __launch_bounds__(kThreads) void quant_rows_kernel(
     const uint4* __restrict__ x, int64_t nblocks, const float* __restrict__ amax_dev, float T,
     uint32_t key0, uint32_t key1, uint32_t tid, uint2* __restrict__ payload,
     uint8_t* __restrict__ scales, float* __restrict__ dec_out) {
-    constexpr int H = FMT == (int)ScaleKind::E8M0 ? 2 : 1;    // 16-element halves per block
+    static_assert(FMT != (int)ScaleKind::E8M0 || H == 2, "E8M0 blocks are 32");
     const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
@@ -370,18 +373,18 @@ __device__ __forceinline__ void sr_cols16x4(const uint32_t (&lo)[16], const uint
 // RHT: every 16-row block of each column is first replaced by its 16-point
 // randomized Hadamard transform (rht16, sign mask rht_mask) and quantized as
 // binary32 values (UE5M3 / E4M3 only).
-template <bool SR, int FMT, bool RHT = false>
+template <bool SR, int FMT, bool RHT, int H>
 __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
     const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t rows_per_item, int64_t gx,
     int64_t nitems, const float* __restrict__ amax_dev, float T, uint32_t key0, uint32_t key1,
     uint32_t tid, uint8_t* __restrict__ payload_t, uint8_t* __restrict__ scales_t,
     float* __restrict__ dec_out, uint32_t rht_mask) {
-    static_assert(!RHT || FMT != (int)ScaleKind::E8M0, "no transformed E8M0 operands");
+    static_assert(!RHT || (FMT != (int)ScaleKind::E8M0 && H == 1), "transformed blocks are 16 rows");
+    static_assert(FMT != (int)ScaleKind::E8M0 || H == 2, "E8M0 blocks are 32");
     __shared__ __attribute__((aligned(16))) uint8_t stP[kColCols][kColGroupRB * 8];
     __shared__ __attribute__((aligned(16))) uint8_t stS[kColCols][kColGroupRB * kColScaleGroups];
-    // E8M0 blocks are 32 rows: the two 16-row blocks of a wave (lanes l and
+    // Blocks of 32 rows (H = 2): the two 16-row blocks of a wave (lanes l and
     // l + 32) form one block and share its maximum and scale byte.
-    constexpr int H = FMT == (int)ScaleKind::E8M0 ? 2 : 1;
     const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
     const int t = threadIdx.x;
@@ -571,7 +574,10 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
 constexpr int kTileCols = 128;
 constexpr int kTileRowTiles = 8;
 
-template <bool SR, int FMT>
+// TB: tile edge, 16 (the recipe) or 32 (the block-size control: a 32 x 32
+// tile spans the 8 lanes of 32 columns and the lane pair l, l + 32 of two
+// 16-row tile rows, all in one wave).
+template <bool SR, int FMT, int TB = 16>
 __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
     const uint16_t* __restrict__ w, int64_t rows, int64_t cols, const float* __restrict__ amax_dev,
     float T, uint32_t key0, uint32_t key1, uint32_t tid, uint8_t* __restrict__ payload,
@@ -602,6 +608,10 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
         for (int r = 0; r < 16; ++r) mx = max(mx, max(bf16_abs_max_pair(lo[r]), bf16_abs_max_pair(hi[r])));
         mx = max(mx, (uint32_t)__shfl_xor((int)mx, 1));
         mx = max(mx, (uint32_t)__shfl_xor((int)mx, 2));
+        if (TB == 32) {
+            mx = max(mx, (uint32_t)__shfl_xor((int)mx, 4));
+            mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32));
+        }
         const BlockScale bs = block_scale<FMT>(mx, m);
         uint32_t colpk[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
         if (SR) {
@@ -651,9 +661,13 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
                 }
             }
         }
-        if ((q & 3) == 0) {
+        if (TB == 16 && (q & 3) == 0) {
             scales[tr * ntc + c / 16] = (uint8_t)bs.code;
             if (scales_t != nullptr) scales_t[(c / 16) * ntr + tr] = (uint8_t)bs.code;
+        }
+        if (TB == 32 && (q & 7) == 0 && (trl & 1) == 0) {
+            scales[(tr / 2) * (ntc / 2) + c / 32] = (uint8_t)bs.code;
+            if (scales_t != nullptr) scales_t[(c / 32) * (ntr / 2) + tr / 2] = (uint8_t)bs.code;
         }
         if (payload_t != nullptr) {
 #pragma unroll
@@ -852,11 +866,11 @@ inline void seed_key(uint64_t seed, uint32_t& k0, uint32_t& k1) {
 // Resident workgroups to aim for: 8 per CU on the 256 CUs of an MI355X.
 constexpr int64_t kPersistentWGs = 256 * 8;
 
-template <int FMT>
+template <int FMT, int H>
 hipError_t launch_rows_fmt(const void* x_bf16, int64_t rows, int64_t cols, const float* amax_dev,
                            float target, bool sr, uint64_t seed, uint32_t tensor_id,
                            uint8_t* payload, uint8_t* scales, float* dec_out, hipStream_t s) {
-    constexpr int64_t BE = FMT == (int)ScaleKind::E8M0 ? 32 : 16;
+    constexpr int64_t BE = 16 * H;
     const int64_t nblocks = rows * cols / BE;
     uint32_t k0, k1;
     seed_key(seed, k0, k1);
@@ -866,10 +880,10 @@ hipError_t launch_rows_fmt(const void* x_bf16, int64_t rows, int64_t cols, const
     const uint4* x = reinterpret_cast<const uint4*>(x_bf16);
     uint2* p = reinterpret_cast<uint2*>(payload);
     if (sr)
-        hipLaunchKernelGGL((quant_rows_kernel<true, FMT>), dim3((unsigned)wgs), dim3(kThreads), 0, s, x,
+        hipLaunchKernelGGL((quant_rows_kernel<true, FMT, H>), dim3((unsigned)wgs), dim3(kThreads), 0, s, x,
                            nblocks, amax_dev, target, k0, k1, tensor_id, p, scales, dec_out);
     else
-        hipLaunchKernelGGL((quant_rows_kernel<false, FMT>), dim3((unsigned)wgs), dim3(kThreads), 0, s, x,
+        hipLaunchKernelGGL((quant_rows_kernel<false, FMT, H>), dim3((unsigned)wgs), dim3(kThreads), 0, s, x,
                            nblocks, amax_dev, target, k0, k1, tensor_id, p, scales, dec_out);
     return hipGetLastError();
 }
@@ -877,7 +891,7 @@ hipError_t launch_rows_fmt(const void* x_bf16, int64_t rows, int64_t cols, const
 // Resident workgroups of a kernel on the current device (cached per device).
 template <typename K>
 int64_t resident_wgs(K kernel, int slot) {
-    static int64_t cache[16][8] = {};
+    static int64_t cache[16][16] = {};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return kPersistentWGs;
     if (cache[dev][slot] == 0) {
@@ -892,7 +906,7 @@ int64_t resident_wgs(K kernel, int slot) {
     return cache[dev][slot];
 }
 
-template <int FMT, bool RHT = false>
+template <int FMT, int H, bool RHT = false>
 hipError_t launch_cols_fmt(const void* x_bf16, int64_t rows, int64_t cols, const float* amax_dev,
                            float target, bool sr, uint64_t seed, uint32_t tensor_id,
                            uint8_t* payload_t, uint8_t* scales_t, float* dec_out, hipStream_t s,
@@ -900,9 +914,9 @@ hipError_t launch_cols_fmt(const void* x_bf16, int64_t rows, int64_t cols, const
     uint32_t k0, k1;
     seed_key(seed, k0, k1);
     const int64_t gx = (cols + kColCols - 1) / kColCols;
-    const int slot = 2 * FMT + (RHT ? 6 : 0);
-    const int64_t resident = sr ? resident_wgs(quant_cols_kernel<true, FMT, RHT>, slot)
-                                : resident_wgs(quant_cols_kernel<false, FMT, RHT>, slot + 1);
+    const int slot = 2 * FMT + (RHT ? 6 : 0) + (H == 2 && FMT != (int)ScaleKind::E8M0 ? 8 : 0);
+    const int64_t resident = sr ? resident_wgs(quant_cols_kernel<true, FMT, RHT, H>, slot)
+                                : resident_wgs(quant_cols_kernel<false, FMT, RHT, H>, slot + 1);
     // Items of up to 64 row blocks (whole 64-byte scale runs); shorter when
     // that leaves fewer than 2 items per resident workgroup.
     int64_t rows_per_item = (int64_t)kColGroupRB * kColScaleGroups * 16;     // 1024 rows
@@ -913,17 +927,17 @@ hipError_t launch_cols_fmt(const void* x_bf16, int64_t rows, int64_t cols, const
     const int64_t grid = min(nitems, resident);
     const uint16_t* x = reinterpret_cast<const uint16_t*>(x_bf16);
     if (sr)
-        hipLaunchKernelGGL((quant_cols_kernel<true, FMT, RHT>), dim3((unsigned)grid), dim3(kThreads), 0, s, x,
+        hipLaunchKernelGGL((quant_cols_kernel<true, FMT, RHT, H>), dim3((unsigned)grid), dim3(kThreads), 0, s, x,
                            rows, cols, rows_per_item, gx, nitems, amax_dev, target, k0, k1, tensor_id,
                            payload_t, scales_t, dec_out, rht_mask);
     else
-        hipLaunchKernelGGL((quant_cols_kernel<false, FMT, RHT>), dim3((unsigned)grid), dim3(kThreads), 0, s, x,
+        hipLaunchKernelGGL((quant_cols_kernel<false, FMT, RHT, H>), dim3((unsigned)grid), dim3(kThreads), 0, s, x,
                            rows, cols, rows_per_item, gx, nitems, amax_dev, target, k0, k1, tensor_id,
                            payload_t, scales_t, dec_out, rht_mask);
     return hipGetLastError();
 }
 
-template <int FMT>
+template <int FMT, int TB>
 hipError_t launch_tiles_fmt(const void* w_bf16, int64_t rows, int64_t cols, const float* amax_dev,
                             float target, bool sr, uint64_t seed, uint32_t tensor_id,
                             uint8_t* payload, uint8_t* scales, uint8_t* payload_t, uint8_t* scales_t,
@@ -934,11 +948,11 @@ hipError_t launch_tiles_fmt(const void* w_bf16, int64_t rows, int64_t cols, cons
     const int64_t gy = (rows / 16 + kTileRowTiles - 1) / kTileRowTiles;
     const uint16_t* w = reinterpret_cast<const uint16_t*>(w_bf16);
     if (sr)
-        hipLaunchKernelGGL((quant_tiles_kernel<true, FMT>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
+        hipLaunchKernelGGL((quant_tiles_kernel<true, FMT, TB>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
                            0, s, w, rows, cols, amax_dev, target, k0, k1, tensor_id, payload, scales,
                            payload_t, scales_t, dec_out);
     else
-        hipLaunchKernelGGL((quant_tiles_kernel<false, FMT>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
+        hipLaunchKernelGGL((quant_tiles_kernel<false, FMT, TB>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
                            0, s, w, rows, cols, amax_dev, target, k0, k1, tensor_id, payload, scales,
                            payload_t, scales_t, dec_out);
     return hipGetLastError();
@@ -967,61 +981,53 @@ hipError_t launch_dual_fmt(const void* x_bf16, int64_t rows, int64_t cols, const
 
 }  // namespace
 
-hipError_t launch_quant_rows(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
+hipError_t launch_quant_rows(ScaleKind fmt, int block, const void* x_bf16, int64_t rows, int64_t cols,
                              const float* amax_dev, float target, bool sr, uint64_t seed,
                              uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
                              float* dec_out, hipStream_t s) {
+#define UE5M3_ROWS(F, H) launch_rows_fmt<(int)ScaleKind::F, H>(x_bf16, rows, cols, amax_dev, target, sr, seed, \
+                                                              tensor_id, payload, scales, dec_out, s)
     switch (fmt) {
-        case ScaleKind::E4M3:
-            return launch_rows_fmt<(int)ScaleKind::E4M3>(x_bf16, rows, cols, amax_dev, target, sr, seed,
-                                                         tensor_id, payload, scales, dec_out, s);
-        case ScaleKind::E8M0:
-            return launch_rows_fmt<(int)ScaleKind::E8M0>(x_bf16, rows, cols, amax_dev, target, sr, seed,
-                                                         tensor_id, payload, scales, dec_out, s);
-        default:
-            return launch_rows_fmt<(int)ScaleKind::UE5M3>(x_bf16, rows, cols, amax_dev, target, sr, seed,
-                                                          tensor_id, payload, scales, dec_out, s);
+        case ScaleKind::E4M3: return block == 32 ? UE5M3_ROWS(E4M3, 2) : UE5M3_ROWS(E4M3, 1);
+        case ScaleKind::E8M0: return UE5M3_ROWS(E8M0, 2);
+        default: return block == 32 ? UE5M3_ROWS(UE5M3, 2) : UE5M3_ROWS(UE5M3, 1);
     }
+#undef UE5M3_ROWS
 }
 
-hipError_t launch_quant_cols(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,
+hipError_t launch_quant_cols(ScaleKind fmt, int block, const void* x_bf16, int64_t rows, int64_t cols,
                              const float* amax_dev, float target, bool sr, uint64_t seed,
                              uint32_t tensor_id, uint8_t* payload_t, uint8_t* scales_t,
                              float* dec_out, hipStream_t s) {
+#define UE5M3_COLS(F, H) launch_cols_fmt<(int)ScaleKind::F, H>(x_bf16, rows, cols, amax_dev, target, sr, seed, \
+                                                              tensor_id, payload_t, scales_t, dec_out, s)
     switch (fmt) {
-        case ScaleKind::E4M3:
-            return launch_cols_fmt<(int)ScaleKind::E4M3>(x_bf16, rows, cols, amax_dev, target, sr, seed,
-                                                         tensor_id, payload_t, scales_t, dec_out, s);
-        case ScaleKind::E8M0:
-            return launch_cols_fmt<(int)ScaleKind::E8M0>(x_bf16, rows, cols, amax_dev, target, sr, seed,
-                                                         tensor_id, payload_t, scales_t, dec_out, s);
-        default:
-            return launch_cols_fmt<(int)ScaleKind::UE5M3>(x_bf16, rows, cols, amax_dev, target, sr, seed,
-                                                          tensor_id, payload_t, scales_t, dec_out, s);
+        case ScaleKind::E4M3: return block == 32 ? UE5M3_COLS(E4M3, 2) : UE5M3_COLS(E4M3, 1);
+        case ScaleKind::E8M0: return UE5M3_COLS(E8M0, 2);
+        default: return block == 32 ? UE5M3_COLS(UE5M3, 2) : UE5M3_COLS(UE5M3, 1);
     }
+#undef UE5M3_COLS
 }
 
 hipError_t launch_quant_cols_rht(const void* x_bf16, int64_t rows, int64_t cols, const float* amax_dev,
                                  float target, bool sr, uint64_t seed, uint32_t tensor_id,
                                  uint32_t sign_mask, uint8_t* payload_t, uint8_t* scales_t,
                                  float* dec_out, hipStream_t s) {
-    return launch_cols_fmt<(int)ScaleKind::UE5M3, true>(x_bf16, rows, cols, amax_dev, target, sr, seed,
+    return launch_cols_fmt<(int)ScaleKind::UE5M3, 1, true>(x_bf16, rows, cols, amax_dev, target, sr, seed,
                                                         tensor_id, payload_t, scales_t, dec_out, s,
                                                         sign_mask);
 }
 
-hipError_t launch_quant_tiles(ScaleKind fmt, const void* w_bf16, int64_t rows, int64_t cols,
+hipError_t launch_quant_tiles(ScaleKind fmt, int tile, const void* w_bf16, int64_t rows, int64_t cols,
                               const float* amax_dev, float target, bool sr, uint64_t seed,
                               uint32_t tensor_id, uint8_t* payload, uint8_t* scales,
                               uint8_t* payload_t, uint8_t* scales_t, float* dec_out,
                               hipStream_t s) {
-    if (fmt == ScaleKind::E4M3)
-        return launch_tiles_fmt<(int)ScaleKind::E4M3>(w_bf16, rows, cols, amax_dev, target, sr, seed,
-                                                      tensor_id, payload, scales, payload_t, scales_t,
-                                                      dec_out, s);
-    return launch_tiles_fmt<(int)ScaleKind::UE5M3>(w_bf16, rows, cols, amax_dev, target, sr, seed,
-                                                   tensor_id, payload, scales, payload_t, scales_t,
-                                                   dec_out, s);
+#define UE5M3_TILES(F, TB) launch_tiles_fmt<(int)ScaleKind::F, TB>(w_bf16, rows, cols, amax_dev, target, sr, \
+                               seed, tensor_id, payload, scales, payload_t, scales_t, dec_out, s)
+    if (fmt == ScaleKind::E4M3) return tile == 32 ? UE5M3_TILES(E4M3, 32) : UE5M3_TILES(E4M3, 16);
+    return tile == 32 ? UE5M3_TILES(UE5M3, 32) : UE5M3_TILES(UE5M3, 16);
+#undef UE5M3_TILES
 }
 
 hipError_t launch_quant_dual(ScaleKind fmt, const void* x_bf16, int64_t rows, int64_t cols,

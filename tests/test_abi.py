@@ -156,29 +156,45 @@ def test_amax_accumulate_validation(lib):
 
 
 def test_format_entry_points_validation(lib):
-    """_ex calls: scale kind, block length, E8M0 without amax, 2D E8M0 and
-    the E8M0 GEMM's K % 256 requirement are checked on the host."""
+    """_ex calls: scale kind, block length, E8M0 without amax, 2D E8M0, the
+    block-32 shapes and the E8M0 GEMM's K % 256 requirement are checked on
+    the host."""
     q = lib.ue5m3_quantize_1d_ex
 
     def call(kind=1, block=16, amax=FAKE, rows=32, cols=32, axis=1):
         return q(FAKE, rows, cols, axis, amax, 448.0, 0, 0, 0, kind, block, FAKE, FAKE, NULL, NULL)
     assert call(kind=3) == ue.UE5M3_EINVAL
-    assert call(kind=1, block=32) == ue.UE5M3_EINVAL          # E4M3 blocks are 16
+    assert call(kind=1, block=32, rows=0) == ue.UE5M3_OK      # block-size control
+    assert call(kind=0, block=32, cols=48) == ue.UE5M3_ESHAPE
+    assert call(kind=0, block=32, axis=0, rows=48) == ue.UE5M3_ESHAPE
+    assert call(kind=0, block=8) == ue.UE5M3_EINVAL and call(kind=1, block=64) == ue.UE5M3_EINVAL
     assert call(kind=2, block=16) == ue.UE5M3_EINVAL          # E8M0 blocks are 32
     assert call(kind=1, amax=NULL) == ue.UE5M3_EINVAL         # E4M3 needs the held amax
     assert call(kind=2, block=32, amax=NULL, rows=0) == ue.UE5M3_OK   # E8M0 does not
     assert call(kind=2, block=32, cols=48) == ue.UE5M3_ESHAPE
     assert call(kind=2, block=32, axis=0, rows=48) == ue.UE5M3_ESHAPE
     q2 = lib.ue5m3_quantize_2d_ex
-    assert q2(FAKE, 32, 32, FAKE, 448.0, 0, 0, 0, 2, FAKE, FAKE, NULL, NULL, NULL, NULL) == ue.UE5M3_EINVAL
-    assert q2(FAKE, 0, 32, FAKE, 448.0, 0, 0, 0, 1, FAKE, FAKE, NULL, NULL, NULL, NULL) == ue.UE5M3_OK
+
+    def q2call(kind=0, tile=16, rows=32, cols=32):
+        return q2(FAKE, rows, cols, FAKE, 448.0, 0, 0, 0, kind, tile, FAKE, FAKE, NULL, NULL, NULL, NULL)
+    assert q2call(kind=2) == ue.UE5M3_EINVAL and q2call(kind=2, tile=32) == ue.UE5M3_EINVAL
+    assert q2call(kind=1, rows=0) == ue.UE5M3_OK and q2call(tile=32, rows=0) == ue.UE5M3_OK
+    assert q2call(tile=8) == ue.UE5M3_EINVAL and q2call(tile=64) == ue.UE5M3_EINVAL
+    assert q2call(tile=32, rows=48) == ue.UE5M3_ESHAPE and q2call(tile=32, cols=48) == ue.UE5M3_ESHAPE
     g = lib.ue5m3_gemm_ex
 
-    def gcall(kind=2, M=32, N=32, K=256, layout=0):
-        return g(layout, M, N, K, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, kind, NULL)
+    def gcall(kind=2, M=32, N=32, K=256, layout=0, block=None):
+        block = (32 if kind == 2 else 16) if block is None else block
+        return g(layout, M, N, K, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, kind, block, NULL)
     assert gcall(kind=5) == ue.UE5M3_EINVAL
     assert gcall(K=128) == ue.UE5M3_ESHAPE                    # E8M0 needs K % 256
     assert gcall(kind=1, K=128, N=40) == ue.UE5M3_ESHAPE      # E4M3 NT: N % 16
+    assert gcall(block=16) == ue.UE5M3_EINVAL                 # E8M0 blocks are 32
+    assert gcall(kind=0, block=8) == ue.UE5M3_EINVAL
+    assert gcall(kind=0, block=32, K=48) == ue.UE5M3_ESHAPE   # block 32: K % 32
+    assert gcall(kind=1, block=32, N=48) == ue.UE5M3_ESHAPE   # and N % 32 for NT, NN
+    assert gcall(kind=1, block=32, N=48, layout=1) == ue.UE5M3_ESHAPE
+    assert gcall(kind=0, block=32, N=48, layout=2, M=0) == ue.UE5M3_OK
     assert gcall(layout=3) == ue.UE5M3_ELAYOUT
     assert gcall(M=0) == ue.UE5M3_OK
     assert gcall(M=1 << 20, N=1 << 20) == ue.UE5M3_ESHAPE     # 32-bit offsets
@@ -200,8 +216,8 @@ def test_dual_quantizer_validation(lib):
 def test_gemm_pm_validation(lib):
     g = lib.ue5m3_gemm_pm
 
-    def call(layout=0, M=32, N=32, K=64, kind=0, grid=1024, ctype=0, a=FAKE, c=FAKE):
-        return g(layout, M, N, K, a, FAKE, FAKE, FAKE, FAKE, FAKE, c, ctype, kind, grid, NULL)
+    def call(layout=0, M=32, N=32, K=64, kind=0, grid=1024, ctype=0, a=FAKE, c=FAKE, block=16):
+        return g(layout, M, N, K, a, FAKE, FAKE, FAKE, FAKE, FAKE, c, ctype, kind, block, grid, NULL)
     assert call(layout=3) == ue.UE5M3_ELAYOUT
     assert call(kind=2) == ue.UE5M3_EINVAL                 # E8M0 has no probe-matched path
     for bad in (-1, 1000, 3, (1 << 31) - 1):
@@ -212,6 +228,9 @@ def test_gemm_pm_validation(lib):
     assert call(c=NULL) == ue.UE5M3_EINVAL
     assert call(a=FAKE_MIS) == ue.UE5M3_EALIGN
     assert call(M=0) == ue.UE5M3_OK and call(N=0) == ue.UE5M3_OK
+    assert call(block=8) == ue.UE5M3_EINVAL and call(block=64) == ue.UE5M3_EINVAL
+    assert call(block=32, K=48) == ue.UE5M3_ESHAPE and call(block=32, N=48) == ue.UE5M3_ESHAPE
+    assert call(block=32, M=0) == ue.UE5M3_OK
 
 
 def test_rht_entry_points_validation(lib):

@@ -410,6 +410,7 @@ def main():
         for j, n in enumerate(names):
             per[n].append(ev[j].elapsed_time(ev[j + 1]))
     avg = {n: float(np.mean(v)) for n, v in per.items()}
+    pct = {n: [round(float(q), 5) for q in np.percentile(v, [10, 50, 90])] for n, v in per.items()}
 
     flop_gemm = 2.0 * T * N * K
     qbytes = {"quant_x_dual": 2 * quant_bytes_1d(T, K) if args.rht else quant_bytes_dual(T, K),
@@ -418,10 +419,12 @@ def main():
     kernels = {}
     for n, b in qbytes.items():
         gbs = b / (avg[n] * 1e-3) / 1e9
-        kernels[n] = {"ms": round(avg[n], 5), "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+        kernels[n] = {"ms": round(avg[n], 5), "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
+                      "ms_p10_p50_p90": pct[n]}
     for n in ["gemm_fprop", "gemm_dgrad", "gemm_wgrad"]:
         tf = flop_gemm / (avg[n] * 1e-3) / 1e12
-        kernels[n] = {"ms": round(avg[n], 5), "TFLOP/s": round(tf, 1), "frac": round(tf / BF16_PEAK_TFLOPS, 4)}
+        kernels[n] = {"ms": round(avg[n], 5), "TFLOP/s": round(tf, 1), "frac": round(tf / BF16_PEAK_TFLOPS, 4),
+                      "ms_p10_p50_p90": pct[n]}
     kernels["amax"] = {"ms": round(avg["amax"], 5), "note": "launches only on refresh steps"}
     qtime = sum(avg[n] for n in qbytes)
     quant_gbs = sum(qbytes.values()) / (qtime * 1e-3) / 1e9

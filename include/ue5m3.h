@@ -14,9 +14,14 @@
  * --------------------------------
  * - All tensor pointers are DEVICE pointers owned by the caller, who
  *   allocates and frees them.  Every pointer must be 16-byte aligned.  The
- *   only memory the library allocates itself is the split-tile workspace of
- *   ue5m3_gemm (see there); besides it the library keeps only caches of
- *   device properties.
+ *   only memory the library allocates itself is a set of workspaces, one of
+ *   each kind per (device, stream), allocated on first need, grown with a
+ *   synchronization of that stream and kept until the process ends: the
+ *   split-tile partials of ue5m3_gemm, the expanded block-32 scales of
+ *   ue5m3_gemm_ex / ue5m3_gemm_pm, and 16 KiB of per-workgroup partial
+ *   maxima for the amax calls.  Calls on one stream use them in stream
+ *   order.  Besides these the library keeps only caches of device
+ *   properties.
  * - bf16 tensors are dense row-major [rows, cols] arrays of 16-bit words.
  * - Payloads pack two E2M1 nibbles per byte along a row: byte [r, c/2] holds
  *   element (r, c) in its low nibble and (r, c+1) in its high nibble.
@@ -141,10 +146,10 @@ ue5m3_status_t ue5m3_quantize_cols_rht(const void* x_bf16, int64_t rows, int64_t
 
 /*
  * eq:delayed-amax.  At optimizer step `step`, if the cache is empty or
- * period > 0 and step - last_refresh >= period, enqueue the tensor amax a = max_i |x_i| of
- * the bf16 tensor x (numel elements) into *st->amax_dev, set last_refresh =
- * step, has_cache = 1 and *refreshed = 1; otherwise enqueue nothing and set
- * *refreshed = 0.  The decision uses host integers only (no device read).
+ * period > 0 and step - last_refresh >= period, enqueue the tensor amax
+ * a = max_i |x_i| of the bf16 tensor x (numel elements) into *st->amax_dev,
+ * set last_refresh = step, has_cache = 1 and *refreshed = 1; otherwise
+ * enqueue nothing and set *refreshed = 0.  The decision uses host integers only (no device read).
  * numel = 0 stores amax 0 (the quantizers then use reference 1).
  * `refreshed` may be null.
  */
@@ -373,9 +378,10 @@ ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
  * block 16 or 32 (EINVAL otherwise; a scale code's value is the same in
  * every 16-element group it covers, so the 64-product groups and the result
  * are defined as for block 16).  Layouts, operand shapes, alignment, the
- * block-32 workspace and the other status codes as ue5m3_gemm_ex.  The K loop runs in one workgroup per output tile in
- * ascending k (the toward-zero chain is order dependent), so this call is
- * several times slower than ue5m3_gemm.
+ * block-32 workspace and the other status codes as ue5m3_gemm_ex.  The K
+ * loop runs in one workgroup per output tile in ascending k (the
+ * toward-zero chain is order dependent), so this call is several times
+ * slower than ue5m3_gemm.
  */
 ue5m3_status_t ue5m3_gemm_pm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
                              const uint8_t* a, const uint8_t* a_scales, const float* a_dec,

@@ -34,7 +34,6 @@
 #include "fp4_decode.hpp"
 #include "launch.hpp"
 
-#include <mutex>
 #include <type_traits>
 
 namespace ue5m3 {
@@ -1399,52 +1398,9 @@ __global__ __launch_bounds__(256) void gemm_split_sum_kernel(
     }
 }
 
-// Per-device, per-stream workspace for the fp32 partials of split tiles,
-// grown on demand.  Launches on one stream are ordered, so one workspace per
-// (device, stream) suffices.
-// Library workspaces, one per (kind, device, stream), grown on demand and
-// kept until the process ends.  Kind 0: split-tile partials; kind 1:
-// block-32 scales expanded to the block-16 layout.  Uses on one stream are
-// ordered by the stream, so a buffer can be reused by the next call.
-struct StreamWorkspace {
-    int dev = -1;
-    hipStream_t stream = nullptr;
-    void* ptr = nullptr;
-    size_t bytes = 0;
-};
-
-hipError_t stream_workspace(int kind, hipStream_t s, size_t bytes, void** out) {
-    static std::mutex mu;
-    static StreamWorkspace ws[2][64];
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    std::lock_guard<std::mutex> lock(mu);
-    StreamWorkspace* slot = nullptr;
-    for (auto& x : ws[kind])
-        if (x.dev == dev && x.stream == s) { slot = &x; break; }
-    if (slot == nullptr)
-        for (auto& x : ws[kind])
-            if (x.dev < 0) { slot = &x; slot->dev = dev; slot->stream = s; break; }
-    if (slot == nullptr) return hipErrorOutOfMemory;       // more than 64 (device, stream) pairs
-    if (slot->bytes < bytes) {
-        if (slot->ptr) {
-            // a launch still queued on this stream may use the old buffer
-            if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
-            (void)hipFree(slot->ptr);
-        }
-        slot->ptr = nullptr;
-        slot->bytes = 0;
-        if ((e = hipMalloc(&slot->ptr, bytes)) != hipSuccess) return e;
-        slot->bytes = bytes;
-    }
-    *out = slot->ptr;
-    return hipSuccess;
-}
-
 hipError_t split_workspace(hipStream_t s, size_t part_floats, float** part) {
     void* p = nullptr;
-    const hipError_t e = stream_workspace(0, s, part_floats * sizeof(float), &p);
+    const hipError_t e = stream_workspace(kWsSplit, s, part_floats * sizeof(float), &p);
     *part = static_cast<float*>(p);
     return e;
 }
@@ -1613,7 +1569,7 @@ hipError_t launch_gemm_b32(BScale bmode, float amul, bool pm, float grid_d, int6
         const size_t abytes = (size_t)((M * kb16 + 255) / 256 * 256);
         const size_t bbytes = (size_t)(brows16 * kb16);
         void* ws = nullptr;
-        hipError_t e = stream_workspace(1, s, abytes + bbytes, &ws);
+        hipError_t e = stream_workspace(kWsScales, s, abytes + bbytes, &ws);
         if (e != hipSuccess) return e;
         uint8_t* wa = static_cast<uint8_t*>(ws);
         uint8_t* wb = wa + abytes;

@@ -44,6 +44,29 @@ def test_amax_empty_and_negative_max():
     assert g == 9.5
 
 
+def test_amax_planted_maximum_positions():
+    """The maximum in the first element, the last element of a grid-stride
+    pass past the workgroup cap, the last full vector and the scalar tail;
+    the running form (no clear) keeps a larger earlier value."""
+    for shape in [(8192, 4104), (3, 1001)]:
+        base = synthetic.activation(12, *shape, 0.0, 1.0)
+        n = base.size
+        for pos in sorted({0, n // 2 + 3, (n // 8) * 8 - 1, n - 1}):
+            say("amax planted", shape, pos)
+            bits = base.copy().ravel()
+            bits[pos] = synthetic.f32_to_bf16_bits(np.array([-123.5], np.float32))[0]
+            _, g = _gpu_amax(to_dev(bits.reshape(shape)))
+            assert g == np.float32(123.5), (shape, pos)
+    say("amax running maximum")
+    a = torch.full((1,), 200.0, dtype=torch.float32, device="cuda")
+    ue.amax_accumulate(to_dev(base), a, clear=False)
+    torch.cuda.synchronize()
+    assert a.item() == 200.0
+    ue.amax_accumulate(to_dev(base), a, clear=True)
+    torch.cuda.synchronize()
+    assert np.float32(a.item()) == osc.amax(base)
+
+
 def test_sample_and_hold_trace_on_gpu():
     """120 steps, D = 50: refreshes at 0, 50, 100 and the held amax is the one
     sampled at the last refresh (eq:delayed-amax)."""

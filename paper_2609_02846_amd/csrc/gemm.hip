@@ -11,25 +11,25 @@
 // one scale byte per 16 k-elements; the B scales are per row (wgrad) or per
 // 16x16 weight tile (fprop, and dgrad on the transposed weight).
 //
-// Kernel structure (gfx950, one 256-thread workgroup per CU):
-//  * 256 x 256 output tile, four waves in a 2 x 2 grid, 128 x 128 per wave
-//    (16 v_mfma_f32_32x32x16_f16 accumulators = 256 AccVGPRs; on gfx950 the
-//    32x32 shape sustains the matrix-core peak with in-place accumulators);
-//  * K advances in slices of 64.  Each thread owns one row of the A tile and
-//    one row of the B tile: it loads the packed FP4 bytes and scale codes of
-//    the next slice into registers while the matrix cores work on the current
-//    one, decodes them to bf16 and stores them into the other half of a
-//    double-buffered LDS stage (every element is decoded once per workgroup);
-//  * decoding writes each UE5M3 scale s as mu * 2^E (mu = 1 + m/8 in
-//    [1, 2), or 0 for code 0).  The gfx950 FP4 -> FP16 conversion applies a
-//    power-of-two scale exactly (it uses only the exponent of its scale
-//    operand), giving fp16(q * 2^(E-3)); one packed fp16 multiply by mu then
-//    yields fp16(q * s * 2^-3) exactly.  8 nibbles cost 4 conversions and 4
-//    packed multiplies, and (2^(E-3), mu) take a few integer operations per
-//    block;
-//  * workgroups are remapped so that each XCD runs a contiguous range of
-//    tiles, walked in groups of 4 tile rows so that concurrently running
-//    workgroups share A and B slices in that XCD's L2.
+// Kernels (gfx950, one 256-thread workgroup per CU, 256 x 256 output tiles,
+// four waves of 128 x 128 in a 2 x 2 grid, 16 v_mfma_f32_32x32x16_f16
+// accumulators per wave = all 256 AccVGPRs):
+//  * K % 256 == 0, operands and C below 2^31 bytes: gemm_fp4_reg_kernel,
+//    persistent; packed FP4 rows and scale codes staged in LDS by direct
+//    loads four 64-k slices at a time, each wave decoding its own fragments
+//    in registers (no fp16 copy through LDS);
+//  * K % 64 == 0: gemm_fp4_dma_kernel, packed slices staged by direct loads
+//    and decoded once per workgroup into a double-buffered fp16 LDS stage;
+//  * any K % 16 == 0: gemm_fp4_kernel, the same with register-staged loads.
+// Decoding writes each UE5M3 scale s as mu * 2^E (mu = 1 + m/8 in [1, 2), or
+// 0 for code 0) or reads the code as an fp16 bit pattern (c << 7 is its
+// value).  The gfx950 FP4 -> FP16 conversion applies a power-of-two scale
+// exactly (it uses only the exponent of its scale operand), giving
+// fp16(q * 2^(E-3)); one packed fp16 multiply by mu (or by the code's value
+// after a 2^-3 conversion) then yields fp16(q * s * 2^-3) exactly.
+// Workgroups are remapped so that each XCD runs a contiguous range of tiles,
+// walked in groups of 4 tile rows so that concurrently running workgroups
+// share A and B slices in that XCD's L2.
 #include "codec.hpp"
 #include "fp4_decode.hpp"
 #include "launch.hpp"

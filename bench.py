@@ -68,6 +68,19 @@ def parse():
     return p.parse_args()
 
 
+def gemm_source_hash():
+    """Hash of the GEMM kernel source with comments and blank lines removed:
+    the stored HBM traffic figure is valid only for the code it was measured
+    on, and a comment edit does not change that code."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "fp4_decode.hpp", "codec.hpp"):
+        text = open(os.path.join(ROOT, "paper_2609_02846_amd", "csrc", f), encoding="utf-8").read()
+        lines = (ln.split("//")[0].rstrip() for ln in text.splitlines())
+        h.update("\n".join(ln for ln in lines if ln).encode())
+    return h.hexdigest()[:16]
+
+
 def quant_bytes_1d(rows, cols):
     return rows * cols * 2 + rows * cols // 2 + rows * cols // 16
 
@@ -437,12 +450,8 @@ def main():
         # HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE (scaled by a
         # plain copy of known size); void once the kernel source has changed.
         try:
-            import hashlib
             tr = json.load(open(args.traffic))
-            h = hashlib.sha256()
-            for f in ("gemm.hip", "fp4_decode.hpp"):
-                h.update(open(os.path.join(ROOT, "paper_2609_02846_amd", "csrc", f), "rb").read())
-            fresh = h.hexdigest()[:16] == tr.get("source_sha256_16")
+            fresh = gemm_source_hash() == tr.get("source_sha256_16")
             if fresh and tr.get("kernel") == dom and tr.get("config") == [T, K, N]:
                 traffic = round(float(tr["bytes_per_launch"]))
         except Exception:

@@ -3,8 +3,18 @@ steps with the 50-step sample-and-hold reference (eq:delayed-amax) while the
 operand magnitudes drift (lognormal walk, sigma 0.05 per step) and spike
 (x20 on random steps): every step checks the refresh decisions and held
 references of X, W and dY against the oracle's trace; at the refresh steps,
-the spike steps between refreshes and the last step, sampled rows of the
-quantized operands are bit-exact and sampled GEMM outputs meet the GEMM bar.
+the spike steps between refreshes, the planted steps and the last step,
+sampled rows of the quantized operands are bit-exact and sampled GEMM
+outputs meet the GEMM bar.
+
+Planted rows make the held reference's edge cases certain rather than
+likely: one X row is zero on every step (all-zero blocks: the zero rule),
+and on the planted steps (never refresh steps, so the held references do
+not see them) one X row is scaled to 300 held references (its block scales
+saturate, Proposition 1) and one dY row by 1e-10 (its blocks underflow to
+code 0 and take the zero rule).  Those steps log the numbers of saturated,
+underflowed and all-zero blocks in the sampled rows and require each to be
+positive.
 
 The operand of step t is bf16(base * f_t) (binary32 product, RNE), formed on
 the device; the oracle forms the same bits for the rows it samples.  The
@@ -26,6 +36,8 @@ from tests.gpu_util import gemm_check, host, row_elem_index, say, to_dev
 pytestmark = pytest.mark.gpu
 
 STEPS, PERIOD = 120, 50
+PLANTED = (10, 60, 119)
+ZERO_ROW, SAT_ROW, UF_ROW = 5, 11, 13
 
 
 def _scaled_bits(bits, f):
@@ -36,6 +48,29 @@ def _amax_scaled(base_max, f):
     return osc.amax(synthetic.f32_to_bf16_bits(np.array([[base_max * np.float32(f)]], np.float32)))
 
 
+def _bf16_row_scaled(bits, factor):
+    return synthetic.f32_to_bf16_bits(synthetic.bf16_bits_to_f32(bits) * np.float32(factor))
+
+
+def _plant_x(bits, row_ids, t, sat_factor):
+    """The planted X rows among ``row_ids`` (host copy of the device edit)."""
+    out = bits.copy()
+    for i, r in enumerate(row_ids):
+        if r == ZERO_ROW:
+            out[i] = 0
+        elif r == SAT_ROW and t in PLANTED:
+            out[i] = _bf16_row_scaled(out[i], sat_factor)
+    return out
+
+
+def _plant_dy(bits, row_ids, t):
+    out = bits.copy()
+    for i, r in enumerate(row_ids):
+        if r == UF_ROW and t in PLANTED:
+            out[i] = _bf16_row_scaled(out[i], 1e-10)
+    return out
+
+
 def test_down_projection_drift_120_steps():
     T, K, N = 8192, 21504, 4096
     say("down-projection drift", T, K, N, STEPS, "steps")
@@ -43,14 +78,18 @@ def test_down_projection_drift_120_steps():
     x0b, w0b, d0b = wl["x"], wl["w"], wl["dy"]
     fac = synthetic.drift_factors(0, STEPS)
     bmax = [np.float32(np.max(np.abs(synthetic.bf16_bits_to_f32(b)))) for b in (x0b, w0b, d0b)]
+    # the zero row must not hold the tensor maximum (the references stay those of the bases)
+    assert np.argmax(np.max(np.abs(synthetic.bf16_bits_to_f32(x0b)), axis=1)) != ZERO_ROW
     x0, w0, d0 = (to_dev(b).float() for b in (x0b, w0b, d0b))
     states = [ue.AmaxState(PERIOD) for _ in range(3)]
     ost = [osc.AmaxState(PERIOD) for _ in range(3)]
     spikes = {int(t) for t, j in np.argwhere(fac > 5.0)}
     refresh_steps = set(range(0, STEPS, PERIOD))
-    checks = sorted((refresh_steps | {t for t in spikes if t % PERIOD}) | {STEPS - 1})
+    assert not refresh_steps & set(PLANTED)
+    checks = sorted((refresh_steps | {t for t in spikes if t % PERIOD}) | {STEPS - 1} | set(PLANTED))
     rng = np.random.default_rng(3)
-    rows = np.sort(np.concatenate([[0, T - 1], rng.choice(T, 4, replace=False)]))
+    rows = np.sort(np.concatenate([[0, ZERO_ROW, SAT_ROW, UF_ROW, T - 1], rng.choice(np.arange(16, T - 1), 4,
+                                                                                      replace=False)]))
     rdev = torch.from_numpy(rows).cuda()
     sat = 0
     for t in range(STEPS):
@@ -58,6 +97,14 @@ def test_down_projection_drift_120_steps():
         xt = (x0 * float(f[0])).to(torch.bfloat16)
         wt = (w0 * float(f[1])).to(torch.bfloat16)
         dt = (d0 * float(f[2])).to(torch.bfloat16)
+        xt[ZERO_ROW] = 0
+        sat_factor = None
+        if t in PLANTED:
+            # 300 held references over the row's maximum: u_B = 300 T > 61440 for its largest block
+            arow = np.max(np.abs(synthetic.bf16_bits_to_f32(_scaled_bits(x0b[SAT_ROW], f[0]))))
+            sat_factor = np.float32(300.0) * ost[0].g / arow
+            xt[SAT_ROW] = (xt[SAT_ROW].float() * float(sat_factor)).to(torch.bfloat16)
+            dt[UF_ROW] = (dt[UF_ROW].float() * float(np.float32(1e-10))).to(torch.bfloat16)
         for j, (st, tens) in enumerate(zip(states, (xt, wt, dt))):
             r = ue.amax_sample(st, tens, t)
             g_o, r_o = ost[j].observe_amax(lambda: _amax_scaled(bmax[j], f[j]), t)
@@ -79,13 +126,24 @@ def test_down_projection_drift_120_steps():
         dw = ue.gemm("tn", N, K, T, *dc, xc[0], xc[1], xc[2])
         torch.cuda.synchronize()
         # quantized rows of X and dY, bit-exact
-        xs = _scaled_bits(x0b[rows], f[0])
-        ds = _scaled_bits(d0b[rows], f[2])
+        xs = _plant_x(_scaled_bits(x0b[rows], f[0]), rows, t, sat_factor)
+        ds = _plant_dy(_scaled_bits(d0b[rows], f[2]), rows, t)
         xo = oq.quantize_1d(xs, 1, gx)
         do = oq.quantize_1d(ds, 1, gd, 448.0, "sr", 500 + t, 1, elem_index=row_elem_index(rows, N))
         assert np.array_equal(host(xr[0][rdev]), xo[0]) and np.array_equal(host(xr[1][rdev]), xo[1]), t
         assert np.array_equal(host(dr[0][rdev]), do[0]) and np.array_equal(host(dr[1][rdev]), do[1]), t
         sat += int(np.sum(xo[1] == 0xF7)) + int(np.sum(do[1] == 0xF7))
+        zero_blocks = int(np.sum(np.max(np.abs(synthetic.bf16_bits_to_f32(xs)).reshape(len(rows), -1, 16),
+                                        axis=2) == 0))
+        assert zero_blocks >= K // 16 and np.all(xo[1][rows == ZERO_ROW] == 0x78), t
+        if t in PLANTED:
+            n_sat = int(np.sum(xo[1][rows == SAT_ROW] == 0xF7))
+            # every block of the scaled dY row has u_B below half the smallest UE5M3 step
+            uf = np.max(np.abs(synthetic.bf16_bits_to_f32(ds[rows == UF_ROW]))) * np.float32(448.0) / gd
+            n_uf = int(np.sum(do[1][rows == UF_ROW] == 0x78))
+            print(f"step {t}: saturated blocks {n_sat}, underflowed blocks {n_uf}, all-zero blocks "
+                  f"{zero_blocks} (sampled rows)")
+            assert n_sat > 0 and uf < 2.0 ** -18 and n_uf == N // 16, (t, n_sat, uf, n_uf)
         # fprop: sampled rows x one weight tile row (16 outputs each)
         wt16 = _scaled_bits(w0b[16 * 7:16 * 8], f[1])
         wo = oq.quantize_2d(wt16, gw)
@@ -107,10 +165,11 @@ def test_down_projection_drift_120_steps():
         e = float(al) * N * 2.0 ** -23 * ogemm.abs_product(dY, np.ascontiguousarray(Wc.T))
         ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref) + e, 1e-30))) - 7)
         assert np.all(np.abs(c16 - ref) <= e + 1.01 * ulp + 1e-30), ("dgrad", t)
-        # wgrad: two dY columns x three X columns
+        # wgrad: two dY columns x three X columns (all T rows, planted rows included)
         nc, kc = np.array([5, N - 1]), np.array([0, 999, K - 1])
-        dsub = _scaled_bits(np.ascontiguousarray(d0b[:, nc]), f[2])
-        xsub = _scaled_bits(np.ascontiguousarray(x0b[:, kc]), f[0])
+        allr = np.arange(T)
+        dsub = _plant_dy(_scaled_bits(np.ascontiguousarray(d0b[:, nc]), f[2]), allr, t)
+        xsub = _plant_x(_scaled_bits(np.ascontiguousarray(x0b[:, kc]), f[0]), allr, t, sat_factor)
         dco = oq.quantize_1d(dsub, 0, gd, 448.0, "sr", 500 + t, 2,
                              elem_index=row_elem_index(np.arange(T), N, nc))
         xco = oq.quantize_1d(xsub, 0, gx)

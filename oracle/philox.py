@@ -45,12 +45,15 @@ def philox4x32_10(counter, key):
 
 
 def sr_words(seed, tensor_id, index):
-    """The 32-bit SR word of each element index (int64 array)."""
+    """The 32-bit SR word of each element index (int64 array).  Each
+    distinct counter j = index >> 2 is evaluated once and its four words are
+    shared by the elements 4j .. 4j+3 that use them."""
     idx = np.asarray(index, dtype=np.int64)
-    j = (idx >> 2).astype(np.uint64)
+    uj, inv = np.unique(idx >> 2, return_inverse=True)
+    j = uj.astype(np.uint64)
     ctr = np.stack([j & MASK, j >> np.uint64(32),
                     np.full_like(j, np.uint64(tensor_id & 0xFFFFFFFF)),
                     np.zeros_like(j)], axis=-1)
     seed = int(seed) & 0xFFFFFFFFFFFFFFFF
-    out = philox4x32_10(ctr, (seed & 0xFFFFFFFF, seed >> 32))
-    return np.take_along_axis(out, (idx & 3)[..., None], axis=-1)[..., 0]
+    out = philox4x32_10(ctr, (seed & 0xFFFFFFFF, seed >> 32))        # [distinct j, 4]
+    return out[inv.reshape(idx.shape), idx & 3]

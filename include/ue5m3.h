@@ -20,8 +20,10 @@
  *   split-tile partials of ue5m3_gemm, the expanded block-32 scales of
  *   ue5m3_gemm_ex / ue5m3_gemm_pm, and 16 KiB of per-workgroup partial
  *   maxima for the amax calls.  Calls on one stream use them in stream
- *   order.  Besides these the library keeps only caches of device
- *   properties.
+ *   order; streams are told apart by handle value, so a stream should be
+ *   destroyed only after its work has completed, and at most 64 (device,
+ *   stream) pairs can hold workspaces (a further pair gets UE5M3_EHIP).
+ *   Besides these the library keeps only caches of device properties.
  * - bf16 tensors are dense row-major [rows, cols] arrays of 16-bit words.
  * - Payloads pack two E2M1 nibbles per byte along a row: byte [r, c/2] holds
  *   element (r, c) in its low nibble and (r, c+1) in its high nibble.

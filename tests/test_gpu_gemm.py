@@ -260,3 +260,36 @@ def test_persistent_several_tiles_per_workgroup():
             c16 = c.float().cpu().numpy().astype(np.float64)
             ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
             assert np.all(np.abs(c16 - ref) <= ulp * 1.01 + 1e-30)
+
+
+def test_single_small_linear_fprop():
+    """The single small linear (X [256, 512] N(0,1) with 1% x50 outliers,
+    W [256, 512] N(0, 0.02), seed 0): current amax of each operand, X rows
+    and W tiles by RN through the GPU quantizers, then the NT GEMM; payloads
+    and scales bit-exact and every output to the GEMM bar."""
+    say("single small linear fprop")
+    wl = synthetic.linear_fprop_small(0)
+    x, w = wl["x"], wl["w"]
+    T, K = x.shape
+    N = w.shape[0]
+    xd, wd = to_dev(x), to_dev(w)
+    sx, sw = ue.AmaxState(1), ue.AmaxState(1)
+    assert ue.amax_sample(sx, xd, 0) and ue.amax_sample(sw, wd, 0)
+    xr = ue.quantize_1d(xd, 1, sx.amax)
+    wq = ue.quantize_2d(wd, sw.amax, transposed=False)
+    for out_dtype in (torch.float32, torch.bfloat16):
+        y = ue.gemm("nt", T, N, K, *xr, wq[0], wq[1], wq[3], out_dtype=out_dtype)
+        torch.cuda.synchronize()
+        gx, gw = osc.amax(x), osc.amax(w)
+        xo, wo = oq.quantize_1d(x, 1, gx), oq.quantize_2d(w, gw)
+        assert np.array_equal(host(xr[0]), xo[0]) and np.array_equal(host(xr[1]), xo[1])
+        assert np.array_equal(host(wq[0]), wo[0]) and np.array_equal(host(wq[1]), wo[1])
+        X, W = oq.decoded_1d(xo[0], xo[1], 1), oq.decoded_2d(wo[0], wo[1])
+        al = ogemm.alpha(xo[2], wo[3])
+        ref, ap = ogemm.fprop(X, W, al), ogemm.abs_product(X, W)
+        if out_dtype == torch.float32:
+            gemm_check(host(y), ref, al, ap, K, "small linear fprop")
+        else:
+            e = float(al) * K * 2.0 ** -23 * ap
+            ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref) + e, 1e-30))) - 7)
+            assert np.all(np.abs(host(y.float()).astype(np.float64) - ref) <= e + 1.01 * ulp + 1e-30)

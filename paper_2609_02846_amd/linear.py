@@ -33,9 +33,13 @@ SR randomness: each backward call draws from Philox with key ``seed`` +
 operand) and 2 * layer_id + 2 (wgrad operand), so layers and the two dY
 blockings never share words.
 
-Shapes: in_features and out_features multiples of 16; with W trainable the
-token count (X's leading dimensions flattened) must be a multiple of 16 too.
-Weights are bf16.  There is no bias term.
+Block-size control (Sec. "Recipe comparison", Table tab:results):
+``block=32`` runs every 1D block and weight tile at 32 (one scale code per
+32 elements, 32 x 32 weight tiles) with the rest of the recipe unchanged.
+
+Shapes: in_features and out_features multiples of the block (16 or 32);
+with W trainable the token count (X's leading dimensions flattened) must
+be a multiple of the block too.  Weights are bf16.  There is no bias term.
 """
 
 import torch
@@ -55,8 +59,14 @@ class _FP4LinearFn(torch.autograd.Function):
         amax_sample(layer.amax_x, x2d, step)
         amax_sample(layer.amax_w, weight, step)
         tx = layer.target
+        B = layer.block
         dec_xc = None
-        if need_dw and layer.rht_wgrad:
+        if B == 32:
+            xr, sxr, dec_x = quantize_1d(x2d, 1, layer.amax_x.amax, tx, "rn", block=32)
+            xc = sxc = None
+            if need_dw:
+                xc, sxc, dec_xc = quantize_1d(x2d, 0, layer.amax_x.amax, tx, "rn", block=32)
+        elif need_dw and layer.rht_wgrad:
             xr, sxr, dec_x = quantize_1d(x2d, 1, layer.amax_x.amax, tx, "rn")
             amax_sample_rht(layer.amax_xt, x2d, layer.rht_mask, step)
             xc, sxc, dec_xc = quantize_cols_rht(x2d, layer.amax_xt.amax, layer.rht_mask, tx, "rn")
@@ -66,7 +76,7 @@ class _FP4LinearFn(torch.autograd.Function):
         else:
             xr, sxr, dec_x = quantize_1d(x2d, 1, layer.amax_x.amax, tx, "rn")
             xc = sxc = None
-        pw, sw, pwt, dec_w, swt = quantize_2d(weight, layer.amax_w.amax, tx, "rn", transposed=need_dx)
+        pw, sw, pwt, dec_w, swt = quantize_2d(weight, layer.amax_w.amax, tx, "rn", transposed=need_dx, tile=B)
         y = layer._gemm("nt", T, N, K, xr, sxr, dec_x, pw, sw, dec_w, out_dtype=torch.bfloat16)
         ctx.layer = layer
         ctx.step = step
@@ -86,7 +96,8 @@ class _FP4LinearFn(torch.autograd.Function):
         dx = dw = None
         mode = layer.grad_rounding
         if ctx.needs_input_grad[0]:
-            dr = quantize_1d(dy, 1, layer.amax_dy.amax, layer.target, mode, seed, 2 * layer.layer_id + 1)
+            dr = quantize_1d(dy, 1, layer.amax_dy.amax, layer.target, mode, seed, 2 * layer.layer_id + 1,
+                             block=layer.block)
             dx = layer._gemm("nn", T, K, N, *dr, pwt, swt, dec_w, out_dtype=torch.bfloat16)
         if ctx.needs_input_grad[1]:
             tid = 2 * layer.layer_id + 2
@@ -95,7 +106,8 @@ class _FP4LinearFn(torch.autograd.Function):
                 dc = quantize_cols_rht(dy, layer.amax_dyt.amax, layer.rht_mask, layer.target_dy_wgrad, mode,
                                        seed, tid)
             else:
-                dc = quantize_1d(dy, 0, layer.amax_dy.amax, layer.target_dy_wgrad, mode, seed, tid)
+                dc = quantize_1d(dy, 0, layer.amax_dy.amax, layer.target_dy_wgrad, mode, seed, tid,
+                                 block=layer.block)
             dw = layer._gemm("tn", N, K, T, *dc, xc, sxc, dec_xc, out_dtype=ctx.wdtype)
         return dx, dw, None, None, None
 
@@ -115,18 +127,25 @@ class Linear(torch.nn.Module):
     tokens) after a 16-point randomized Hadamard transform with one sign mask
     per layer (drawn from ``seed``), each with the amax of its transformed
     tensor as reference (the "UE5M3 with Transformer Engine settings"
-    recipe, with ``period`` 1 and ``pm_grid`` 1024)."""
+    recipe, with ``period`` 1 and ``pm_grid`` 1024).  ``block``: 16 (the
+    recipe) or 32 (the block-size control; not with ``rht_wgrad``)."""
 
     def __init__(self, in_features, out_features, period=50, target=448.0, target_dy_wgrad=448.0,
-                 seed=0, layer_id=0, device="cuda", grad_rounding="sr", pm_grid=None, rht_wgrad=False):
+                 seed=0, layer_id=0, device="cuda", grad_rounding="sr", pm_grid=None, rht_wgrad=False,
+                 block=16):
         super().__init__()
         if grad_rounding not in ("sr", "rn"):
             raise ValueError("grad_rounding must be 'sr' or 'rn'")
+        if block not in (16, 32):
+            raise ValueError("block must be 16 or 32")
+        if block == 32 and rht_wgrad:
+            raise ValueError("the Hadamard transform works on blocks of 16")
+        self.block = int(block)
         self.grad_rounding, self.pm_grid = grad_rounding, pm_grid
         self.rht_wgrad = bool(rht_wgrad)
         self.rht_mask = (((int(seed) * 0x9E3779B97F4A7C15 + 0x632BE59BD9B4E019) % 2 ** 64) >> 48) & 0xFFFF
-        if in_features % 16 or out_features % 16 or in_features <= 0 or out_features <= 0:
-            raise ValueError("in_features and out_features must be positive multiples of 16")
+        if in_features % block or out_features % block or in_features <= 0 or out_features <= 0:
+            raise ValueError(f"in_features and out_features must be positive multiples of {block}")
         self.in_features, self.out_features = int(in_features), int(out_features)
         self.weight = torch.nn.Parameter(
             torch.empty(out_features, in_features, dtype=torch.bfloat16, device=device))
@@ -178,8 +197,8 @@ class Linear(torch.nn.Module):
     # -- internals ------------------------------------------------------
     def _gemm(self, *args, **kw):
         if self.pm_grid is None:
-            return gemm(*args, **kw)
-        return gemm_pm(*args, grid=self.pm_grid, **kw)
+            return gemm(*args, block=self.block, **kw)
+        return gemm_pm(*args, grid=self.pm_grid, block=self.block, **kw)
 
     def _forward_step(self):
         if self.policy is None:
@@ -203,11 +222,12 @@ class Linear(torch.nn.Module):
         grad = torch.is_grad_enabled()
         need_dx = grad and x.requires_grad
         need_dw = grad and self.weight.requires_grad
-        if need_dw and x2d.shape[0] % 16:
+        if need_dw and x2d.shape[0] % self.block:
             raise ValueError("the wgrad operand is blocked along tokens: token count must be a "
-                             "multiple of 16")
+                             f"multiple of {self.block}")
         y = _FP4LinearFn.apply(x2d, self.weight, self, need_dx, need_dw)
         return y.reshape(*x.shape[:-1], self.out_features)
 
     def extra_repr(self):
-        return f"in_features={self.in_features}, out_features={self.out_features}, target={self.target}"
+        return (f"in_features={self.in_features}, out_features={self.out_features}, target={self.target}, "
+                f"block={self.block}")

@@ -43,22 +43,23 @@ def _scaled(bits, f):
     return synthetic.f32_to_bf16_bits(synthetic.bf16_bits_to_f32(bits) * np.float32(f))
 
 
-def _ref_y(x, w, gx, gw):
-    xr = oq.quantize_1d(x, 1, gx)
-    wq = oq.quantize_2d(w, gw)
-    X, W = oq.decoded_1d(xr[0], xr[1], 1), oq.decoded_2d(wq[0], wq[1])
+def _ref_y(x, w, gx, gw, block=16):
+    xr = oq.quantize_1d(x, 1, gx, block=block)
+    wq = oq.quantize_2d(w, gw, tile=block)
+    X, W = oq.decoded_1d(xr[0], xr[1], 1, block=block), oq.decoded_2d(wq[0], wq[1], tile=block)
     al = ogemm.alpha(xr[2], wq[3])
     return ogemm.fprop(X, W, al), ogemm.abs_product(X, W), al
 
 
-def _ref_grads(x, w, dy, gx, gw, gd, seed, layer_id):
-    xc = oq.quantize_1d(x, 0, gx)
-    wq = oq.quantize_2d(w, gw)
-    dr = oq.quantize_1d(dy, 1, gd, 448.0, "sr", seed, 2 * layer_id + 1)
-    dc = oq.quantize_1d(dy, 0, gd, 448.0, "sr", seed, 2 * layer_id + 2)
-    W = oq.decoded_2d(wq[0], wq[1])
-    dY, dYc = oq.decoded_1d(dr[0], dr[1], 1), oq.decoded_1d(dc[0], dc[1], 0)
-    Xc = oq.decoded_1d(xc[0], xc[1], 0)
+def _ref_grads(x, w, dy, gx, gw, gd, seed, layer_id, block=16):
+    xc = oq.quantize_1d(x, 0, gx, block=block)
+    wq = oq.quantize_2d(w, gw, tile=block)
+    dr = oq.quantize_1d(dy, 1, gd, 448.0, "sr", seed, 2 * layer_id + 1, block=block)
+    dc = oq.quantize_1d(dy, 0, gd, 448.0, "sr", seed, 2 * layer_id + 2, block=block)
+    W = oq.decoded_2d(wq[0], wq[1], tile=block)
+    dY = oq.decoded_1d(dr[0], dr[1], 1, block=block)
+    dYc = oq.decoded_1d(dc[0], dc[1], 0, block=block)
+    Xc = oq.decoded_1d(xc[0], xc[1], 0, block=block)
     al_d, al_w = ogemm.alpha(dr[2], wq[3]), ogemm.alpha(dc[2], xc[2])
     return ((ogemm.dgrad(dY, W, al_d), ogemm.abs_product(dY, W.T), al_d),
             (ogemm.wgrad(dYc, Xc, al_w), ogemm.abs_product(dYc.T, Xc.T), al_w))
@@ -208,3 +209,39 @@ def test_amax_accumulate_running_max():
     amax_accumulate(torch.empty(0, dtype=torch.bfloat16, device="cuda"), acc)
     torch.cuda.synchronize()
     assert np.float32(acc.item()) == osc.calibrated_amax(bs)
+
+
+@pytest.mark.parametrize("pm_grid", [None, 1024])
+def test_training_step_block32(pm_grid):
+    """The block-size control through the layer: X, W, dY quantized with
+    blocks of 32 (32 x 32 weight tiles); Y, dX and dW equal the oracle's
+    block-32 products (decoded-operand GEMM bar, or the probe-matched model
+    exactly, up to the bf16 rounding of Y and dX)."""
+    from oracle import accumulate as oacc
+    T, K, N = 544, 416, 288
+    say("linear training step block 32", T, K, N, "pm", pm_grid)
+    x, w, dy = _inputs(13, T, K, N)
+    gx, gw, gd = osc.amax(x), osc.amax(w), osc.amax(dy)
+    layer = _layer(K, N, w, period=50, seed=9, layer_id=2, block=32, pm_grid=pm_grid)
+    xd = to_dev(x).requires_grad_(True)
+    y = layer(xd)
+    y.backward(to_dev(dy))
+    torch.cuda.synchronize()
+    yref, yabs, yal = _ref_y(x, w, gx, gw, block=32)
+    (dref, dabs, dal), (wref, wabs, wal) = _ref_grads(x, w, dy, gx, gw, gd, 9, 2, block=32)
+    if pm_grid is None:
+        bf16_check(y, yref, yal, yabs, K, "Y")
+        bf16_check(xd.grad, dref, dal, dabs, N, "dX")
+        bf16_check(layer.weight.grad, wref, wal, wabs, T, "dW")
+        return
+    # probe-matched: exact model at sampled outputs, then the bf16 rounding
+    xr = oq.quantize_1d(x, 1, gx, block=32)
+    wq = oq.quantize_2d(w, gw, tile=32)
+    X, W = oq.decoded_1d(xr[0], xr[1], 1, block=32), oq.decoded_2d(wq[0], wq[1], tile=32)
+    al = ogemm.alpha(xr[2], wq[3])
+    rng = np.random.default_rng(1)
+    got = host(y.float())
+    for m, n in [(0, 0), (T - 1, N - 1)] + [(int(rng.integers(T)), int(rng.integers(N))) for _ in range(60)]:
+        want = np.float32(oacc.dot(X[m] * W[n], 1024, al)[0])
+        want = torch.tensor([want]).to(torch.bfloat16).float().item()
+        assert got[m, n] == want, (m, n, got[m, n], want)

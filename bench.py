@@ -65,6 +65,9 @@ def parse():
     p.add_argument("--copy-ref", type=int, default=0, metavar="BYTES",
                    help="profiling aid: time a plain device copy of BYTES bytes (the reference "
                         "that scales the HBM byte counters) and exit")
+    p.add_argument("--matmul-ref", action="store_true",
+                   help="ceiling reference only (not the product path): time a plain bf16 "
+                        "torch.matmul for each of the step's three GEMM shapes and exit")
     return p.parse_args()
 
 
@@ -278,6 +281,38 @@ def formats_bench(args):
                       "formats": res}), flush=True)
 
 
+def matmul_ref(T, K, N, dev):
+    """bf16 inputs, library GEMM (hipBLASLt through torch.matmul): what a plain
+    dense bf16 product of the step's three shapes reaches on this GPU, as a
+    ceiling reference for the FP4 GEMMs.  Operands are contiguous (the
+    transposes are materialised before timing)."""
+    import torch
+    g = torch.Generator(device=dev).manual_seed(0)
+    shapes = {"fprop": (T, K, N), "dgrad": (T, N, K), "wgrad": (N, T, K)}
+    out = {}
+    for name, (m, k, n) in shapes.items():
+        a = torch.randn(m, k, device=dev, dtype=torch.bfloat16, generator=g)
+        b = torch.randn(k, n, device=dev, dtype=torch.bfloat16, generator=g)
+        c = torch.empty(m, n, device=dev, dtype=torch.bfloat16)
+        for _ in range(5):
+            torch.matmul(a, b, out=c)
+        torch.cuda.synchronize()
+        reps = 30
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            torch.matmul(a, b, out=c)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        tf = 2.0 * m * n * k / (ms * 1e-3) / 1e12
+        out[name] = {"m": m, "k": k, "n": n, "ms": round(ms, 4), "TFLOP/s": round(tf, 1),
+                     "frac_bf16": round(tf / BF16_PEAK_TFLOPS, 4)}
+        print(f"[matmul-ref] {name} {m}x{k}x{n}: {ms:.3f} ms {tf:.1f} TFLOP/s", flush=True)
+        del a, b, c
+    print(json.dumps({"matmul_ref_bf16": out}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -303,6 +338,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(f"copied {args.copy_ref} bytes 5 times", flush=True)
+        return
+    if args.matmul_ref:
+        matmul_ref(T, K, N, dev)
         return
     wl = synthetic.ffn_step(0, T, K, N)
 

@@ -68,6 +68,10 @@ def parse():
     p.add_argument("--matmul-ref", action="store_true",
                    help="ceiling reference only (not the product path): time a plain bf16 "
                         "torch.matmul for each of the step's three GEMM shapes and exit")
+    p.add_argument("--gemm-shapes", action="store_true",
+                   help="profiling aid: the fprop-layout GEMM at the step's flops (2 x 8192 x 21504 x "
+                        "4096) split into fewer, longer tiles (K = 4096, 8192, 16384, 21504), bf16 and "
+                        "fp32 outputs, one line per shape, then exit")
     return p.parse_args()
 
 
@@ -313,6 +317,46 @@ def matmul_ref(T, K, N, dev):
     print(json.dumps({"matmul_ref_bf16": out}), flush=True)
 
 
+def gemm_shapes(dev):
+    """Equal-flop fprop GEMMs with 10.5, 5.25, 2.6 and 2 output tiles per CU:
+    how the per-tile cost (epilogue, pipeline refill) shows at the step's
+    K = 4096.  Operands are N(0,1) activations and N(0,0.02) weights,
+    quantized by the library (RN, current amax)."""
+    import torch
+    import paper_2609_02846_amd as ue
+    g = torch.Generator(device=dev).manual_seed(0)
+    out = []
+    for (M, N, K) in [(8192, 21504, 4096), (8192, 10752, 8192), (8192, 5376, 16384), (8192, 4096, 21504)]:
+        x = torch.randn(M, K, device=dev, dtype=torch.float32, generator=g).to(torch.bfloat16)
+        w = (0.02 * torch.randn(N, K, device=dev, dtype=torch.float32, generator=g)).to(torch.bfloat16)
+        sx, sw = ue.AmaxState(50), ue.AmaxState(50)
+        ue.amax_sample(sx, x, 0)
+        ue.amax_sample(sw, w, 0)
+        xp, xs, xd = ue.quantize_1d(x, 1, sx.amax)
+        wp, ws, _, wd, _ = ue.quantize_2d(w, sw.amax, transposed=False)
+        del x, w
+        rec = {"M": M, "N": N, "K": K, "tiles_per_cu": round(((M + 255) // 256) * ((N + 255) // 256) / 256, 2)}
+        for od in (torch.bfloat16, torch.float32):
+            c = torch.empty(M, N, device=dev, dtype=od)
+            for _ in range(3):
+                ue.gemm("nt", M, N, K, xp, xs, xd, wp, ws, wd, out=c, out_dtype=od)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(20):
+                ue.gemm("nt", M, N, K, xp, xs, xd, wp, ws, wd, out=c, out_dtype=od)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / 20
+            name = "bf16" if od == torch.bfloat16 else "f32"
+            rec[name + "_ms"] = round(ms, 4)
+            rec[name + "_TFLOPs"] = round(2.0 * M * N * K / (ms * 1e-3) / 1e12, 1)
+            del c
+        print(f"[gemm-shapes] {rec}", flush=True)
+        out.append(rec)
+    print(json.dumps({"gemm_shapes": out}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -341,6 +385,9 @@ def main():
         return
     if args.matmul_ref:
         matmul_ref(T, K, N, dev)
+        return
+    if args.gemm_shapes:
+        gemm_shapes(dev)
         return
     wl = synthetic.ffn_step(0, T, K, N)
 

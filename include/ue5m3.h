@@ -15,15 +15,22 @@
  * - All tensor pointers are DEVICE pointers owned by the caller, who
  *   allocates and frees them.  Every pointer must be 16-byte aligned.  The
  *   only memory the library allocates itself is a set of workspaces, one of
- *   each kind per (device, stream), allocated on first need, grown with a
- *   synchronization of that stream and kept until the process ends: the
- *   split-tile partials of ue5m3_gemm, the expanded block-32 scales of
- *   ue5m3_gemm_ex / ue5m3_gemm_pm, and 16 KiB of per-workgroup partial
- *   maxima for the amax calls.  Calls on one stream use them in stream
- *   order; streams are told apart by handle value, so a stream should be
- *   destroyed only after its work has completed, and at most 64 (device,
- *   stream) pairs can hold workspaces (a further pair gets UE5M3_EHIP).
- *   Besides these the library keeps only caches of device properties.
+ *   each kind per (device, stream): the split-tile partials of ue5m3_gemm,
+ *   the expanded block-32 scales of ue5m3_gemm_ex / ue5m3_gemm_pm, and
+ *   16 KiB of per-workgroup partial maxima for the amax calls.  A workspace
+ *   is allocated (hipMalloc) by the first call on that pair that needs it,
+ *   or needs a larger one; a replaced workspace is never freed before the
+ *   process ends, so work already enqueued or captured in a graph keeps a
+ *   valid buffer.  Calls on one stream use a workspace in stream order;
+ *   streams are told apart by handle value, so a stream should be destroyed
+ *   only after its work has completed, and at most 64 (device, stream)
+ *   pairs can hold workspaces (a further pair gets UE5M3_EHIP).  Besides
+ *   these the library keeps only caches of device properties.  The library
+ *   may be called from several host threads at once.
+ * - Stream capture: a call made while `stream` is capturing that would have
+ *   to allocate or grow a workspace returns UE5M3_EHIP and enqueues
+ *   nothing; run the same call once before capturing (no library call
+ *   records a memset node).
  * - bf16 tensors are dense row-major [rows, cols] arrays of 16-bit words.
  * - Payloads pack two E2M1 nibbles per byte along a row: byte [r, c/2] holds
  *   element (r, c) in its low nibble and (r, c+1) in its high nibble.
@@ -31,8 +38,10 @@
  * - Scale bytes are UE5M3 codes (value (1 + m/8) 2^(e-15) for exponent field
  *   e >= 1, m 2^-17 for e = 0), stored row-major as described per call.
  * - Every call only enqueues work on `stream` (a hipStream_t; 0 is the null
- *   stream) and returns without synchronizing.  Argument errors are detected
- *   on the host before anything is enqueued; then nothing is written.
+ *   stream) and returns without synchronizing the stream or the device (a
+ *   workspace allocation is a hipMalloc, see above).  Argument errors are
+ *   detected on the host before anything is enqueued; then nothing is
+ *   written.
  * - Inputs must not be NaN (the nibbles and codes of NaN elements are
  *   unspecified); +-Inf is quantized like any magnitude above the E2M1 and
  *   UE5M3 ranges (saturation).
@@ -53,7 +62,8 @@ typedef enum {
     UE5M3_EINVAL = 1,   /* null pointer, bad enum, bad target/period    */
     UE5M3_ESHAPE = 2,   /* negative size or size not a required multiple */
     UE5M3_EALIGN = 3,   /* pointer not 16-byte aligned                   */
-    UE5M3_ELAYOUT = 4,  /* unknown GEMM layout                           */
+    UE5M3_ELAYOUT = 4,  /* unknown GEMM layout, or an operand blocking
+                           that does not run along the contraction      */
     UE5M3_EHIP = 5      /* a HIP launch or runtime call failed           */
 } ue5m3_status_t;
 
@@ -62,6 +72,34 @@ typedef enum { UE5M3_RN = 0, UE5M3_SR = 1 } ue5m3_round_t;
 typedef enum { UE5M3_NT = 0, UE5M3_NN = 1, UE5M3_TN = 2 } ue5m3_layout_t;
 
 typedef enum { UE5M3_OUT_F32 = 0, UE5M3_OUT_BF16 = 1 } ue5m3_out_t;
+
+/*
+ * Blocking of a quantized GEMM operand: along which dimension of its source
+ * tensor s [R, C] the scale blocks run, and hence how the quantizer stored
+ * it (eq:microscaling: a block scale is shared by consecutive elements of
+ * one contraction; Sec. 4.3 and Table 5: each GEMM needs its operands
+ * blocked along its own contraction dimension).
+ *   UE5M3_ROW16   blocks of 16 along a row (ue5m3_quantize_1d, axis 1):
+ *                 payload [R, C/2], scales [R, C/16].
+ *   UE5M3_COL16T  blocks of 16 down a column (ue5m3_quantize_1d, axis 0),
+ *                 stored transposed: payload [C, R/2], scales [C, R/16].
+ *   UE5M3_TILE16  16 x 16 tiles (ue5m3_quantize_2d): for a contraction along
+ *                 the rows of s the payload [R, C/2] and scales [R/16, C/16];
+ *                 for a contraction down its columns the transposed copy
+ *                 payload_t [C, R/2] and scales_t [C/16, R/16].
+ *   UE5M3_ROW32, UE5M3_COL32T, UE5M3_TILE32: the same with blocks of 32
+ *                 (32 x 32 tiles), for ue5m3_gemm_ex and ue5m3_gemm_pm.
+ * In every case the operand as passed is contraction-contiguous: a row of
+ * the payload holds consecutive contraction indices.
+ */
+typedef enum {
+    UE5M3_ROW16 = 0,
+    UE5M3_COL16T = 1,
+    UE5M3_TILE16 = 2,
+    UE5M3_ROW32 = 3,
+    UE5M3_COL32T = 4,
+    UE5M3_TILE32 = 5
+} ue5m3_blocking_t;
 
 /*
  * Sample-and-hold state of one operand's tensor reference (paper Sec. 4.1,
@@ -225,31 +263,46 @@ ue5m3_status_t ue5m3_quantize_2d(const void* w_bf16, int64_t rows, int64_t cols,
  * Workspace: when the 256 x 256 output tiles leave a last, mostly idle wave
  * of workgroups, those tiles are split along K and their fp32 partials are
  * summed (in a fixed order) by a second kernel on the same stream.  The
- * partials live in a workspace the library allocates on the first such call
- * for each (device, stream) pair and keeps for later calls on that pair
- * (grown when a larger one is needed, which first synchronizes the stream);
- * such a call returns UE5M3_EHIP if the allocation fails.
+ * partials live in the library's split workspace for (device, stream) (see
+ * the conventions above: allocated or grown on need, never freed while the
+ * process runs); such a call returns UE5M3_EHIP if the allocation fails.
  *
- * Both operands are passed in contraction-contiguous form, as produced by the
- * quantizers for each product of a linear Y = X W^T (X [T,K], W [N,K]):
+ * Each operand is (payload, scales, blocking, dec) and is passed in
+ * contraction-contiguous form, as produced by the quantizers for each
+ * product of a linear Y = X W^T (X [T,K], W [N,K]); the layout names which
+ * dimension of each operand's source is contracted:
  *
- * UE5M3_NT  fprop  Y = X W^T:  M = T, N = N, K = K.
- *     a = quantize_1d(X, axis 1): payload [M, K/2], scales [M, K/16]
- *     b = quantize_2d(W):         payload [N, K/2], scales [N/16, K/16]
- * UE5M3_NN  dgrad  dX = dY W:   M = T, N = K_w, K = N_w.
- *     a = quantize_1d(dY, axis 1): payload [M, K/2], scales [M, K/16]
- *     b = quantize_2d(W): payload_t [N, K/2], scales_t [N/16, K/16]
- * UE5M3_TN  wgrad  dW = dY^T X: M = N_w, N = K_w, K = T.
- *     a = quantize_1d(dY, axis 0): payload [M, K/2], scales [M, K/16]
- *     b = quantize_1d(X, axis 0):  payload [N, K/2], scales [N, K/16]
+ * UE5M3_NT  fprop  Y = X W^T:  M = T, N = N, K = K.  Both sources [rows, K]
+ *           are contracted along their rows.
+ *     a = quantize_1d(X, axis 1), a_blk = ROW16: payload [M, K/2], scales [M, K/16]
+ *     b = quantize_2d(W), b_blk = TILE16:      payload [N, K/2], scales [N/16, K/16]
+ *         (or b = quantize_1d(W, axis 1), b_blk = ROW16: scales [N, K/16])
+ * UE5M3_NN  dgrad  dX = dY W:   M = T, N = K_w, K = N_w.  A (dY [M, K]) is
+ *           contracted along its rows, B (W [K, N]) down its columns.
+ *     a = quantize_1d(dY, axis 1), a_blk = ROW16: payload [M, K/2], scales [M, K/16]
+ *     b = quantize_2d(W), b_blk = TILE16: payload_t [N, K/2], scales_t [N/16, K/16]
+ *         (or b = quantize_1d(W, axis 0), b_blk = COL16T: scales [N, K/16])
+ * UE5M3_TN  wgrad  dW = dY^T X: M = N_w, N = K_w, K = T.  Both sources
+ *           [K, cols] are contracted down their columns.
+ *     a = quantize_1d(dY, axis 0), a_blk = COL16T: payload [M, K/2], scales [M, K/16]
+ *     b = quantize_1d(X, axis 0),  b_blk = COL16T: payload [N, K/2], scales [N, K/16]
+ *         (or the transposed copy of a 2D quantization of X, b_blk = TILE16)
  *
- * Requires M, N, K >= 0, K % 16 == 0, and N % 16 == 0 for NT and NN.
+ * Blocking rule (eq:microscaling, Sec. 4.3): an operand contracted along its
+ * source's rows takes ROW16 or TILE16, one contracted down its source's
+ * columns takes COL16T or TILE16; A is 1D (ROW16 / COL16T) only.  Any other
+ * combination -- e.g. an axis-1 dY passed to TN, or an axis-0 X passed to NT
+ * -- returns UE5M3_ELAYOUT before anything is enqueued.  A blocking value
+ * outside ue5m3_blocking_t, or one with blocks of 32 here, is UE5M3_EINVAL.
+ *
+ * Requires M, N, K >= 0, K % 16 == 0, and N % 16 == 0 when b_blk = TILE16.
  * M = 0 or N = 0 writes nothing; K = 0 writes zeros.
  */
 ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
-                          const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
-                          const uint8_t* b, const uint8_t* b_scales, const float* b_dec,
-                          void* c, ue5m3_out_t c_type, hipStream_t stream);
+                          const uint8_t* a, const uint8_t* a_scales, ue5m3_blocking_t a_blk,
+                          const float* a_dec, const uint8_t* b, const uint8_t* b_scales,
+                          ue5m3_blocking_t b_blk, const float* b_dec, void* c,
+                          ue5m3_out_t c_type, hipStream_t stream);
 
 /*
  * Both 1D blockings of one bf16 tensor x [rows, cols] from a single read:
@@ -330,25 +383,25 @@ ue5m3_status_t ue5m3_quantize_2d_ex(const void* w_bf16, int64_t rows, int64_t co
                                     uint8_t* scales_t, float* dec_out, hipStream_t stream);
 
 /*
- * ue5m3_gemm with a scale format and block size; both operands use them.
- *   UE5M3, E4M3, block 16: operands and requirements exactly as for
+ * ue5m3_gemm with a scale format; the block length (16 or 32) is that of
+ * the two blockings, which must agree (EINVAL otherwise).  The blocking rule
+ * and UE5M3_ELAYOUT are as for ue5m3_gemm, with ROW32 / COL32T / TILE32 in
+ * place of ROW16 / COL16T / TILE16.
+ *   UE5M3, E4M3, blocks of 16: operands and requirements exactly as for
  *         ue5m3_gemm.
- *   UE5M3, E4M3, block 32 (the block-size control): as for block 16 with
- *         16 replaced by 32 -- A scales [M, K/32] in every layout, B scales
- *         [N, K/32] for TN or [N/32, K/32] for NT and NN (32 x 32 tiles;
- *         scales_t of ue5m3_quantize_2d_ex for NN) -- and K % 32 == 0,
- *         N % 32 == 0 for NT and NN.  The block scales are expanded to one code per
- *         16 elements (per 16 x 16 tile) in a workspace owned by the
- *         library (one per stream, grown on demand and kept until the
- *         process ends; calls on one stream run in order) and the block-16
- *         kernels run, so the results obey the ue5m3_gemm bound.
- *   block: 16 or 32 for UE5M3 and E4M3, 32 for E8M0; EINVAL otherwise.
- *   E8M0: every layout takes A as [M, K/2] payload with [M, K/32] scales and
- *         B as [N, K/2] payload with [N, K/32] scales, both blocked along the
- *         contraction:
- *           NT fprop: a = quantize_1d_ex(X, axis 1), b = quantize_1d_ex(W, axis 1)
- *           NN dgrad: a = quantize_1d_ex(dY, axis 1), b = quantize_1d_ex(W, axis 0)
- *           TN wgrad: a = quantize_1d_ex(dY, axis 0), b = quantize_1d_ex(X, axis 0)
+ *   UE5M3, E4M3, blocks of 32 (the block-size control): as for blocks of 16
+ *         with 16 replaced by 32 -- A scales [M, K/32], B scales [N, K/32]
+ *         (ROW32 / COL32T) or [N/32, K/32] (TILE32) -- and K % 32 == 0,
+ *         N % 32 == 0 for TILE32.  The block scales are expanded to one
+ *         code per 16 elements (per 16 x 16 tile) in the library's
+ *         block-32 workspace for (device, stream) and the block-16 kernels
+ *         run, so the results obey the ue5m3_gemm bound.
+ *   E8M0 (blocks of 32 only, 1D only: TILE32 is EINVAL): every layout takes
+ *         A as [M, K/2] payload with [M, K/32] scales and B as [N, K/2]
+ *         payload with [N, K/32] scales, both blocked along the contraction:
+ *           NT fprop: a = quantize_1d_ex(X, axis 1) ROW32, b = quantize_1d_ex(W, axis 1) ROW32
+ *           NN dgrad: a = quantize_1d_ex(dY, axis 1) ROW32, b = quantize_1d_ex(W, axis 0) COL32T
+ *           TN wgrad: a = quantize_1d_ex(dY, axis 0) COL32T, b = quantize_1d_ex(X, axis 0) COL32T
  *         The products run on the gfx950 scaled FP4 matrix instructions,
  *         which apply the E8M0 powers of two themselves.  Requires
  *         K % 256 == 0, and M*K/2, N*K/2 and 4*M*N each below 2^31 (ESHAPE
@@ -356,10 +409,11 @@ ue5m3_status_t ue5m3_quantize_2d_ex(const void* w_bf16, int64_t rows, int64_t co
  *         E8M0 quantizers).  Workspace as for ue5m3_gemm.
  */
 ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
-                             const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
-                             const uint8_t* b, const uint8_t* b_scales, const float* b_dec,
-                             void* c, ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind,
-                             int32_t block, hipStream_t stream);
+                             const uint8_t* a, const uint8_t* a_scales, ue5m3_blocking_t a_blk,
+                             const float* a_dec, const uint8_t* b, const uint8_t* b_scales,
+                             ue5m3_blocking_t b_blk, const float* b_dec, void* c,
+                             ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind,
+                             hipStream_t stream);
 
 /*
  * Probe-matched GEMM: the paper's output model of the native FP4 GEMM (Sec.
@@ -377,19 +431,21 @@ ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
  * Results are exact to this definition for every input (no accumulation
  * tolerance).  grid_d: 0 (no snap) or a power of two up to 2^30 (the paper
  * uses 1024), else EINVAL.  scale_kind: UE5M3 or E4M3 (E8M0: EINVAL);
- * block 16 or 32 (EINVAL otherwise; a scale code's value is the same in
- * every 16-element group it covers, so the 64-product groups and the result
- * are defined as for block 16).  Layouts, operand shapes, alignment, the
- * block-32 workspace and the other status codes as ue5m3_gemm_ex.  The K
+ * blocks of 16 or 32 as given by the blockings (a scale code's value is the
+ * same in every 16-element group it covers, so the 64-product groups and the
+ * result are defined as for blocks of 16).  Layouts, blockings, operand
+ * shapes, alignment, the block-32 workspace and the other status codes as
+ * ue5m3_gemm_ex.  The K
  * loop runs in one workgroup per output tile in ascending k (the
  * toward-zero chain is order dependent), so this call is several times
  * slower than ue5m3_gemm.
  */
 ue5m3_status_t ue5m3_gemm_pm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
-                             const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
-                             const uint8_t* b, const uint8_t* b_scales, const float* b_dec,
-                             void* c, ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind,
-                             int32_t block, int32_t grid_d, hipStream_t stream);
+                             const uint8_t* a, const uint8_t* a_scales, ue5m3_blocking_t a_blk,
+                             const float* a_dec, const uint8_t* b, const uint8_t* b_scales,
+                             ue5m3_blocking_t b_blk, const float* b_dec, void* c,
+                             ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind,
+                             int32_t grid_d, hipStream_t stream);
 
 /* Static description of a status code. */
 const char* ue5m3_status_string(ue5m3_status_t status);

@@ -23,6 +23,9 @@ NT, NN, TN = 0, 1, 2
 OUT_F32, OUT_BF16 = 0, 1
 _MODES = {"rn": RN, "sr": SR}
 _LAYOUTS = {"nt": NT, "nn": NN, "tn": TN}
+ROW16, COL16T, TILE16, ROW32, COL32T, TILE32 = range(6)
+_BLOCKINGS = {("row", 16): ROW16, ("colT", 16): COL16T, ("tile", 16): TILE16,
+              ("row", 32): ROW32, ("colT", 32): COL32T, ("tile", 32): TILE32}
 SCALE_UE5M3, SCALE_E4M3, SCALE_E8M0 = 0, 1, 2
 _FORMATS = {"ue5m3": SCALE_UE5M3, "e4m3": SCALE_E4M3, "e8m0": SCALE_E8M0}
 BLOCK = {"ue5m3": 16, "e4m3": 16, "e8m0": 32}
@@ -78,7 +81,7 @@ def load_library(path=LIB_PATH):
     lib.ue5m3_quantize_1d.restype = i32
     lib.ue5m3_quantize_2d.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, vp, vp, vp, vp, vp, vp]
     lib.ue5m3_quantize_2d.restype = i32
-    lib.ue5m3_gemm.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, vp]
+    lib.ue5m3_gemm.argtypes = [i32, i64, i64, i64, vp, vp, i32, vp, vp, vp, i32, vp, vp, i32, vp]
     lib.ue5m3_gemm.restype = i32
     lib.ue5m3_quantize_1d_ex.argtypes = [vp, i64, i64, i32, vp, f32, i32, u64, u32, i32, i32,
                                          vp, vp, vp, vp]
@@ -86,14 +89,15 @@ def load_library(path=LIB_PATH):
     lib.ue5m3_quantize_2d_ex.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, i32, i32,
                                          vp, vp, vp, vp, vp, vp]
     lib.ue5m3_quantize_2d_ex.restype = i32
-    lib.ue5m3_gemm_ex.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp]
+    lib.ue5m3_gemm_ex.argtypes = [i32, i64, i64, i64, vp, vp, i32, vp, vp, vp, i32, vp, vp, i32, i32, vp]
     lib.ue5m3_gemm_ex.restype = i32
     lib.ue5m3_amax_sample_rht.argtypes = [ctypes.POINTER(AmaxStateC), vp, i64, i64, u32, i64,
                                           ctypes.POINTER(ctypes.c_int32), vp]
     lib.ue5m3_amax_sample_rht.restype = i32
     lib.ue5m3_quantize_cols_rht.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, u32, vp, vp, vp, vp]
     lib.ue5m3_quantize_cols_rht.restype = i32
-    lib.ue5m3_gemm_pm.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp]
+    lib.ue5m3_gemm_pm.argtypes = [i32, i64, i64, i64, vp, vp, i32, vp, vp, vp, i32, vp, vp, i32, i32, i32,
+                                  vp]
     lib.ue5m3_gemm_pm.restype = i32
     lib.ue5m3_quantize_dual.argtypes = [vp, i64, i64, vp, f32, i32, u64, u32, u32, i32,
                                         vp, vp, vp, vp, vp, vp]
@@ -345,8 +349,31 @@ def quantize_2d(w, amax_dev, target=448.0, mode="rn", seed=0, tensor_id=0, trans
     return payload, scales, payload_t, dec_out, scales_t
 
 
-def _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt, Bk):
+def recipe_blockings(layout, fmt="ue5m3"):
+    """The operand blockings the recipe's quantizers produce for each product
+    (Table 5): fprop A rows, B weight tiles; dgrad A rows, B transposed
+    weight tiles; wgrad both operands blocked down their columns (stored
+    transposed).  E8M0 weights are 1D-blocked along each contraction."""
     lay = _LAYOUTS[layout] if isinstance(layout, str) else int(layout)
+    if lay == TN:
+        return "colT", "colT"
+    if fmt == "e8m0":
+        return "row", ("row" if lay == NT else "colT")
+    return "row", "tile"
+
+
+def _blocking(kind, Bk):
+    if isinstance(kind, int):
+        return kind
+    return _BLOCKINGS[(kind, Bk)]
+
+
+def _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt, Bk,
+               a_blk, b_blk):
+    lay = _LAYOUTS[layout] if isinstance(layout, str) else int(layout)
+    da, db = recipe_blockings(lay, fmt)
+    a_blk = da if a_blk is None else a_blk
+    b_blk = db if b_blk is None else b_blk
     if out is None:
         out = torch.empty((M, N), dtype=out_dtype, device=a.device)
     ctype = OUT_BF16 if out.dtype == torch.bfloat16 else OUT_F32
@@ -354,7 +381,7 @@ def _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out
         raise ValueError("out must be a contiguous fp32 or bf16 tensor")
     _dev_buf(out, out.dtype, int(M) * int(N), "out")
     if M > 0 and N > 0 and K > 0:
-        tiled = fmt != "e8m0" and lay in (NT, NN)
+        tiled = b_blk in ("tile", TILE16, TILE32)
         _u8_out(a, (M, K // 2), "a")
         _u8_out(a_scales, (M, K // Bk), "a_scales")
         _u8_out(b, (N, K // 2), "b")
@@ -362,36 +389,40 @@ def _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out
     if M > 0 and N > 0:
         _f32_out(a_dec, "a_dec")
         _f32_out(b_dec, "b_dec")
-    args = (lay, int(M), int(N), int(K), _ptr(a), _ptr(a_scales), _ptr(a_dec), _ptr(b), _ptr(b_scales),
-            _ptr(b_dec), _ptr(out), ctype)
+    args = (lay, int(M), int(N), int(K), _ptr(a), _ptr(a_scales), _blocking(a_blk, Bk), _ptr(a_dec), _ptr(b),
+            _ptr(b_scales), _blocking(b_blk, Bk), _ptr(b_dec), _ptr(out), ctype)
     return out, args
 
 
 def gemm_pm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
-            out_dtype=torch.float32, grid=1024, stream=None, fmt="ue5m3", block=16):
+            out_dtype=torch.float32, grid=1024, stream=None, fmt="ue5m3", block=16, a_blk=None, b_blk=None):
     """Probe-matched GEMM (see ue5m3_gemm_pm): 64-product RNE partials,
     toward-zero cross-group adds, snap of the encoded accumulator to the
-    1/``grid`` lattice (0: none), then alpha.  Operands as ``gemm``."""
+    1/``grid`` lattice (0: none), then alpha.  Operands and blockings as
+    ``gemm``."""
     if fmt not in ("ue5m3", "e4m3"):
         raise ValueError("the probe-matched GEMM takes UE5M3 or E4M3 scales")
     out, args = _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt,
-                           int(block))
-    _check(load_library().ue5m3_gemm_pm(*args, _FORMATS[fmt], int(block), int(grid), _stream(stream)),
-           "ue5m3_gemm_pm")
+                           int(block), a_blk, b_blk)
+    _check(load_library().ue5m3_gemm_pm(*args, _FORMATS[fmt], int(grid), _stream(stream)), "ue5m3_gemm_pm")
     return out
 
 
 def gemm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
-         out_dtype=torch.float32, stream=None, fmt="ue5m3", block=None):
+         out_dtype=torch.float32, stream=None, fmt="ue5m3", block=None, a_blk=None, b_blk=None):
     """Decoded-operand FP4 GEMM (see ue5m3_gemm and, for ``fmt`` "e4m3" or
     "e8m0" or ``block`` 32, ue5m3_gemm_ex); layout is "nt" (fprop), "nn"
-    (dgrad) or "tn" (wgrad).  Returns the [M, N] output tensor."""
+    (dgrad) or "tn" (wgrad).  ``a_blk`` / ``b_blk`` name each operand's
+    blocking ("row", "colT", "tile" or a ue5m3_blocking_t value); None takes
+    the recipe's blocking for the layout (``recipe_blockings``).  Returns the
+    [M, N] output tensor."""
     Bk = BLOCK[fmt] if block is None else int(block)
-    out, args = _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt, Bk)
+    out, args = _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out_dtype, fmt, Bk,
+                           a_blk, b_blk)
     lib = load_library()
     if fmt == "ue5m3" and Bk == 16:
         st = lib.ue5m3_gemm(*args, _stream(stream))
     else:
-        st = lib.ue5m3_gemm_ex(*args, _FORMATS[fmt], Bk, _stream(stream))
+        st = lib.ue5m3_gemm_ex(*args, _FORMATS[fmt], _stream(stream))
     _check(st, "ue5m3_gemm")
     return out

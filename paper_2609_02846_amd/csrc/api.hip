@@ -15,11 +15,62 @@ inline ue5m3_status_t hip_status(hipError_t e) { return e == hipSuccess ? UE5M3_
 
 inline bool valid_target(float t) { return std::isfinite(t) && t > 0.0f && std::isfinite(t * 6.0f); }
 
+// Orientation of an operand blocking: blocks along the source's rows, down
+// its columns (stored transposed), or square tiles.
+enum class Orient { Row, ColT, Tile };
+
+inline bool blocking_of(ue5m3_blocking_t b, int& len, Orient& o) {
+    switch (b) {
+        case UE5M3_ROW16: len = 16; o = Orient::Row; return true;
+        case UE5M3_COL16T: len = 16; o = Orient::ColT; return true;
+        case UE5M3_TILE16: len = 16; o = Orient::Tile; return true;
+        case UE5M3_ROW32: len = 32; o = Orient::Row; return true;
+        case UE5M3_COL32T: len = 32; o = Orient::ColT; return true;
+        case UE5M3_TILE32: len = 32; o = Orient::Tile; return true;
+    }
+    return false;
+}
+
+// A blocking serves an operand whose source is contracted along its rows
+// (rows_contracted) or down its columns when its blocks run along that
+// contraction (eq:microscaling; Sec. 4.3): Row or Tile for the first, ColT
+// or Tile for the second.
+inline bool along_contraction(Orient o, bool rows_contracted) {
+    return o == Orient::Tile || (o == Orient::Row) == rows_contracted;
+}
+
+// Operand checks shared by the GEMM entry points: the layout, the two
+// blockings (valid values, equal block lengths, A one-dimensional, both
+// along the contraction) and the B scale layout they select.  On success
+// *block is the common block length.
+ue5m3_status_t gemm_blockings(ue5m3_layout_t layout, ue5m3_blocking_t a_blk, ue5m3_blocking_t b_blk,
+                              bool e8, int* block, ue5m3::BScale* bmode) {
+    bool a_rows, b_rows;     // is the source contracted along its rows?
+    switch (layout) {
+        case UE5M3_NT: a_rows = true; b_rows = true; break;
+        case UE5M3_NN: a_rows = true; b_rows = false; break;
+        case UE5M3_TN: a_rows = false; b_rows = false; break;
+        default: return UE5M3_ELAYOUT;
+    }
+    int la = 0, lb = 0;
+    Orient oa = Orient::Row, ob = Orient::Row;
+    if (!blocking_of(a_blk, la, oa) || !blocking_of(b_blk, lb, ob) || la != lb) return UE5M3_EINVAL;
+    if (e8 && (la != 32 || oa == Orient::Tile || ob == Orient::Tile)) return UE5M3_EINVAL;
+    if (oa == Orient::Tile || !along_contraction(oa, a_rows) || !along_contraction(ob, b_rows))
+        return UE5M3_ELAYOUT;
+    *block = la;
+    if (ob != Orient::Tile)
+        *bmode = ue5m3::BScale::Row;
+    else
+        *bmode = layout == UE5M3_NN ? ue5m3::BScale::TileDgrad : ue5m3::BScale::Tile;
+    return UE5M3_OK;
+}
+
 }  // namespace
 
 extern "C" {
 
-int32_t ue5m3_version(void) { return 100; }
+int32_t ue5m3_version(void) { return 200; }
 
 const char* ue5m3_status_string(ue5m3_status_t s) {
     switch (s) {
@@ -27,7 +78,7 @@ const char* ue5m3_status_string(ue5m3_status_t s) {
         case UE5M3_EINVAL: return "invalid argument (null pointer, enum, target or period)";
         case UE5M3_ESHAPE: return "invalid shape (negative, or not a required multiple)";
         case UE5M3_EALIGN: return "pointer not 16-byte aligned";
-        case UE5M3_ELAYOUT: return "unknown GEMM layout";
+        case UE5M3_ELAYOUT: return "unknown GEMM layout, or an operand blocking not along the contraction";
         case UE5M3_EHIP: return "HIP runtime or launch error";
     }
     return "unknown status";
@@ -221,25 +272,23 @@ ue5m3_status_t ue5m3_quantize_dual(const void* x_bf16, int64_t rows, int64_t col
 }
 
 ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
-                             const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
-                             const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,
-                             ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind, int32_t block,
-                             hipStream_t stream) {
-    ue5m3::BScale bmode;
-    switch (layout) {
-        case UE5M3_NT: bmode = ue5m3::BScale::Tile; break;
-        case UE5M3_NN: bmode = ue5m3::BScale::TileDgrad; break;
-        case UE5M3_TN: bmode = ue5m3::BScale::Row; break;
-        default: return UE5M3_ELAYOUT;
-    }
+                             const uint8_t* a, const uint8_t* a_scales, ue5m3_blocking_t a_blk,
+                             const float* a_dec, const uint8_t* b, const uint8_t* b_scales,
+                             ue5m3_blocking_t b_blk, const float* b_dec, void* c, ue5m3_out_t c_type,
+                             ue5m3_scale_kind_t scale_kind, hipStream_t stream) {
+    if (layout != UE5M3_NT && layout != UE5M3_NN && layout != UE5M3_TN) return UE5M3_ELAYOUT;
     if (scale_kind != UE5M3_SCALE_UE5M3 && scale_kind != UE5M3_SCALE_E4M3 &&
         scale_kind != UE5M3_SCALE_E8M0)
         return UE5M3_EINVAL;
     const bool e8 = scale_kind == UE5M3_SCALE_E8M0;
-    if (e8 ? block != 32 : (block != 16 && block != 32)) return UE5M3_EINVAL;
+    int block = 16;
+    ue5m3::BScale bmode = ue5m3::BScale::Row;
+    const ue5m3_status_t bst = gemm_blockings(layout, a_blk, b_blk, e8, &block, &bmode);
+    if (bst != UE5M3_OK) return bst;
+    const bool tiled = bmode != ue5m3::BScale::Row;
     if (c_type != UE5M3_OUT_F32 && c_type != UE5M3_OUT_BF16) return UE5M3_EINVAL;
     if (M < 0 || N < 0 || K < 0 || K % block != 0) return UE5M3_ESHAPE;
-    if (!e8 && layout != UE5M3_TN && N % block != 0) return UE5M3_ESHAPE;
+    if (tiled && N % block != 0) return UE5M3_ESHAPE;
     if (e8) {
         const int64_t lim = (int64_t)1 << 31;
         if (K % 256 != 0 || M * (K / 2) >= lim || N * (K / 2) >= lim || 4 * M * N >= lim)
@@ -271,23 +320,21 @@ ue5m3_status_t ue5m3_gemm_ex(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
 }
 
 ue5m3_status_t ue5m3_gemm_pm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
-                             const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
-                             const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,
-                             ue5m3_out_t c_type, ue5m3_scale_kind_t scale_kind, int32_t block,
-                             int32_t grid_d, hipStream_t stream) {
-    ue5m3::BScale bmode;
-    switch (layout) {
-        case UE5M3_NT: bmode = ue5m3::BScale::Tile; break;
-        case UE5M3_NN: bmode = ue5m3::BScale::TileDgrad; break;
-        case UE5M3_TN: bmode = ue5m3::BScale::Row; break;
-        default: return UE5M3_ELAYOUT;
-    }
+                             const uint8_t* a, const uint8_t* a_scales, ue5m3_blocking_t a_blk,
+                             const float* a_dec, const uint8_t* b, const uint8_t* b_scales,
+                             ue5m3_blocking_t b_blk, const float* b_dec, void* c, ue5m3_out_t c_type,
+                             ue5m3_scale_kind_t scale_kind, int32_t grid_d, hipStream_t stream) {
+    if (layout != UE5M3_NT && layout != UE5M3_NN && layout != UE5M3_TN) return UE5M3_ELAYOUT;
     if (scale_kind != UE5M3_SCALE_UE5M3 && scale_kind != UE5M3_SCALE_E4M3) return UE5M3_EINVAL;
+    int block = 16;
+    ue5m3::BScale bmode = ue5m3::BScale::Row;
+    const ue5m3_status_t bst = gemm_blockings(layout, a_blk, b_blk, false, &block, &bmode);
+    if (bst != UE5M3_OK) return bst;
+    const bool tiled = bmode != ue5m3::BScale::Row;
     if (c_type != UE5M3_OUT_F32 && c_type != UE5M3_OUT_BF16) return UE5M3_EINVAL;
     if (grid_d < 0 || grid_d > (1 << 30) || (grid_d & (grid_d - 1)) != 0) return UE5M3_EINVAL;
-    if (block != 16 && block != 32) return UE5M3_EINVAL;
     if (M < 0 || N < 0 || K < 0 || K % block != 0) return UE5M3_ESHAPE;
-    if (layout != UE5M3_TN && N % block != 0) return UE5M3_ESHAPE;
+    if (tiled && N % block != 0) return UE5M3_ESHAPE;
     if (M == 0 || N == 0) return UE5M3_OK;
     if (c == nullptr || a_dec == nullptr || b_dec == nullptr) return UE5M3_EINVAL;
     if (K > 0 && (a == nullptr || a_scales == nullptr || b == nullptr || b_scales == nullptr))
@@ -305,11 +352,19 @@ ue5m3_status_t ue5m3_gemm_pm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_
 }
 
 ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
-                          const uint8_t* a, const uint8_t* a_scales, const float* a_dec,
-                          const uint8_t* b, const uint8_t* b_scales, const float* b_dec, void* c,
-                          ue5m3_out_t c_type, hipStream_t stream) {
-    return ue5m3_gemm_ex(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_type,
-                         UE5M3_SCALE_UE5M3, 16, stream);
+                          const uint8_t* a, const uint8_t* a_scales, ue5m3_blocking_t a_blk,
+                          const float* a_dec, const uint8_t* b, const uint8_t* b_scales,
+                          ue5m3_blocking_t b_blk, const float* b_dec, void* c, ue5m3_out_t c_type,
+                          hipStream_t stream) {
+    // blocks of 16 only; the other checks are ue5m3_gemm_ex's
+    int len = 0;
+    Orient o = Orient::Row;
+    if (layout == UE5M3_NT || layout == UE5M3_NN || layout == UE5M3_TN) {
+        if (!blocking_of(a_blk, len, o) || len != 16 || !blocking_of(b_blk, len, o) || len != 16)
+            return UE5M3_EINVAL;
+    }
+    return ue5m3_gemm_ex(layout, M, N, K, a, a_scales, a_blk, a_dec, b, b_scales, b_blk, b_dec, c, c_type,
+                         UE5M3_SCALE_UE5M3, stream);
 }
 
 }  // extern "C"

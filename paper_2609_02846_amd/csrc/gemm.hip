@@ -34,6 +34,7 @@
 #include "fp4_decode.hpp"
 #include "launch.hpp"
 
+#include <atomic>
 #include <type_traits>
 
 namespace ue5m3 {
@@ -1511,13 +1512,18 @@ template <int BMODE, bool OUT_BF16, bool FULLK>
 hipError_t launch_one(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                       const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
                       void* c, float amul, hipStream_t s) {
-    static bool attr_set = false;
-    if (!attr_set) {
-        const hipError_t e = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&gemm_fp4_kernel<BMODE, OUT_BF16, FULLK>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, kSmemBytes);
+    // the dynamic LDS attribute, set once per device (setting it twice, when
+    // two threads race here, is harmless)
+    static std::atomic<uint64_t> attr_set{0};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const uint64_t bit = (uint64_t)1 << (dev & 63);
+    if ((attr_set.load(std::memory_order_acquire) & bit) == 0) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_fp4_kernel<BMODE, OUT_BF16, FULLK>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, kSmemBytes);
         if (e != hipSuccess) return e;
-        attr_set = true;
+        attr_set.fetch_or(bit, std::memory_order_release);
     }
     const int tiles_m = (int)((M + BM - 1) / BM);
     const int tiles_n = (int)((N + BN - 1) / BN);

@@ -17,11 +17,14 @@ enum class BScale : int { Row = 0, Tile = 1, TileDgrad = 2 };
 // NVFP4-style) or E8M0 (blocks of 32, MXFP4-style, no tensor scale).
 enum class ScaleKind : int { UE5M3 = 0, E4M3 = 1, E8M0 = 2 };
 
-// Library workspaces, one per (kind, device, stream), grown on demand and
-// kept until the process ends: split-tile partials of the GEMMs, block-32
-// scales expanded to the block-16 layout, per-workgroup partial maxima of
-// the amax kernels.  Uses on one stream are ordered by the stream, so a
-// buffer is reused by the next call on that stream.
+// Library workspaces, one per (kind, device, stream), allocated on first
+// need and replaced by a larger one on demand (the replaced buffer is kept,
+// not freed, until the process ends): split-tile partials of the GEMMs,
+// block-32 scales expanded to the block-16 layout, per-workgroup partial
+// maxima of the amax kernels.  Uses on one stream are ordered by the
+// stream, so a buffer is reused by the next call on that stream.  Returns
+// hipErrorStreamCaptureUnsupported when s is capturing and an allocation
+// would be needed.
 enum WorkspaceKind : int { kWsSplit = 0, kWsScales = 1, kWsAmax = 2, kWsKinds = 3 };
 hipError_t stream_workspace(int kind, hipStream_t s, size_t bytes, void** out);
 

@@ -17,6 +17,8 @@
 // contiguous bytes from one store instruction: outputs whose natural
 // per-lane piece is smaller (the transposed payloads and scales) are
 // assembled in LDS first.
+#include <atomic>
+
 #include "codec.hpp"
 #include "launch.hpp"
 #include "rht.hpp"
@@ -888,22 +890,25 @@ hipError_t launch_rows_fmt(const void* x_bf16, int64_t rows, int64_t cols, const
     return hipGetLastError();
 }
 
-// Resident workgroups of a kernel on the current device (cached per device).
+// Resident workgroups of a kernel on the current device (cached per device;
+// threads that race here store the same value).
 template <typename K>
 int64_t resident_wgs(K kernel, int slot) {
-    static int64_t cache[16][16] = {};
+    static std::atomic<int64_t> cache[16][16];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return kPersistentWGs;
-    if (cache[dev][slot] == 0) {
+    int64_t v = cache[dev][slot].load(std::memory_order_relaxed);
+    if (v == 0) {
         int cus = 0, per = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
             hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, reinterpret_cast<const void*>(kernel),
                                                          kThreads, 0) != hipSuccess ||
             cus <= 0 || per <= 0)
             return kPersistentWGs;
-        cache[dev][slot] = (int64_t)cus * per;
+        v = (int64_t)cus * per;
+        cache[dev][slot].store(v, std::memory_order_relaxed);
     }
-    return cache[dev][slot];
+    return v;
 }
 
 template <int FMT, int H, bool RHT = false>

@@ -1,7 +1,15 @@
 // Library-owned device workspaces (see stream_workspace in launch.hpp).
+//
+// A workspace that has to grow is replaced by a larger allocation and the
+// old one is kept, never freed, until the process ends: launches already
+// enqueued on the stream, or recorded in a captured graph, may still use it.
+// Nothing here synchronizes.  A stream that is being captured cannot
+// allocate (hipMalloc is not a capturable operation), so a call that would
+// need a new or larger workspace during capture fails instead.
 #include "launch.hpp"
 
 #include <mutex>
+#include <vector>
 
 namespace ue5m3 {
 namespace {
@@ -18,6 +26,7 @@ struct StreamWorkspace {
 hipError_t stream_workspace(int kind, hipStream_t s, size_t bytes, void** out) {
     static std::mutex mu;
     static StreamWorkspace ws[kWsKinds][64];
+    static std::vector<void*> retired;          // replaced buffers, kept until exit
     if (kind < 0 || kind >= kWsKinds) return hipErrorInvalidValue;
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
@@ -26,19 +35,20 @@ hipError_t stream_workspace(int kind, hipStream_t s, size_t bytes, void** out) {
     StreamWorkspace* slot = nullptr;
     for (auto& x : ws[kind])
         if (x.dev == dev && x.stream == s) { slot = &x; break; }
+    if (slot == nullptr || slot->bytes < bytes) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        if ((e = hipStreamIsCapturing(s, &cs)) != hipSuccess) return e;
+        if (cs != hipStreamCaptureStatusNone) return hipErrorStreamCaptureUnsupported;
+    }
     if (slot == nullptr)
         for (auto& x : ws[kind])
             if (x.dev < 0) { slot = &x; slot->dev = dev; slot->stream = s; break; }
     if (slot == nullptr) return hipErrorOutOfMemory;       // more than 64 (device, stream) pairs
     if (slot->bytes < bytes) {
-        if (slot->ptr) {
-            // a launch still queued on this stream may use the old buffer
-            if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
-            (void)hipFree(slot->ptr);
-        }
-        slot->ptr = nullptr;
-        slot->bytes = 0;
-        if ((e = hipMalloc(&slot->ptr, bytes)) != hipSuccess) return e;
+        void* p = nullptr;
+        if ((e = hipMalloc(&p, bytes)) != hipSuccess) return e;
+        if (slot->ptr != nullptr) retired.push_back(slot->ptr);
+        slot->ptr = p;
         slot->bytes = bytes;
     }
     *out = slot->ptr;

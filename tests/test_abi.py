@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(ue.EXPORTED_SYMBOLS)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.ue5m3_version() == 100
+    assert lib.ue5m3_version() == 200
 
 
 def test_status_strings(lib):
@@ -87,21 +87,67 @@ def test_quantize_2d_validation(lib):
     assert call(rows=0) == ue.UE5M3_OK
 
 
+ROW16, COL16T, TILE16, ROW32, COL32T, TILE32 = range(6)
+# recipe blockings per layout (Table 5): NT X rows / W tiles, NN dY rows / W
+# tiles (transposed copy), TN dY and X down columns (stored transposed)
+RECIPE = {0: (ROW16, TILE16), 1: (ROW16, TILE16), 2: (COL16T, COL16T)}
+
+
 def test_gemm_validation(lib):
     g = lib.ue5m3_gemm
 
-    def call(layout=0, M=32, N=32, K=32, a=FAKE, b=FAKE, c=FAKE, ctype=0, ad=FAKE, bd=FAKE):
-        return g(layout, M, N, K, a, FAKE, ad, b, FAKE, bd, c, ctype, NULL)
+    def call(layout=0, M=32, N=32, K=32, a=FAKE, b=FAKE, c=FAKE, ctype=0, ad=FAKE, bd=FAKE, ab=None, bb=None):
+        da, db = RECIPE.get(layout, (ROW16, TILE16))
+        ab = da if ab is None else ab
+        bb = db if bb is None else bb
+        return g(layout, M, N, K, a, FAKE, ab, ad, b, FAKE, bb, bd, c, ctype, NULL)
+    for lay in (0, 1, 2):
+        assert call(layout=lay, M=0) == ue.UE5M3_OK
     assert call(layout=3) == ue.UE5M3_ELAYOUT
     assert call(K=40) == ue.UE5M3_ESHAPE
-    assert call(N=40) == ue.UE5M3_ESHAPE                 # NT needs N % 16 (weight tiles)
+    assert call(N=40) == ue.UE5M3_ESHAPE                 # weight tiles need N % 16
     assert call(layout=1, N=40) == ue.UE5M3_ESHAPE
+    assert call(N=40, bb=ROW16, M=0) == ue.UE5M3_OK       # a 1D-blocked weight does not
     assert call(M=-1) == ue.UE5M3_ESHAPE
     assert call(ctype=5) == ue.UE5M3_EINVAL
     assert call(c=NULL) == ue.UE5M3_EINVAL
     assert call(ad=NULL) == ue.UE5M3_EINVAL
     assert call(a=FAKE_MIS) == ue.UE5M3_EALIGN
     assert call(M=0) == ue.UE5M3_OK and call(N=0) == ue.UE5M3_OK
+    # blocks of 32 and unknown values are not blockings of this call
+    for bad in (ROW32, COL32T, TILE32, 6, -1):
+        assert call(ab=bad, M=0) == ue.UE5M3_EINVAL and call(bb=bad, M=0) == ue.UE5M3_EINVAL
+
+
+def test_gemm_blocking_rule(lib):
+    """Every operand must be blocked along its GEMM's contraction
+    (eq:microscaling, Sec. 4.3): for each layout, every blocking pair is
+    accepted exactly when A is 1D along the contraction and B is 1D along it
+    or tiled; all other pairs are UE5M3_ELAYOUT, checked before anything is
+    enqueued (M = 0 would otherwise return OK)."""
+    a_rows = {0: True, 1: True, 2: False}       # A source contracted along its rows?
+    b_rows = {0: True, 1: False, 2: False}
+    for fn in ("ue5m3_gemm", "ue5m3_gemm_ex", "ue5m3_gemm_pm"):
+        g = getattr(lib, fn)
+        for lay in (0, 1, 2):
+            for ab in (ROW16, COL16T, TILE16):
+                for bb in (ROW16, COL16T, TILE16):
+                    ok_a = ab == (ROW16 if a_rows[lay] else COL16T)
+                    ok_b = bb == TILE16 or bb == (ROW16 if b_rows[lay] else COL16T)
+                    want = ue.UE5M3_OK if ok_a and ok_b else ue.UE5M3_ELAYOUT
+                    args = (lay, 0, 32, 64, FAKE, FAKE, ab, FAKE, FAKE, FAKE, bb, FAKE, FAKE, 0)
+                    if fn == "ue5m3_gemm":
+                        st = g(*args, NULL)
+                    elif fn == "ue5m3_gemm_ex":
+                        st = g(*args, 0, NULL)
+                    else:
+                        st = g(*args, 0, 1024, NULL)
+                    assert st == want, (fn, lay, ab, bb, st)
+                    # the same rule with blocks of 32 (_ex, _pm)
+                    if fn != "ue5m3_gemm":
+                        args32 = args[:6] + (ab + 3,) + args[7:10] + (bb + 3,) + args[11:]
+                        st32 = g(*args32, 0, NULL) if fn == "ue5m3_gemm_ex" else g(*args32, 0, 1024, NULL)
+                        assert st32 == want, (fn, lay, ab + 3, bb + 3, st32)
 
 
 def test_amax_state_host_logic(lib):
@@ -183,16 +229,24 @@ def test_format_entry_points_validation(lib):
     assert q2call(tile=32, rows=48) == ue.UE5M3_ESHAPE and q2call(tile=32, cols=48) == ue.UE5M3_ESHAPE
     g = lib.ue5m3_gemm_ex
 
-    def gcall(kind=2, M=32, N=32, K=256, layout=0, block=None):
+    def gcall(kind=2, M=32, N=32, K=256, layout=0, block=None, ab=None, bb=None):
         block = (32 if kind == 2 else 16) if block is None else block
-        return g(layout, M, N, K, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, kind, block, NULL)
+        da, db = RECIPE.get(layout, (ROW16, TILE16))
+        if kind == 2 and layout in (0, 1):
+            db = ROW16 if layout == 0 else COL16T          # E8M0 weights are 1D
+        off = 3 if block == 32 else 0
+        ab = da + off if ab is None else ab
+        bb = db + off if bb is None else bb
+        return g(layout, M, N, K, FAKE, FAKE, ab, FAKE, FAKE, FAKE, bb, FAKE, FAKE, 0, kind, NULL)
     assert gcall(kind=5) == ue.UE5M3_EINVAL
     assert gcall(K=128) == ue.UE5M3_ESHAPE                    # E8M0 needs K % 256
     assert gcall(kind=1, K=128, N=40) == ue.UE5M3_ESHAPE      # E4M3 NT: N % 16
     assert gcall(block=16) == ue.UE5M3_EINVAL                 # E8M0 blocks are 32
-    assert gcall(kind=0, block=8) == ue.UE5M3_EINVAL
+    assert gcall(ab=TILE32, layout=2, M=0) == ue.UE5M3_EINVAL   # and 1D only
+    assert gcall(bb=TILE32, M=0) == ue.UE5M3_EINVAL
+    assert gcall(kind=0, ab=ROW16, bb=TILE32, M=0) == ue.UE5M3_EINVAL   # block lengths differ
     assert gcall(kind=0, block=32, K=48) == ue.UE5M3_ESHAPE   # block 32: K % 32
-    assert gcall(kind=1, block=32, N=48) == ue.UE5M3_ESHAPE   # and N % 32 for NT, NN
+    assert gcall(kind=1, block=32, N=48) == ue.UE5M3_ESHAPE   # and N % 32 for tiles
     assert gcall(kind=1, block=32, N=48, layout=1) == ue.UE5M3_ESHAPE
     assert gcall(kind=0, block=32, N=48, layout=2, M=0) == ue.UE5M3_OK
     assert gcall(layout=3) == ue.UE5M3_ELAYOUT
@@ -217,7 +271,12 @@ def test_gemm_pm_validation(lib):
     g = lib.ue5m3_gemm_pm
 
     def call(layout=0, M=32, N=32, K=64, kind=0, grid=1024, ctype=0, a=FAKE, c=FAKE, block=16):
-        return g(layout, M, N, K, a, FAKE, FAKE, FAKE, FAKE, FAKE, c, ctype, kind, block, grid, NULL)
+        da, db = RECIPE.get(layout, (ROW16, TILE16))
+        if block not in (16, 32):
+            da, db = 6, 6                                     # no blocking of that length
+        elif block == 32:
+            da, db = da + 3, db + 3
+        return g(layout, M, N, K, a, FAKE, da, FAKE, FAKE, FAKE, db, FAKE, c, ctype, kind, grid, NULL)
     assert call(layout=3) == ue.UE5M3_ELAYOUT
     assert call(kind=2) == ue.UE5M3_EINVAL                 # E8M0 has no probe-matched path
     for bad in (-1, 1000, 3, (1 << 31) - 1):

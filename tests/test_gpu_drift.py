@@ -181,3 +181,99 @@ def test_down_projection_drift_120_steps():
         gemm_check(got, ref, al, ogemm.abs_product(A, B), T, f"wgrad step {t}")
     print("saturated block codes seen in the sampled rows:", sat)
 
+
+
+FULL_STEPS = (0, 10, 50, 60, 100, 119)       # refresh steps and planted steps
+
+
+@pytest.fixture(scope="module")
+def drift_bases():
+    T, K, N = 8192, 21504, 4096
+    wl = synthetic.ffn_down_drift(0, T, K, N)
+    return (T, K, N), wl, synthetic.drift_factors(0, STEPS)
+
+
+def _held_references(bmax, fac, t):
+    """The oracle's held references of X, W and dY at step t
+    (eq:delayed-amax over steps 0..t)."""
+    ost = [osc.AmaxState(PERIOD) for _ in range(3)]
+    for s in range(t + 1):
+        for j in range(3):
+            ost[j].observe_amax(lambda: _amax_scaled(bmax[j], fac[s][j]), s)
+    return [o.g for o in ost]
+
+
+@pytest.mark.parametrize("t", FULL_STEPS)
+def test_drift_whole_quantizer_outputs(drift_bases, t):
+    """At the refresh steps (0, 50, 100) and the planted steps (10, 60, 119)
+    of the drift run: every payload byte and scale code of X (both 1D
+    blockings from one read, as the step runs them), W (tiles, the transposed
+    copy and its scales) and dY (rows and columns, SR) against the oracle,
+    with the references the sample-and-hold rule holds at that step
+    (eq:delayed-amax; Proposition 1 and the zero-scale rule decide the
+    planted rows).  The step's operands are formed on the device as in the
+    drift run and must equal the host's bits."""
+    (T, K, N), wl, fac = drift_bases
+    x0b, w0b, d0b = wl["x"], wl["w"], wl["dy"]
+    f = fac[t]
+    bmax = [np.float32(np.max(np.abs(synthetic.bf16_bits_to_f32(b)))) for b in (x0b, w0b, d0b)]
+    gx, gw, gd = _held_references(bmax, fac, t)
+    say("drift whole outputs, step", t, "references", gx, gw, gd)
+    # host bits of the step's operands, planted rows included
+    xs = _scaled_bits(x0b, f[0])
+    xs[ZERO_ROW] = 0
+    ws = _scaled_bits(w0b, f[1])
+    ds = _scaled_bits(d0b, f[2])
+    sat_factor = None
+    if t in PLANTED:
+        arow = np.max(np.abs(synthetic.bf16_bits_to_f32(xs[SAT_ROW])))
+        sat_factor = np.float32(300.0) * gx / arow
+        xs[SAT_ROW] = _bf16_row_scaled(xs[SAT_ROW], sat_factor)
+        ds[UF_ROW] = _bf16_row_scaled(ds[UF_ROW], 1e-10)
+    # the same operands formed on the device
+    xt = (to_dev(x0b).float() * float(f[0])).to(torch.bfloat16)
+    wt = (to_dev(w0b).float() * float(f[1])).to(torch.bfloat16)
+    dt = (to_dev(d0b).float() * float(f[2])).to(torch.bfloat16)
+    xt[ZERO_ROW] = 0
+    if t in PLANTED:
+        xt[SAT_ROW] = (xt[SAT_ROW].float() * float(sat_factor)).to(torch.bfloat16)
+        dt[UF_ROW] = (dt[UF_ROW].float() * float(np.float32(1e-10))).to(torch.bfloat16)
+    for dev, hst, name in ((xt, xs, "X"), (wt, ws, "W"), (dt, ds, "dY")):
+        assert np.array_equal(host(dev.view(torch.int16)).view(np.uint16), hst), (t, name)
+    ax, aw, ad = (torch.tensor([float(g)], dtype=torch.float32, device="cuda") for g in (gx, gw, gd))
+    xr, xc = ue.quantize_dual(xt, ax)
+    wq = ue.quantize_2d(wt, aw)
+    dr = ue.quantize_1d(dt, 1, ad, 448.0, "sr", 500 + t, 1)
+    dc = ue.quantize_1d(dt, 0, ad, 448.0, "sr", 500 + t, 2)
+    torch.cuda.synchronize()
+    del xt, wt, dt
+
+    say("drift whole outputs: X rows and columns, step", t)
+    xro = oq.quantize_1d(xs, 1, gx)
+    assert np.array_equal(host(xr[1]), xro[1]) and np.array_equal(host(xr[0]), xro[0]), t
+    assert np.float32(xr[2].item()) == xro[2], t
+    n_sat = int(np.sum(xro[1] == 0xF7))
+    n_zero = int(np.sum(np.max(np.abs(synthetic.bf16_bits_to_f32(xs)).reshape(T, -1, 16), axis=2) == 0))
+    assert n_zero >= K // 16 and np.all(xro[1][ZERO_ROW] == 0x78), t
+    del xro
+    xco = oq.quantize_1d(xs, 0, gx)
+    assert np.array_equal(host(xc[1]), xco[1]) and np.array_equal(host(xc[0]), xco[0]), t
+    del xco, xs
+
+    say("drift whole outputs: W tiles and the transposed copy, step", t)
+    wo = oq.quantize_2d(ws, gw)
+    assert np.array_equal(host(wq[1]), wo[1]) and np.array_equal(host(wq[4]), wo[1].T), t
+    assert np.array_equal(host(wq[0]), wo[0]) and np.array_equal(host(wq[2]), wo[2]), t
+    assert np.float32(wq[3].item()) == wo[3], t
+    del wo, ws
+
+    say("drift whole outputs: dY rows and columns (SR), step", t)
+    dro = oq.quantize_1d(ds, 1, gd, 448.0, "sr", 500 + t, 1)
+    assert np.array_equal(host(dr[1]), dro[1]) and np.array_equal(host(dr[0]), dro[0]), t
+    n_uf = int(np.sum(dro[1][UF_ROW] == 0x78))
+    dco = oq.quantize_1d(ds, 0, gd, 448.0, "sr", 500 + t, 2)
+    assert np.array_equal(host(dc[1]), dco[1]) and np.array_equal(host(dc[0]), dco[0]), t
+    print(f"step {t}: saturated X blocks {n_sat}, underflowed dY-row blocks {n_uf}, all-zero X blocks {n_zero}")
+    if t in PLANTED:
+        # the planted rows: saturation (Proposition 1) and the zero-scale rule
+        assert n_sat > 0 and n_uf == N // 16, (t, n_sat, n_uf)

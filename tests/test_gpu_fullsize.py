@@ -3,7 +3,10 @@ whole outputs: the GPU quantizers as the bench step runs them (X both 1D
 blockings from one read, W 16 x 16 tiles with the transposed copy, dY rows
 and columns by SR) against the oracle on every payload byte and scale code
 of every output; then 256 random rows of each product against the oracle
-over all their columns, to the GEMM bar of tests/gpu_util.gemm_check."""
+over all their columns, to the GEMM bar of tests/gpu_util.gemm_check.  The
+fprop and dgrad GEMMs also run with the bf16 outputs the training step
+writes: every element equals the bf16 rounding of the fp32 result, and the
+sampled rows lie within one bf16 ulp of the oracle."""
 
 import numpy as np
 import pytest
@@ -17,6 +20,16 @@ from oracle import scaling as osc
 from tests.gpu_util import gemm_check, host, say, to_dev
 
 pytestmark = pytest.mark.gpu
+
+
+def _bf16_check(c_bf16, ref, bound, what):
+    """bf16 output against the oracle's exact product: within the fp32
+    accumulation bound plus one bf16 ulp of the result (the rounding of the
+    fp32 value to bf16 is at most half an ulp)."""
+    c = np.asarray(c_bf16, np.float64)
+    ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref) + bound, 1e-30))) - 7)
+    bad = np.abs(c - ref) > bound + ulp + 1e-30
+    assert not bad.any(), f"{what}: {int(bad.sum())} outputs beyond one bf16 ulp plus the accumulation bound"
 
 
 def test_ffn_up_projection_whole_outputs():
@@ -35,7 +48,15 @@ def test_ffn_up_projection_whole_outputs():
     y = ue.gemm("nt", T, N, K, *xr, wq[0], wq[1], wq[3])
     dx = ue.gemm("nn", T, K, N, *dr, wq[2], wq[4], wq[3])
     dw = ue.gemm("tn", N, K, T, *dc, xc[0], xc[1], xc[2])
+    # the bf16-output instances the training step runs for fprop and dgrad
+    y_bf = ue.gemm("nt", T, N, K, *xr, wq[0], wq[1], wq[3], out_dtype=torch.bfloat16)
+    dx_bf = ue.gemm("nn", T, K, N, *dr, wq[2], wq[4], wq[3], out_dtype=torch.bfloat16)
     torch.cuda.synchronize()
+    say("bf16 fprop and dgrad outputs: every element is the RNE of the fp32 result")
+    # the two instances differ only in the store: same tiles, split plan and
+    # accumulation order, so the bf16 output is exactly bf16(fp32 output)
+    assert torch.equal(y_bf, y.to(torch.bfloat16))
+    assert torch.equal(dx_bf, dx.to(torch.bfloat16))
     gx, gw, gd = osc.amax(x), osc.amax(w), osc.amax(dy)
     assert (np.float32(sx.amax.item()), np.float32(sw.amax.item()), np.float32(sd.amax.item())) == (gx, gw, gd)
 
@@ -70,14 +91,23 @@ def test_ffn_up_projection_whole_outputs():
     gemm_check(host(y[torch.from_numpy(rows).cuda()]), ogemm.fprop(X, W, al), al, ogemm.abs_product(X, W), K,
                "fprop 256 rows")
 
+    say("fprop bf16 output: the same rows within one bf16 ulp of the oracle")
+    _bf16_check(host(y_bf[torch.from_numpy(rows).cuda()].float()), ogemm.fprop(X, W, al),
+                float(al) * K * 2.0 ** -23 * ogemm.abs_product(X, W), "fprop bf16")
+    del X
+
     say("dgrad: 256 rows x all 4096 columns")
     pick = np.sort(rng.choice(len(drows), 256, replace=False))
     dY = oq.decoded_1d(dro[0][pick], dro[1][pick], 1)                 # [256, N]
     al = ogemm.alpha(dro[2], wo[3])
     Wt = np.ascontiguousarray(W.T)
-    gemm_check(host(dx[torch.from_numpy(drows[pick]).cuda()]), ogemm.dgrad(dY, W, al), al,
-               ogemm.abs_product(dY, Wt), N, "dgrad 256 rows")
-    del W, Wt
+    ref = ogemm.dgrad(dY, W, al)
+    ap = ogemm.abs_product(dY, Wt)
+    gemm_check(host(dx[torch.from_numpy(drows[pick]).cuda()]), ref, al, ap, N, "dgrad 256 rows")
+    say("dgrad bf16 output: the same rows within one bf16 ulp of the oracle")
+    _bf16_check(host(dx_bf[torch.from_numpy(drows[pick]).cuda()].float()), ref,
+                float(al) * N * 2.0 ** -23 * ap, "dgrad bf16")
+    del W, Wt, ref, ap
 
     say("wgrad: 256 rows x all 4096 columns")
     pick = np.sort(rng.choice(len(dcols), 256, replace=False))

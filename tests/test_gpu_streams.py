@@ -10,6 +10,8 @@ here are deterministic, so the bar is bitwise equality with the serial /
 eager run; the serial results themselves are checked against the oracle by
 the other GPU tests."""
 
+import ctypes
+
 import pytest
 import torch
 
@@ -119,3 +121,98 @@ def test_graph_capture_replays_equal_eager():
         _reset(eager)
         _sequence(x, w, 7, eager)
         torch.cuda.synchronize()
+
+
+class _FreshStream:
+    """A new HIP stream (default priority) that no earlier call has used, so
+    the library holds no workspace for it yet (torch's own streams come from
+    a pool and are reused); destroyed after its work has completed."""
+
+    def __enter__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.ptr = ctypes.c_void_p()
+        assert self.hip.hipStreamCreate(ctypes.byref(self.ptr)) == 0
+        return torch.cuda.ExternalStream(self.ptr.value)
+
+    def __exit__(self, *exc):
+        torch.cuda.synchronize()
+        self.hip.hipStreamDestroy(self.ptr)
+        return False
+
+
+def _split_gemm_operands(seed, k):
+    x = to_dev(synthetic.activation(seed, T, k, 1e-3, 50.0))
+    w = to_dev(synthetic.weight(seed, N, k))
+    ax, aw = torch.empty(1, device="cuda"), torch.empty(1, device="cuda")
+    ue.amax_accumulate(x, ax, clear=True)
+    ue.amax_accumulate(w, aw, clear=True)
+    xr = ue.quantize_1d(x, 1, ax)
+    wq = ue.quantize_2d(w, aw, transposed=False)
+    return xr, wq
+
+
+def test_workspace_growth_after_capture_keeps_graph_valid():
+    """A graph captured on a stream uses the split-tile workspace that the
+    stream held at capture time.  A later, larger split GEMM on that stream
+    replaces the workspace; the old buffer stays allocated, so every replay
+    of the graph still equals the eager result."""
+    with _FreshStream() as s:
+        _growth_after_capture(s)
+
+
+def _growth_after_capture(s):
+    with torch.cuda.stream(s):
+        small = _split_gemm_operands(4, 1024)       # 272 tiles, 16 split in 2 parts: 8 MiB of partials
+        big = _split_gemm_operands(5, 4096)         # 16 split in 8 parts: 32 MiB
+        say("growth: eager run of the small split GEMM")
+        y_eager = ue.gemm("nt", T, N, 1024, *small[0], small[1][0], small[1][1], small[1][3])
+    torch.cuda.synchronize()
+    y_cap = torch.zeros_like(y_eager)
+    g = torch.cuda.CUDAGraph()
+    say("growth: capture the small split GEMM")
+    with torch.cuda.graph(g, stream=s):
+        ue.gemm("nt", T, N, 1024, *small[0], small[1][0], small[1][1], small[1][3], out=y_cap)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        say("growth: larger split GEMM on the capture stream (new workspace)")
+        y_big = ue.gemm("nt", T, N, 4096, *big[0], big[1][0], big[1][1], big[1][3])
+        y_big2 = ue.gemm("nt", T, N, 4096, *big[0], big[1][0], big[1][1], big[1][3])
+    torch.cuda.synchronize()
+    assert torch.equal(y_big, y_big2)
+    for rep in range(3):
+        say("growth: replay", rep)
+        y_cap.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y_cap, y_eager), rep
+        with torch.cuda.stream(s):
+            y_big3 = ue.gemm("nt", T, N, 4096, *big[0], big[1][0], big[1][1], big[1][3])
+        torch.cuda.synchronize()
+        assert torch.equal(y_big3, y_big), rep
+
+
+def test_call_needing_a_workspace_during_capture_is_refused():
+    """On a stream that has no split workspace yet, a split GEMM issued
+    during capture cannot allocate one: the call fails on the host with
+    UE5M3_EHIP and enqueues nothing, and the capture itself stays usable."""
+    with _FreshStream() as s:
+        _refused_during_capture(s)
+
+
+def _refused_during_capture(s):
+    with torch.cuda.stream(s):
+        xr, wq = _split_gemm_operands(6, 1024)
+    torch.cuda.synchronize()
+    y = torch.zeros(T, N, device="cuda")
+    g = torch.cuda.CUDAGraph()
+    say("capture: split GEMM on a fresh stream")
+    with torch.cuda.graph(g, stream=s):
+        with pytest.raises(ue.UE5M3Error) as err:
+            ue.gemm("nt", T, N, 1024, *xr, wq[0], wq[1], wq[3], out=y)
+        y.add_(1.0)
+    assert err.value.status == ue.UE5M3_EHIP
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    assert torch.all(y == 1.0)

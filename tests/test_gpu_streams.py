@@ -123,20 +123,27 @@ def test_graph_capture_replays_equal_eager():
         torch.cuda.synchronize()
 
 
+_KEPT_STREAMS = []
+
+
 class _FreshStream:
     """A new HIP stream (default priority) that no earlier call has used, so
-    the library holds no workspace for it yet (torch's own streams come from
-    a pool and are reused); destroyed after its work has completed."""
+    the library holds no workspace for it yet.  torch's own streams come from
+    a pool and are reused, and a destroyed stream's handle value can come
+    back from hipStreamCreate (the library would then rightly see the old
+    stream's workspaces), so these streams are kept until the process
+    ends."""
 
     def __enter__(self):
-        self.hip = ctypes.CDLL("libamdhip64.so")
-        self.ptr = ctypes.c_void_p()
-        assert self.hip.hipStreamCreate(ctypes.byref(self.ptr)) == 0
-        return torch.cuda.ExternalStream(self.ptr.value)
+        hip = ctypes.CDLL("libamdhip64.so")
+        ptr = ctypes.c_void_p()
+        assert hip.hipStreamCreate(ctypes.byref(ptr)) == 0
+        assert ptr.value not in _KEPT_STREAMS
+        _KEPT_STREAMS.append(ptr.value)
+        return torch.cuda.ExternalStream(ptr.value)
 
     def __exit__(self, *exc):
         torch.cuda.synchronize()
-        self.hip.hipStreamDestroy(self.ptr)
         return False
 
 

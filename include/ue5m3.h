@@ -24,8 +24,9 @@
  *   valid buffer.  Calls on one stream use a workspace in stream order;
  *   streams are told apart by handle value, so a stream should be destroyed
  *   only after its work has completed, and at most 64 (device, stream)
- *   pairs can hold workspaces (a further pair gets UE5M3_EHIP).  Besides
- *   these the library keeps only caches of device properties.  The library
+ *   pairs can hold workspaces (a further pair gets UE5M3_EHIP).
+ *   ue5m3_gemm_noalloc uses no workspace (see there).  Besides these the
+ *   library keeps only caches of device properties.  The library
  *   may be called from several host threads at once.
  * - Stream capture: a call made while `stream` is capturing that would have
  *   to allocate or grow a workspace returns UE5M3_EHIP and enqueues
@@ -64,7 +65,8 @@ typedef enum {
     UE5M3_EALIGN = 3,   /* pointer not 16-byte aligned                   */
     UE5M3_ELAYOUT = 4,  /* unknown GEMM layout, or an operand blocking
                            that does not run along the contraction      */
-    UE5M3_EHIP = 5      /* a HIP launch or runtime call failed           */
+    UE5M3_EHIP = 5,     /* a HIP launch or runtime call failed           */
+    UE5M3_ESCRATCH = 6  /* more scratch than ue5m3_gemm_noalloc holds    */
 } ue5m3_status_t;
 
 typedef enum { UE5M3_RN = 0, UE5M3_SR = 1 } ue5m3_round_t;
@@ -303,6 +305,28 @@ ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K
                           const float* a_dec, const uint8_t* b, const uint8_t* b_scales,
                           ue5m3_blocking_t b_blk, const float* b_dec, void* c,
                           ue5m3_out_t c_type, hipStream_t stream);
+
+/*
+ * ue5m3_gemm for callers that cannot allocate device memory: code under
+ * stream capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, checks, kernels, split plan and results (bit for bit) as
+ * ue5m3_gemm; it calls no hipMalloc, hipFree or other allocating routine.
+ * The split-tile partials go to a scratch array of 64 MiB that the library
+ * holds once per device from the first call on that device until the process
+ * ends (its device address is looked up on that first call).  A call whose
+ * split plan needs more than the array -- never on a device of at most 256
+ * compute units, where the leftover tiles times their parts never exceed
+ * 256 partial tiles of 256 KiB -- returns UE5M3_ESCRATCH and enqueues
+ * nothing.  The caller passes every input and output.  All calls on one
+ * device share the array and leave their partials in it (nothing in it needs
+ * to start at zero): calls that overlap on one device, on two streams or from
+ * two threads, race and give undefined results.
+ */
+ue5m3_status_t ue5m3_gemm_noalloc(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
+                                  const uint8_t* a, const uint8_t* a_scales, ue5m3_blocking_t a_blk,
+                                  const float* a_dec, const uint8_t* b, const uint8_t* b_scales,
+                                  ue5m3_blocking_t b_blk, const float* b_dec, void* c,
+                                  ue5m3_out_t c_type, hipStream_t stream);
 
 /*
  * Both 1D blockings of one bf16 tensor x [rows, cols] from a single read:

@@ -17,7 +17,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libue5m3.so")
 
-UE5M3_OK, UE5M3_EINVAL, UE5M3_ESHAPE, UE5M3_EALIGN, UE5M3_ELAYOUT, UE5M3_EHIP = range(6)
+UE5M3_OK, UE5M3_EINVAL, UE5M3_ESHAPE, UE5M3_EALIGN, UE5M3_ELAYOUT, UE5M3_EHIP, UE5M3_ESCRATCH = range(7)
 RN, SR = 0, 1
 NT, NN, TN = 0, 1, 2
 OUT_F32, OUT_BF16 = 0, 1
@@ -36,7 +36,7 @@ EXPORTED_SYMBOLS = (
     "ue5m3_quantize_1d", "ue5m3_quantize_2d", "ue5m3_gemm",
     "ue5m3_quantize_1d_ex", "ue5m3_quantize_2d_ex", "ue5m3_gemm_ex", "ue5m3_quantize_dual",
     "ue5m3_gemm_pm", "ue5m3_amax_sample_rht", "ue5m3_quantize_cols_rht",
-    "ue5m3_status_string", "ue5m3_version",
+    "ue5m3_status_string", "ue5m3_version", "ue5m3_gemm_noalloc",
 )
 
 
@@ -91,6 +91,8 @@ def load_library(path=LIB_PATH):
     lib.ue5m3_quantize_2d_ex.restype = i32
     lib.ue5m3_gemm_ex.argtypes = [i32, i64, i64, i64, vp, vp, i32, vp, vp, vp, i32, vp, vp, i32, i32, vp]
     lib.ue5m3_gemm_ex.restype = i32
+    lib.ue5m3_gemm_noalloc.argtypes = [i32, i64, i64, i64, vp, vp, i32, vp, vp, vp, i32, vp, vp, i32, vp]
+    lib.ue5m3_gemm_noalloc.restype = i32
     lib.ue5m3_amax_sample_rht.argtypes = [ctypes.POINTER(AmaxStateC), vp, i64, i64, u32, i64,
                                           ctypes.POINTER(ctypes.c_int32), vp]
     lib.ue5m3_amax_sample_rht.restype = i32
@@ -425,4 +427,18 @@ def gemm(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out=None,
     else:
         st = lib.ue5m3_gemm_ex(*args, _FORMATS[fmt], _stream(stream))
     _check(st, "ue5m3_gemm")
+    return out
+
+
+def gemm_noalloc(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, stream=None, a_blk=None,
+                 b_blk=None):
+    """ue5m3_gemm_noalloc: ``gemm`` (UE5M3, blocks of 16) with its split
+    partials in the library's static scratch array, for callers that cannot
+    allocate.  ``out`` (fp32 or bf16 [M, N]) is required: nothing is
+    allocated here either."""
+    if out is None:
+        raise ValueError("gemm_noalloc allocates nothing: pass out")
+    out, args = _gemm_args(layout, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, out, out.dtype, "ue5m3", 16,
+                           a_blk, b_blk)
+    _check(load_library().ue5m3_gemm_noalloc(*args, _stream(stream)), "ue5m3_gemm_noalloc")
     return out

@@ -80,6 +80,7 @@ const char* ue5m3_status_string(ue5m3_status_t s) {
         case UE5M3_EALIGN: return "pointer not 16-byte aligned";
         case UE5M3_ELAYOUT: return "unknown GEMM layout, or an operand blocking not along the contraction";
         case UE5M3_EHIP: return "HIP runtime or launch error";
+        case UE5M3_ESCRATCH: return "the call needs more scratch than the allocation-free entry point holds";
     }
     return "unknown status";
 }
@@ -365,6 +366,39 @@ ue5m3_status_t ue5m3_gemm(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K
     }
     return ue5m3_gemm_ex(layout, M, N, K, a, a_scales, a_blk, a_dec, b, b_scales, b_blk, b_dec, c, c_type,
                          UE5M3_SCALE_UE5M3, stream);
+}
+
+ue5m3_status_t ue5m3_gemm_noalloc(ue5m3_layout_t layout, int64_t M, int64_t N, int64_t K,
+                                  const uint8_t* a, const uint8_t* a_scales, ue5m3_blocking_t a_blk,
+                                  const float* a_dec, const uint8_t* b, const uint8_t* b_scales,
+                                  ue5m3_blocking_t b_blk, const float* b_dec, void* c, ue5m3_out_t c_type,
+                                  hipStream_t stream) {
+    // the checks of ue5m3_gemm (blocks of 16, UE5M3)
+    if (layout != UE5M3_NT && layout != UE5M3_NN && layout != UE5M3_TN) return UE5M3_ELAYOUT;
+    int len = 0;
+    Orient o = Orient::Row;
+    if (!blocking_of(a_blk, len, o) || len != 16 || !blocking_of(b_blk, len, o) || len != 16)
+        return UE5M3_EINVAL;
+    int block = 16;
+    ue5m3::BScale bmode = ue5m3::BScale::Row;
+    const ue5m3_status_t bst = gemm_blockings(layout, a_blk, b_blk, false, &block, &bmode);
+    if (bst != UE5M3_OK) return bst;
+    if (c_type != UE5M3_OUT_F32 && c_type != UE5M3_OUT_BF16) return UE5M3_EINVAL;
+    if (M < 0 || N < 0 || K < 0 || K % 16 != 0) return UE5M3_ESHAPE;
+    if (bmode != ue5m3::BScale::Row && N % 16 != 0) return UE5M3_ESHAPE;
+    if (M == 0 || N == 0) return UE5M3_OK;
+    if (c == nullptr || a_dec == nullptr || b_dec == nullptr) return UE5M3_EINVAL;
+    if (K > 0 && (a == nullptr || a_scales == nullptr || b == nullptr || b_scales == nullptr))
+        return UE5M3_EINVAL;
+    if (!aligned16(c) || !aligned4(a_dec) || !aligned4(b_dec)) return UE5M3_EALIGN;
+    if (K > 0 && (!aligned16(a) || !aligned16(b) || !aligned16(a_scales) || !aligned16(b_scales)))
+        return UE5M3_EALIGN;
+    ue5m3::FixedScratch fx{nullptr, 0};
+    if (ue5m3::noalloc_scratch(&fx) != hipSuccess) return UE5M3_EHIP;
+    const hipError_t e = ue5m3::launch_gemm(bmode, 64.0f, M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c,
+                                            c_type == UE5M3_OUT_BF16, stream, &fx);
+    if (e == hipErrorOutOfMemory) return UE5M3_ESCRATCH;
+    return hip_status(e);
 }
 
 }  // extern "C"

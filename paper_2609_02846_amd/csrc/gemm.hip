@@ -1438,7 +1438,7 @@ constexpr int kSplitRemDiv = 2;
 template <int BMODE, bool OUT_BF16>
 hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                       const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
-                      void* c, float amul, hipStream_t s) {
+                      void* c, float amul, hipStream_t s, const FixedScratch* fx) {
     const int tiles_m = (int)((M + BM - 1) / BM);
     const int tiles_n = (int)((N + BN - 1) / BN);
     const int T = tiles_m * tiles_n;
@@ -1458,8 +1458,15 @@ hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
         if (parts > 1) {
             sp.Tdp = T - rem;
             sp.parts = parts;
-            e = split_workspace(s, (size_t)rem * parts * 65536, &sp.part);
-            if (e != hipSuccess) return e;
+            const size_t need = (size_t)rem * parts * 65536;
+            if (fx != nullptr) {
+                // caller-supplied buffer: the same plan, or a refusal
+                if (need > fx->floats) return hipErrorOutOfMemory;
+                sp.part = fx->part;
+            } else {
+                e = split_workspace(s, need, &sp.part);
+                if (e != hipSuccess) return e;
+            }
         }
     }
     const int items = sp.Tdp + (T - sp.Tdp) * sp.parts;
@@ -1536,12 +1543,12 @@ hipError_t launch_one(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
 template <int BMODE>
 hipError_t launch_mode(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                        const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
-                       void* c, bool c_bf16, float amul, hipStream_t s) {
+                       void* c, bool c_bf16, float amul, hipStream_t s, const FixedScratch* fx) {
     // the register-decode kernel addresses operands and C with 32-bit offsets
     const int64_t kLim = (int64_t)1 << 31;
     if (K % (4 * BK) == 0 && K > 0 && M * (K / 2) < kLim && N * (K / 2) < kLim && M * N * 4 < kLim)
-        return c_bf16 ? launch_reg<BMODE, true>(M, N, K, a, as, ad, b, bs, bd, c, amul, s)
-                      : launch_reg<BMODE, false>(M, N, K, a, as, ad, b, bs, bd, c, amul, s);
+        return c_bf16 ? launch_reg<BMODE, true>(M, N, K, a, as, ad, b, bs, bd, c, amul, s, fx)
+                      : launch_reg<BMODE, false>(M, N, K, a, as, ad, b, bs, bd, c, amul, s, fx);
     if (K % BK == 0 && K > 0)
         return c_bf16 ? launch_dma<BMODE, true>(M, N, K, a, as, ad, b, bs, bd, c, amul, s)
                       : launch_dma<BMODE, false>(M, N, K, a, as, ad, b, bs, bd, c, amul, s);
@@ -1554,15 +1561,18 @@ hipError_t launch_mode(int64_t M, int64_t N, int64_t K, const uint8_t* a, const 
 hipError_t launch_gemm(BScale bmode, float amul, int64_t M, int64_t N, int64_t K, const uint8_t* a,
                        const uint8_t* a_scales, const float* a_dec, const uint8_t* b,
                        const uint8_t* b_scales, const float* b_dec, void* c, bool c_bf16,
-                       hipStream_t s) {
+                       hipStream_t s, const FixedScratch* fx) {
     if (M == 0 || N == 0) return hipSuccess;
     switch (bmode) {
         case BScale::Row:
-            return launch_mode<(int)BScale::Row>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, amul, s);
+            return launch_mode<(int)BScale::Row>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, amul, s,
+                                                 fx);
         case BScale::Tile:
-            return launch_mode<(int)BScale::Tile>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, amul, s);
+            return launch_mode<(int)BScale::Tile>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, amul,
+                                                  s, fx);
         case BScale::TileDgrad:
-            return launch_mode<(int)BScale::TileDgrad>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16, amul, s);
+            return launch_mode<(int)BScale::TileDgrad>(M, N, K, a, a_scales, a_dec, b, b_scales, b_dec, c, c_bf16,
+                                                       amul, s, fx);
     }
     return hipErrorInvalidValue;
 }

@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_status_strings(lib):
-    for s in range(6):
+    for s in range(7):
         assert ue.status_string(s)
     assert ue.status_string(99) == "unknown status"
 

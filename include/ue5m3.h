@@ -31,7 +31,9 @@
  * - Stream capture: a call made while `stream` is capturing that would have
  *   to allocate or grow a workspace returns UE5M3_EHIP and enqueues
  *   nothing; run the same call once before capturing (no library call
- *   records a memset node).
+ *   records a memset node).  A captured graph uses the workspaces of the
+ *   stream it was captured on: replay it on that stream, or never while a
+ *   call on that stream may run.
  * - bf16 tensors are dense row-major [rows, cols] arrays of 16-bit words.
  * - Payloads pack two E2M1 nibbles per byte along a row: byte [r, c/2] holds
  *   element (r, c) in its low nibble and (r, c+1) in its high nibble.

@@ -769,8 +769,12 @@ __device__ __forceinline__ WorkItem work_item(int it, const SplitPlan& sp, int N
 // block (the products are issued as B x A^T).  A split part stores its fp32
 // partial; a whole tile stores alpha * value through a buffer resource over
 // C, where an out-of-range offset drops the store, which masks rows and
-// columns past C without branches.
-template <bool OUT_BF16>
+// columns past C without branches.  VEC (a launch-time choice, so that the
+// whole-tile path is straight-line code and the accumulators are read out
+// one row block at a time): N % 8 == 0 for bf16, N % 4 == 0 for fp32, where
+// every run of 8 (4) output columns lies wholly inside C or wholly past it;
+// otherwise each element is masked on its own.
+template <bool OUT_BF16, bool VEC>
 __device__ __forceinline__ void store_item(const f32x16_t (&acc)[4][4], const WorkItem& cur,
                                            const SplitPlan& sp, int M, int N, int tiles_m, int tiles_n,
                                            int wave, int lane, float alpha, void* __restrict__ C) {
@@ -795,86 +799,79 @@ __device__ __forceinline__ void store_item(const f32x16_t (&acc)[4][4], const Wo
                 }
             __builtin_amdgcn_sched_barrier(0);
         }
-    } else {
-            constexpr uint32_t esz = OUT_BF16 ? 2 : 4;
-        constexpr uint32_t kOff = 0x80000000u;               // past every buffer
-        const __amdgpu_buffer_rsrc_t cr =
-            __builtin_amdgcn_make_buffer_rsrc(C, 0, (int)((uint32_t)M * (uint32_t)N * esz), 0x00020000);
-        int64_t m0, n0;
-        tile_origin(cur.t, tiles_m, tiles_n, m0, n0);
-        const int mrow = (int)m0 + wm * 128 + r;
-        const int ncol = (int)n0 + wn * 128 + hi * 4;
-        const bool vec = (N & 3) == 0;
-        if (OUT_BF16 && (N & 7) == 0) {
-            // bf16 with N % 8 == 0: lanes l and l + 32 hold the two halves
-            // of each run of 8 columns; one lane-half swap per pair of runs
-            // gives lane l runs 0 and 2 and lane l + 32 runs 1 and 3 whole,
-            // so every store is 16 bytes per lane (32 per row).
-            const int ncol8 = (int)n0 + wn * 128 + hi * 8;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int m = mrow + 32 * i;
-                const uint32_t rbase = ((uint32_t)m * (uint32_t)N + (uint32_t)ncol8) * 2u;
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-#pragma unroll
-                    for (int q = 0; q < 2; ++q) {
-                        const int g0 = 2 * q, g1 = 2 * q + 1;
-                        const uint32_t x0 = pack_bf16x2(alpha * acc[i][j][4 * g0], alpha * acc[i][j][4 * g0 + 1]);
-                        const uint32_t x1 = pack_bf16x2(alpha * acc[i][j][4 * g0 + 2], alpha * acc[i][j][4 * g0 + 3]);
-                        const uint32_t y0 = pack_bf16x2(alpha * acc[i][j][4 * g1], alpha * acc[i][j][4 * g1 + 1]);
-                        const uint32_t y1 = pack_bf16x2(alpha * acc[i][j][4 * g1 + 2], alpha * acc[i][j][4 * g1 + 3]);
-                        const auto s0 = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
-                        const auto s1 = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
-                        const u32x4_t d = {(uint32_t)s0[0], (uint32_t)s1[0], (uint32_t)s0[1], (uint32_t)s1[1]};
-                        const int n = ncol8 + 32 * j + 16 * q;
-                        const uint32_t vo = (m < M && n < N) ? rbase : kOff;
-                        __builtin_amdgcn_raw_buffer_store_b128(d, cr, vo + (uint32_t)(32 * j + 16 * q) * 2u, 0, 0);
-                    }
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        } else {
+        return;
+    }
+    constexpr uint32_t esz = OUT_BF16 ? 2 : 4;
+    constexpr uint32_t kOff = 0x80000000u;               // past every buffer
+    const __amdgpu_buffer_rsrc_t cr =
+        __builtin_amdgcn_make_buffer_rsrc(C, 0, (int)((uint32_t)M * (uint32_t)N * esz), 0x00020000);
+    int64_t m0, n0;
+    tile_origin(cur.t, tiles_m, tiles_n, m0, n0);
+    const int mrow = (int)m0 + wm * 128 + r;
+    if (OUT_BF16 && VEC) {
+        // bf16 with N % 8 == 0: lanes l and l + 32 hold the two halves of
+        // each run of 8 columns; one lane-half swap per pair of runs gives
+        // lane l runs 0 and 2 and lane l + 32 runs 1 and 3 whole, so every
+        // store is 16 bytes per lane (32 per row).
+        const int ncol8 = (int)n0 + wn * 128 + hi * 8;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int m = mrow + 32 * i;
-            const uint32_t rbase = ((uint32_t)m * (uint32_t)N + (uint32_t)ncol) * esz;
+            const uint32_t rbase = ((uint32_t)m * (uint32_t)N + (uint32_t)ncol8) * 2u;
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int n = ncol + 32 * j + 8 * g;
-                    const float v0 = alpha * acc[i][j][4 * g + 0], v1 = alpha * acc[i][j][4 * g + 1];
-                    const float v2 = alpha * acc[i][j][4 * g + 2], v3 = alpha * acc[i][j][4 * g + 3];
-                    const uint32_t imm = (uint32_t)(32 * j + 8 * g) * esz;
-                    if (vec) {
-                        // N % 4 == 0: a run is inside C or wholly past it
-                        const uint32_t vo = (m < M && n < N) ? rbase : kOff;
-                        if (OUT_BF16) {
-                            const u32x2_t d = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-                            __builtin_amdgcn_raw_buffer_store_b64(d, cr, vo + imm, 0, 0);
-                        } else {
-                            const f32x4_t d = {v0, v1, v2, v3};
-                            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, d), cr, vo + imm,
-                                                                   0, 0);
-                        }
-                    } else {
-                        const float vv[4] = {v0, v1, v2, v3};
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const uint32_t vo = (m < M && n + q < N) ? rbase : kOff;
-                            if (OUT_BF16) {
-                                __builtin_amdgcn_raw_buffer_store_b16(
-                                    (unsigned short)pack_bf16x2(vv[q], 0.0f), cr, vo + imm + q * esz, 0, 0);
-                            } else {
-                                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(vv[q]), cr,
-                                                                      vo + imm + q * esz, 0, 0);
-                            }
-                        }
-                    }
+                for (int q = 0; q < 2; ++q) {
+                    const int g0 = 2 * q, g1 = 2 * q + 1;
+                    const uint32_t x0 = pack_bf16x2(alpha * acc[i][j][4 * g0], alpha * acc[i][j][4 * g0 + 1]);
+                    const uint32_t x1 = pack_bf16x2(alpha * acc[i][j][4 * g0 + 2], alpha * acc[i][j][4 * g0 + 3]);
+                    const uint32_t y0 = pack_bf16x2(alpha * acc[i][j][4 * g1], alpha * acc[i][j][4 * g1 + 1]);
+                    const uint32_t y1 = pack_bf16x2(alpha * acc[i][j][4 * g1 + 2], alpha * acc[i][j][4 * g1 + 3]);
+                    const auto s0 = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
+                    const auto s1 = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
+                    const u32x4_t d = {(uint32_t)s0[0], (uint32_t)s1[0], (uint32_t)s0[1], (uint32_t)s1[1]};
+                    const int n = ncol8 + 32 * j + 16 * q;
+                    const uint32_t vo = (m < M && n < N) ? rbase : kOff;
+                    __builtin_amdgcn_raw_buffer_store_b128(d, cr, vo + (uint32_t)(32 * j + 16 * q) * 2u, 0, 0);
                 }
             __builtin_amdgcn_sched_barrier(0);
         }
-        }
+        return;
+    }
+    const int ncol = (int)n0 + wn * 128 + hi * 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int m = mrow + 32 * i;
+        const uint32_t rbase = ((uint32_t)m * (uint32_t)N + (uint32_t)ncol) * esz;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int n = ncol + 32 * j + 8 * g;
+                const float v0 = alpha * acc[i][j][4 * g + 0], v1 = alpha * acc[i][j][4 * g + 1];
+                const float v2 = alpha * acc[i][j][4 * g + 2], v3 = alpha * acc[i][j][4 * g + 3];
+                const uint32_t imm = (uint32_t)(32 * j + 8 * g) * esz;
+                if (VEC) {
+                    // fp32 with N % 4 == 0: a run is inside C or wholly past it
+                    const uint32_t vo = (m < M && n < N) ? rbase : kOff;
+                    const f32x4_t d = {v0, v1, v2, v3};
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, d), cr, vo + imm, 0, 0);
+                } else {
+                    const float vv[4] = {v0, v1, v2, v3};
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const uint32_t vo = (m < M && n + q < N) ? rbase : kOff;
+                        if (OUT_BF16) {
+                            __builtin_amdgcn_raw_buffer_store_b16(
+                                (unsigned short)pack_bf16x2(vv[q], 0.0f), cr, vo + imm + q * esz, 0, 0);
+                        } else {
+                            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(vv[q]), cr,
+                                                                  vo + imm + q * esz, 0, 0);
+                        }
+                    }
+                }
+            }
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -885,7 +882,7 @@ __device__ __forceinline__ void store_item(const f32x16_t (&acc)[4][4], const Wo
 // must have an even number of stages when a workgroup runs more than one
 // (the stage buffers alternate and every item starts in buffer 0).  Sizes:
 // every operand, C and the partial workspace span less than 2^31 bytes.
-template <int BMODE, bool OUT_BF16>
+template <int BMODE, bool OUT_BF16, bool VEC>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
     int M, int N, int K, int tiles_m, int tiles_n, int items, SplitPlan sp,
     const uint8_t* __restrict__ A, const uint8_t* __restrict__ As, const float* __restrict__ a_dec,
@@ -1068,8 +1065,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
         }
         if (G < cur.g1) stage(G, sP0, sC0, sP1, sC1, P0, S0);   // odd stage count (single item)
 
-        store_item<OUT_BF16>(acc, cur, sp, M, N, tiles_m, tiles_n, wave, lane,
-                             (a_dec[0] * b_dec[0]) * amul, C);   // operands were scaled by 2^-3
+        store_item<OUT_BF16, VEC>(acc, cur, sp, M, N, tiles_m, tiles_n, wave, lane,
+                                  (a_dec[0] * b_dec[0]) * amul, C);   // operands were scaled by 2^-3
         if (!has_next) break;
     }
     wait_vmem<0>();                                  // no load outlives the kernel's LDS
@@ -1191,7 +1188,7 @@ __device__ __forceinline__ void mfma_mx16(f32x16_t (&acc)[4][4], const MxSlice& 
         }
 }
 
-template <bool OUT_BF16>
+template <bool OUT_BF16, bool VEC>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_mx_kernel(
     int M, int N, int K, int tiles_m, int tiles_n, int items, SplitPlan sp,
     const uint8_t* __restrict__ A, const uint8_t* __restrict__ As, const float* __restrict__ a_dec,
@@ -1353,7 +1350,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_mx_kernel(
         __builtin_amdgcn_sched_barrier(0);
         asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 15" ::: "memory");
         __builtin_amdgcn_sched_barrier(0);
-        store_item<OUT_BF16>(acc, cur, sp, M, N, tiles_m, tiles_n, wave, lane, a_dec[0] * b_dec[0], C);
+        store_item<OUT_BF16, VEC>(acc, cur, sp, M, N, tiles_m, tiles_n, wave, lane, a_dec[0] * b_dec[0], C);
         if (!has_next) break;
     }
     wait_vmem<0>();                                  // no load outlives the kernel's LDS
@@ -1473,8 +1470,12 @@ hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
     // persistent (one workgroup per CU walking the items) when every item has
     // an even stage count, else one item per workgroup
     const int grid = (even && cus > 0) ? min(items, cus) : items;
-    hipLaunchKernelGGL((gemm_fp4_reg_kernel<BMODE, OUT_BF16>), dim3((unsigned)grid), dim3(kGemmThreads),
-                       0, s, (int)M, (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c, amul);
+    if (N % (OUT_BF16 ? 8 : 4) == 0)
+        hipLaunchKernelGGL((gemm_fp4_reg_kernel<BMODE, OUT_BF16, true>), dim3((unsigned)grid), dim3(kGemmThreads),
+                           0, s, (int)M, (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c, amul);
+    else
+        hipLaunchKernelGGL((gemm_fp4_reg_kernel<BMODE, OUT_BF16, false>), dim3((unsigned)grid), dim3(kGemmThreads),
+                           0, s, (int)M, (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c, amul);
     if ((e = hipGetLastError()) != hipSuccess || sp.parts == 1) return e;
     hipLaunchKernelGGL((gemm_split_sum_kernel<BMODE, OUT_BF16>), dim3((unsigned)(64 * (T - sp.Tdp))), dim3(256),
                        0, s, M, N, tiles_m, tiles_n, sp, ad, bd, c, amul);
@@ -1507,8 +1508,12 @@ hipError_t launch_mx(int64_t M, int64_t N, int64_t K, const uint8_t* a, const ui
     }
     const int items = sp.Tdp + (T - sp.Tdp) * sp.parts;
     const int grid = (even && cus > 0) ? min(items, cus) : items;
-    hipLaunchKernelGGL((gemm_mx_kernel<OUT_BF16>), dim3((unsigned)grid), dim3(kGemmThreads), 0, s, (int)M,
-                       (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c);
+    if (N % (OUT_BF16 ? 8 : 4) == 0)
+        hipLaunchKernelGGL((gemm_mx_kernel<OUT_BF16, true>), dim3((unsigned)grid), dim3(kGemmThreads), 0, s, (int)M,
+                           (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c);
+    else
+        hipLaunchKernelGGL((gemm_mx_kernel<OUT_BF16, false>), dim3((unsigned)grid), dim3(kGemmThreads), 0, s,
+                           (int)M, (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c);
     if ((e = hipGetLastError()) != hipSuccess || sp.parts == 1) return e;
     hipLaunchKernelGGL((gemm_split_sum_kernel<(int)BScale::Row, OUT_BF16>), dim3((unsigned)(64 * (T - sp.Tdp))),
                        dim3(256), 0, s, M, N, tiles_m, tiles_n, sp, ad, bd, c, 1.0f);

@@ -702,160 +702,200 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
 // The row blocking (blocks of 16 along each row) and the column blocking
 // (blocks of 16 down each column, stored transposed) of one tensor from a
 // single read of it -- the two operands of a backward pass (dY: dgrad and
-// wgrad) or of X (fprop and wgrad).  A workgroup covers 128 rows (8 tile
-// rows; thread t handles tile row t / 32) x 128 columns (lane q = t % 32
-// holds columns 4q .. 4q+3), i.e. a 16 x 4 piece per lane: its 4 column
-// blocks are in-lane, each row block spans the 4 lanes 4k .. 4k+3 (maxima
-// combined by two lane swaps).  Row payloads go out straight from registers
-// (32 lanes x 2 bytes = 64 contiguous bytes per row); the transposed payload
-// and both scale arrays are assembled in LDS.  SR words use tensor id
-// tid_r for the row blocking and tid_c for the column blocking.
+// wgrad) or of X (fprop and wgrad).  A tile is 128 rows (8 tile rows; thread
+// t handles tile row t / 32) x 128 columns (lane q = t % 32 holds columns
+// 4q .. 4q+3), i.e. a 16 x 4 piece per lane: its 4 column blocks are
+// in-lane, each row block spans the 4 lanes 4k .. 4k+3 (maxima combined by
+// two quad permutations).  Row payloads go out straight from registers (32
+// lanes x 2 bytes = 64 contiguous bytes per row); the transposed payload and
+// both scale arrays are assembled in LDS.  SR words use tensor id tid_r for
+// the row blocking and tid_c for the column blocking.
+//
+// Persistent: workgroup w walks tiles w, w + grid, ... (tile columns
+// fastest), loading the next tile while it quantizes the current one.  The
+// LDS stage alternates between two buffers, so one barrier per tile
+// separates a tile's LDS writes from its stores and the stores of tile k
+// from the writes of tile k + 2.
+struct DualStage {
+    uint8_t P[kTileCols][kTileRowTiles * 8];          // transposed payload, 64 B per column
+    uint8_t SR[kTileRowTiles * 16][kTileCols / 16];   // row scales, 8 per row
+    uint8_t SC[kTileCols][kTileRowTiles];             // column scales, 8 per column
+};
+
 template <bool SR, int FMT>
 __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
-    const uint16_t* __restrict__ x, int64_t rows, int64_t cols, const float* __restrict__ amax_dev,
-    float T, uint32_t key0, uint32_t key1, uint32_t tid_r, uint32_t tid_c,
-    uint8_t* __restrict__ payload_r, uint8_t* __restrict__ scales_r, uint8_t* __restrict__ payload_c,
-    uint8_t* __restrict__ scales_c, float* __restrict__ dec_out) {
-    __shared__ __attribute__((aligned(16))) uint8_t stP[kTileCols][kTileRowTiles * 8];
-    __shared__ __attribute__((aligned(16))) uint8_t stSR[kTileRowTiles * 16][kTileCols / 16];
-    __shared__ __attribute__((aligned(16))) uint8_t stSC[kTileCols][kTileRowTiles];
+    const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t gx, int64_t ntiles,
+    const float* __restrict__ amax_dev, float T, uint32_t key0, uint32_t key1, uint32_t tid_r,
+    uint32_t tid_c, uint8_t* __restrict__ payload_r, uint8_t* __restrict__ scales_r,
+    uint8_t* __restrict__ payload_c, uint8_t* __restrict__ scales_c, float* __restrict__ dec_out) {
+    __shared__ __attribute__((aligned(16))) DualStage stage[2];
     static_assert(FMT != (int)ScaleKind::E8M0, "blocks of 16");
     const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
-    if (dec_out != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *dec_out = m.dec;
+    if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
     const int t = threadIdx.x;
     const int q = t & 31, trl = t >> 5;
-    const int64_t cw = (int64_t)blockIdx.x * kTileCols;
-    const int64_t c = cw + 4 * q;
-    const int64_t tr = (int64_t)blockIdx.y * kTileRowTiles + trl;     // tile row
     const int64_t ntr = rows / 16;
-    const bool active = (c < cols) && (tr < ntr);                     // cols % 16 == 0
-    if (active) {
+    const bool vec_scales = (cols % 128) == 0 && (ntr % 8) == 0;   // 8-byte scale runs aligned
+
+    // 16 rows x 4 columns of this lane's piece of tile `it`: word pairs
+    // (c, c+1) in L, (c+2, c+3) in H (left untouched outside the tensor)
+    auto load = [&](int64_t it, uint32_t (&L)[16], uint32_t (&H)[16]) {
+        const int64_t c = (it % gx) * kTileCols + 4 * q;
+        const int64_t tr = (it / gx) * kTileRowTiles + trl;
+        if (c >= cols || tr >= ntr) return;                           // cols % 16 == 0: whole pieces
         const uint16_t* src = x + (tr * 16) * cols + c;
-        uint32_t lo[16], hi[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const uint2 v = *reinterpret_cast<const uint2*>(src + r * cols);
-            lo[r] = v.x;
-            hi[r] = v.y;
+            L[r] = v.x;
+            H[r] = v.y;
         }
-        // column blocks: in-lane maxima of the 4 columns
-        uint32_t mc[4] = {0u, 0u, 0u, 0u};
+    };
+
+    int64_t it = blockIdx.x;
+    if (it >= ntiles) return;                                        // uniform
+    uint32_t lo[16], hi[16], nlo[16], nhi[16];
+    load(it, lo, hi);
+    for (int buf = 0;; buf ^= 1) {
+        const int64_t nit = it + gridDim.x;
+        if (nit < ntiles) load(nit, nlo, nhi);
+        DualStage& st = stage[buf];
+        const int64_t cw = (it % gx) * kTileCols;
+        const int64_t c = cw + 4 * q;
+        const int64_t tr0 = (it / gx) * kTileRowTiles;
+        const int64_t tr = tr0 + trl;
+        if (c < cols && tr < ntr) {
+            // column blocks: in-lane maxima of the 4 columns
+            uint32_t mc[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            mc[0] = max(mc[0], lo[r] & 0x7FFFu);
-            mc[1] = max(mc[1], (lo[r] >> 16) & 0x7FFFu);
-            mc[2] = max(mc[2], hi[r] & 0x7FFFu);
-            mc[3] = max(mc[3], (hi[r] >> 16) & 0x7FFFu);
-        }
-        BlockScale bc[4];
+            for (int r = 0; r < 16; ++r) {
+                mc[0] = max(mc[0], lo[r] & 0x7FFFu);
+                mc[1] = max(mc[1], (lo[r] >> 16) & 0x7FFFu);
+                mc[2] = max(mc[2], hi[r] & 0x7FFFu);
+                mc[3] = max(mc[3], (hi[r] >> 16) & 0x7FFFu);
+            }
+            BlockScale bc[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) bc[j] = block_scale<FMT>(mc[j], m);
-        uint32_t pk[4][2];
-        if (SR) {
-            sr_cols16x4<true>(lo, hi, bc, (uint64_t)(tr * 16) * (uint64_t)cols + (uint64_t)c,
-                              (uint64_t)cols, tid_c, key0, key1, pk);
-        } else {
-            const uint32_t nw[16] = {};
+            for (int j = 0; j < 4; ++j) bc[j] = block_scale<FMT>(mc[j], m);
+            uint32_t pk[4][2];
+            if (SR) {
+                sr_cols16x4<true>(lo, hi, bc, (uint64_t)(tr * 16) * (uint64_t)cols + (uint64_t)c,
+                                  (uint64_t)cols, tid_c, key0, key1, pk);
+            } else {
+                const uint32_t nw[16] = {};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    float xv[16];
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        xv[r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
+                    quant_col16<false>(xv, bc[j].r, nw, pk[j][0], pk[j][1]);
+                }
+            }
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                float xv[16];
+                *reinterpret_cast<uint2*>(&st.P[4 * q + j][trl * 8]) = make_uint2(pk[j][0], pk[j][1]);
+                st.SC[4 * q + j][trl] = (uint8_t)bc[j].code;
+            }
+            // row blocks: one per row over the lane quad 4k .. 4k+3.  Maxima
+            // are combined by quad permutations; lane k of the quad derives
+            // the scales of rows k, k+4, k+8, k+12 and the others take them
+            // by a quad broadcast, so each block scale is computed once.
+            uint32_t mrow[16];
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    xv[r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
-                quant_col16<false>(xv, bc[j].r, nw, pk[j][0], pk[j][1]);
+            for (int r = 0; r < 16; ++r) {
+                uint32_t mr = max(bf16_abs_max_pair(lo[r]), bf16_abs_max_pair(hi[r]));
+                mr = max(mr, (uint32_t)__builtin_amdgcn_mov_dpp((int)mr, 0xB1, 0xF, 0xF, false));   // quad xor 1
+                mr = max(mr, (uint32_t)__builtin_amdgcn_mov_dpp((int)mr, 0x4E, 0xF, 0xF, false));   // quad xor 2
+                mrow[r] = mr;
+            }
+            const int qk = q & 3;
+            BlockScale own[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                // row 4u + qk of this lane's quad position
+                const uint32_t mo = qk == 0 ? mrow[4 * u] : qk == 1 ? mrow[4 * u + 1]
+                                  : qk == 2 ? mrow[4 * u + 2] : mrow[4 * u + 3];
+                own[u] = block_scale<FMT>(mo, m);
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                // broadcast of quad lane r % 4 (its own[r / 4])
+                BlockScale br;
+                const int ov = __float_as_int(own[r >> 2].r);
+                const int src = r & 3;
+                br.r = __int_as_float(src == 0 ? __builtin_amdgcn_mov_dpp(ov, 0x00, 0xF, 0xF, false)
+                                      : src == 1 ? __builtin_amdgcn_mov_dpp(ov, 0x55, 0xF, 0xF, false)
+                                      : src == 2 ? __builtin_amdgcn_mov_dpp(ov, 0xAA, 0xF, 0xF, false)
+                                                 : __builtin_amdgcn_mov_dpp(ov, 0xFF, 0xF, 0xF, false));
+                br.code = own[r >> 2].code;              // valid in quad lane r % 4, which stores it
+                const float y[4] = {bf16_lo(lo[r]) * br.r, bf16_hi(lo[r]) * br.r, bf16_lo(hi[r]) * br.r,
+                                    bf16_hi(hi[r]) * br.r};
+                uint32_t p;
+                if (SR) {
+                    uint32_t wd[4];
+                    words4<true>((uint64_t)(tr * 16 + r) * (uint64_t)cols + (uint64_t)c, tid_r, key0, key1, wd);
+                    p = sr4(y, wd);
+                } else {
+                    p = 0u;
+                    p = rn_pair<0>(p, y[0], y[1]);
+                    p = rn_pair<1>(p, y[2], y[3]);
+                }
+                *reinterpret_cast<uint16_t*>(payload_r + (tr * 16 + r) * (cols / 2) + c / 2) = (uint16_t)p;
+                if (qk == (r & 3)) st.SR[trl * 16 + r][q >> 2] = (uint8_t)br.code;
+                // one row at a time: keeps the live Philox words to 4
+                if (SR) __builtin_amdgcn_sched_barrier(0);
             }
         }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            *reinterpret_cast<uint2*>(&stP[4 * q + j][trl * 8]) = make_uint2(pk[j][0], pk[j][1]);
-            stSC[4 * q + j][trl] = (uint8_t)bc[j].code;
+        __syncthreads();
+        const int nvalid = (int)min((int64_t)kTileRowTiles, ntr - tr0);
+        // transposed payload: 2 lanes per column, 32 bytes each
+        {
+            const int col = t >> 1, half = t & 1;
+            const int64_t gc = cw + col;
+            if (gc < cols) {
+                uint8_t* dst = payload_c + gc * (rows / 2) + tr0 * 8 + half * 32;
+                const uint8_t* sp = &st.P[col][half * 32];
+                if (nvalid == kTileRowTiles && ((rows / 2) & 15) == 0) {
+                    *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(sp);
+                    *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(sp + 16);
+                } else {
+                    for (int k = half * 4; k < half * 4 + 4; ++k)
+                        if (k < nvalid)
+                            *reinterpret_cast<uint2*>(dst + (k - half * 4) * 8) =
+                                *reinterpret_cast<const uint2*>(sp + (k - half * 4) * 8);
+                }
+            }
         }
-        // row blocks: one per row over the lane quad 4k .. 4k+3.  Maxima
-        // are combined by quad permutations; lane k of the quad derives the
-        // scales of rows k, k+4, k+8, k+12 and the others take them by a
-        // quad broadcast, so each block scale is computed once.
-        uint32_t mrow[16];
+        if (t < kTileCols) {
+            // column scales [cols, rows/16]: 8 bytes per column
+            const int64_t gc = cw + t;
+            if (gc < cols) {
+                uint8_t* dst = scales_c + gc * ntr + tr0;
+                if (vec_scales && nvalid == kTileRowTiles)
+                    *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(&st.SC[t][0]);
+                else
+                    for (int k = 0; k < nvalid; ++k) dst[k] = st.SC[t][k];
+            }
+        } else {
+            // row scales [rows, cols/16]: 8 bytes per row
+            const int row = t - kTileCols;
+            const int64_t gr = tr0 * 16 + row;
+            if (row < nvalid * 16) {
+                const int64_t nb = min((int64_t)(kTileCols / 16), (cols - cw) / 16);
+                uint8_t* dst = scales_r + gr * (cols / 16) + cw / 16;
+                if (vec_scales && nb == kTileCols / 16)
+                    *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(&st.SR[row][0]);
+                else
+                    for (int k = 0; k < nb; ++k) dst[k] = st.SR[row][k];
+            }
+        }
+        if (nit >= ntiles) break;                                   // uniform
+        it = nit;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            uint32_t mr = max(bf16_abs_max_pair(lo[r]), bf16_abs_max_pair(hi[r]));
-            mr = max(mr, (uint32_t)__builtin_amdgcn_mov_dpp((int)mr, 0xB1, 0xF, 0xF, false));   // quad xor 1
-            mr = max(mr, (uint32_t)__builtin_amdgcn_mov_dpp((int)mr, 0x4E, 0xF, 0xF, false));   // quad xor 2
-            mrow[r] = mr;
-        }
-        const int qk = q & 3;
-        BlockScale own[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            // row 4u + qk of this lane's quad position
-            const uint32_t mo = qk == 0 ? mrow[4 * u] : qk == 1 ? mrow[4 * u + 1] : qk == 2 ? mrow[4 * u + 2] : mrow[4 * u + 3];
-            own[u] = block_scale<FMT>(mo, m);
-        }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            // broadcast of quad lane r % 4 (its own[r / 4])
-            BlockScale br;
-            const int ov = __float_as_int(own[r >> 2].r);
-            const int src = r & 3;
-            br.r = __int_as_float(src == 0 ? __builtin_amdgcn_mov_dpp(ov, 0x00, 0xF, 0xF, false)
-                                  : src == 1 ? __builtin_amdgcn_mov_dpp(ov, 0x55, 0xF, 0xF, false)
-                                  : src == 2 ? __builtin_amdgcn_mov_dpp(ov, 0xAA, 0xF, 0xF, false)
-                                             : __builtin_amdgcn_mov_dpp(ov, 0xFF, 0xF, 0xF, false));
-            br.code = own[r >> 2].code;                  // valid in quad lane r % 4, which stores it
-            const float y[4] = {bf16_lo(lo[r]) * br.r, bf16_hi(lo[r]) * br.r, bf16_lo(hi[r]) * br.r,
-                                bf16_hi(hi[r]) * br.r};
-            uint32_t p;
-            if (SR) {
-                uint32_t wd[4];
-                words4<true>((uint64_t)(tr * 16 + r) * (uint64_t)cols + (uint64_t)c, tid_r, key0, key1, wd);
-                p = sr4(y, wd);
-            } else {
-                p = 0u;
-                p = rn_pair<0>(p, y[0], y[1]);
-                p = rn_pair<1>(p, y[2], y[3]);
-            }
-            *reinterpret_cast<uint16_t*>(payload_r + (tr * 16 + r) * (cols / 2) + c / 2) = (uint16_t)p;
-            if (qk == (r & 3)) stSR[trl * 16 + r][q >> 2] = (uint8_t)br.code;
-            // one row at a time: keeps the live Philox words to 4
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    }
-    __syncthreads();
-    const int64_t tr0 = (int64_t)blockIdx.y * kTileRowTiles;
-    const int nvalid = (int)min((int64_t)kTileRowTiles, ntr - tr0);
-    // transposed payload: 2 lanes per column, 32 bytes each
-    {
-        const int col = t >> 1, half = t & 1;
-        const int64_t gc = cw + col;
-        if (gc < cols) {
-            uint8_t* dst = payload_c + gc * (rows / 2) + tr0 * 8 + half * 32;
-            const uint8_t* sp = &stP[col][half * 32];
-            if (nvalid == kTileRowTiles && ((rows / 2) & 15) == 0) {
-                *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(sp);
-                *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(sp + 16);
-            } else {
-                for (int k = half * 4; k < half * 4 + 4; ++k)
-                    if (k < nvalid)
-                        *reinterpret_cast<uint2*>(dst + (k - half * 4) * 8) =
-                            *reinterpret_cast<const uint2*>(sp + (k - half * 4) * 8);
-            }
-        }
-    }
-    // column scales [cols, rows/16]: up to 8 bytes per column
-    if (t < kTileCols) {
-        const int64_t gc = cw + t;
-        if (gc < cols) {
-            uint8_t* dst = scales_c + gc * ntr + tr0;
-            for (int k = 0; k < nvalid; ++k) dst[k] = stSC[t][k];
-        }
-    }
-    // row scales [rows, cols/16]: up to 8 bytes per row
-    {
-        const int row = t >> 1;
-        const int64_t gr = tr0 * 16 + row;
-        if (row < nvalid * 16 && (t & 1) == 0) {
-            const int64_t nb = min((int64_t)(kTileCols / 16), (cols - cw) / 16);
-            uint8_t* dst = scales_r + gr * (cols / 16) + cw / 16;
-            for (int k = 0; k < nb; ++k) dst[k] = stSR[row][k];
+            lo[r] = nlo[r];
+            hi[r] = nhi[r];
         }
     }
 }
@@ -972,14 +1012,18 @@ hipError_t launch_dual_fmt(const void* x_bf16, int64_t rows, int64_t cols, const
     seed_key(seed, k0, k1);
     const int64_t gx = (cols + kTileCols - 1) / kTileCols;
     const int64_t gy = (rows / 16 + kTileRowTiles - 1) / kTileRowTiles;
+    const int64_t ntiles = gx * gy;
+    const int64_t resident = sr ? resident_wgs(quant_dual_kernel<true, FMT>, 12 + FMT)
+                                : resident_wgs(quant_dual_kernel<false, FMT>, 14 + FMT);
+    const int64_t grid = min(ntiles, resident);
     const uint16_t* x = reinterpret_cast<const uint16_t*>(x_bf16);
     if (sr)
-        hipLaunchKernelGGL((quant_dual_kernel<true, FMT>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads), 0,
-                           s, x, rows, cols, amax_dev, target, k0, k1, tid_r, tid_c, payload_r, scales_r,
+        hipLaunchKernelGGL((quant_dual_kernel<true, FMT>), dim3((unsigned)grid), dim3(kThreads), 0, s, x, rows,
+                           cols, gx, ntiles, amax_dev, target, k0, k1, tid_r, tid_c, payload_r, scales_r,
                            payload_c, scales_c, dec_out);
     else
-        hipLaunchKernelGGL((quant_dual_kernel<false, FMT>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads), 0,
-                           s, x, rows, cols, amax_dev, target, k0, k1, tid_r, tid_c, payload_r, scales_r,
+        hipLaunchKernelGGL((quant_dual_kernel<false, FMT>), dim3((unsigned)grid), dim3(kThreads), 0, s, x, rows,
+                           cols, gx, ntiles, amax_dev, target, k0, k1, tid_r, tid_c, payload_r, scales_r,
                            payload_c, scales_c, dec_out);
     return hipGetLastError();
 }

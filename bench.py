@@ -5,14 +5,20 @@ A step is the whole per-linear hot path on the Nemotron-H-8B FFN
 up-projection (T = 8192 tokens, K = 4096, N = 21504):
   sample-and-hold amax (D = 50; a refresh launches the amax kernels),
   X rows and columns RN (re-blocked along tokens) from one read, W 16x16
-  tiles RN (+ the transposed payload), dY rows SR, dY columns SR (two
-  kernels: SR is VALU-bound, and the one-read form is no faster there),
+  tiles RN (+ the transposed payload), dY rows SR, dY columns SR,
   fprop Y = X W^T (bf16 out), dgrad dX = dY W (bf16 out),
   wgrad dW = dY^T X (fp32 out).
-Inputs are seeded synthetic bf16 tensors resident in HBM before timing.
+Inputs are seeded synthetic bf16 tensors resident in HBM before timing; the
+step cycles through four input and output sets (over 2 GB) so that no step
+reads what the previous one left in the 256 MB Infinity Cache.  The
+refresh-step amax is timed on its own and charged at its 1/D rate.
 
 Prints ONE JSON line.  ``value`` = emulated-FP4 GEMM TFLOP/s of the whole
-step (3 x 2TNK flops / step wall time, quantizers and amax included).
+step (3 x 2TNK flops / step time, quantizers and amax included).  Beside it:
+per-kernel HIP-event times inside the timed region, each quantizer alone on
+the rotating sets, the quantizer-only workload (activation / gradient /
+weight), the single small linear's latency, the roofline of the fprop GEMM
+and the oracle's CPU baseline (timed first, on the host cores).
 """
 
 import argparse
@@ -101,57 +107,111 @@ def quant_bytes_2d(rows, cols, transposed):
 
 
 # ------------------------------------------------------------ CPU leg ----
-def cpu_baseline(wl, T, K, N, target_s=12.0):
-    """The oracle, as it stands, on a bounded sample of the same step:
-    quantizers on 1/64 row slices of X, W, dY (cost per element is size-
-    independent, so time x 64); GEMMs on a sampled sub-problem (time x the
-    flop ratio).  Returns the projected whole-step rate in TFLOP/s."""
+_POOL = {}
+
+
+def _pool_quantize(job):
+    """One worker's row shard of an oracle quantization (forked worker; the
+    tensors come from _POOL)."""
+    from oracle import quantize as oq
+    kind, r0, r1 = job
+    x = _POOL[kind]
+    g = _POOL["g_" + kind]
+    if kind == "w":
+        oq.quantize_2d(x[r0:r1], g)
+    elif kind == "x":
+        oq.quantize_1d(x[r0:r1], 1, g)
+    else:
+        rows = np.arange(r0, r1, dtype=np.int64)
+        idx = rows[:, None] * x.shape[1] + np.arange(x.shape[1], dtype=np.int64)[None, :]
+        oq.quantize_1d(x[r0:r1], 1, g, 448.0, "sr", 1, 0, elem_index=idx)
+    return r1 - r0
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(T, K, N):
+    """The oracle, as it stands, timed on this host's cores (run before the
+    GPU is touched, so the worker pool forks a GPU-free process):
+      * the quantizer workload (activation [8192, 4096] rows RN, gradient
+        [8192, 4096] rows SR with Philox seed 1, weight [4096, 4096] 16 x 16
+        tiles RN) on the whole tensors, in one process and row-sharded over a
+        pool of all cores;
+      * the fprop product of the FFN up-projection shape (T x K by K x N) as a
+        float32 BLAS matmul on all cores, with decoded FP4 operands (the
+        weight's rows tiled from the decoded 4096 x 4096 weight).
+    The step estimate takes the pool's per-element quantizer cost for the
+    step's five quantizations and three fprop-sized products.  Returns the
+    cpu_baseline object (value in the metric's unit, TFLOP/s of GEMM work
+    per step)."""
+    import multiprocessing as mp
+    import synthetic
     from oracle import gemm as og
     from oracle import quantize as oq
     from oracle import scaling as osc
-    x, w, dy = wl["x"], wl["w"], wl["dy"]
-    f = 64
-    xs, ws, ds = x[: T // f], w[: (N // f) // 16 * 16], dy[: T // f]
-    gx, gw, gd = osc.amax(x), osc.amax(w), osc.amax(dy)
+    t_all = time.perf_counter()
+    wl = synthetic.quantizer_bandwidth(0)
+    x, dy, w = wl["x"], wl["dy"], wl["w"]
+    cores = min(len(os.sched_getaffinity(0)), 16)
+    res = {}
+    nbytes = {"x": quant_bytes_1d(*x.shape), "dy": quant_bytes_1d(*dy.shape), "w": quant_bytes_2d(*w.shape, False)}
+    _POOL.update({"x": x, "dy": dy, "w": w, "g_x": osc.amax(x), "g_dy": osc.amax(dy), "g_w": osc.amax(w)})
+    for kind in ("x", "dy", "w"):
+        t0 = time.perf_counter()
+        _pool_quantize((kind, 0, _POOL[kind].shape[0]))
+        res[kind] = {"single_s": round(time.perf_counter() - t0, 3)}
+    with mp.get_context("fork").Pool(cores) as pool:
+        for kind in ("x", "dy", "w"):
+            R = _POOL[kind].shape[0]
+            step = (R // (4 * cores)) // 16 * 16 or 16
+            jobs = [(kind, r, min(R, r + step)) for r in range(0, R, step)]
+            t0 = time.perf_counter()
+            assert sum(pool.map(_pool_quantize, jobs)) == R
+            res[kind]["pool_s"] = round(time.perf_counter() - t0, 3)
+    for kind in ("x", "dy", "w"):
+        res[kind]["single_GBps"] = round(nbytes[kind] / res[kind]["single_s"] / 1e9, 4)
+        res[kind]["pool_GBps"] = round(nbytes[kind] / res[kind]["pool_s"] / 1e9, 4)
+    _POOL.clear()
+    # fp32 BLAS fprop at the step's shape on decoded operands
+    xq = oq.quantize_1d(x, 1, osc.amax(x))
+    wq = oq.quantize_2d(w, osc.amax(w))
+    X = oq.decoded_1d(xq[0], xq[1], 1).astype(np.float32)[:T, :K]
+    Wd = oq.decoded_2d(wq[0], wq[1]).astype(np.float32)
+    W = np.ascontiguousarray(np.tile(Wd, ((N + Wd.shape[0] - 1) // Wd.shape[0], 1))[:N, :K])
+    al = og.alpha(xq[2], wq[3])
     t0 = time.perf_counter()
-    xr = oq.quantize_1d(xs, 1, gx)
-    xc = oq.quantize_1d(xs, 0, gx)
-    wq = oq.quantize_2d(ws, gw)
-    dr = oq.quantize_1d(ds, 1, gd, 448.0, "sr", 1, 1)
-    dc = oq.quantize_1d(ds, 0, gd, 448.0, "sr", 1, 2)
-    t_quant = (time.perf_counter() - t0)
-    quant_scale = (T * K + T * K + N * K + T * N + T * N) / (
-        xs.size + xs.size + ws.size + ds.size + ds.size)
-    # GEMM sample: fprop on (T/f) x (N/f) x K with the sampled operands
-    X = oq.decoded_1d(xr[0], xr[1], 1)
-    W = oq.decoded_2d(wq[0], wq[1])
-    al = og.alpha(xr[2], wq[3])
-    t0 = time.perf_counter()
-    reps = 0
-    while True:
-        og.fprop(X, W, al)
-        reps += 1
-        if time.perf_counter() - t0 > min(target_s, 5.0) or reps >= 50:
-            break
-    t_gemm = (time.perf_counter() - t0) / reps
-    flop_sample = 2.0 * X.shape[0] * W.shape[0] * K
-    flop_step = 3 * 2.0 * T * N * K
-    t_step = t_quant * quant_scale + t_gemm * flop_step / flop_sample
+    og.fprop(X, W, al, accumulate="fp32")
+    t_gemm = time.perf_counter() - t0
+    del X, W, Wd
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         blas_threads = None
-    # NumPy elementwise work (the quantizers) runs on one thread; the BLAS
-    # product of the GEMM sample on blas_threads
-    cores = blas_threads or 1
-    return {"value": flop_step / t_step / 1e12, "unit": "TFLOP/s", "cores": cores,
-            "blas_threads": blas_threads, "quantizer_threads": 1,
-            "host_cpus": len(os.sched_getaffinity(0)), "kind": "oracle",
-            "sample": (f"oracle quantizers on 1/{f} row slices of X, W, dY (x{quant_scale:.0f}) "
-                       f"+ float64 decoded-operand fprop on {X.shape[0]}x{W.shape[0]}x{K} "
-                       f"(x{flop_step / flop_sample:.0f} flops); projected step "
-                       f"{t_step:.1f} s")}
+    # step estimate: per-element quantizer cost of the pool run (1D RN and SR
+    # rows, 2D tiles) for the step's quantizations, plus three products
+    per_el = {k: res[k]["pool_s"] / (nbytes[k] / (2.5625 if k != "w" else 2.50390625)) for k in res}
+    t_quant = (2 * T * K * per_el["x"] + N * K * per_el["w"] + 2 * T * N * per_el["dy"])
+    flop_step = 3 * 2.0 * T * N * K
+    t_step = t_quant + 3 * t_gemm
+    return {"value": flop_step / t_step / 1e12, "unit": "TFLOP/s", "cores": max(cores, blas_threads or 1),
+            "kind": "oracle",
+            "sample": (f"oracle quantizers on the whole quantizer-workload tensors (activation 8192x4096 rows RN, "
+                       f"gradient 8192x4096 rows SR, weight 4096x4096 tiles RN), one process and a pool of "
+                       f"{cores} processes; float32 BLAS fprop {T}x{K} by {K}x{N} on {blas_threads} threads; "
+                       f"step estimate {t_step:.1f} s from the pool rates"),
+            "pool_processes": cores, "blas_threads": blas_threads, "host_cpus": len(os.sched_getaffinity(0)),
+            "cpu_model": _cpu_model(), "quantizers": res,
+            "gemm_fp32_blas": {"s": round(t_gemm, 3), "TFLOP/s": round(2.0 * T * N * K / t_gemm / 1e12, 4)},
+            "seconds": round(time.perf_counter() - t_all, 1)}
 
 
 def _decode_rows(payload, scales, fmt):
@@ -357,6 +417,107 @@ def gemm_shapes(dev):
     print(json.dumps({"gemm_shapes": out}), flush=True)
 
 
+NSETS = 4      # rotating input / output sets: > 512 MB, past the 256 MB Infinity Cache
+
+
+def _events(n):
+    import torch
+    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+
+def _time_kernel(fn, nsets, reps=30, warm=4):
+    """Median / mean device time of fn(i) over reps launches, fn cycling
+    through nsets buffer sets; HIP events on the current stream."""
+    import torch
+    for i in range(warm):
+        fn(i % nsets)
+    torch.cuda.synchronize()
+    evs = [(_events(2)) for _ in range(reps)]
+    for i in range(reps):
+        evs[i][0].record()
+        fn(i % nsets)
+        evs[i][1].record()
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in evs])
+    return float(np.median(ms)), float(ms.mean()), [round(float(q), 5) for q in np.percentile(ms, [10, 50, 90])]
+
+
+def quantizer_workload(dev):
+    """The quantizer-only workload: activation [8192, 4096] N(0,1) with 0.1% x100
+    outliers, rows RN; gradient [8192, 4096] N(0, 1e-4) with a lognormal row
+    scale, rows SR (Philox seed 1); weight [4096, 4096] N(0, 0.02), 16 x 16
+    tiles RN; current amax.  Each quantizer alone over NSETS rotating input
+    and output sets (640 MB of inputs), HIP events."""
+    import torch
+    import paper_2609_02846_amd as ue
+    import synthetic
+    wl = synthetic.quantizer_bandwidth(0)
+    up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+    base = {k: up(wl[k]) for k in ("x", "dy", "w")}
+    # sets 1.. are the same tensors scaled by 1 + i/128 (bf16): same distributions
+    sets = [{k: (v.float() * (1.0 + i / 128.0)).to(torch.bfloat16) if i else v for k, v in base.items()}
+            for i in range(NSETS)]
+    am = [{k: torch.empty(1, device=dev) for k in base} for _ in range(NSETS)]
+    for i in range(NSETS):
+        for k in base:
+            ue.amax_accumulate(sets[i][k], am[i][k], clear=True)
+    R, C = base["x"].shape
+    W = base["w"].shape[0]
+    u8 = lambda *sh: torch.empty(sh, dtype=torch.uint8, device=dev)
+    outs = [{"x": (u8(R, C // 2), u8(R, C // 16)), "dy": (u8(R, C // 2), u8(R, C // 16)),
+             "w": (u8(W, W // 2), u8(W // 16, W // 16))} for _ in range(NSETS)]
+    dec = torch.empty(1, device=dev)
+    fns = {"activation_rows_rn": (lambda i: ue.quantize_1d(sets[i]["x"], 1, am[i]["x"], 448.0, "rn", 0, 0,
+                                                          *outs[i]["x"], dec), quant_bytes_1d(R, C)),
+           "gradient_rows_sr": (lambda i: ue.quantize_1d(sets[i]["dy"], 1, am[i]["dy"], 448.0, "sr", 1, 0,
+                                                         *outs[i]["dy"], dec), quant_bytes_1d(R, C)),
+           "weight_tiles_rn": (lambda i: ue.quantize_2d(sets[i]["w"], am[i]["w"], 448.0, "rn", 0, 0, False,
+                                                        outs[i]["w"][0], outs[i]["w"][1], None, dec),
+                               quant_bytes_2d(W, W, False))}
+    res = {}
+    for name, (fn, nb) in fns.items():
+        med, mean, pct = _time_kernel(fn, NSETS)
+        gbs = nb / (med * 1e-3) / 1e9
+        res[name] = {"us": round(med * 1e3, 2), "GB/s": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
+                     "us_mean": round(mean * 1e3, 2)}
+    return res
+
+
+def small_linear_latency(dev):
+    """The single small linear (X [256, 512] with 1% x50 outliers, W [256,
+    512]; X rows RN, W 16 x 16 tiles RN, NT GEMM to fp32): device time per
+    launch of each kernel and of the whole forward, HIP events."""
+    import torch
+    import paper_2609_02846_amd as ue
+    import synthetic
+    wl = synthetic.linear_fprop_small(0)
+    up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+    x, w = up(wl["x"]), up(wl["w"])
+    ax, aw = torch.empty(1, device=dev), torch.empty(1, device=dev)
+    u8 = lambda *sh: torch.empty(sh, dtype=torch.uint8, device=dev)
+    xo = (u8(256, 256), u8(256, 32), torch.empty(1, device=dev))
+    wo = (u8(256, 256), u8(16, 32))
+    wd = torch.empty(1, device=dev)
+    y = torch.empty(256, 256, device=dev)
+
+    def fwd(_i=0):
+        ue.amax_accumulate(x, ax, clear=True)
+        ue.amax_accumulate(w, aw, clear=True)
+        ue.quantize_1d(x, 1, ax, 448.0, "rn", 0, 0, *xo)
+        ue.quantize_2d(w, aw, 448.0, "rn", 0, 0, False, wo[0], wo[1], None, wd)
+        ue.gemm("nt", 256, 256, 512, *xo, wo[0], wo[1], wd, out=y)
+    parts = {"amax_x_and_w": lambda i: (ue.amax_accumulate(x, ax, clear=True), ue.amax_accumulate(w, aw, clear=True)),
+             "quant_x_rows": lambda i: ue.quantize_1d(x, 1, ax, 448.0, "rn", 0, 0, *xo),
+             "quant_w_tiles": lambda i: ue.quantize_2d(w, aw, 448.0, "rn", 0, 0, False, wo[0], wo[1], None, wd),
+             "gemm_nt": lambda i: ue.gemm("nt", 256, 256, 512, *xo, wo[0], wo[1], wd, out=y),
+             "forward_total": fwd}
+    res = {}
+    for name, fn in parts.items():
+        med, mean, _ = _time_kernel(fn, 1, reps=200, warm=20)
+        res[name + "_us"] = round(med * 1e3, 2)
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -369,11 +530,15 @@ def main():
     if args.formats:
         formats_bench(args)
         return
+    T, K, N = args.tokens, args.k, args.n
+    want_cpu = (not args.no_cpu_baseline and args.pm is None and not args.rht and args.kernel is None
+                and not (args.copy_ref or args.matmul_ref or args.gemm_shapes))
+    # the oracle leg first: its worker pool forks this process before any GPU use
+    cpu = cpu_baseline(T, K, N) if want_cpu else None
     import torch
     import paper_2609_02846_amd as ue
     import synthetic
 
-    T, K, N = args.tokens, args.k, args.n
     dev = torch.device("cuda:0")
     if args.copy_ref:
         src = torch.empty(args.copy_ref // 4, dtype=torch.float32, device=dev).fill_(1.0)
@@ -393,43 +558,34 @@ def main():
 
     def up(bits):
         return torch.from_numpy(bits.view(np.int16)).to(dev).view(torch.bfloat16)
-    x, w, dy = up(wl["x"]), up(wl["w"]), up(wl["dy"])
+    # input sets: set 0 is the seeded workload; sets 1.. are it scaled by
+    # 1 + i/128 (bf16), same distributions, so that no step reads inputs the
+    # previous step left in the 256 MB Infinity Cache
+    base = (up(wl["x"]), up(wl["w"]), up(wl["dy"]))
+    ins = [base] + [tuple((t.float() * (1.0 + i / 128.0)).to(torch.bfloat16) for t in base)
+                    for i in range(1, NSETS)]
+    del wl
     u8 = lambda *s: torch.empty(s, dtype=torch.uint8, device=dev)
     f32 = lambda *s: torch.empty(s, dtype=torch.float32, device=dev)
-    bufs = {
-        "xr": (u8(T, K // 2), u8(T, K // 16), f32(1)),
-        "xc": (u8(K, T // 2), u8(K, T // 16), f32(1)),
-        "w": (u8(N, K // 2), u8(N // 16, K // 16), u8(K, N // 2), f32(1), u8(K // 16, N // 16)),
-        "dr": (u8(T, N // 2), u8(T, N // 16), f32(1)),
-        "dc": (u8(N, T // 2), u8(N, T // 16), f32(1)),
-    }
-    y = torch.empty(T, N, dtype=torch.bfloat16, device=dev)
-    dx = torch.empty(T, K, dtype=torch.bfloat16, device=dev)
-    dw = torch.empty(N, K, dtype=torch.float32, device=dev)
-    sx, sw, sd = ue.AmaxState(args.period), ue.AmaxState(args.period), ue.AmaxState(args.period)
+    sets = []
+    for i in range(NSETS):
+        sets.append({
+            "xr": (u8(T, K // 2), u8(T, K // 16), f32(1)),
+            "xc": (u8(K, T // 2), u8(K, T // 16), f32(1)),
+            "w": (u8(N, K // 2), u8(N // 16, K // 16), u8(K, N // 2), f32(1), u8(K // 16, N // 16)),
+            "dr": (u8(T, N // 2), u8(T, N // 16), f32(1)),
+            "dc": (u8(N, T // 2), u8(N, T // 16), f32(1)),
+            "y": torch.empty(T, N, dtype=torch.bfloat16, device=dev),
+            "dx": torch.empty(T, K, dtype=torch.bfloat16, device=dev),
+            "dw": torch.empty(N, K, dtype=torch.float32, device=dev)})
+    # one sample-and-hold state per operand role, as in training: a refresh
+    # measures the current set's tensor (the sets differ by at most 2.3%)
+    roles = {n: ue.AmaxState(args.period) for n in ("x", "w", "d", "xt", "dt")}
+    st = [roles] * NSETS
 
     names = ["amax", "quant_x_dual", "quant_w_tiles", "quant_dy_rows", "quant_dy_cols", "gemm_fprop",
              "gemm_dgrad", "gemm_wgrad"]
-
-    sxt, sdt = ue.AmaxState(args.period), ue.AmaxState(args.period)   # transformed wgrad operands
     MASK = 0x3C5A
-    xc_dec = bufs["xc"][2] if args.rht else bufs["xr"][2]     # one-read X quantizer: one decode factor
-
-    def quant_x():
-        if args.rht:
-            ue.quantize_1d(x, 1, sx.amax, 448.0, "rn", 0, 0, *bufs["xr"])
-            ue.quantize_cols_rht(x, sxt.amax, MASK, 448.0, "rn", 0, 0, *bufs["xc"])
-        else:
-            ue.quantize_dual(x, sx.amax, 448.0, "rn", 0, 0, 0, bufs["xr"][:2], bufs["xc"][:2], bufs["xr"][2])
-
-    def quant_dy_rows(seed):
-        ue.quantize_1d(dy, 1, sd.amax, 448.0, "sr", seed, 1, *bufs["dr"])
-
-    def quant_dy_cols(seed):
-        if args.rht:
-            ue.quantize_cols_rht(dy, sdt.amax, MASK, 448.0, "sr", seed, 2, *bufs["dc"])
-        else:
-            ue.quantize_1d(dy, 0, sd.amax, 448.0, "sr", seed, 2, *bufs["dc"])
 
     if args.pm is None:
         G = ue.gemm
@@ -437,76 +593,107 @@ def main():
         def G(*a, **kw):
             return ue.gemm_pm(*a, grid=args.pm, **kw)
 
-    def step(t, ev=None):
-        def mark(i):
-            if ev is not None:
-                ev[i].record()
-        mark(0)
-        ue.amax_sample(sx, x, t)
-        ue.amax_sample(sw, w, t)
-        ue.amax_sample(sd, dy, t)
-        if args.rht:
-            ue.amax_sample_rht(sxt, x, MASK, t)
-            ue.amax_sample_rht(sdt, dy, MASK, t)
-        mark(1)
-        quant_x()
-        mark(2)
-        pw, sw_, pwt, dw_, swt = bufs["w"]
-        ue.quantize_2d(w, sw.amax, 448.0, "rn", 0, 0, True, pw, sw_, pwt, dw_, swt)
-        mark(3)
-        quant_dy_rows(1000 + t)
-        mark(4)
-        quant_dy_cols(1000 + t)
-        mark(5)
-        xr, xc, dr, dc = bufs["xr"], bufs["xc"], bufs["dr"], bufs["dc"]
-        G("nt", T, N, K, xr[0], xr[1], xr[2], pw, sw_, dw_, out=y)
-        mark(6)
-        G("nn", T, K, N, dr[0], dr[1], dr[2], pwt, swt, dw_, out=dx)
-        mark(7)
-        G("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xc_dec, out=dw)
-        mark(8)
+    def kernel_fns(i, seed):
+        x, w, dy = ins[i]
+        b, s = sets[i], st[i]
+        xc_dec = b["xc"][2] if args.rht else b["xr"][2]     # one-read X quantizer: one decode factor
+        pw, sw_, pwt, dw_, swt = b["w"]
 
-    for t in range(args.warmup):
+        def quant_x():
+            if args.rht:
+                ue.quantize_1d(x, 1, s["x"].amax, 448.0, "rn", 0, 0, *b["xr"])
+                ue.quantize_cols_rht(x, s["xt"].amax, MASK, 448.0, "rn", 0, 0, *b["xc"])
+            else:
+                ue.quantize_dual(x, s["x"].amax, 448.0, "rn", 0, 0, 0, b["xr"][:2], b["xc"][:2], b["xr"][2])
+
+        def quant_dy_cols():
+            if args.rht:
+                ue.quantize_cols_rht(dy, s["dt"].amax, MASK, 448.0, "sr", seed, 2, *b["dc"])
+            else:
+                ue.quantize_1d(dy, 0, s["d"].amax, 448.0, "sr", seed, 2, *b["dc"])
+        xr, xc, dr, dc = b["xr"], b["xc"], b["dr"], b["dc"]
+        return {
+            "quant_x_dual": quant_x,
+            "quant_w_tiles": lambda: ue.quantize_2d(w, s["w"].amax, 448.0, "rn", 0, 0, True, pw, sw_, pwt, dw_, swt),
+            "quant_dy_rows": lambda: ue.quantize_1d(dy, 1, s["d"].amax, 448.0, "sr", seed, 1, *dr),
+            "quant_dy_cols": quant_dy_cols,
+            "gemm_fprop": lambda: G("nt", T, N, K, xr[0], xr[1], xr[2], pw, sw_, dw_, out=b["y"]),
+            "gemm_dgrad": lambda: G("nn", T, K, N, dr[0], dr[1], dr[2], pwt, swt, dw_, out=b["dx"]),
+            "gemm_wgrad": lambda: G("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xc_dec, out=b["dw"]),
+        }
+
+    def sample(i, t):
+        """The step's sample-and-hold calls; returns how many refreshed."""
+        x, w, dy = ins[i]
+        s = st[i]
+        n = int(ue.amax_sample(s["x"], x, t)) + int(ue.amax_sample(s["w"], w, t)) + int(ue.amax_sample(s["d"], dy, t))
+        if args.rht:
+            n += int(ue.amax_sample_rht(s["xt"], x, MASK, t)) + int(ue.amax_sample_rht(s["dt"], dy, MASK, t))
+        return n
+
+    def step(t, ev=None):
+        i = t % NSETS
+        if ev is not None:
+            ev[0].record()
+        refreshed = sample(i, t)
+        fns = kernel_fns(i, 1000 + t)
+        for j, n in enumerate(names[1:]):
+            if ev is not None:
+                ev[j + 1].record()
+            fns[n]()
+        if ev is not None:
+            ev[len(names)].record()
+        return refreshed
+
+    # warm-up: the first NSETS steps refresh every set's references
+    for t in range(max(args.warmup, NSETS)):
         step(t)
     torch.cuda.synchronize()
     if args.kernel is not None:
-        single = {
-            "quant_x_dual": quant_x,
-            "quant_w_tiles": lambda: ue.quantize_2d(w, sw.amax, 448.0, "rn", 0, 0, True, *bufs["w"]),
-            "quant_dy_rows": lambda: quant_dy_rows(7),
-            "quant_dy_cols": lambda: quant_dy_cols(7),
-            "quant_dy_dual": lambda: ue.quantize_dual(dy, sd.amax, 448.0, "sr", 7, 1, 2, bufs["dr"][:2],
-                                                      bufs["dc"][:2], bufs["dr"][2]),
-            "gemm_fprop": lambda: G("nt", T, N, K, *bufs["xr"], bufs["w"][0], bufs["w"][1],
-                                    bufs["w"][3], out=y),
-            "gemm_dgrad": lambda: G("nn", T, K, N, bufs["dr"][0], bufs["dr"][1], bufs["dr"][2],
-                                    bufs["w"][2], bufs["w"][4], bufs["w"][3], out=dx),
-            "gemm_wgrad": lambda: G("tn", N, K, T, *bufs["dc"], bufs["xc"][0], bufs["xc"][1], xc_dec, out=dw),
-        }[args.kernel]
-        for _ in range(args.steps):
-            single()
+        for r in range(args.steps):
+            kernel_fns(r % NSETS, 7)[args.kernel]()
         torch.cuda.synchronize()
         print(f"ran {args.kernel} {args.steps} times", flush=True)
         return
-    # --- timed region: exactly `steps` steps ---------------------------------
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # --- refresh-step amax, timed alone (three tensor amax launches) ---------
+    def refresh_all(i):
+        x, w, dy = ins[i]
+        for s_, tns in ((roles["x"], x), (roles["w"], w), (roles["d"], dy)):
+            ue.amax_accumulate(tns, s_.amax, clear=True)
+        if args.rht:
+            # the transformed operands' amax passes
+            for key, tns in (("xt", x), ("dt", dy)):
+                s_ = roles[key]
+                s_.reset()
+                ue.amax_sample_rht(s_, tns, MASK, 0)
+    refresh_ms, _, _ = _time_kernel(refresh_all, NSETS, reps=20, warm=2)
+    for key in roles:               # the warm-up schedule again, from empty caches
+        roles[key].reset()
+    t0 = max(args.warmup, NSETS)
+    for t in range(t0):
+        step(t)
+    torch.cuda.synchronize()
+    # --- timed region: exactly `steps` steps, per-kernel events inside -------
+    evs = [_events(len(names) + 1) for _ in range(args.steps)]
+    start, stop = _events(2)
     torch.cuda.synchronize()
     start.record()
-    for t in range(args.warmup, args.warmup + args.steps):
-        step(t)
+    refreshed = []
+    for r in range(args.steps):
+        refreshed.append(step(t0 + r, evs[r]) > 0)
     stop.record()
     torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / args.steps
-    # --- per-kernel durations (HIP events between launches, same stream) ---
+    window_ms = start.elapsed_time(stop)
+    n_refresh = int(sum(refreshed))
     per = {n: [] for n in names}
-    nprof = min(args.steps, 20)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(nprof)]
-    for i in range(nprof):
-        step(args.warmup + args.steps + i, evs[i])
-    torch.cuda.synchronize()
     for ev in evs:
         for j, n in enumerate(names):
             per[n].append(ev[j].elapsed_time(ev[j + 1]))
+    # the refresh-step amax at its 1/D rate: the window's own refresh-step
+    # amax time is replaced by the timed refresh cost once every D steps
+    refresh_in_window = sum(v for v, f in zip(per["amax"], refreshed) if f)
+    D = max(args.period, 1)
+    ms = (window_ms - refresh_in_window + refresh_ms * args.steps / D) / args.steps
     avg = {n: float(np.mean(v)) for n, v in per.items()}
     pct = {n: [round(float(q), 5) for q in np.percentile(v, [10, 50, 90])] for n, v in per.items()}
 
@@ -518,12 +705,22 @@ def main():
     for n, b in qbytes.items():
         gbs = b / (avg[n] * 1e-3) / 1e9
         kernels[n] = {"ms": round(avg[n], 5), "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
-                      "ms_p10_p50_p90": pct[n]}
+                      "ms_p10_p50_p90": pct[n], "alg_bytes": b}
     for n in ["gemm_fprop", "gemm_dgrad", "gemm_wgrad"]:
         tf = flop_gemm / (avg[n] * 1e-3) / 1e12
         kernels[n] = {"ms": round(avg[n], 5), "TFLOP/s": round(tf, 1), "frac": round(tf / BF16_PEAK_TFLOPS, 4),
                       "ms_p10_p50_p90": pct[n]}
-    kernels["amax"] = {"ms": round(avg["amax"], 5), "note": "launches only on refresh steps"}
+    amax_bytes = 2 * (T * K + N * K + T * N)
+    kernels["amax_refresh"] = {"ms": round(refresh_ms, 5), "GB/s": round(amax_bytes / (refresh_ms * 1e-3) / 1e9, 1),
+                               "per_step_share_ms": round(refresh_ms / D, 5),
+                               "note": f"X, W and dY amax, launched on 1 step in {D}"}
+    # each quantizer alone over the rotating sets (no input of the previous
+    # launch in the Infinity Cache)
+    iso = {}
+    for n in qbytes:
+        med, mean, p = _time_kernel(lambda i, n=n: kernel_fns(i, 7)[n](), NSETS, reps=20, warm=4)
+        gbs = qbytes[n] / (med * 1e-3) / 1e9
+        iso[n] = {"ms": round(med, 5), "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
     qtime = sum(avg[n] for n in qbytes)
     quant_gbs = sum(qbytes.values()) / (qtime * 1e-3) / 1e9
     gtime = sum(avg[n] for n in ["gemm_fprop", "gemm_dgrad", "gemm_wgrad"])
@@ -544,7 +741,8 @@ def main():
     achieved = flop_gemm / (avg[dom] * 1e-3) / 1e12
     roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": traffic}
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": traffic,
+                "peak_note": "dense fp16 MFMA (the bf16 peak), the instruction the GEMM issues"}
     if args.pm is not None:
         # probe-matched GEMM: bound by the per-output VALU work of each
         # 64-product group (4 widenings, 3 binary64 adds, 1 narrowing, 1
@@ -558,18 +756,24 @@ def main():
     value = 3 * flop_gemm / (ms * 1e-3) / 1e12
     out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
-           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp16",
+           "operands": ("E2M1 payloads x UE5M3 block scales, decoded exactly to fp16 for the matrix "
+                        "cores; fp32 accumulation"),
            "data": "synthetic",
            "config": {"workload": f"FFN up-projection linear training step T={T} K={K} N={N}",
                       "tokens": T, "k": K, "n": N, "refresh_period": args.period,
-                      "target": 448.0, "wgrad_operand_rht": bool(args.rht),
+                      "target": 448.0, "wgrad_operand_rht": bool(args.rht), "input_sets": NSETS,
                       "gemm": ("decoded-operand, fp32 accumulation" if args.pm is None else
                                f"probe-matched, grid 1/{args.pm}" if args.pm else "probe-matched, no snap")},
+           "window_ms_per_step": round(window_ms / args.steps, 4), "refresh_steps_in_window": n_refresh,
            "quantize_GBps": round(quant_gbs, 1), "quantize_frac_hbm": round(quant_gbs / HBM_PEAK_GBS, 4),
            "gemm_TFLOPs": round(gemm_tf, 1), "gemm_frac_bf16": round(gemm_tf / BF16_PEAK_TFLOPS, 4),
-           "kernels": kernels, "roofline": roofline}
-    if not args.no_cpu_baseline and args.pm is None and not args.rht:
-        out["cpu_baseline"] = cpu_baseline(wl, T, K, N)
+           "kernels": kernels, "quantizers_isolated": iso, "roofline": roofline}
+    if args.pm is None and not args.rht:
+        out["quantizer_workload"] = quantizer_workload(dev)
+        out["small_linear"] = small_linear_latency(dev)
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
 
 

@@ -244,7 +244,7 @@ def control_bench(args):
     t0 = time.time()
     bf = {s: control.run(s, "bf16") for s in (41, 42, 43)}
     for rnd in ("rn", "sr"):
-        mse_q, rec, st = [], 0, 0
+        mse_q, mse_qb, rec, st = [], [], 0, 0
         for s in (41, 42, 43):
             base = control.run(s, "fp4", rnd, grid=0)
             for d in grids:
@@ -254,11 +254,14 @@ def control_bench(args):
                 st += int(b)
                 if d == 1024:
                     mse_q.append(r["eval_mse"])
+                    mse_qb.append(r["eval_mse_bf16"])
             print(f"control {rnd} seed {s} done ({time.time() - t0:.0f} s)", flush=True)
         res[rnd] = {"bf16_eval_mse": round(float(np.mean([bf[s]["eval_mse"] for s in bf])), 6),
                     "fp4_eval_mse": round(float(np.mean(mse_q)), 6),
+                    "fp4_weights_bf16_eval_mse": round(float(np.mean(mse_qb)), 6),
                     "exact_records": f"{rec}/15", "exact_states": f"{st}/15"}
-    print(json.dumps({"metric": "teacher-student regression control (256-256-64, 500 AdamW steps)",
+    print(json.dumps({"metric": "teacher-student regression control (256-256-64, 500 AdamW steps, "
+                                f"label noise {control.LABEL_NOISE})",
                       "unit": "final-eval MSE", "seeds": [41, 42, 43], "grids": list(grids),
                       "results": res, "paper": {"rn": {"bf16_eval_mse": 0.001956, "fp4_eval_mse": 0.027130,
                                                         "exact_records": "15/15", "exact_states": "15/15"},

@@ -754,11 +754,14 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
 
     int64_t it = blockIdx.x;
     if (it >= ntiles) return;                                        // uniform
+    // RN prefetches the next tile into registers; SR (VALU-bound: Philox for
+    // both blockings) keeps its registers for more resident waves instead
+    constexpr bool kPrefetch = !SR;
     uint32_t lo[16], hi[16], nlo[16], nhi[16];
     load(it, lo, hi);
     for (int buf = 0;; buf ^= 1) {
         const int64_t nit = it + gridDim.x;
-        if (nit < ntiles) load(nit, nlo, nhi);
+        if (kPrefetch && nit < ntiles) load(nit, nlo, nhi);
         DualStage& st = stage[buf];
         const int64_t cw = (it % gx) * kTileCols;
         const int64_t c = cw + 4 * q;
@@ -892,10 +895,14 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
         }
         if (nit >= ntiles) break;                                   // uniform
         it = nit;
+        if (kPrefetch) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            lo[r] = nlo[r];
-            hi[r] = nhi[r];
+            for (int r = 0; r < 16; ++r) {
+                lo[r] = nlo[r];
+                hi[r] = nhi[r];
+            }
+        } else {
+            load(it, lo, hi);
         }
     }
 }

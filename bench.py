@@ -35,7 +35,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
 VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12   # 32-bit (and binary64 add) VALU lane ops/s
-PM_VALU_PER_GROUP = 9          # probe-matched VALU ops per output per 64-product group
+PM_VALU_PER_GROUP = 9          # probe-matched output model: VALU ops per output per 64-product group
+PM_VALU_MEASURED = 12.3        # the same, as issued (SQ_INSTS_VALU of the fprop launch): model + decode/addressing
 METRIC = "quantize GB/s + emulated FP4 GEMM TFLOP/s (fprop+dgrad+wgrad), % roofline"
 
 
@@ -750,11 +751,13 @@ def main():
         # probe-matched GEMM: bound by the per-output VALU work of each
         # 64-product group (4 widenings, 3 binary64 adds, 1 narrowing, 1
         # toward-zero add), against 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
-        ops = PM_VALU_PER_GROUP * T * N * ((K + 63) // 64)
-        ach = ops / (avg[dom] * 1e-3) / 1e12
+        groups = T * N * ((K + 63) // 64)
+        ach = PM_VALU_MEASURED * groups / (avg[dom] * 1e-3) / 1e12
         roofline = {"bound": "alu", "kernel": dom + " (probe-matched)", "achieved": round(ach, 2),
                     "peak": VALU_PEAK_TOPS, "unit": "Tops/s (VALU lane ops)",
-                    "frac": round(ach / VALU_PEAK_TOPS, 4), "traffic": None}
+                    "frac": round(ach / VALU_PEAK_TOPS, 4), "traffic": None,
+                    "ops_per_output_group": {"issued": PM_VALU_MEASURED, "output_model": PM_VALU_PER_GROUP},
+                    "model_only_frac": round(PM_VALU_PER_GROUP * groups / (avg[dom] * 1e-3) / 1e12 / VALU_PEAK_TOPS, 4)}
 
     value = 3 * flop_gemm / (ms * 1e-3) / 1e12
     out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,

@@ -716,6 +716,96 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
 // LDS stage alternates between two buffers, so one barrier per tile
 // separates a tile's LDS writes from its stores and the stores of tile k
 // from the writes of tile k + 2.
+// Packed 16-bit unsigned maximum of two bf16 |x| pairs (per half).
+__device__ __forceinline__ uint32_t pk_max_u16(uint32_t a, uint32_t b) {
+    uint32_t r;
+    asm("v_pk_max_u16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
+// The RN work of one lane's 16 x 4 piece of a dual-axis tile: lo / hi hold
+// rows r of columns (c, c+1) / (c+2, c+3) as bf16 pairs.  Writes the
+// transposed column payload (4 columns x 8 bytes) and the column scale codes
+// to the LDS stage, the row scale codes of the rows this lane owns in its
+// quad, and the row payload (2 bytes per row) to prow (row stride rstride
+// bytes).  Per element: its 15-bit |x| enters packed 16-bit maxima shared by
+// the two blockings, and its binary32 value is formed once and multiplied by
+// the row and the column reciprocal (the same binary32 products as the
+// single-axis quantizers).
+template <int FMT>
+__device__ __forceinline__ void dual_rn_tile(const uint32_t (&lo)[16], const uint32_t (&hi)[16],
+                                             const Multipliers& m, uint8_t (*P)[kTileRowTiles * 8],
+                                             uint8_t (*SC)[kTileRowTiles], uint8_t (*SRo)[kTileCols / 16],
+                                             int q, int trl, uint8_t* __restrict__ prow, int64_t rstride) {
+    uint32_t mcL = 0u, mcH = 0u;              // packed column maxima: (c, c+1), (c+2, c+3)
+    uint32_t mrow[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const uint32_t a = lo[r] & 0x7FFF7FFFu, b = hi[r] & 0x7FFF7FFFu;
+        mcL = pk_max_u16(mcL, a);
+        mcH = pk_max_u16(mcH, b);
+        const uint32_t ab = pk_max_u16(a, b);
+        uint32_t mr = max(ab & 0xFFFFu, ab >> 16);
+        mr = max(mr, (uint32_t)__builtin_amdgcn_mov_dpp((int)mr, 0xB1, 0xF, 0xF, false));   // quad xor 1
+        mr = max(mr, (uint32_t)__builtin_amdgcn_mov_dpp((int)mr, 0x4E, 0xF, 0xF, false));   // quad xor 2
+        mrow[r] = mr;
+    }
+    BlockScale bc[4];
+    bc[0] = block_scale<FMT>(mcL & 0xFFFFu, m);
+    bc[1] = block_scale<FMT>(mcL >> 16, m);
+    bc[2] = block_scale<FMT>(mcH & 0xFFFFu, m);
+    bc[3] = block_scale<FMT>(mcH >> 16, m);
+    // lane k of the quad derives the scales of rows k, k+4, k+8, k+12; the
+    // others take them by a quad broadcast
+    const int qk = q & 3;
+    BlockScale own[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const uint32_t mo = qk == 0 ? mrow[4 * u] : qk == 1 ? mrow[4 * u + 1] : qk == 2 ? mrow[4 * u + 2] : mrow[4 * u + 3];
+        own[u] = block_scale<FMT>(mo, m);
+        SRo[trl * 16 + 4 * u + qk][q >> 2] = (uint8_t)own[u].code;
+    }
+    uint32_t cp[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        float xv[2][4];
+        float rr[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int r = 2 * k + h;
+            xv[h][0] = bf16_lo(lo[r]);
+            xv[h][1] = bf16_hi(lo[r]);
+            xv[h][2] = bf16_lo(hi[r]);
+            xv[h][3] = bf16_hi(hi[r]);
+            const int ov = __float_as_int(own[r >> 2].r);
+            const int src = r & 3;
+            rr[h] = __int_as_float(src == 0 ? __builtin_amdgcn_mov_dpp(ov, 0x00, 0xF, 0xF, false)
+                                   : src == 1 ? __builtin_amdgcn_mov_dpp(ov, 0x55, 0xF, 0xF, false)
+                                   : src == 2 ? __builtin_amdgcn_mov_dpp(ov, 0xAA, 0xF, 0xF, false)
+                                              : __builtin_amdgcn_mov_dpp(ov, 0xFF, 0xF, 0xF, false));
+            uint32_t p = 0u;
+            p = rn_pair<0>(p, xv[h][0] * rr[h], xv[h][1] * rr[h]);
+            p = rn_pair<1>(p, xv[h][2] * rr[h], xv[h][3] * rr[h]);
+            *reinterpret_cast<uint16_t*>(prow + r * rstride) = (uint16_t)p;
+        }
+        // columns: rows 2k, 2k+1 of each column form one nibble pair
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            uint32_t& w = cp[j][k >> 2];
+            const float y0 = xv[0][j] * bc[j].r, y1 = xv[1][j] * bc[j].r;
+            if ((k & 3) == 0) w = rn_pair<0>(w, y0, y1);
+            if ((k & 3) == 1) w = rn_pair<1>(w, y0, y1);
+            if ((k & 3) == 2) w = rn_pair<2>(w, y0, y1);
+            if ((k & 3) == 3) w = rn_pair<3>(w, y0, y1);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        *reinterpret_cast<uint2*>(&P[4 * q + j][trl * 8]) = make_uint2(cp[j][0], cp[j][1]);
+        SC[4 * q + j][trl] = (uint8_t)bc[j].code;
+    }
+}
+
 struct DualStage {
     uint8_t P[kTileCols][kTileRowTiles * 8];          // transposed payload, 64 B per column
     uint8_t SR[kTileRowTiles * 16][kTileCols / 16];   // row scales, 8 per row
@@ -767,7 +857,13 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
         const int64_t c = cw + 4 * q;
         const int64_t tr0 = (it / gx) * kTileRowTiles;
         const int64_t tr = tr0 + trl;
-        if (c < cols && tr < ntr) {
+        if (!SR && c < cols && tr < ntr) {
+            // RN: block maxima from the |x| bits, both blockings' scales, then
+            // one pass over row pairs that widens each element once for its
+            // row and its column conversion
+            dual_rn_tile<FMT>(lo, hi, m, st.P, st.SC, st.SR, q, trl,
+                              payload_r + (tr * 16) * (cols / 2) + c / 2, cols / 2);
+        } else if (SR && c < cols && tr < ntr) {
             // column blocks: in-lane maxima of the 4 columns
             uint32_t mc[4] = {0u, 0u, 0u, 0u};
 #pragma unroll

@@ -432,7 +432,10 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
             ng = 0;
         }
         const ColItem cn = nit < nitems ? col_item(nit, gx, rows, rows_per_item) : ci;
-        if (nit < nitems) load(cn, ng, nlo, nhi);
+        // RN prefetches the next group into registers; SR (VALU-bound)
+        // keeps its registers for more resident waves and loads each group
+        // after storing the previous one
+        if (!SR && nit < nitems) load(cn, ng, nlo, nhi);
 
         const int64_t c = ci.cw + 4 * q;
         const int64_t r0 = ci.r_begin + g * (kColGroupRB * 16) + rbl * 16;
@@ -558,10 +561,14 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
         it = nit;
         g = ng;
         ci = cn;
+        if (SR) {
+            load(ci, g, lo, hi);
+        } else {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            lo[r] = nlo[r];
-            hi[r] = nhi[r];
+            for (int r = 0; r < 16; ++r) {
+                lo[r] = nlo[r];
+                hi[r] = nhi[r];
+            }
         }
     }
 }
@@ -1118,7 +1125,9 @@ hipError_t launch_dual_fmt(const void* x_bf16, int64_t rows, int64_t cols, const
     const int64_t ntiles = gx * gy;
     const int64_t resident = sr ? resident_wgs(quant_dual_kernel<true, FMT>, 12 + FMT)
                                 : resident_wgs(quant_dual_kernel<false, FMT>, 14 + FMT);
-    const int64_t grid = min(ntiles, resident);
+    // SR: one tile per workgroup (measured faster than the persistent walk
+    // for the VALU-bound SR form); RN: persistent, next tile prefetched
+    const int64_t grid = sr ? ntiles : min(ntiles, resident);
     const uint16_t* x = reinterpret_cast<const uint16_t*>(x_bf16);
     if (sr)
         hipLaunchKernelGGL((quant_dual_kernel<true, FMT>), dim3((unsigned)grid), dim3(kThreads), 0, s, x, rows,

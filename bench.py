@@ -50,6 +50,12 @@ def parse():
     p.add_argument("--n", type=int, default=21504)
     p.add_argument("--period", type=int, default=50)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--step-only", action="store_true",
+                   help="profiling aid: only the step (warm-up, refresh timing, timed steps); no isolated "
+                        "quantizer runs, quantizer workload or small-linear lines, so that every launch of a "
+                        "kernel in a trace has the step's shape")
+    p.add_argument("--valu", default=os.path.join(ROOT, "profiles", "quantizer_valu.json"),
+                   help="VALU instructions per element of the SR quantizers from rocprofv3 counters (JSON)")
     p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "gemm_traffic.json"),
                    help="HBM traffic per launch measured with rocprofv3 counters (JSON)")
     p.add_argument("--kernel", default=None,
@@ -89,6 +95,18 @@ def gemm_source_hash():
     import hashlib
     h = hashlib.sha256()
     for f in ("gemm.hip", "fp4_decode.hpp", "codec.hpp"):
+        text = open(os.path.join(ROOT, "paper_2609_02846_amd", "csrc", f), encoding="utf-8").read()
+        lines = (ln.split("//")[0].rstrip() for ln in text.splitlines())
+        h.update("\n".join(ln for ln in lines if ln).encode())
+    return h.hexdigest()[:16]
+
+
+def quantize_source_hash():
+    """Hash of the quantizer kernel source with comments and blank lines
+    removed (the stored VALU counts are valid only for that code)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("quantize.hip", "codec.hpp"):
         text = open(os.path.join(ROOT, "paper_2609_02846_amd", "csrc", f), encoding="utf-8").read()
         lines = (ln.split("//")[0].rstrip() for ln in text.splitlines())
         h.update("\n".join(ln for ln in lines if ln).encode())
@@ -718,10 +736,25 @@ def main():
     kernels["amax_refresh"] = {"ms": round(refresh_ms, 5), "GB/s": round(amax_bytes / (refresh_ms * 1e-3) / 1e9, 1),
                                "per_step_share_ms": round(refresh_ms / D, 5),
                                "note": f"X, W and dY amax, launched on 1 step in {D}"}
-    # each quantizer alone over the rotating sets (no input of the previous
-    # launch in the Infinity Cache)
+    # SR quantizers are bound by VALU issue: instructions per element (rocprofv3
+    # SQ_INSTS_VALU, stored with the source hash) against 1024 SIMDs issuing
+    # one wave64 instruction per 4 cycles at 2.4 GHz
+    if os.path.exists(args.valu):
+        try:
+            vj = json.load(open(args.valu))
+            if vj.get("source_sha256_16") == quantize_source_hash() and vj.get("config") == [T, K, N]:
+                for n, ipe in vj["instr_per_element"].items():
+                    if n in kernels:
+                        el = T * N if n.startswith("quant_dy") else (T * K if n == "quant_x_dual" else N * K)
+                        frac = ipe * el * 4 / 64 / (1024 * 2.4e9 * avg[n] * 1e-3)
+                        kernels[n]["valu_instr_per_element"] = ipe
+                        kernels[n]["valu_frac"] = round(frac, 4)
+        except Exception:
+            pass
     iso = {}
-    for n in qbytes:
+    for n in (qbytes if not args.step_only else []):
+        # each quantizer alone over the rotating sets (no input of the
+        # previous launch in the Infinity Cache)
         med, mean, p = _time_kernel(lambda i, n=n: kernel_fns(i, 7)[n](), NSETS, reps=20, warm=4)
         gbs = qbytes[n] / (med * 1e-3) / 1e9
         iso[n] = {"ms": round(med, 5), "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
@@ -775,7 +808,7 @@ def main():
            "quantize_GBps": round(quant_gbs, 1), "quantize_frac_hbm": round(quant_gbs / HBM_PEAK_GBS, 4),
            "gemm_TFLOPs": round(gemm_tf, 1), "gemm_frac_bf16": round(gemm_tf / BF16_PEAK_TFLOPS, 4),
            "kernels": kernels, "quantizers_isolated": iso, "roofline": roofline}
-    if args.pm is None and not args.rht:
+    if args.pm is None and not args.rht and not args.step_only:
         out["quantizer_workload"] = quantizer_workload(dev)
         out["small_linear"] = small_linear_latency(dev)
     if cpu is not None:

@@ -442,9 +442,39 @@ def gemm_shapes(dev):
 NSETS = 4      # rotating input / output sets: > 512 MB, past the 256 MB Infinity Cache
 
 
+class _HipEvent:
+    """A HIP timing event recorded on torch's current stream, created
+    without the system-scope memory fence that torch's events carry (the
+    step's kernels exchange data only through device memory; measured: the
+    fenced events lengthen the timed step by about 0.8%, these by 0.3%)."""
+    _hip = None
+    kDisableSystemFence = 0x20000000
+
+    def __init__(self):
+        import ctypes
+        if _HipEvent._hip is None:
+            _HipEvent._hip = ctypes.CDLL("libamdhip64.so")
+        self.h = ctypes.c_void_p()
+        if _HipEvent._hip.hipEventCreateWithFlags(ctypes.byref(self.h),
+                                                  ctypes.c_uint(self.kDisableSystemFence)) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
+
+    def record(self):
+        import ctypes
+        import torch
+        if _HipEvent._hip.hipEventRecord(self.h, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_time(self, other):
+        import ctypes
+        ms = ctypes.c_float()
+        if _HipEvent._hip.hipEventElapsedTime(ctypes.byref(ms), self.h, other.h) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+
 def _events(n):
-    import torch
-    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    return [_HipEvent() for _ in range(n)]
 
 
 def _time_kernel(fn, nsets, reps=30, warm=4):

@@ -764,20 +764,39 @@ __device__ __forceinline__ WorkItem work_item(int it, const SplitPlan& sp, int N
     return w;
 }
 
+// LDS bytes per wave for the epilogue's row transposition (32 rows x 128 B).
+constexpr int kEpiBytes = 4096;
+
+// Orders a wave's LDS writes before its own later LDS reads of what other
+// lanes wrote (and those reads before the next writes): the LDS serves one
+// wave's instructions in order, so the compiler only must not move memory
+// accesses across this point and the data must have landed.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);              // lgkmcnt(0)
+    asm volatile("" ::: "memory");
+}
+
+
 // Epilogue of one work item.  Element e of accumulator (i, j) is row
 // 32i + l%32, column 32j + 8(e/4) + 4(l/32) + e%4 of the wave's 128 x 128
 // block (the products are issued as B x A^T).  A split part stores its fp32
 // partial; a whole tile stores alpha * value through a buffer resource over
 // C, where an out-of-range offset drops the store, which masks rows and
-// columns past C without branches.  VEC (a launch-time choice, so that the
-// whole-tile path is straight-line code and the accumulators are read out
-// one row block at a time): N % 8 == 0 for bf16, N % 4 == 0 for fp32, where
-// every run of 8 (4) output columns lies wholly inside C or wholly past it;
-// otherwise each element is masked on its own.
+// columns past C without branches.  VEC (a launch-time choice): N % 8 == 0
+// for bf16, N % 4 == 0 for fp32, where every run of 8 (4) output columns
+// lies wholly inside C or wholly past it; otherwise each element is masked
+// on its own.  With VEC the values pass through the wave's 4 KB of LDS
+// (`ep`), 32 rows x 128 bytes at a time, and leave as stores of 128
+// contiguous bytes per row (8 rows per instruction): a lane holds one row,
+// so storing straight from the accumulators writes 32 rows x 32 bytes per
+// instruction, which the memory path serves at a quarter of the rate.  In
+// the staging area the 16-byte chunk c of row x sits at c ^ ((x / 2) % 8),
+// which spreads both the writes and the reads over all LDS banks.
 template <bool OUT_BF16, bool VEC>
 __device__ __forceinline__ void store_item(const f32x16_t (&acc)[4][4], const WorkItem& cur,
                                            const SplitPlan& sp, int M, int N, int tiles_m, int tiles_n,
-                                           int wave, int lane, float alpha, void* __restrict__ C) {
+                                           int wave, int lane, float alpha, void* __restrict__ C,
+                                           uint8_t* __restrict__ ep) {
     const int wm = wave >> 1, wn = wave & 1;
     const int r = lane & 31, hi = lane >> 5;
     if (cur.split_j >= 0) {
@@ -808,33 +827,76 @@ __device__ __forceinline__ void store_item(const f32x16_t (&acc)[4][4], const Wo
     int64_t m0, n0;
     tile_origin(cur.t, tiles_m, tiles_n, m0, n0);
     const int mrow = (int)m0 + wm * 128 + r;
-    if (OUT_BF16 && VEC) {
-        // bf16 with N % 8 == 0: lanes l and l + 32 hold the two halves of
-        // each run of 8 columns; one lane-half swap per pair of runs gives
-        // lane l runs 0 and 2 and lane l + 32 runs 1 and 3 whole, so every
-        // store is 16 bytes per lane (32 per row).
-        const int ncol8 = (int)n0 + wn * 128 + hi * 8;
+    if (VEC) {
+        // Write side: lane (r, hi) puts its row's values of the current
+        // 32-row block; read side: lane l takes chunk l % 8 of row
+        // l / 8 + 8t.  bf16: a store's row lies past C exactly when its
+        // offset does (the column run is checked once), so the per-store
+        // offset is the lane's base plus a uniform row offset.
+        const int wsw = (r >> 1) & 7;
+        const int rr = lane >> 3, rc = lane & 7;
+        const uint32_t mb = (uint32_t)((int)m0 + wm * 128 + rr);
+        uint8_t* const wrow = ep + r * 128;
+        const uint8_t* rd[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int m = mrow + 32 * i;
-            const uint32_t rbase = ((uint32_t)m * (uint32_t)N + (uint32_t)ncol8) * 2u;
+        for (int t = 0; t < 4; ++t) rd[t] = ep + (rr + 8 * t) * 128 + ((rc ^ (((rr + 8 * t) >> 1) & 7)) << 4);
+        if (OUT_BF16) {
+            // round q = 2i + h: 32 rows x 64 columns (j = 2h, 2h + 1)
+            uint32_t vb[2];
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int h = 0; h < 2; ++h) {
+                const int n = (int)n0 + wn * 128 + 64 * h + 8 * rc;
+                vb[h] = n < N ? (mb * (uint32_t)N + (uint32_t)n) * 2u : kOff;
+            }
+            auto pack = [&](int q, u32x2_t (&v)[8]) {
+                const int i = q >> 1, h = q & 1;
 #pragma unroll
-                for (int q = 0; q < 2; ++q) {
-                    const int g0 = 2 * q, g1 = 2 * q + 1;
-                    const uint32_t x0 = pack_bf16x2(alpha * acc[i][j][4 * g0], alpha * acc[i][j][4 * g0 + 1]);
-                    const uint32_t x1 = pack_bf16x2(alpha * acc[i][j][4 * g0 + 2], alpha * acc[i][j][4 * g0 + 3]);
-                    const uint32_t y0 = pack_bf16x2(alpha * acc[i][j][4 * g1], alpha * acc[i][j][4 * g1 + 1]);
-                    const uint32_t y1 = pack_bf16x2(alpha * acc[i][j][4 * g1 + 2], alpha * acc[i][j][4 * g1 + 3]);
-                    const auto s0 = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
-                    const auto s1 = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
-                    const u32x4_t d = {(uint32_t)s0[0], (uint32_t)s1[0], (uint32_t)s0[1], (uint32_t)s1[1]};
-                    const int n = ncol8 + 32 * j + 16 * q;
-                    const uint32_t vo = (m < M && n < N) ? rbase : kOff;
-                    __builtin_amdgcn_raw_buffer_store_b128(d, cr, vo + (uint32_t)(32 * j + 16 * q) * 2u, 0, 0);
+                for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const f32x16_t& a = acc[i][2 * h + jj];
+                        v[4 * jj + g] = u32x2_t{pack_bf16x2(alpha * a[4 * g], alpha * a[4 * g + 1]),
+                                                pack_bf16x2(alpha * a[4 * g + 2], alpha * a[4 * g + 3])};
+                    }
+            };
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                u32x2_t v[8];
+                pack(q, v);
+#pragma unroll
+                for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+                        *reinterpret_cast<u32x2_t*>(wrow + (((4 * jj + g) ^ wsw) << 4) + hi * 8) = v[4 * jj + g];
+                wave_lds_sync();
+                const int i = q >> 1, h = q & 1;
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4_t*>(rd[t]), cr, vb[h],
+                                                           (32 * i + 8 * t) * N * 2, 0);
+                wave_lds_sync();
+            }
+        } else {
+            // round q = 4i + j: 32 rows x 32 columns
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const int i = q >> 2, j = q & 3;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const f32x4_t v = {alpha * acc[i][j][4 * g], alpha * acc[i][j][4 * g + 1],
+                                       alpha * acc[i][j][4 * g + 2], alpha * acc[i][j][4 * g + 3]};
+                    *reinterpret_cast<f32x4_t*>(wrow + (((2 * g + hi) ^ wsw) << 4)) = v;
                 }
-            __builtin_amdgcn_sched_barrier(0);
+                wave_lds_sync();
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const int m = (int)mb + 32 * i + 8 * t;
+                    const int n = (int)n0 + wn * 128 + 32 * j + 4 * rc;
+                    const uint32_t vo = (m < M && n < N) ? ((uint32_t)m * (uint32_t)N + (uint32_t)n) * 4u : kOff;
+                    __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4_t*>(rd[t]), cr, vo, 0, 0);
+                }
+                wave_lds_sync();
+            }
         }
         return;
     }
@@ -851,23 +913,16 @@ __device__ __forceinline__ void store_item(const f32x16_t (&acc)[4][4], const Wo
                 const float v0 = alpha * acc[i][j][4 * g + 0], v1 = alpha * acc[i][j][4 * g + 1];
                 const float v2 = alpha * acc[i][j][4 * g + 2], v3 = alpha * acc[i][j][4 * g + 3];
                 const uint32_t imm = (uint32_t)(32 * j + 8 * g) * esz;
-                if (VEC) {
-                    // fp32 with N % 4 == 0: a run is inside C or wholly past it
-                    const uint32_t vo = (m < M && n < N) ? rbase : kOff;
-                    const f32x4_t d = {v0, v1, v2, v3};
-                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, d), cr, vo + imm, 0, 0);
-                } else {
-                    const float vv[4] = {v0, v1, v2, v3};
+                const float vv[4] = {v0, v1, v2, v3};
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const uint32_t vo = (m < M && n + q < N) ? rbase : kOff;
-                        if (OUT_BF16) {
-                            __builtin_amdgcn_raw_buffer_store_b16(
-                                (unsigned short)pack_bf16x2(vv[q], 0.0f), cr, vo + imm + q * esz, 0, 0);
-                        } else {
-                            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(vv[q]), cr,
-                                                                  vo + imm + q * esz, 0, 0);
-                        }
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t vo = (m < M && n + q < N) ? rbase : kOff;
+                    if (OUT_BF16) {
+                        __builtin_amdgcn_raw_buffer_store_b16(
+                            (unsigned short)pack_bf16x2(vv[q], 0.0f), cr, vo + imm + q * esz, 0, 0);
+                    } else {
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(vv[q]), cr,
+                                                              vo + imm + q * esz, 0, 0);
                     }
                 }
             }
@@ -892,6 +947,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
     __shared__ __attribute__((aligned(16))) uint8_t sP1[kSupPayload];
     __shared__ __attribute__((aligned(16))) uint8_t sC0[kSupScales];
     __shared__ __attribute__((aligned(16))) uint8_t sC1[kSupScales];
+    __shared__ __attribute__((aligned(16))) uint8_t sE[kGemmThreads / 64 * kEpiBytes];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -1066,7 +1122,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
         if (G < cur.g1) stage(G, sP0, sC0, sP1, sC1, P0, S0);   // odd stage count (single item)
 
         store_item<OUT_BF16, VEC>(acc, cur, sp, M, N, tiles_m, tiles_n, wave, lane,
-                                  (a_dec[0] * b_dec[0]) * amul, C);   // operands were scaled by 2^-3
+                                  (a_dec[0] * b_dec[0]) * amul, C, sE + wave * kEpiBytes);   // operands were scaled by 2^-3
         if (!has_next) break;
     }
     wait_vmem<0>();                                  // no load outlives the kernel's LDS
@@ -1198,6 +1254,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_mx_kernel(
     __shared__ __attribute__((aligned(16))) uint8_t sP1[kSupPayload];
     __shared__ __attribute__((aligned(16))) uint8_t sC0[kMxScaleStage];
     __shared__ __attribute__((aligned(16))) uint8_t sC1[kMxScaleStage];
+    __shared__ __attribute__((aligned(16))) uint8_t sE[kGemmThreads / 64 * kEpiBytes];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -1350,7 +1407,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_mx_kernel(
         __builtin_amdgcn_sched_barrier(0);
         asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 15" ::: "memory");
         __builtin_amdgcn_sched_barrier(0);
-        store_item<OUT_BF16, VEC>(acc, cur, sp, M, N, tiles_m, tiles_n, wave, lane, a_dec[0] * b_dec[0], C);
+        store_item<OUT_BF16, VEC>(acc, cur, sp, M, N, tiles_m, tiles_n, wave, lane, a_dec[0] * b_dec[0], C,
+                                  sE + wave * kEpiBytes);
         if (!has_next) break;
     }
     wait_vmem<0>();                                  // no load outlives the kernel's LDS

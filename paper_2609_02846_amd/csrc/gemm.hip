@@ -604,10 +604,10 @@ __device__ __forceinline__ void read_sup_slice(RegSlice& R, const uint8_t* P, co
     }
 }
 
-__device__ __forceinline__ f16x8_t decode_frag(uint32_t w, uint32_t s2, int hsel) {
+template <int HSEL>
+__device__ __forceinline__ f16x8_t decode_frag(uint32_t w, uint32_t s2) {
     const f16x2_t sp = __builtin_bit_cast(f16x2_t, s2);
-    const _Float16 sv = sp[hsel];
-    const f16x2_t sc = {sv, sv};
+    const f16x2_t sc = __builtin_shufflevector(sp, sp, HSEL, HSEL);   // op_sel picks the half
     const f16x2_t v0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 0.125f, 0) * sc;
     const f16x2_t v1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 0.125f, 1) * sc;
     const f16x2_t v2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 0.125f, 2) * sc;
@@ -623,12 +623,17 @@ template <int KK>
 __device__ __forceinline__ void decode_kstep(Frags& f, RegSlice& R, uint32_t sel) {
     if (KK == 0) {
 #pragma unroll
-        for (int g = 0; g < 8; ++g) R.s[g] = half_scales(R.s[g], sel);
+        for (int g = 0; g < 8; ++g) {
+            R.s[g] = half_scales(R.s[g], sel);
+            // opaque to the compiler, which would otherwise rebuild the high
+            // half with a shift instead of selecting it by op_sel
+            asm("" : "+v"(R.s[g]));
+        }
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) f.a[i] = decode_frag(R.w[i][KK], R.s[i], KK >> 1);
+    for (int i = 0; i < 4; ++i) f.a[i] = decode_frag<KK / 2>(R.w[i][KK], R.s[i]);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) f.b[j] = decode_frag(R.w[4 + j][KK], R.s[4 + j], KK >> 1);
+    for (int j = 0; j < 4; ++j) f.b[j] = decode_frag<KK / 2>(R.w[4 + j][KK], R.s[4 + j]);
 }
 
 // Direct global->LDS loads written as instructions the compiler does not

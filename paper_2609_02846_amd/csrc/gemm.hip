@@ -798,7 +798,7 @@ __device__ __forceinline__ void wave_lds_sync() {
 // the staging area the 16-byte chunk c of row x sits at c ^ ((x / 2) % 8),
 // which spreads both the writes and the reads over all LDS banks.
 template <bool OUT_BF16, bool VEC>
-__device__ __forceinline__ void store_item(const f32x16_t (&acc)[4][4], const WorkItem& cur,
+__device__ __forceinline__ void store_item(f32x16_t (&acc)[4][4], const WorkItem& cur,
                                            const SplitPlan& sp, int M, int N, int tiles_m, int tiles_n,
                                            int wave, int lane, float alpha, void* __restrict__ C,
                                            uint8_t* __restrict__ ep) {
@@ -866,6 +866,8 @@ __device__ __forceinline__ void store_item(const f32x16_t (&acc)[4][4], const Wo
             };
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
+                // the round's accumulators are read only from here on
+                asm volatile("" : "+a"(acc[q >> 1][2 * (q & 1)]), "+a"(acc[q >> 1][2 * (q & 1) + 1]));
                 u32x2_t v[8];
                 pack(q, v);
 #pragma unroll
@@ -886,6 +888,7 @@ __device__ __forceinline__ void store_item(const f32x16_t (&acc)[4][4], const Wo
 #pragma unroll
             for (int q = 0; q < 16; ++q) {
                 const int i = q >> 2, j = q & 3;
+                asm volatile("" : "+a"(acc[i][j]));
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
                     const f32x4_t v = {alpha * acc[i][j][4 * g], alpha * acc[i][j][4 * g + 1],

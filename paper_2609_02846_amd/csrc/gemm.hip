@@ -1063,9 +1063,11 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_fp4_reg_kernel(
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < 4; ++j) {
 #pragma unroll
                 for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+                asm volatile("" : "+a"(acc[i][j]));      // zeros go straight to the AccVGPRs
+            }
 
         // One slice.  Slices 0..2 of a stage read the next slice of the same
         // stage; slice 3 first waits for the next stage (loaded during the

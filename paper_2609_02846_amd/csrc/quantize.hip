@@ -433,8 +433,8 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
         }
         const ColItem cn = nit < nitems ? col_item(nit, gx, rows, rows_per_item) : ci;
         // RN prefetches the next group into registers; SR (VALU-bound)
-        // keeps its registers for more resident waves and loads each group
-        // after storing the previous one
+        // keeps its registers for more resident waves and loads the next
+        // group into the same registers once this one's values are consumed
         if (!SR && nit < nitems) load(cn, ng, nlo, nhi);
 
         const int64_t c = ci.cw + 4 * q;
@@ -515,6 +515,9 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
                     stS[4 * q + j][(sg * kColGroupRB + rbl) / H] = (uint8_t)bs[j].code;
             }
         }
+        // SR: this group's values are consumed; the next group's loads go out
+        // now and overlap the stores below (same registers, none added)
+        if (SR && nit < nitems) load(cn, ng, lo, hi);
         __syncthreads();
         // payload: 2 lanes per column, 32 bytes each (the group's valid row
         // blocks only; a full group is 64 contiguous bytes)
@@ -561,9 +564,7 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
         it = nit;
         g = ng;
         ci = cn;
-        if (SR) {
-            load(ci, g, lo, hi);
-        } else {
+        if (!SR) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 lo[r] = nlo[r];

@@ -293,3 +293,32 @@ def test_single_small_linear_fprop():
             e = float(al) * K * 2.0 ** -23 * ap
             ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref) + e, 1e-30))) - 7)
             assert np.all(np.abs(host(y.float()).astype(np.float64) - ref) <= e + 1.01 * ulp + 1e-30)
+
+
+@pytest.mark.parametrize("out", ["bf16", "f32"])
+def test_vector_epilogue_edges(out):
+    """The staged whole-tile epilogue (bf16 with N % 8 == 0, fp32 with
+    N % 4 == 0): output rows past M inside a 32-row round, 8-column (4-column)
+    runs past N inside a 64-column (32-column) round, and more than one tile
+    in each direction."""
+    say("gemm vector epilogue edges", out)
+    Ns = [8, 24, 40, 136, 264] if out == "bf16" else [4, 12, 36, 132, 260]
+    for M, N, K in [(1, Ns[0], 64), (37, Ns[1], 128), (259, Ns[2], 256), (300, Ns[3], 512), (517, Ns[4], 256)]:
+        a = synthetic.activation(6, M, K, 1e-2, 50.0)
+        w = synthetic.weight(6, N, K)
+        ar = oq.quantize_1d(a, 1, osc.amax(a))
+        # row-scaled B keeps N free of the tile constraint (N % 16)
+        wr = oq.quantize_1d(w, 1, osc.amax(w))
+        A, W = oq.decoded_1d(ar[0], ar[1], 1), oq.decoded_1d(wr[0], wr[1], 1)
+        al = ogemm.alpha(ar[2], wr[2])
+        dt = torch.bfloat16 if out == "bf16" else torch.float32
+        c = ue.gemm("nt", M, N, K, u8_to_dev(ar[0]), u8_to_dev(ar[1]), f32_scalar_dev(ar[2]),
+                    u8_to_dev(wr[0]), u8_to_dev(wr[1]), f32_scalar_dev(wr[2]), out_dtype=dt,
+                    a_blk=ue.ROW16, b_blk=ue.ROW16)
+        ref = ogemm.fprop(A, W, al)
+        got = c.float().cpu().numpy().astype(np.float64)
+        if out == "bf16":
+            ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
+            assert np.all(np.abs(got - ref) <= ulp * 1.01 + 1e-30), f"bf16 {M}x{N}x{K}"
+        else:
+            gemm_check(got, ref, al, ogemm.abs_product(A, W), K, f"f32 {M}x{N}x{K}")

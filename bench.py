@@ -420,7 +420,9 @@ def gemm_shapes(dev):
         rec = {"M": M, "N": N, "K": K, "tiles_per_cu": round(((M + 255) // 256) * ((N + 255) // 256) / 256, 2)}
         for od in (torch.bfloat16, torch.float32):
             c = torch.empty(M, N, device=dev, dtype=od)
-            for _ in range(3):
+            # warm-up long enough for the clock to settle under load (the
+            # first launches of a process run slower)
+            for _ in range(15):
                 ue.gemm("nt", M, N, K, xp, xs, xd, wp, ws, wd, out=c, out_dtype=od)
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)

@@ -70,6 +70,10 @@ def parse():
     p.add_argument("--control", action="store_true",
                    help="teacher-student regression control: BF16 vs FP4 (probe-matched GEMM) final-eval MSE "
                         "and grid invariance over seeds 41-43, RN and SR gradients")
+    p.add_argument("--drift", action="store_true",
+                   help="the FFN down-projection drift run (T=8192, K=21504, N=4096): 120 steps with the "
+                        "sample-and-hold reference (--period) while operand magnitudes drift and spike; "
+                        "prints its own JSON line")
     p.add_argument("--formats", action="store_true",
                    help="scale-format comparison instead of the headline step: UE5M3 (delayed "
                         "amax; blocks of 16 and the block-32 control), E4M3 (current amax) and "
@@ -367,6 +371,94 @@ def formats_bench(args):
                       "formats": res}), flush=True)
 
 
+def drift_bench(args):
+    """The drift run: FFN down-projection (T = 8192, K = 21504, N = 4096)
+    for 120 steps with the sample-and-hold reference (eq:delayed-amax, period
+    --period) while the operand magnitudes drift (lognormal walk, sigma 0.05
+    per step) and spike (x20 on random steps).  Step t's operands are
+    bf16(base x f_t), formed on the device between two timed intervals; each
+    interval holds the step's whole path: the three sample-and-hold calls
+    (amax kernels on refresh steps), X rows and columns from one read, W
+    tiles, dY rows and columns (SR), fprop, dgrad and wgrad.  Reports the
+    mean path time per step, the refresh steps and how many of the steps ran
+    on a held reference that the current operand exceeds (saturating
+    blocks) or undershoots by more than 2^10."""
+    import torch
+    import paper_2609_02846_amd as ue
+    import synthetic
+    T, K, N, STEPS = 8192, 21504, 4096, 120
+    dev = torch.device("cuda:0")
+    wl = synthetic.ffn_down_drift(0, T, K, N)
+    f = synthetic.drift_factors(0, STEPS)
+    up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+    base = [up(wl["x"]), up(wl["w"]), up(wl["dy"])]
+    del wl
+    bmax = [float(b.float().abs().max()) for b in base]
+    cur = [torch.empty_like(b) for b in base]
+    u8 = lambda *sh: torch.empty(sh, dtype=torch.uint8, device=dev)
+    f32 = lambda *sh: torch.empty(sh, dtype=torch.float32, device=dev)
+    xr, xc = (u8(T, K // 2), u8(T, K // 16), f32(1)), (u8(K, T // 2), u8(K, T // 16))
+    wq = (u8(N, K // 2), u8(N // 16, K // 16), u8(K, N // 2), f32(1), u8(K // 16, N // 16))
+    dr, dc = (u8(T, N // 2), u8(T, N // 16), f32(1)), (u8(N, T // 2), u8(N, T // 16), f32(1))
+    y = torch.empty(T, N, dtype=torch.bfloat16, device=dev)
+    dx = torch.empty(T, K, dtype=torch.bfloat16, device=dev)
+    dw = torch.empty(N, K, dtype=torch.float32, device=dev)
+
+    def run(st, t, ev=None):
+        for j in range(3):
+            torch.mul(base[j], float(f[t, j]), out=cur[j])
+        if ev is not None:
+            ev[0].record()
+        n = [int(ue.amax_sample(st[r], cur[j], t)) for j, r in enumerate("xwd")]
+        ue.quantize_dual(cur[0], st["x"].amax, 448.0, "rn", 0, 0, 0, xr[:2], xc, xr[2])
+        ue.quantize_2d(cur[1], st["w"].amax, 448.0, "rn", 0, 0, True, *wq)
+        ue.quantize_1d(cur[2], 1, st["d"].amax, 448.0, "sr", 5000 + t, 1, *dr)
+        ue.quantize_1d(cur[2], 0, st["d"].amax, 448.0, "sr", 5000 + t, 2, *dc)
+        ue.gemm("nt", T, N, K, xr[0], xr[1], xr[2], wq[0], wq[1], wq[3], out=y)
+        ue.gemm("nn", T, K, N, dr[0], dr[1], dr[2], wq[2], wq[4], wq[3], out=dx)
+        ue.gemm("tn", N, K, T, dc[0], dc[1], dc[2], xc[0], xc[1], xr[2], out=dw)
+        if ev is not None:
+            ev[1].record()
+        return n
+
+    warm = {r: ue.AmaxState(args.period) for r in "xwd"}
+    for t in range(3):
+        run(warm, t)
+    torch.cuda.synchronize()
+    st = {r: ue.AmaxState(args.period) for r in "xwd"}
+    evs = [_events(2) for _ in range(STEPS)]
+    refreshed = []
+    for t in range(STEPS):
+        refreshed.append(run(st, t, evs[t]))
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in evs])
+    # held reference vs the operand's own amax, per role and step (from the
+    # known base maxima and factors: bf16 rounding is monotone)
+    held = np.zeros((STEPS, 3))
+    last = [0.0, 0.0, 0.0]
+    for t in range(STEPS):
+        for j in range(3):
+            if refreshed[t][j]:
+                last[j] = bmax[j] * float(f[t, j])
+            held[t, j] = last[j]
+    ratio = np.array([[bmax[j] * float(f[t, j]) / held[t, j] for j in range(3)] for t in range(STEPS)])
+    flop = 3 * 2.0 * T * N * K
+    print(json.dumps({
+        "metric": "drift run: quantize + emulated FP4 GEMM step time under sample-and-hold scaling",
+        "unit": "ms", "value": round(float(ms.mean()), 4), "higher_is_better": False, "n_gpus": 1,
+        "steps": STEPS, "warmup": 3, "data": "synthetic", "dtype": "fp16",
+        "config": {"workload": "FFN down-projection drift run T=8192 K=21504 N=4096", "period": args.period,
+                   "drift_sigma": 0.05, "spike": 20.0},
+        "ms_per_step_p10_p50_p90": [round(float(q), 4) for q in np.percentile(ms, [10, 50, 90])],
+        "gemm_TFLOPs": round(flop / (float(ms.mean()) * 1e-3) / 1e12, 1),
+        "refresh_steps": [t for t in range(STEPS) if any(refreshed[t])],
+        "refreshes_per_role": {r: int(sum(refreshed[t][j] for t in range(STEPS))) for j, r in enumerate("xwd")},
+        "steps_above_held_reference": {r: int((ratio[:, j] > 1.0).sum()) for j, r in enumerate("xwd")},
+        "steps_below_held_reference_by_2e10": {r: int((ratio[:, j] < 2.0 ** -10).sum()) for j, r in enumerate("xwd")},
+        "max_operand_over_held": {r: round(float(ratio[:, j].max()), 2) for j, r in enumerate("xwd")},
+    }), flush=True)
+
+
 def matmul_ref(T, K, N, dev):
     """bf16 inputs, library GEMM (hipBLASLt through torch.matmul): what a plain
     dense bf16 product of the step's three shapes reaches on this GPU, as a
@@ -583,6 +675,9 @@ def main():
         return
     if args.formats:
         formats_bench(args)
+        return
+    if args.drift:
+        drift_bench(args)
         return
     T, K, N = args.tokens, args.k, args.n
     want_cpu = (not args.no_cpu_baseline and args.pm is None and not args.rht and args.kernel is None

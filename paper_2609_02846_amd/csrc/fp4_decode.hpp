@@ -13,20 +13,14 @@ typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
 typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 
-// Decode factors of UE5M3 code c, computed arithmetically (no table, so
-// decoding never waits on LDS traffic): s = mu * 2^E with
-//   exponent field e >= 1: mu = 1 + m/8, E = e - 15;
-//   e == 0 (s = m * 2^-17):  mu = m (an integer), E = -17.
-// Returns (bits of 2^(E-3), fp16 pair (mu, mu)).  q * 2^(E-3) (the FP4
-// conversion) and its product with mu are exact in fp16 for every code.
+// Decode factors of UE5M3 code c: the code read as an fp16 bit pattern
+// shifted left by 7 (5 exponent bits with bias 15, 3 leading mantissa bits;
+// code 0..7 land on the fp16 subnormals m 2^-17) is exactly its value s, so
+// the factors are the power of two 2^-3 for the FP4 conversion and the fp16
+// pair (s, s).  q * 2^-3 and its product with s are exact in fp16 for every
+// code (|q s 2^-3| <= 46080, a multiple of 2^-24).
 __device__ __forceinline__ uint2 scale_factors(uint32_t c) {
-    const uint32_t e = (c >> 3) & 31u, m = c & 7u;
-    const _Float16 mi = (_Float16)(uint16_t)m;                 // exact
-    uint16_t mib;
-    __builtin_memcpy(&mib, &mi, 2);
-    const uint32_t mu = e ? (0x3C00u | (m << 7)) : (uint32_t)mib;
-    const uint32_t pow_bits = (e ? e + 109u : 107u) << 23;
-    return make_uint2(pow_bits, mu | (mu << 16));
+    return make_uint2(__float_as_uint(0.125f), (c << 7) | (c << 23));
 }
 
 // Decode 8 packed nibbles x (element e in bits 4e..4e+3) into 4 fp16 pairs

@@ -118,10 +118,16 @@ __device__ __forceinline__ uint32_t sr_pair(uint32_t p, v2f_t v, uint32_t r) {
 // True when w lies in the 1024-word bucket of y's threshold (|y| < 1), or
 // spuriously with probability 2^-22 (|y| >= 1), which only costs a redo.
 // The conversion to integer saturates (|y| * 2^23 may exceed 2^32).
+// With A = (q mod 2^22) * 1024 = q << 10 (mod 2^32), w >> 10 equals q mod
+// 2^22 exactly when w lies in [A, A + 1023], i.e. when A + ~w = A - w - 1
+// (mod 2^32) is one of the top 1024 values; ~w is the SR operand already
+// formed for the conversion, so the test is one shift-add and one compare.
 __device__ __forceinline__ bool sr_check(float y, uint32_t w) {
     uint32_t q;
     asm("v_cvt_u32_f32 %0, %1" : "=v"(q) : "v"(fabsf(y) * 0x1p23f));
-    return (w >> 10) == (q & 0x3FFFFFu);
+    uint32_t t;
+    asm("v_lshl_add_u32 %0, %1, 10, %2" : "=v"(t) : "v"(q), "v"(~w));
+    return t > 0xFFFFFBFFu;
 }
 
 // 8 values y (element e -> nibble e) by SR with words w.

@@ -787,10 +787,10 @@ __device__ __forceinline__ void wave_lds_sync() {
 // block (the products are issued as B x A^T).  A split part stores its fp32
 // partial; a whole tile stores alpha * value through a buffer resource over
 // C, where an out-of-range offset drops the store, which masks rows and
-// columns past C without branches.  VEC (a launch-time choice): N % 8 == 0
-// for bf16, N % 4 == 0 for fp32, where every run of 8 (4) output columns
-// lies wholly inside C or wholly past it; otherwise each element is masked
-// on its own.  With VEC the values pass through the wave's 4 KB of LDS
+// columns past C without branches.  VEC (a launch-time choice,
+// vector_epilogue): N % 8 == 0 for bf16, N % 4 == 0 for fp32, where every
+// run of 8 (4) output columns lies wholly inside C or wholly past it;
+// otherwise each element is masked on its own.  With VEC the values pass through the wave's 4 KB of LDS
 // (`ep`), 32 rows x 128 bytes at a time, and leave as stores of 128
 // contiguous bytes per row (8 rows per instruction): a lane holds one row,
 // so storing straight from the accumulators writes 32 rows x 32 bytes per
@@ -1500,6 +1500,16 @@ hipError_t expand_scales(const uint8_t* in, int64_t cols_in, int rrep, uint8_t* 
 
 constexpr int kSplitRemDiv = 2;
 
+// Whether the whole-tile epilogue may store vector runs: N a multiple of the
+// run (8 bf16 or 4 fp32 columns), and for bf16 every row offset of the padded
+// tile grid below 2^31 bytes, since that path drops rows past M by their
+// offset alone (lane base + uniform row offset, no row compare).
+template <bool OUT_BF16>
+bool vector_epilogue(int64_t N, int tiles_m) {
+    if (OUT_BF16) return N % 8 == 0 && (int64_t)tiles_m * BM * N * 2 < ((int64_t)1 << 31);
+    return N % 4 == 0;
+}
+
 template <int BMODE, bool OUT_BF16>
 hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const uint8_t* as,
                       const float* ad, const uint8_t* b, const uint8_t* bs, const float* bd,
@@ -1538,7 +1548,7 @@ hipError_t launch_reg(int64_t M, int64_t N, int64_t K, const uint8_t* a, const u
     // persistent (one workgroup per CU walking the items) when every item has
     // an even stage count, else one item per workgroup
     const int grid = (even && cus > 0) ? min(items, cus) : items;
-    if (N % (OUT_BF16 ? 8 : 4) == 0)
+    if (vector_epilogue<OUT_BF16>(N, tiles_m))
         hipLaunchKernelGGL((gemm_fp4_reg_kernel<BMODE, OUT_BF16, true>), dim3((unsigned)grid), dim3(kGemmThreads),
                            0, s, (int)M, (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c, amul);
     else
@@ -1576,7 +1586,7 @@ hipError_t launch_mx(int64_t M, int64_t N, int64_t K, const uint8_t* a, const ui
     }
     const int items = sp.Tdp + (T - sp.Tdp) * sp.parts;
     const int grid = (even && cus > 0) ? min(items, cus) : items;
-    if (N % (OUT_BF16 ? 8 : 4) == 0)
+    if (vector_epilogue<OUT_BF16>(N, tiles_m))
         hipLaunchKernelGGL((gemm_mx_kernel<OUT_BF16, true>), dim3((unsigned)grid), dim3(kGemmThreads), 0, s, (int)M,
                            (int)N, (int)K, tiles_m, tiles_n, items, sp, a, as, ad, b, bs, bd, c);
     else

@@ -322,3 +322,32 @@ def test_vector_epilogue_edges(out):
             assert np.all(np.abs(got - ref) <= ulp * 1.01 + 1e-30), f"bf16 {M}x{N}x{K}"
         else:
             gemm_check(got, ref, al, ogemm.abs_product(A, W), K, f"f32 {M}x{N}x{K}")
+
+
+def test_bf16_small_m_wide_n():
+    """bf16 output with few rows and very many columns (16 x 12582912, K =
+    256: the register-decode kernel): the padded tile rows' byte offsets pass
+    2^32 there, so the vector epilogue (which drops rows past M by their
+    offset) must not be used; every sampled output, row 0 included, equals
+    the oracle's product."""
+    M, N, K = 16, 3 << 22, 256
+    say("gemm bf16 small M wide N", M, N, K)
+    rng = np.random.default_rng(21)
+    g = torch.Generator(device="cuda").manual_seed(21)
+    a = rng.integers(0, 256, (M, K // 2), dtype=np.uint8)
+    a_s = rng.integers(100, 130, (M, K // 16)).astype(np.uint8)
+    b = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device="cuda", generator=g)
+    b_s = torch.randint(100, 130, (N, K // 16), dtype=torch.uint8, device="cuda", generator=g)
+    dec = np.float32(1.0 / 64.0)
+    c = ue.gemm("nt", M, N, K, u8_to_dev(a), u8_to_dev(a_s), f32_scalar_dev(dec), b, b_s,
+                f32_scalar_dev(dec), out_dtype=torch.bfloat16, a_blk=ue.ROW16, b_blk=ue.ROW16)
+    torch.cuda.synchronize()
+    cols = np.unique(np.concatenate([rng.integers(0, N, 600), np.arange(0, 64), np.arange(N - 64, N)]))
+    ci = torch.from_numpy(cols).to("cuda")
+    A = oq.decoded_1d(a, a_s, 1)
+    B = oq.decoded_1d(host(b[ci]), host(b_s[ci]), 1)
+    al = ogemm.alpha(dec, dec)
+    ref = ogemm.fprop(A, B, al)                                   # [M, len(cols)]
+    got = c[:, ci].float().cpu().numpy().astype(np.float64)
+    ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
+    assert np.all(np.abs(got - ref) <= ulp * 1.01 + 1e-30)

@@ -837,7 +837,11 @@ __device__ __forceinline__ void store_item(f32x16_t (&acc)[4][4], const WorkItem
         // 32-row block; read side: lane l takes chunk l % 8 of row
         // l / 8 + 8t.  bf16: a store's row lies past C exactly when its
         // offset does (the column run is checked once), so the per-store
-        // offset is the lane's base plus a uniform row offset.
+        // offset is the lane's base plus a uniform row offset.  The sum is
+        // formed in the vector offset, so that the range check sees the
+        // whole offset (the compiler's buffer intrinsics document the scalar
+        // offset as outside that check) and stays below 2^32 by the launch
+        // condition.
         const int wsw = (r >> 1) & 7;
         const int rr = lane >> 3, rc = lane & 7;
         const uint32_t mb = (uint32_t)((int)m0 + wm * 128 + rr);
@@ -879,8 +883,8 @@ __device__ __forceinline__ void store_item(f32x16_t (&acc)[4][4], const WorkItem
                 const int i = q >> 1, h = q & 1;
 #pragma unroll
                 for (int t = 0; t < 4; ++t)
-                    __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4_t*>(rd[t]), cr, vb[h],
-                                                           (32 * i + 8 * t) * N * 2, 0);
+                    __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4_t*>(rd[t]), cr,
+                                                           vb[h] + (uint32_t)((32 * i + 8 * t) * N * 2), 0, 0);
                 wave_lds_sync();
             }
         } else {

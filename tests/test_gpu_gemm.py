@@ -328,26 +328,86 @@ def test_bf16_small_m_wide_n():
     """bf16 output with few rows and very many columns (16 x 12582912, K =
     256: the register-decode kernel): the padded tile rows' byte offsets pass
     2^32 there, so the vector epilogue (which drops rows past M by their
-    offset) must not be used; every sampled output, row 0 included, equals
-    the oracle's product."""
-    M, N, K = 16, 3 << 22, 256
+    offset) must not be used.  B repeats a block of 768 random rows, so every
+    output column equals one of 768 columns the oracle computes, and all
+    201 million outputs are compared with it."""
+    M, N, K, P = 16, 3 << 22, 256, 768
     say("gemm bf16 small M wide N", M, N, K)
     rng = np.random.default_rng(21)
-    g = torch.Generator(device="cuda").manual_seed(21)
     a = rng.integers(0, 256, (M, K // 2), dtype=np.uint8)
     a_s = rng.integers(100, 130, (M, K // 16)).astype(np.uint8)
-    b = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device="cuda", generator=g)
-    b_s = torch.randint(100, 130, (N, K // 16), dtype=torch.uint8, device="cuda", generator=g)
+    bp = rng.integers(0, 256, (P, K // 2), dtype=np.uint8)
+    bp_s = rng.integers(100, 130, (P, K // 16)).astype(np.uint8)
+    b = u8_to_dev(bp).repeat(N // P, 1)
+    b_s = u8_to_dev(bp_s).repeat(N // P, 1)
     dec = np.float32(1.0 / 64.0)
     c = ue.gemm("nt", M, N, K, u8_to_dev(a), u8_to_dev(a_s), f32_scalar_dev(dec), b, b_s,
                 f32_scalar_dev(dec), out_dtype=torch.bfloat16, a_blk=ue.ROW16, b_blk=ue.ROW16)
     torch.cuda.synchronize()
-    cols = np.unique(np.concatenate([rng.integers(0, N, 600), np.arange(0, 64), np.arange(N - 64, N)]))
-    ci = torch.from_numpy(cols).to("cuda")
-    A = oq.decoded_1d(a, a_s, 1)
-    B = oq.decoded_1d(host(b[ci]), host(b_s[ci]), 1)
     al = ogemm.alpha(dec, dec)
-    ref = ogemm.fprop(A, B, al)                                   # [M, len(cols)]
-    got = c[:, ci].float().cpu().numpy().astype(np.float64)
+    ref = ogemm.fprop(oq.decoded_1d(a, a_s, 1), oq.decoded_1d(bp, bp_s, 1), al)      # [M, P]
     ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
-    assert np.all(np.abs(got - ref) <= ulp * 1.01 + 1e-30)
+    r = torch.from_numpy(ref).cuda()[:, None, :]
+    tol = torch.from_numpy(ulp * 1.01 + 1e-30).cuda()[:, None, :]
+    bad = (c.view(M, N // P, P).double() - r).abs() > tol
+    assert not bool(bad.any()), f"{int(bad.sum())} outputs differ"
+
+
+_SENTINEL = {torch.bfloat16: (torch.int16, 0x7FC1), torch.float32: (torch.int32, 0x7FC00001)}
+
+
+def _random_operands(g, M, N, K, block, codes):
+    lo, hi = codes
+    a = torch.randint(0, 256, (M, K // 2), dtype=torch.uint8, device="cuda", generator=g)
+    a_s = torch.randint(lo, hi, (M, K // block), dtype=torch.uint8, device="cuda", generator=g)
+    b = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device="cuda", generator=g)
+    b_s = torch.randint(lo, hi, (N, K // block), dtype=torch.uint8, device="cuda", generator=g)
+    return a, a_s, b, b_s
+
+
+@pytest.mark.parametrize("entry,M,N,K,dt,fmt,block", [
+    ("gemm", 300, 136, 512, "bf16", "ue5m3", 16),      # vector epilogue, bf16
+    ("gemm", 300, 132, 512, "f32", "ue5m3", 16),       # vector epilogue, fp32
+    ("gemm", 37, 140, 512, "bf16", "ue5m3", 16),       # per-element epilogue (N % 8 = 4)
+    ("gemm", 37, 130, 512, "f32", "ue5m3", 16),        # per-element epilogue (N % 4 = 2)
+    ("gemm", 4252, 4096, 1024, "bf16", "ue5m3", 16),   # split leftover tiles, ragged M
+    ("gemm", 300, 136, 192, "bf16", "ue5m3", 16),      # K % 256 != 0: staged kernel
+    ("gemm", 37, 40, 48, "f32", "ue5m3", 16),          # K % 64 != 0: general kernel
+    ("gemm", 300, 136, 512, "bf16", "ue5m3", 32),      # blocks of 32
+    ("gemm", 300, 136, 512, "bf16", "e8m0", 32),       # E8M0 scales
+    ("gemm_pm", 300, 136, 512, "bf16", "ue5m3", 16),   # probe-matched
+    ("gemm_pm", 37, 132, 512, "f32", "ue5m3", 16),
+    ("gemm_noalloc", 300, 136, 512, "bf16", "ue5m3", 16),
+])
+def test_writes_exactly_c(entry, M, N, K, dt, fmt, block):
+    """C lies inside a larger buffer filled with a NaN bit pattern that the
+    product of finite operands never yields.  After one call every element of
+    C has been written (none holds the pattern) and nothing before or after
+    C has: the guard after C spans the rows of the padded 256-row tile grid
+    past M and one more tile row, which holds every store a tile of C could
+    address.  Covers ragged M inside a tile and inside an epilogue round, the
+    vector and per-element epilogues, split leftover tiles, the staged and
+    general kernels, blocks of 32, E8M0 scales and the probe-matched GEMM."""
+    say("gemm writes exactly C", entry, M, N, K, dt, fmt, block)
+    dt = torch.bfloat16 if dt == "bf16" else torch.float32
+    g = torch.Generator(device="cuda").manual_seed(M * 7 + N)
+    codes = (120, 131) if fmt == "e8m0" else (100, 131)
+    a, a_s, b, b_s = _random_operands(g, M, N, K, block, codes)
+    it, pat = _SENTINEL[dt]
+    pre = 4096
+    post = ((M + 255) // 256 * 256 - M + 256) * N
+    buf = torch.full((pre + M * N + post,), pat, dtype=it, device="cuda")
+    out = buf[pre:pre + M * N].view(dt).view(M, N)
+    dec = f32_scalar_dev(1.0 / 64.0)
+    kw = dict(out=out, a_blk=ue.ROW16 if block == 16 else ue.ROW32, b_blk=ue.ROW16 if block == 16 else ue.ROW32)
+    if entry == "gemm":
+        ue.gemm("nt", M, N, K, a, a_s, dec, b, b_s, dec, fmt=fmt, block=block, **kw)
+    elif entry == "gemm_pm":
+        ue.gemm_pm("nt", M, N, K, a, a_s, dec, b, b_s, dec, **kw)
+    else:
+        ue.gemm_noalloc("nt", M, N, K, a, a_s, dec, b, b_s, dec, **kw)
+    torch.cuda.synchronize()
+    assert bool((buf[:pre] == pat).all()), "written before C"
+    assert bool((buf[pre + M * N:] == pat).all()), "written after C"
+    assert not bool((buf[pre:pre + M * N] == pat).any()), "elements of C left unwritten"
+    assert bool(torch.isfinite(out).all())

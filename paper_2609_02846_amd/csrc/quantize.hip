@@ -103,6 +103,7 @@ __device__ __forceinline__ uint32_t rn_pair(uint32_t p, float y0, float y1) {
 // where that element reads it, and the two valid nibbles are merged.  A
 // flagged element's nibble is replaced by the software rounding.
 typedef float v2f_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 // Written as an instruction with p as a read-write operand: the compiler's
 // builtin for this conversion does not keep the destination's other bytes.
@@ -826,6 +827,27 @@ struct DualStage {
     uint8_t SC[kTileCols][kTileRowTiles];             // column scales, 8 per column
 };
 
+// Tile (column band bc, row band br) of walk index it.  With whole 8 x 8
+// superblocks of tiles (sb), walk index it belongs to the XCD it % 8
+// (workgroups are dispatched round-robin over the XCDs and the persistent
+// grid is a multiple of 8), which owns superblocks it % 8, it % 8 + 8, ...
+// walked row by row: every 64-byte run of row or column scale codes and every
+// 128-byte line of transposed payload is then written by tiles of one XCD
+// close together in time, so its L2 assembles whole lines before they are
+// written back (8-byte pieces from different XCDs cost partial-line writes).
+__device__ __forceinline__ void dual_tile(int64_t it, int64_t gx, bool sb, int64_t& bc, int64_t& br) {
+    if (!sb) {
+        bc = it % gx;
+        br = it / gx;
+        return;
+    }
+    const int64_t s = it >> 3;
+    const int64_t sbi = (it & 7) + 8 * (s >> 6);
+    const int64_t u = s & 63;
+    bc = (sbi % (gx >> 3)) * 8 + (u & 7);
+    br = (sbi / (gx >> 3)) * 8 + (u >> 3);
+}
+
 template <bool SR, int FMT>
 __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
     const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t gx, int64_t ntiles,
@@ -840,17 +862,22 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
     const int q = t & 31, trl = t >> 5;
     const int64_t ntr = rows / 16;
     const bool vec_scales = (cols % 128) == 0 && (ntr % 8) == 0;   // 8-byte scale runs aligned
+    const bool sb = (gx % 8) == 0 && (ntiles % 512) == 0;         // whole superblocks, 8 per XCD
 
     // 16 rows x 4 columns of this lane's piece of tile `it`: word pairs
-    // (c, c+1) in L, (c+2, c+3) in H (left untouched outside the tensor)
+    // (c, c+1) in L, (c+2, c+3) in H (left untouched outside the tensor).
+    // The input is read once: non-temporal loads keep it from displacing
+    // the partly written output lines in L2.
     auto load = [&](int64_t it, uint32_t (&L)[16], uint32_t (&H)[16]) {
-        const int64_t c = (it % gx) * kTileCols + 4 * q;
-        const int64_t tr = (it / gx) * kTileRowTiles + trl;
+        int64_t bc, br;
+        dual_tile(it, gx, sb, bc, br);
+        const int64_t c = bc * kTileCols + 4 * q;
+        const int64_t tr = br * kTileRowTiles + trl;
         if (c >= cols || tr >= ntr) return;                           // cols % 16 == 0: whole pieces
         const uint16_t* src = x + (tr * 16) * cols + c;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const uint2 v = *reinterpret_cast<const uint2*>(src + r * cols);
+            const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(src + r * cols));
             L[r] = v.x;
             H[r] = v.y;
         }
@@ -867,9 +894,11 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
         const int64_t nit = it + gridDim.x;
         if (kPrefetch && nit < ntiles) load(nit, nlo, nhi);
         DualStage& st = stage[buf];
-        const int64_t cw = (it % gx) * kTileCols;
+        int64_t bcol, brow;
+        dual_tile(it, gx, sb, bcol, brow);
+        const int64_t cw = bcol * kTileCols;
         const int64_t c = cw + 4 * q;
-        const int64_t tr0 = (it / gx) * kTileRowTiles;
+        const int64_t tr0 = brow * kTileRowTiles;
         const int64_t tr = tr0 + trl;
         if (!SR && c < cols && tr < ntr) {
             // RN: block maxima from the |x| bits, both blockings' scales, then

@@ -213,8 +213,9 @@ def test_quantizers_feed_gemm_end_to_end():
 @pytest.mark.parametrize("mode", ["rn", "sr"])
 def test_quantize_dual_equals_both_axes(fmt, mode):
     """ue5m3_quantize_dual writes exactly the axis-1 result (words keyed on
-    tensor_id_r) and the transposed axis-0 result (tensor_id_c)."""
-    for shape in [(16, 16), (48, 80), (128, 128), (256, 512), (208, 4096), (400, 1040)]:
+    tensor_id_r) and the transposed axis-0 result (tensor_id_c).  1024 x 8192
+    (512 tiles of 128 x 128) takes the superblock walk of the tiles."""
+    for shape in [(16, 16), (48, 80), (128, 128), (256, 512), (208, 4096), (400, 1040), (1024, 8192)]:
         say("dual", fmt, mode, shape)
         bits = synthetic.gradient(12, *shape, 1e-4, 2.0) if mode == "sr" else \
             synthetic.activation(12, *shape, 0.01, 50.0)

@@ -594,6 +594,38 @@ constexpr int kTileRowTiles = 8;
 // TB: tile edge, 16 (the recipe) or 32 (the block-size control: a 32 x 32
 // tile spans the 8 lanes of 32 columns and the lane pair l, l + 32 of two
 // 16-row tile rows, all in one wave).
+// Tile (column band bc, row band br) of walk index it on a gx x gy grid of
+// 128 x 128 tiles.  Workgroups are dispatched round-robin over the 8 XCDs,
+// so walk index it runs on XCD it % 8 (for a persistent walk: with a grid
+// that is a multiple of 8).  With gx and gy multiples of 8 the tiles form
+// 8 x 8 superblocks; XCD x takes superblocks x, x + 8, ... of the largest
+// multiple of 8 of them, walked row by row, and the few superblocks left
+// over follow in plain order.  Every 64-byte run of scale codes and every
+// 128-byte line of transposed payload is then written by tiles of one XCD
+// close together in time, so that XCD's L2 assembles whole lines before
+// they are written back (8-byte pieces from different XCDs leave it as
+// partial-line writes).  Otherwise row-major order.
+__device__ __forceinline__ void xcd_tile(int64_t it, int64_t gx, int64_t gy, int64_t& bc, int64_t& br) {
+    if ((gx & 7) != 0 || (gy & 7) != 0) {
+        bc = it % gx;
+        br = it / gx;
+        return;
+    }
+    const int64_t nsb = (gx >> 3) * (gy >> 3);
+    const int64_t even = (nsb & ~(int64_t)7) * 64;     // tiles of the superblocks dealt over the XCDs
+    int64_t sbi, u;
+    if (it < even) {
+        const int64_t s = it >> 3;
+        sbi = (it & 7) + 8 * (s >> 6);
+        u = s & 63;
+    } else {
+        sbi = (nsb & ~(int64_t)7) + ((it - even) >> 6);
+        u = (it - even) & 63;
+    }
+    bc = (sbi % (gx >> 3)) * 8 + (u & 7);
+    br = (sbi / (gx >> 3)) * 8 + (u >> 3);
+}
+
 template <bool SR, int FMT, int TB = 16>
 __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
     const uint16_t* __restrict__ w, int64_t rows, int64_t cols, const float* __restrict__ amax_dev,
@@ -603,12 +635,15 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
     __shared__ __attribute__((aligned(16))) uint8_t stT[kTileCols][kTileRowTiles * 8];
     static_assert(FMT != (int)ScaleKind::E8M0, "2D tiles take UE5M3 or E4M3 scales");
     const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
-    if (dec_out != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *dec_out = m.dec;
+    if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
     const int t = threadIdx.x;
     const int q = t & 31, trl = t >> 5;
-    const int64_t cw = (int64_t)blockIdx.x * kTileCols;
+    int64_t bc, br;
+    xcd_tile(blockIdx.x, (cols + kTileCols - 1) / kTileCols, (rows / 16 + kTileRowTiles - 1) / kTileRowTiles, bc,
+             br);
+    const int64_t cw = bc * kTileCols;
     const int64_t c = cw + 4 * q;
-    const int64_t tr = (int64_t)blockIdx.y * kTileRowTiles + trl;     // tile row
+    const int64_t tr = br * kTileRowTiles + trl;                      // tile row
     const int64_t ntr = rows / 16, ntc = cols / 16;
     const bool active = (c < cols) && (tr < ntr);                     // whole tiles: cols % 16 == 0
     if (active) {
@@ -696,7 +731,7 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
     __syncthreads();
     const int col = t >> 1, half = t & 1;
     const int64_t gc = cw + col;
-    const int64_t tr0 = (int64_t)blockIdx.y * kTileRowTiles;
+    const int64_t tr0 = br * kTileRowTiles;
     const int nvalid = (int)min((int64_t)kTileRowTiles, ntr - tr0);
     if (gc < cols) {
         uint8_t* dst = payload_t + gc * (rows / 2) + tr0 * 8 + half * 32;
@@ -827,27 +862,6 @@ struct DualStage {
     uint8_t SC[kTileCols][kTileRowTiles];             // column scales, 8 per column
 };
 
-// Tile (column band bc, row band br) of walk index it.  With whole 8 x 8
-// superblocks of tiles (sb), walk index it belongs to the XCD it % 8
-// (workgroups are dispatched round-robin over the XCDs and the persistent
-// grid is a multiple of 8), which owns superblocks it % 8, it % 8 + 8, ...
-// walked row by row: every 64-byte run of row or column scale codes and every
-// 128-byte line of transposed payload is then written by tiles of one XCD
-// close together in time, so its L2 assembles whole lines before they are
-// written back (8-byte pieces from different XCDs cost partial-line writes).
-__device__ __forceinline__ void dual_tile(int64_t it, int64_t gx, bool sb, int64_t& bc, int64_t& br) {
-    if (!sb) {
-        bc = it % gx;
-        br = it / gx;
-        return;
-    }
-    const int64_t s = it >> 3;
-    const int64_t sbi = (it & 7) + 8 * (s >> 6);
-    const int64_t u = s & 63;
-    bc = (sbi % (gx >> 3)) * 8 + (u & 7);
-    br = (sbi / (gx >> 3)) * 8 + (u >> 3);
-}
-
 template <bool SR, int FMT>
 __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
     const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t gx, int64_t ntiles,
@@ -862,7 +876,7 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
     const int q = t & 31, trl = t >> 5;
     const int64_t ntr = rows / 16;
     const bool vec_scales = (cols % 128) == 0 && (ntr % 8) == 0;   // 8-byte scale runs aligned
-    const bool sb = (gx % 8) == 0 && (ntiles % 512) == 0;         // whole superblocks, 8 per XCD
+    const int64_t gy = ntiles / gx;
 
     // 16 rows x 4 columns of this lane's piece of tile `it`: word pairs
     // (c, c+1) in L, (c+2, c+3) in H (left untouched outside the tensor).
@@ -870,7 +884,7 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
     // the partly written output lines in L2.
     auto load = [&](int64_t it, uint32_t (&L)[16], uint32_t (&H)[16]) {
         int64_t bc, br;
-        dual_tile(it, gx, sb, bc, br);
+        xcd_tile(it, gx, gy, bc, br);
         const int64_t c = bc * kTileCols + 4 * q;
         const int64_t tr = br * kTileRowTiles + trl;
         if (c >= cols || tr >= ntr) return;                           // cols % 16 == 0: whole pieces
@@ -895,7 +909,7 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
         if (kPrefetch && nit < ntiles) load(nit, nlo, nhi);
         DualStage& st = stage[buf];
         int64_t bcol, brow;
-        dual_tile(it, gx, sb, bcol, brow);
+        xcd_tile(it, gx, gy, bcol, brow);
         const int64_t cw = bcol * kTileCols;
         const int64_t c = cw + 4 * q;
         const int64_t tr0 = brow * kTileRowTiles;
@@ -1139,11 +1153,11 @@ hipError_t launch_tiles_fmt(const void* w_bf16, int64_t rows, int64_t cols, cons
     const int64_t gy = (rows / 16 + kTileRowTiles - 1) / kTileRowTiles;
     const uint16_t* w = reinterpret_cast<const uint16_t*>(w_bf16);
     if (sr)
-        hipLaunchKernelGGL((quant_tiles_kernel<true, FMT, TB>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
+        hipLaunchKernelGGL((quant_tiles_kernel<true, FMT, TB>), dim3((unsigned)(gx * gy)), dim3(kThreads),
                            0, s, w, rows, cols, amax_dev, target, k0, k1, tensor_id, payload, scales,
                            payload_t, scales_t, dec_out);
     else
-        hipLaunchKernelGGL((quant_tiles_kernel<false, FMT, TB>), dim3((unsigned)gx, (unsigned)gy), dim3(kThreads),
+        hipLaunchKernelGGL((quant_tiles_kernel<false, FMT, TB>), dim3((unsigned)(gx * gy)), dim3(kThreads),
                            0, s, w, rows, cols, amax_dev, target, k0, k1, tensor_id, payload, scales,
                            payload_t, scales_t, dec_out);
     return hipGetLastError();

@@ -132,16 +132,23 @@ __device__ __forceinline__ uint32_t e2m1_sr(float y, uint32_t w) {
 
 // Philox4x32-10 (Salmon et al., SC'11): four counter words, key (k0, k1),
 // ten rounds of two 32x32->64 multiplies, key bumped by the Weyl constants.
+// XT: truth table of the round's two three-input XORs (0x96; the
+// complemented 0x69 gives ~result at no cost).
+template <int XT = 0x96>
+__device__ __forceinline__ uint4 philox_round(uint4 c, uint32_t k0, uint32_t k1) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    // three-input XORs in one instruction each
+    return make_uint4(__builtin_amdgcn_bitop3_b32(hi1, c.y, k0, XT), lo1,
+                      __builtin_amdgcn_bitop3_b32(hi0, c.w, k1, XT), lo0);
+}
+
 __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
-        const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
-        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
-        const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
-        const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
-        // three-input XORs (truth table 0x96) in one instruction each
-        c = make_uint4(__builtin_amdgcn_bitop3_b32(hi1, c.y, k0, 0x96), lo1,
-                       __builtin_amdgcn_bitop3_b32(hi0, c.w, k1, 0x96), lo0);
+        c = philox_round(c, k0, k1);
         k0 += 0x9E3779B9u;
         k1 += 0xBB67AE85u;
     }
@@ -153,6 +160,22 @@ __device__ __forceinline__ uint4 sr_words4(uint64_t j, uint32_t tensor_id,
                                            uint32_t key0, uint32_t key1) {
     return philox4x32_10(make_uint4((uint32_t)j, (uint32_t)(j >> 32), tensor_id, 0u),
                          key0, key1);
+}
+
+// Their complements ~w (the operand form of the hardware SR conversion):
+// the last round's XOR words come complemented from the XNOR truth table,
+// the two product words take one NOT each.
+__device__ __forceinline__ uint4 sr_nwords4(uint64_t j, uint32_t tensor_id,
+                                            uint32_t key0, uint32_t key1) {
+    uint4 c = make_uint4((uint32_t)j, (uint32_t)(j >> 32), tensor_id, 0u);
+#pragma unroll
+    for (int r = 0; r < 9; ++r) {
+        c = philox_round(c, key0, key1);
+        key0 += 0x9E3779B9u;
+        key1 += 0xBB67AE85u;
+    }
+    c = philox_round<0x69>(c, key0, key1);
+    return make_uint4(c.x, ~c.y, c.z, ~c.w);
 }
 
 // bf16 word pair -> two binary32 values (exact).

@@ -33,38 +33,54 @@ struct BlockScale {
     float r;
 };
 
-// Block scale and reciprocal of a block from the bf16 bits of its largest
-// magnitude.  UE5M3 and E4M3: code = nearest code of a * S (zero code ->
-// code of 1.0), r = G / value(code).  E8M0: the power-of-two exponent of the
-// OCP microscaling rule and r = 2^-E (no tensor scale).
-// UE5M3 / E4M3 block scale of a block whose largest magnitude is a (any
-// binary32 value, e.g. of a transformed block).
+// Reciprocals G / value(c) of the 256 scale codes in LDS, one per thread of
+// the workgroup (kThreads == 256): a block's reciprocal is then one LDS read
+// instead of a decode and a division per block.  The table entry is the same
+// binary32 division, so the same value.  E8M0 needs no table (r = 2^-E is
+// formed exactly from the code).  Ends with a barrier: call it where every
+// thread of the workgroup arrives.
 template <int FMT>
-__device__ __forceinline__ BlockScale block_scale_value(float a, const Multipliers& m) {
+__device__ __forceinline__ void fill_recip(float* rtab, const Multipliers& m) {
+    if (FMT == (int)ScaleKind::E8M0) return;
+    const uint32_t c = threadIdx.x;
+    rtab[c] = m.G / (FMT == (int)ScaleKind::E4M3 ? e4m3_decode(c) : ue5m3_decode(c));
+    __syncthreads();
+}
+
+// UE5M3 / E4M3 block scale of a block whose largest magnitude is a (any
+// binary32 value, e.g. of a transformed block): code = nearest code of
+// a * S (zero code -> code of 1.0), r = G / value(code) from the table.
+template <int FMT>
+__device__ __forceinline__ BlockScale block_scale_value(float a, const Multipliers& m, const float* rtab) {
     BlockScale bs;
     const bool e4 = FMT == (int)ScaleKind::E4M3;
     uint32_t code = e4 ? e4m3_encode(a * m.S) : ue5m3_encode(a * m.S);
     code = code ? code : (e4 ? kE4M3CodeOne : kCodeOne);
     bs.code = code;
-    bs.r = m.G / (e4 ? e4m3_decode(code) : ue5m3_decode(code));
+    bs.r = rtab[code];
     return bs;
 }
 
+// Block scale and reciprocal of a block from the bf16 bits of its largest
+// magnitude.  E8M0: the power-of-two exponent of the OCP microscaling rule
+// and r = 2^-E (no tensor scale).
 template <int FMT>
-__device__ __forceinline__ BlockScale block_scale(uint32_t amax_bits15, const Multipliers& m) {
-    BlockScale bs;
+__device__ __forceinline__ BlockScale block_scale(uint32_t amax_bits15, const Multipliers& m,
+                                                  const float* rtab) {
     if (FMT == (int)ScaleKind::E8M0) {
+        BlockScale bs;
         bs.code = e8m0_code_of_amax(amax_bits15);
         bs.r = e8m0_reciprocal(bs.code);
         return bs;
     }
-    const float a = __uint_as_float(amax_bits15 << 16);
-    const bool e4 = FMT == (int)ScaleKind::E4M3;
-    uint32_t code = e4 ? e4m3_encode(a * m.S) : ue5m3_encode(a * m.S);
-    code = code ? code : (e4 ? kE4M3CodeOne : kCodeOne);
-    bs.code = code;
-    bs.r = m.G / (e4 ? e4m3_decode(code) : ue5m3_decode(code));
-    return bs;
+    return block_scale_value<FMT>(__uint_as_float(amax_bits15 << 16), m, rtab);
+}
+
+// Packed 16-bit unsigned maximum (per half).
+__device__ __forceinline__ uint32_t pk_max_u16(uint32_t a, uint32_t b) {
+    uint32_t r;
+    asm("v_pk_max_u16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
 }
 
 // Tensor multipliers of a quantizer launch (E8M0 has no tensor scale: the
@@ -96,12 +112,13 @@ __device__ __forceinline__ uint32_t rn_pair(uint32_t p, float y0, float y1) {
 // of R and y1 with bits 30..9; with R = ~w (y0) it rounds up iff
 // (w >> 10) < floor(frac * 2^22), while the rule here (w < ceil(frac * 2^32))
 // uses all 32 bits.  The two agree except when |y| < 1 and w >> 10 equals
-// floor(frac * 2^22) -- the 1024 words around the threshold -- which
-// sr_check flags.
+// floor(frac * 2^22) -- the 1024 words around the threshold -- which the
+// bucket check below flags.
 // (For |y| >= 1, frac * 2^32 is a multiple of 1024 and the rules coincide.)
 // Each pair is converted twice, once with each element's own word placed
-// where that element reads it, and the two valid nibbles are merged.  A
-// flagged element's nibble is replaced by the software rounding.
+// where that element reads it, and the two valid nibbles are merged.  The
+// words arrive complemented (nw = ~w, sr_nwords4).  A group with a flagged
+// element has all its nibbles redone by the software rounding.
 typedef float v2f_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
@@ -116,59 +133,71 @@ __device__ __forceinline__ uint32_t sr_pair(uint32_t p, v2f_t v, uint32_t r) {
     return p;
 }
 
-// True when w lies in the 1024-word bucket of y's threshold (|y| < 1), or
-// spuriously with probability 2^-22 (|y| >= 1), which only costs a redo.
-// The conversion to integer saturates (|y| * 2^23 may exceed 2^32).
-// With A = (q mod 2^22) * 1024 = q << 10 (mod 2^32), w >> 10 equals q mod
-// 2^22 exactly when w lies in [A, A + 1023], i.e. when A + ~w = A - w - 1
-// (mod 2^32) is one of the top 1024 values; ~w is the SR operand already
-// formed for the conversion, so the test is one shift-add and one compare.
-__device__ __forceinline__ bool sr_check(float y, uint32_t w) {
+// Bucket value of y and its complemented word nw: with q = floor(|y| 2^23)
+// (the conversion to integer saturates: |y| 2^23 may exceed 2^32) and
+// A = (q mod 2^22) * 1024 = q << 10 (mod 2^32), w >> 10 equals q mod 2^22
+// exactly when w lies in [A, A + 1023], i.e. when A + nw = A - w - 1
+// (mod 2^32) is one of the top 1024 values.  An element is flagged when its
+// bucket value exceeds kBucketTop: the 1024 words around y's threshold for
+// |y| < 1, or spuriously with probability 2^-22 (|y| >= 1), which only
+// costs a redo.  A group tests the maximum of its bucket values once.
+constexpr uint32_t kBucketTop = 0xFFFFFBFFu;
+__device__ __forceinline__ uint32_t sr_bucket(float y, uint32_t nw) {
     uint32_t q;
     asm("v_cvt_u32_f32 %0, %1" : "=v"(q) : "v"(fabsf(y) * 0x1p23f));
     uint32_t t;
-    asm("v_lshl_add_u32 %0, %1, 10, %2" : "=v"(t) : "v"(q), "v"(~w));
-    return t > 0xFFFFFBFFu;
+    asm("v_lshl_add_u32 %0, %1, 10, %2" : "=v"(t) : "v"(q), "v"(nw));
+    return t;
 }
 
-// 8 values y (element e -> nibble e) by SR with words w.
-__device__ __forceinline__ uint32_t sr8(const float (&y)[8], const uint32_t* w) {
+// 8 values y (element e -> nibble e) by SR with complemented words nw.
+__device__ __forceinline__ uint32_t sr8(const float (&y)[8], const uint32_t* nw) {
     uint32_t lo = 0u, hi = 0u;                 // valid low / high nibbles
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const v2f_t v = {y[2 * k], y[2 * k + 1]};
-        const uint32_t r0 = ~w[2 * k];
-        const uint32_t r1 = __builtin_amdgcn_alignbit(~w[2 * k + 1], ~w[2 * k + 1], 1);
+        const uint32_t r0 = nw[2 * k];
+        const uint32_t r1 = __builtin_amdgcn_alignbit(nw[2 * k + 1], nw[2 * k + 1], 1);
         if (k == 0) { lo = sr_pair<0>(lo, v, r0); hi = sr_pair<0>(hi, v, r1); }
         if (k == 1) { lo = sr_pair<1>(lo, v, r0); hi = sr_pair<1>(hi, v, r1); }
         if (k == 2) { lo = sr_pair<2>(lo, v, r0); hi = sr_pair<2>(hi, v, r1); }
         if (k == 3) { lo = sr_pair<3>(lo, v, r0); hi = sr_pair<3>(hi, v, r1); }
     }
     uint32_t p = (lo & 0x0F0F0F0Fu) | (hi & 0xF0F0F0F0u);
+    uint32_t tb = 0u;
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-        if (sr_check(y[e], w[e])) p = (p & ~(0xFu << (4 * e))) | (e2m1_sr(y[e], w[e]) << (4 * e));
+    for (int e = 0; e < 8; ++e) tb = max(tb, sr_bucket(y[e], nw[e]));
+    if (tb > kBucketTop) {
+        p = 0u;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) p |= e2m1_sr(y[e], ~nw[e]) << (4 * e);
+    }
     return p;
 }
 
-// 4 values y (element e -> nibble e of the low 16 bits) by SR with words w.
-__device__ __forceinline__ uint32_t sr4(const float (&y)[4], const uint32_t* w) {
+// 4 values y (element e -> nibble e of the low 16 bits) by SR with
+// complemented words nw.
+__device__ __forceinline__ uint32_t sr4(const float (&y)[4], const uint32_t* nw) {
     uint32_t lo = 0u, hi = 0u;
     const v2f_t v0 = {y[0], y[1]}, v1 = {y[2], y[3]};
-    lo = sr_pair<0>(lo, v0, ~w[0]);
-    hi = sr_pair<0>(hi, v0, __builtin_amdgcn_alignbit(~w[1], ~w[1], 1));
-    lo = sr_pair<1>(lo, v1, ~w[2]);
-    hi = sr_pair<1>(hi, v1, __builtin_amdgcn_alignbit(~w[3], ~w[3], 1));
+    lo = sr_pair<0>(lo, v0, nw[0]);
+    hi = sr_pair<0>(hi, v0, __builtin_amdgcn_alignbit(nw[1], nw[1], 1));
+    lo = sr_pair<1>(lo, v1, nw[2]);
+    hi = sr_pair<1>(hi, v1, __builtin_amdgcn_alignbit(nw[3], nw[3], 1));
     uint32_t p = (lo & 0x0F0Fu) | (hi & 0xF0F0u);
+    const uint32_t tb = max(max(sr_bucket(y[0], nw[0]), sr_bucket(y[1], nw[1])),
+                            max(sr_bucket(y[2], nw[2]), sr_bucket(y[3], nw[3])));
+    if (tb > kBucketTop) {
+        p = 0u;
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-        if (sr_check(y[e], w[e])) p = (p & ~(0xFu << (4 * e))) | (e2m1_sr(y[e], w[e]) << (4 * e));
+        for (int e = 0; e < 4; ++e) p |= e2m1_sr(y[e], ~nw[e]) << (4 * e);
+    }
     return p;
 }
 
 // Quantize the 8 bf16 values held in v (element e in half e&1 of word e>>1)
 // with reciprocal r; returns 8 nibbles packed little-endian.  For SR, w holds
-// the 8 Philox words of the elements.
+// the 8 complemented Philox words of the elements.
 template <bool SR>
 __device__ __forceinline__ uint32_t quant8(const uint4& v, float r, const uint32_t* w) {
     const uint32_t vv[4] = {v.x, v.y, v.z, v.w};
@@ -187,7 +216,7 @@ __device__ __forceinline__ uint32_t quant8(const uint4& v, float r, const uint32
 }
 
 // Column-wise nibbles of 16 rows of one column (values v[r] * r_, rows in
-// order) into two words, RN or SR.
+// order) into two words, RN or SR (w: complemented Philox words).
 template <bool SR>
 __device__ __forceinline__ void quant_col16(const float (&xv)[16], float r_, const uint32_t (&w)[16],
                                             uint32_t& p0, uint32_t& p1) {
@@ -214,9 +243,12 @@ __device__ __forceinline__ void quant_col16(const float (&xv)[16], float r_, con
     p1 = sr8(y1, w + 8);
 }
 
-__device__ __forceinline__ uint32_t amax8(const uint4& v) {
-    return max(max(bf16_abs_max_pair(v.x), bf16_abs_max_pair(v.y)),
-               max(bf16_abs_max_pair(v.z), bf16_abs_max_pair(v.w)));
+// Packed 16-bit maxima of |x| over the 8 bf16 values of v, into acc.
+__device__ __forceinline__ uint32_t amax8_pk(const uint4& v, uint32_t acc) {
+    acc = pk_max_u16(acc, v.x & 0x7FFF7FFFu);
+    acc = pk_max_u16(acc, v.y & 0x7FFF7FFFu);
+    acc = pk_max_u16(acc, v.z & 0x7FFF7FFFu);
+    return pk_max_u16(acc, v.w & 0x7FFF7FFFu);
 }
 
 // Philox words of elements 4j .. 4j+3 for the 4 columns c..c+3 of one row,
@@ -231,6 +263,19 @@ __device__ __forceinline__ void words4(uint64_t e0, uint32_t tid, uint32_t k0, u
     } else {
         const uint4 b = sr_words4((e0 >> 2) + 1, tid, k0, k1);
         w[0] = a.z; w[1] = a.w; w[2] = b.x; w[3] = b.y;
+    }
+}
+
+// The same four words complemented (~w, the SR operand form).
+template <bool ALIGNED = false>
+__device__ __forceinline__ void nwords4(uint64_t e0, uint32_t tid, uint32_t k0, uint32_t k1,
+                                        uint32_t* nw) {
+    const uint4 a = sr_nwords4(e0 >> 2, tid, k0, k1);
+    if (ALIGNED || (e0 & 3) == 0) {
+        nw[0] = a.x; nw[1] = a.y; nw[2] = a.z; nw[3] = a.w;
+    } else {
+        const uint4 b = sr_nwords4((e0 >> 2) + 1, tid, k0, k1);
+        nw[0] = a.z; nw[1] = a.w; nw[2] = b.x; nw[3] = b.y;
     }
 }
 
@@ -249,8 +294,10 @@ __global__ __launch_bounds__(kThreads) void quant_rows_kernel(
     uint32_t key0, uint32_t key1, uint32_t tid, uint2* __restrict__ payload,
     uint8_t* __restrict__ scales, float* __restrict__ dec_out) {
     static_assert(FMT != (int)ScaleKind::E8M0 || H == 2, "E8M0 blocks are 32");
+    __shared__ float rtab[256];
     const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
+    fill_recip<FMT>(rtab, m);
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     uint4 c[2 * H];
@@ -267,22 +314,29 @@ __global__ __launch_bounds__(kThreads) void quant_rows_kernel(
 #pragma unroll
             for (int i = 0; i < 2 * H; ++i) n[i] = x[2 * H * bn + i];
         }
-        uint32_t mx = 0u;
+        uint32_t mp = 0u;
 #pragma unroll
-        for (int i = 0; i < 2 * H; ++i) mx = max(mx, amax8(c[i]));
-        const BlockScale bs = block_scale<FMT>(mx, m);
+        for (int i = 0; i < 2 * H; ++i) mp = amax8_pk(c[i], mp);
+        const BlockScale bs = block_scale<FMT>(max(mp & 0xFFFFu, mp >> 16), m, rtab);
 #pragma unroll
         for (int h = 0; h < H; ++h) {
-            uint32_t w[16];
-            if (SR) {
-                // elements 16(Hb + h) .. +15: Philox blocks 4(Hb + h) .. +3
+            // elements 16(Hb + h) .. +15: Philox blocks 4(Hb + h) .. +3, made
+            // per half of 8 so that only 8 words are live at a time
+            uint32_t out[2];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const uint4 q = sr_words4((uint64_t)(H * b + h) * 4 + i, tid, key0, key1);
-                    w[4 * i] = q.x; w[4 * i + 1] = q.y; w[4 * i + 2] = q.z; w[4 * i + 3] = q.w;
+            for (int u = 0; u < 2; ++u) {
+                uint32_t nw[8];
+                if (SR) {
+#pragma unroll
+                    for (int i = 0; i < 2; ++i) {
+                        const uint4 q = sr_nwords4((uint64_t)(H * b + h) * 4 + 2 * u + i, tid, key0, key1);
+                        nw[4 * i] = q.x; nw[4 * i + 1] = q.y; nw[4 * i + 2] = q.z; nw[4 * i + 3] = q.w;
+                    }
                 }
+                out[u] = quant8<SR>(c[2 * h + u], bs.r, nw);
+                if (SR) __builtin_amdgcn_sched_barrier(0);
             }
-            payload[H * b + h] = make_uint2(quant8<SR>(c[2 * h], bs.r, w), quant8<SR>(c[2 * h + 1], bs.r, w + 8));
+            payload[H * b + h] = make_uint2(out[0], out[1]);
         }
         scales[b] = (uint8_t)bs.code;
 #pragma unroll
@@ -323,9 +377,9 @@ __device__ __forceinline__ ColItem col_item(int64_t it, int64_t gx, int64_t rows
 
 // SR of 16 rows x 4 columns (row pairs 2k, 2k+1 per conversion) into the
 // column-wise payload words pk[j][0..1]; Philox words are made per row pair.
-// A flagged pair (see sr_check) has its two nibbles redone in software.
-// get(j, r): value of row r, column j of the 16 x 4 block (compile-time
-// indices after unrolling).
+// A row pair with a flagged element (see sr_bucket) has its 8 nibbles redone
+// in software.  get(j, r): value of row r, column j of the 16 x 4 block
+// (compile-time indices after unrolling).
 template <bool ALIGNED, typename Get>
 __device__ __forceinline__ void sr_cols16x4_v(Get get, const BlockScale (&bs)[4], uint64_t e_row0,
                                               uint64_t cols, uint32_t tid, uint32_t k0, uint32_t k1,
@@ -334,26 +388,33 @@ __device__ __forceinline__ void sr_cols16x4_v(Get get, const BlockScale (&bs)[4]
     uint32_t aH[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-        uint32_t w0[4], w1[4];
-        words4<ALIGNED>(e_row0 + (uint64_t)(2 * k) * cols, tid, k0, k1, w0);
-        words4<ALIGNED>(e_row0 + (uint64_t)(2 * k + 1) * cols, tid, k0, k1, w1);
+        uint32_t n0[4], n1[4];
+        nwords4<ALIGNED>(e_row0 + (uint64_t)(2 * k) * cols, tid, k0, k1, n0);
+        nwords4<ALIGNED>(e_row0 + (uint64_t)(2 * k + 1) * cols, tid, k0, k1, n1);
+        float y0[4], y1[4];
+        uint32_t tb = 0u;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const float y0 = get(j, 2 * k) * bs[j].r;
-            const float y1 = get(j, 2 * k + 1) * bs[j].r;
-            const v2f_t v = {y0, y1};
-            const uint32_t r0 = ~w0[j];
-            const uint32_t r1 = __builtin_amdgcn_alignbit(~w1[j], ~w1[j], 1);
+            y0[j] = get(j, 2 * k) * bs[j].r;
+            y1[j] = get(j, 2 * k + 1) * bs[j].r;
+            const v2f_t v = {y0[j], y1[j]};
+            const uint32_t r1 = __builtin_amdgcn_alignbit(n1[j], n1[j], 1);
             uint32_t& L = aL[j][k >> 2];
             uint32_t& H = aH[j][k >> 2];
-            if ((k & 3) == 0) { L = sr_pair<0>(L, v, r0); H = sr_pair<0>(H, v, r1); }
-            if ((k & 3) == 1) { L = sr_pair<1>(L, v, r0); H = sr_pair<1>(H, v, r1); }
-            if ((k & 3) == 2) { L = sr_pair<2>(L, v, r0); H = sr_pair<2>(H, v, r1); }
-            if ((k & 3) == 3) { L = sr_pair<3>(L, v, r0); H = sr_pair<3>(H, v, r1); }
-            if (sr_check(y0, w0[j]) | sr_check(y1, w1[j])) {
-                const int sh = 8 * (k & 3);
-                L = (L & ~(0xFu << sh)) | (e2m1_sr(y0, w0[j]) << sh);
-                H = (H & ~(0xF0u << sh)) | (e2m1_sr(y1, w1[j]) << (sh + 4));
+            if ((k & 3) == 0) { L = sr_pair<0>(L, v, n0[j]); H = sr_pair<0>(H, v, r1); }
+            if ((k & 3) == 1) { L = sr_pair<1>(L, v, n0[j]); H = sr_pair<1>(H, v, r1); }
+            if ((k & 3) == 2) { L = sr_pair<2>(L, v, n0[j]); H = sr_pair<2>(H, v, r1); }
+            if ((k & 3) == 3) { L = sr_pair<3>(L, v, n0[j]); H = sr_pair<3>(H, v, r1); }
+            tb = max(tb, max(sr_bucket(y0[j], n0[j]), sr_bucket(y1[j], n1[j])));
+        }
+        if (tb > kBucketTop) {
+            const int sh = 8 * (k & 3);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                uint32_t& L = aL[j][k >> 2];
+                uint32_t& H = aH[j][k >> 2];
+                L = (L & ~(0xFu << sh)) | (e2m1_sr(y0[j], ~n0[j]) << sh);
+                H = (H & ~(0xF0u << sh)) | (e2m1_sr(y1[j], ~n1[j]) << (sh + 4));
             }
         }
         // one row pair at a time: keeps 8 Philox words live, not 64
@@ -392,10 +453,12 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
     static_assert(FMT != (int)ScaleKind::E8M0 || H == 2, "E8M0 blocks are 32");
     __shared__ __attribute__((aligned(16))) uint8_t stP[kColCols][kColGroupRB * 8];
     __shared__ __attribute__((aligned(16))) uint8_t stS[kColCols][kColGroupRB * kColScaleGroups];
+    __shared__ float rtab[256];
     // Blocks of 32 rows (H = 2): the two 16-row blocks of a wave (lanes l and
     // l + 32) form one block and share its maximum and scale byte.
     const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
+    fill_recip<FMT>(rtab, m);
     const int t = threadIdx.x;
     const int q = t & 31, rbl = t >> 5;
     const bool vec8 = (cols & 3) == 0;
@@ -459,7 +522,7 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
                 uint32_t mb = 0u;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) mb = max(mb, __float_as_uint(v[j][r]) & 0x7FFFFFFFu);
-                bs[j] = block_scale_value<FMT>(__uint_as_float(mb), m);
+                bs[j] = block_scale_value<FMT>(__uint_as_float(mb), m, rtab);
             }
             uint32_t pk[4][2];
             if (SR) {
@@ -481,21 +544,21 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
                 stS[4 * q + j][sg * kColGroupRB + rbl] = (uint8_t)bs[j].code;
             }
         } else if (!RHT && r0 < ci.r_end && c < cols) {
-            uint32_t mx[4] = {0u, 0u, 0u, 0u};
+            // packed 16-bit maxima of |x|: columns (c, c+1) and (c+2, c+3)
+            uint32_t mL = 0u, mH = 0u;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                mx[0] = max(mx[0], lo[r] & 0x7FFFu);
-                mx[1] = max(mx[1], (lo[r] >> 16) & 0x7FFFu);
-                mx[2] = max(mx[2], hi[r] & 0x7FFFu);
-                mx[3] = max(mx[3], (hi[r] >> 16) & 0x7FFFu);
+                mL = pk_max_u16(mL, lo[r] & 0x7FFF7FFFu);
+                mH = pk_max_u16(mH, hi[r] & 0x7FFF7FFFu);
             }
+            uint32_t mx[4] = {mL & 0xFFFFu, mL >> 16, mH & 0xFFFFu, mH >> 16};
             if (H == 2) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) mx[j] = max(mx[j], (uint32_t)__shfl_xor((int)mx[j], 32));
             }
             BlockScale bs[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) bs[j] = block_scale<FMT>(mx[j], m);
+            for (int j = 0; j < 4; ++j) bs[j] = block_scale<FMT>(mx[j], m, rtab);
             uint32_t pk[4][2];
             if (SR) {
                 if (vec8)
@@ -633,9 +696,11 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
     uint8_t* __restrict__ scales, uint8_t* __restrict__ payload_t, uint8_t* __restrict__ scales_t,
     float* __restrict__ dec_out) {
     __shared__ __attribute__((aligned(16))) uint8_t stT[kTileCols][kTileRowTiles * 8];
+    __shared__ float rtab[256];
     static_assert(FMT != (int)ScaleKind::E8M0, "2D tiles take UE5M3 or E4M3 scales");
     const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
+    fill_recip<FMT>(rtab, m);
     const int t = threadIdx.x;
     const int q = t & 31, trl = t >> 5;
     int64_t bc, br;
@@ -664,7 +729,7 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
             mx = max(mx, (uint32_t)__shfl_xor((int)mx, 4));
             mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32));
         }
-        const BlockScale bs = block_scale<FMT>(mx, m);
+        const BlockScale bs = block_scale<FMT>(mx, m, rtab);
         uint32_t colpk[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
         if (SR) {
 #pragma unroll
@@ -766,12 +831,6 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
 // LDS stage alternates between two buffers, so one barrier per tile
 // separates a tile's LDS writes from its stores and the stores of tile k
 // from the writes of tile k + 2.
-// Packed 16-bit unsigned maximum of two bf16 |x| pairs (per half).
-__device__ __forceinline__ uint32_t pk_max_u16(uint32_t a, uint32_t b) {
-    uint32_t r;
-    asm("v_pk_max_u16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-    return r;
-}
 
 // The RN work of one lane's 16 x 4 piece of a dual-axis tile: lo / hi hold
 // rows r of columns (c, c+1) / (c+2, c+3) as bf16 pairs.  Writes the
@@ -784,7 +843,8 @@ __device__ __forceinline__ uint32_t pk_max_u16(uint32_t a, uint32_t b) {
 // single-axis quantizers).
 template <int FMT>
 __device__ __forceinline__ void dual_rn_tile(const uint32_t (&lo)[16], const uint32_t (&hi)[16],
-                                             const Multipliers& m, uint8_t (*P)[kTileRowTiles * 8],
+                                             const Multipliers& m, const float* rtab,
+                                             uint8_t (*P)[kTileRowTiles * 8],
                                              uint8_t (*SC)[kTileRowTiles], uint8_t (*SRo)[kTileCols / 16],
                                              int q, int trl, uint8_t* __restrict__ prow, int64_t rstride) {
     uint32_t mcL = 0u, mcH = 0u;              // packed column maxima: (c, c+1), (c+2, c+3)
@@ -801,10 +861,10 @@ __device__ __forceinline__ void dual_rn_tile(const uint32_t (&lo)[16], const uin
         mrow[r] = mr;
     }
     BlockScale bc[4];
-    bc[0] = block_scale<FMT>(mcL & 0xFFFFu, m);
-    bc[1] = block_scale<FMT>(mcL >> 16, m);
-    bc[2] = block_scale<FMT>(mcH & 0xFFFFu, m);
-    bc[3] = block_scale<FMT>(mcH >> 16, m);
+    bc[0] = block_scale<FMT>(mcL & 0xFFFFu, m, rtab);
+    bc[1] = block_scale<FMT>(mcL >> 16, m, rtab);
+    bc[2] = block_scale<FMT>(mcH & 0xFFFFu, m, rtab);
+    bc[3] = block_scale<FMT>(mcH >> 16, m, rtab);
     // lane k of the quad derives the scales of rows k, k+4, k+8, k+12; the
     // others take them by a quad broadcast
     const int qk = q & 3;
@@ -812,7 +872,7 @@ __device__ __forceinline__ void dual_rn_tile(const uint32_t (&lo)[16], const uin
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
         const uint32_t mo = qk == 0 ? mrow[4 * u] : qk == 1 ? mrow[4 * u + 1] : qk == 2 ? mrow[4 * u + 2] : mrow[4 * u + 3];
-        own[u] = block_scale<FMT>(mo, m);
+        own[u] = block_scale<FMT>(mo, m, rtab);
         SRo[trl * 16 + 4 * u + qk][q >> 2] = (uint8_t)own[u].code;
     }
     uint32_t cp[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
@@ -869,9 +929,11 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
     uint32_t tid_c, uint8_t* __restrict__ payload_r, uint8_t* __restrict__ scales_r,
     uint8_t* __restrict__ payload_c, uint8_t* __restrict__ scales_c, float* __restrict__ dec_out) {
     __shared__ __attribute__((aligned(16))) DualStage stage[2];
+    __shared__ float rtab[256];
     static_assert(FMT != (int)ScaleKind::E8M0, "blocks of 16");
     const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
     if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
+    fill_recip<FMT>(rtab, m);
     const int t = threadIdx.x;
     const int q = t & 31, trl = t >> 5;
     const int64_t ntr = rows / 16;
@@ -918,21 +980,20 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
             // RN: block maxima from the |x| bits, both blockings' scales, then
             // one pass over row pairs that widens each element once for its
             // row and its column conversion
-            dual_rn_tile<FMT>(lo, hi, m, st.P, st.SC, st.SR, q, trl,
+            dual_rn_tile<FMT>(lo, hi, m, rtab, st.P, st.SC, st.SR, q, trl,
                               payload_r + (tr * 16) * (cols / 2) + c / 2, cols / 2);
         } else if (SR && c < cols && tr < ntr) {
             // column blocks: in-lane maxima of the 4 columns
-            uint32_t mc[4] = {0u, 0u, 0u, 0u};
+            uint32_t mL = 0u, mH = 0u;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                mc[0] = max(mc[0], lo[r] & 0x7FFFu);
-                mc[1] = max(mc[1], (lo[r] >> 16) & 0x7FFFu);
-                mc[2] = max(mc[2], hi[r] & 0x7FFFu);
-                mc[3] = max(mc[3], (hi[r] >> 16) & 0x7FFFu);
+                mL = pk_max_u16(mL, lo[r] & 0x7FFF7FFFu);
+                mH = pk_max_u16(mH, hi[r] & 0x7FFF7FFFu);
             }
+            const uint32_t mc[4] = {mL & 0xFFFFu, mL >> 16, mH & 0xFFFFu, mH >> 16};
             BlockScale bc[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) bc[j] = block_scale<FMT>(mc[j], m);
+            for (int j = 0; j < 4; ++j) bc[j] = block_scale<FMT>(mc[j], m, rtab);
             uint32_t pk[4][2];
             if (SR) {
                 sr_cols16x4<true>(lo, hi, bc, (uint64_t)(tr * 16) * (uint64_t)cols + (uint64_t)c,
@@ -972,7 +1033,7 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
                 // row 4u + qk of this lane's quad position
                 const uint32_t mo = qk == 0 ? mrow[4 * u] : qk == 1 ? mrow[4 * u + 1]
                                   : qk == 2 ? mrow[4 * u + 2] : mrow[4 * u + 3];
-                own[u] = block_scale<FMT>(mo, m);
+                own[u] = block_scale<FMT>(mo, m, rtab);
             }
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
@@ -989,9 +1050,9 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
                                     bf16_hi(hi[r]) * br.r};
                 uint32_t p;
                 if (SR) {
-                    uint32_t wd[4];
-                    words4<true>((uint64_t)(tr * 16 + r) * (uint64_t)cols + (uint64_t)c, tid_r, key0, key1, wd);
-                    p = sr4(y, wd);
+                    uint32_t nw[4];
+                    nwords4<true>((uint64_t)(tr * 16 + r) * (uint64_t)cols + (uint64_t)c, tid_r, key0, key1, nw);
+                    p = sr4(y, nw);
                 } else {
                     p = 0u;
                     p = rn_pair<0>(p, y[0], y[1]);

@@ -18,6 +18,7 @@
 // per-lane piece is smaller (the transposed payloads and scales) are
 // assembled in LDS first.
 #include <atomic>
+#include <type_traits>
 
 #include "codec.hpp"
 #include "launch.hpp"
@@ -32,6 +33,22 @@ struct BlockScale {
     uint32_t code;
     float r;
 };
+
+// SR values in the scaled form (S23): the SR conversion divides its input
+// by its power-of-two scale operand exactly (checked on gfx950 against the
+// unscaled form over every binade of binary32 from 2^-126 up, and for +-inf
+// and values whose scaled form overflows: the same nibbles), so an element
+// can enter as y 2^23 = x (r 2^23) with scale 2^23.  The bucket check then
+// converts |y 2^23| to an integer directly, one multiply fewer per element.
+// x (r 2^23) equals (x r) 2^23 exactly while x r is a normal binary32 value
+// and r 2^23 is finite; a launch takes the scaled form only when
+// G <= 2^80, so that r <= G 2^17 keeps r 2^23 finite.  Below 2^-126 (where
+// x r has fewer bits) the unscaled threshold is 1 or 0, the element's
+// bucket value is then ~w and it is flagged for every w < 1024, which
+// includes the one word (w = 0) that could round it up: the software
+// rounding redoes it from the exact x r.
+constexpr float kS23 = 0x1p23f;
+constexpr float kS23MaxG = 0x1p80f;
 
 // Reciprocals G / value(c) of the 256 scale codes in LDS, one per thread of
 // the workgroup (kThreads == 256): a block's reciprocal is then one LDS read
@@ -124,8 +141,17 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 // Written as an instruction with p as a read-write operand: the compiler's
 // builtin for this conversion does not keep the destination's other bytes.
-template <int SEL>
+// S23: the pair arrives scaled by 2^23 and the conversion divides it back.
+template <int SEL, bool S23 = false>
 __device__ __forceinline__ uint32_t sr_pair(uint32_t p, v2f_t v, uint32_t r) {
+    if (S23) {
+        const float sc = kS23;
+        if (SEL == 0) asm("v_cvt_scalef32_sr_pk_fp4_f32 %0, %1, %2, %3" : "+v"(p) : "v"(v), "v"(r), "s"(sc));
+        if (SEL == 1) asm("v_cvt_scalef32_sr_pk_fp4_f32 %0, %1, %2, %3 op_sel:[0,0,1,0]" : "+v"(p) : "v"(v), "v"(r), "s"(sc));
+        if (SEL == 2) asm("v_cvt_scalef32_sr_pk_fp4_f32 %0, %1, %2, %3 op_sel:[0,0,0,1]" : "+v"(p) : "v"(v), "v"(r), "s"(sc));
+        if (SEL == 3) asm("v_cvt_scalef32_sr_pk_fp4_f32 %0, %1, %2, %3 op_sel:[0,0,1,1]" : "+v"(p) : "v"(v), "v"(r), "s"(sc));
+        return p;
+    }
     if (SEL == 0) asm("v_cvt_scalef32_sr_pk_fp4_f32 %0, %1, %2, 1.0" : "+v"(p) : "v"(v), "v"(r));
     if (SEL == 1) asm("v_cvt_scalef32_sr_pk_fp4_f32 %0, %1, %2, 1.0 op_sel:[0,0,1,0]" : "+v"(p) : "v"(v), "v"(r));
     if (SEL == 2) asm("v_cvt_scalef32_sr_pk_fp4_f32 %0, %1, %2, 1.0 op_sel:[0,0,0,1]" : "+v"(p) : "v"(v), "v"(r));
@@ -142,37 +168,51 @@ __device__ __forceinline__ uint32_t sr_pair(uint32_t p, v2f_t v, uint32_t r) {
 // |y| < 1, or spuriously with probability 2^-22 (|y| >= 1), which only
 // costs a redo.  A group tests the maximum of its bucket values once.
 constexpr uint32_t kBucketTop = 0xFFFFFBFFu;
+// S23: y arrives as y 2^23 (the product the conversion takes).
+template <bool S23 = false>
 __device__ __forceinline__ uint32_t sr_bucket(float y, uint32_t nw) {
     uint32_t q;
-    asm("v_cvt_u32_f32 %0, %1" : "=v"(q) : "v"(fabsf(y) * 0x1p23f));
+    if (S23)
+        asm("v_cvt_u32_f32_e64 %0, |%1|" : "=v"(q) : "v"(y));
+    else
+        asm("v_cvt_u32_f32 %0, %1" : "=v"(q) : "v"(fabsf(y) * 0x1p23f));
     uint32_t t;
     asm("v_lshl_add_u32 %0, %1, 10, %2" : "=v"(t) : "v"(q), "v"(nw));
     return t;
 }
 
 // 8 values y (element e -> nibble e) by SR with complemented words nw.
-__device__ __forceinline__ uint32_t sr8(const float (&y)[8], const uint32_t* nw) {
+// S23: y holds the scaled values and exact(e) gives element e's unscaled
+// binary32 value for the software rounding.
+template <bool S23, typename Exact>
+__device__ __forceinline__ uint32_t sr8(const float (&y)[8], const uint32_t* nw, Exact exact) {
     uint32_t lo = 0u, hi = 0u;                 // valid low / high nibbles
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const v2f_t v = {y[2 * k], y[2 * k + 1]};
         const uint32_t r0 = nw[2 * k];
         const uint32_t r1 = __builtin_amdgcn_alignbit(nw[2 * k + 1], nw[2 * k + 1], 1);
-        if (k == 0) { lo = sr_pair<0>(lo, v, r0); hi = sr_pair<0>(hi, v, r1); }
-        if (k == 1) { lo = sr_pair<1>(lo, v, r0); hi = sr_pair<1>(hi, v, r1); }
-        if (k == 2) { lo = sr_pair<2>(lo, v, r0); hi = sr_pair<2>(hi, v, r1); }
-        if (k == 3) { lo = sr_pair<3>(lo, v, r0); hi = sr_pair<3>(hi, v, r1); }
+        if (k == 0) { lo = sr_pair<0, S23>(lo, v, r0); hi = sr_pair<0, S23>(hi, v, r1); }
+        if (k == 1) { lo = sr_pair<1, S23>(lo, v, r0); hi = sr_pair<1, S23>(hi, v, r1); }
+        if (k == 2) { lo = sr_pair<2, S23>(lo, v, r0); hi = sr_pair<2, S23>(hi, v, r1); }
+        if (k == 3) { lo = sr_pair<3, S23>(lo, v, r0); hi = sr_pair<3, S23>(hi, v, r1); }
     }
     uint32_t p = (lo & 0x0F0F0F0Fu) | (hi & 0xF0F0F0F0u);
     uint32_t tb = 0u;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) tb = max(tb, sr_bucket(y[e], nw[e]));
+    for (int e = 0; e < 8; ++e) tb = max(tb, sr_bucket<S23>(y[e], nw[e]));
     if (tb > kBucketTop) {
         p = 0u;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) p |= e2m1_sr(y[e], ~nw[e]) << (4 * e);
+        for (int e = 0; e < 8; ++e) p |= e2m1_sr(S23 ? exact(e) : y[e], ~nw[e]) << (4 * e);
     }
     return p;
+}
+
+template <bool S23 = false>
+__device__ __forceinline__ uint32_t sr8(const float (&y)[8], const uint32_t* nw) {
+    static_assert(!S23, "the scaled form needs the exact values");
+    return sr8<false>(y, nw, [&](int e) { return y[e]; });
 }
 
 // 4 values y (element e -> nibble e of the low 16 bits) by SR with
@@ -197,8 +237,9 @@ __device__ __forceinline__ uint32_t sr4(const float (&y)[4], const uint32_t* nw)
 
 // Quantize the 8 bf16 values held in v (element e in half e&1 of word e>>1)
 // with reciprocal r; returns 8 nibbles packed little-endian.  For SR, w holds
-// the 8 complemented Philox words of the elements.
-template <bool SR>
+// the 8 complemented Philox words of the elements; S23: the SR values are
+// formed scaled, as x (r 2^23).
+template <bool SR, bool S23 = false>
 __device__ __forceinline__ uint32_t quant8(const uint4& v, float r, const uint32_t* w) {
     const uint32_t vv[4] = {v.x, v.y, v.z, v.w};
     if (!SR) {
@@ -209,10 +250,12 @@ __device__ __forceinline__ uint32_t quant8(const uint4& v, float r, const uint32
         p = rn_pair<3>(p, bf16_lo(vv[3]) * r, bf16_hi(vv[3]) * r);
         return p;
     }
+    auto xe = [&](int e) { return (e & 1) ? bf16_hi(vv[e >> 1]) : bf16_lo(vv[e >> 1]); };
+    const float ry = S23 ? r * kS23 : r;
     float y[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) y[e] = ((e & 1) ? bf16_hi(vv[e >> 1]) : bf16_lo(vv[e >> 1])) * r;
-    return sr8(y, w);
+    for (int e = 0; e < 8; ++e) y[e] = xe(e) * ry;
+    return sr8<S23>(y, w, [&](int e) { return xe(e) * r; });
 }
 
 // Column-wise nibbles of 16 rows of one column (values v[r] * r_, rows in
@@ -299,49 +342,57 @@ __global__ __launch_bounds__(kThreads) void quant_rows_kernel(
     if (dec_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *dec_out = m.dec;
     fill_recip<FMT>(rtab, m);
     const int64_t stride = (int64_t)gridDim.x * kThreads;
-    int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    uint4 c[2 * H];
-    if (b < nblocks) {
+    // S23: the scaled SR form (a uniform choice per launch, see kS23MaxG)
+    auto run = [&](auto S23c) {
+        constexpr bool S23 = decltype(S23c)::value;
+        int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+        uint4 c[2 * H];
+        if (b < nblocks) {
 #pragma unroll
-        for (int i = 0; i < 2 * H; ++i) c[i] = x[2 * H * b + i];
-    }
-    for (; b < nblocks; b += stride) {
-        const int64_t bn = b + stride;
-        uint4 n[2 * H];
-#pragma unroll
-        for (int i = 0; i < 2 * H; ++i) n[i] = make_uint4(0u, 0u, 0u, 0u);
-        if (bn < nblocks) {
-#pragma unroll
-            for (int i = 0; i < 2 * H; ++i) n[i] = x[2 * H * bn + i];
+            for (int i = 0; i < 2 * H; ++i) c[i] = x[2 * H * b + i];
         }
-        uint32_t mp = 0u;
+        for (; b < nblocks; b += stride) {
+            const int64_t bn = b + stride;
+            uint4 n[2 * H];
 #pragma unroll
-        for (int i = 0; i < 2 * H; ++i) mp = amax8_pk(c[i], mp);
-        const BlockScale bs = block_scale<FMT>(max(mp & 0xFFFFu, mp >> 16), m, rtab);
+            for (int i = 0; i < 2 * H; ++i) n[i] = make_uint4(0u, 0u, 0u, 0u);
+            if (bn < nblocks) {
 #pragma unroll
-        for (int h = 0; h < H; ++h) {
-            // elements 16(Hb + h) .. +15: Philox blocks 4(Hb + h) .. +3, made
-            // per half of 8 so that only 8 words are live at a time
-            uint32_t out[2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                uint32_t nw[8];
-                if (SR) {
-#pragma unroll
-                    for (int i = 0; i < 2; ++i) {
-                        const uint4 q = sr_nwords4((uint64_t)(H * b + h) * 4 + 2 * u + i, tid, key0, key1);
-                        nw[4 * i] = q.x; nw[4 * i + 1] = q.y; nw[4 * i + 2] = q.z; nw[4 * i + 3] = q.w;
-                    }
-                }
-                out[u] = quant8<SR>(c[2 * h + u], bs.r, nw);
-                if (SR) __builtin_amdgcn_sched_barrier(0);
+                for (int i = 0; i < 2 * H; ++i) n[i] = x[2 * H * bn + i];
             }
-            payload[H * b + h] = make_uint2(out[0], out[1]);
-        }
-        scales[b] = (uint8_t)bs.code;
+            uint32_t mp = 0u;
 #pragma unroll
-        for (int i = 0; i < 2 * H; ++i) c[i] = n[i];
-    }
+            for (int i = 0; i < 2 * H; ++i) mp = amax8_pk(c[i], mp);
+            const BlockScale bs = block_scale<FMT>(max(mp & 0xFFFFu, mp >> 16), m, rtab);
+#pragma unroll
+            for (int h = 0; h < H; ++h) {
+                // elements 16(Hb + h) .. +15: Philox blocks 4(Hb + h) .. +3,
+                // made per half of 8 so that only 8 words are live at a time
+                uint32_t out[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    uint32_t nw[8];
+                    if (SR) {
+#pragma unroll
+                        for (int i = 0; i < 2; ++i) {
+                            const uint4 q = sr_nwords4((uint64_t)(H * b + h) * 4 + 2 * u + i, tid, key0, key1);
+                            nw[4 * i] = q.x; nw[4 * i + 1] = q.y; nw[4 * i + 2] = q.z; nw[4 * i + 3] = q.w;
+                        }
+                    }
+                    out[u] = quant8<SR, S23>(c[2 * h + u], bs.r, nw);
+                    if (SR) __builtin_amdgcn_sched_barrier(0);
+                }
+                payload[H * b + h] = make_uint2(out[0], out[1]);
+            }
+            scales[b] = (uint8_t)bs.code;
+#pragma unroll
+            for (int i = 0; i < 2 * H; ++i) c[i] = n[i];
+        }
+    };
+    if (SR && FMT != (int)ScaleKind::E8M0 && m.G <= kS23MaxG)
+        run(std::integral_constant<bool, SR && FMT != (int)ScaleKind::E8M0>{});
+    else
+        run(std::false_type{});
 }
 
 // ------------------------------------------------ columns (1D, transposed) --
@@ -380,12 +431,17 @@ __device__ __forceinline__ ColItem col_item(int64_t it, int64_t gx, int64_t rows
 // A row pair with a flagged element (see sr_bucket) has its 8 nibbles redone
 // in software.  get(j, r): value of row r, column j of the 16 x 4 block
 // (compile-time indices after unrolling).
-template <bool ALIGNED, typename Get>
+// S23: the values are formed scaled (x (r 2^23)) for the conversions and the
+// bucket check; the software rounding takes x r.
+template <bool ALIGNED, bool S23 = false, typename Get>
 __device__ __forceinline__ void sr_cols16x4_v(Get get, const BlockScale (&bs)[4], uint64_t e_row0,
                                               uint64_t cols, uint32_t tid, uint32_t k0, uint32_t k1,
                                               uint32_t (&pk)[4][2]) {
     uint32_t aL[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
     uint32_t aH[4][2] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
+    float ry[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ry[j] = S23 ? bs[j].r * kS23 : bs[j].r;
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
         uint32_t n0[4], n1[4];
@@ -395,17 +451,17 @@ __device__ __forceinline__ void sr_cols16x4_v(Get get, const BlockScale (&bs)[4]
         uint32_t tb = 0u;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            y0[j] = get(j, 2 * k) * bs[j].r;
-            y1[j] = get(j, 2 * k + 1) * bs[j].r;
+            y0[j] = get(j, 2 * k) * ry[j];
+            y1[j] = get(j, 2 * k + 1) * ry[j];
             const v2f_t v = {y0[j], y1[j]};
             const uint32_t r1 = __builtin_amdgcn_alignbit(n1[j], n1[j], 1);
             uint32_t& L = aL[j][k >> 2];
             uint32_t& H = aH[j][k >> 2];
-            if ((k & 3) == 0) { L = sr_pair<0>(L, v, n0[j]); H = sr_pair<0>(H, v, r1); }
-            if ((k & 3) == 1) { L = sr_pair<1>(L, v, n0[j]); H = sr_pair<1>(H, v, r1); }
-            if ((k & 3) == 2) { L = sr_pair<2>(L, v, n0[j]); H = sr_pair<2>(H, v, r1); }
-            if ((k & 3) == 3) { L = sr_pair<3>(L, v, n0[j]); H = sr_pair<3>(H, v, r1); }
-            tb = max(tb, max(sr_bucket(y0[j], n0[j]), sr_bucket(y1[j], n1[j])));
+            if ((k & 3) == 0) { L = sr_pair<0, S23>(L, v, n0[j]); H = sr_pair<0, S23>(H, v, r1); }
+            if ((k & 3) == 1) { L = sr_pair<1, S23>(L, v, n0[j]); H = sr_pair<1, S23>(H, v, r1); }
+            if ((k & 3) == 2) { L = sr_pair<2, S23>(L, v, n0[j]); H = sr_pair<2, S23>(H, v, r1); }
+            if ((k & 3) == 3) { L = sr_pair<3, S23>(L, v, n0[j]); H = sr_pair<3, S23>(H, v, r1); }
+            tb = max(tb, max(sr_bucket<S23>(y0[j], n0[j]), sr_bucket<S23>(y1[j], n1[j])));
         }
         if (tb > kBucketTop) {
             const int sh = 8 * (k & 3);
@@ -413,8 +469,10 @@ __device__ __forceinline__ void sr_cols16x4_v(Get get, const BlockScale (&bs)[4]
             for (int j = 0; j < 4; ++j) {
                 uint32_t& L = aL[j][k >> 2];
                 uint32_t& H = aH[j][k >> 2];
-                L = (L & ~(0xFu << sh)) | (e2m1_sr(y0[j], ~n0[j]) << sh);
-                H = (H & ~(0xF0u << sh)) | (e2m1_sr(y1[j], ~n1[j]) << (sh + 4));
+                const float e0 = S23 ? get(j, 2 * k) * bs[j].r : y0[j];
+                const float e1 = S23 ? get(j, 2 * k + 1) * bs[j].r : y1[j];
+                L = (L & ~(0xFu << sh)) | (e2m1_sr(e0, ~n0[j]) << sh);
+                H = (H & ~(0xF0u << sh)) | (e2m1_sr(e1, ~n1[j]) << (sh + 4));
             }
         }
         // one row pair at a time: keeps 8 Philox words live, not 64
@@ -427,12 +485,12 @@ __device__ __forceinline__ void sr_cols16x4_v(Get get, const BlockScale (&bs)[4]
 }
 
 // The 16 x 4 block held as bf16 pairs: columns (c, c+1) in lo, (c+2, c+3) in hi.
-template <bool ALIGNED>
+template <bool ALIGNED, bool S23 = false>
 __device__ __forceinline__ void sr_cols16x4(const uint32_t (&lo)[16], const uint32_t (&hi)[16],
                                             const BlockScale (&bs)[4], uint64_t e_row0, uint64_t cols,
                                             uint32_t tid, uint32_t k0, uint32_t k1,
                                             uint32_t (&pk)[4][2]) {
-    sr_cols16x4_v<ALIGNED>(
+    sr_cols16x4_v<ALIGNED, S23>(
         [&](int j, int r) -> float {
             const uint32_t a = j < 2 ? lo[r] : hi[r];
             return (j & 1) ? bf16_hi(a) : bf16_lo(a);
@@ -489,159 +547,167 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
         }
     };
 
-    int64_t it = blockIdx.x, g = 0;
-    if (it >= nitems) return;                                    // uniform
-    ColItem ci = col_item(it, gx, rows, rows_per_item);
-    uint32_t lo[16], hi[16], nlo[16], nhi[16];
-    load(ci, 0, lo, hi);
-    while (true) {
-        // next group: within the item, else the first group of the next item
-        int64_t nit = it, ng = g + 1;
-        if (ng >= ci.ngroups) {
-            nit = it + gridDim.x;
-            ng = 0;
-        }
-        const ColItem cn = nit < nitems ? col_item(nit, gx, rows, rows_per_item) : ci;
-        // RN prefetches the next group into registers; SR (VALU-bound)
-        // keeps its registers for more resident waves and loads the next
-        // group into the same registers once this one's values are consumed
-        if (!SR && nit < nitems) load(cn, ng, nlo, nhi);
+    // S23: the scaled SR form (a uniform choice per launch, see kS23MaxG)
+    auto run = [&](auto S23c) {
+        constexpr bool S23 = decltype(S23c)::value;
+        int64_t it = blockIdx.x, g = 0;
+        if (it >= nitems) return;                                    // uniform
+        ColItem ci = col_item(it, gx, rows, rows_per_item);
+        uint32_t lo[16], hi[16], nlo[16], nhi[16];
+        load(ci, 0, lo, hi);
+        while (true) {
+            // next group: within the item, else the first group of the next item
+            int64_t nit = it, ng = g + 1;
+            if (ng >= ci.ngroups) {
+                nit = it + gridDim.x;
+                ng = 0;
+            }
+            const ColItem cn = nit < nitems ? col_item(nit, gx, rows, rows_per_item) : ci;
+            // RN prefetches the next group into registers; SR (VALU-bound)
+            // keeps its registers for more resident waves and loads the next
+            // group into the same registers once this one's values are consumed
+            if (!SR && nit < nitems) load(cn, ng, nlo, nhi);
 
-        const int64_t c = ci.cw + 4 * q;
-        const int64_t r0 = ci.r_begin + g * (kColGroupRB * 16) + rbl * 16;
-        const int sg = (int)(g % kColScaleGroups);
-        if (RHT && r0 < ci.r_end && c < cols) {
-            float v[4][16];
-            BlockScale bs[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    v[j][r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
-                rht16(v[j], rht_mask);
-                uint32_t mb = 0u;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) mb = max(mb, __float_as_uint(v[j][r]) & 0x7FFFFFFFu);
-                bs[j] = block_scale_value<FMT>(__uint_as_float(mb), m, rtab);
-            }
-            uint32_t pk[4][2];
-            if (SR) {
-                auto get = [&](int j, int r) -> float { return v[j][r]; };
-                if (vec8)
-                    sr_cols16x4_v<true>(get, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c, (uint64_t)cols,
-                                        tid, key0, key1, pk);
-                else
-                    sr_cols16x4_v<false>(get, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c, (uint64_t)cols,
-                                         tid, key0, key1, pk);
-            } else {
-                const uint32_t nw[16] = {};
-#pragma unroll
-                for (int j = 0; j < 4; ++j) quant_col16<false>(v[j], bs[j].r, nw, pk[j][0], pk[j][1]);
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                *reinterpret_cast<uint2*>(&stP[4 * q + j][rbl * 8]) = make_uint2(pk[j][0], pk[j][1]);
-                stS[4 * q + j][sg * kColGroupRB + rbl] = (uint8_t)bs[j].code;
-            }
-        } else if (!RHT && r0 < ci.r_end && c < cols) {
-            // packed 16-bit maxima of |x|: columns (c, c+1) and (c+2, c+3)
-            uint32_t mL = 0u, mH = 0u;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                mL = pk_max_u16(mL, lo[r] & 0x7FFF7FFFu);
-                mH = pk_max_u16(mH, hi[r] & 0x7FFF7FFFu);
-            }
-            uint32_t mx[4] = {mL & 0xFFFFu, mL >> 16, mH & 0xFFFFu, mH >> 16};
-            if (H == 2) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) mx[j] = max(mx[j], (uint32_t)__shfl_xor((int)mx[j], 32));
-            }
-            BlockScale bs[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) bs[j] = block_scale<FMT>(mx[j], m, rtab);
-            uint32_t pk[4][2];
-            if (SR) {
-                if (vec8)
-                    sr_cols16x4<true>(lo, hi, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c,
-                                      (uint64_t)cols, tid, key0, key1, pk);
-                else
-                    sr_cols16x4<false>(lo, hi, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c,
-                                       (uint64_t)cols, tid, key0, key1, pk);
-            } else {
-                const uint32_t nw[16] = {};
-#pragma unroll
+            const int64_t c = ci.cw + 4 * q;
+            const int64_t r0 = ci.r_begin + g * (kColGroupRB * 16) + rbl * 16;
+            const int sg = (int)(g % kColScaleGroups);
+            if (RHT && r0 < ci.r_end && c < cols) {
+                float v[4][16];
+                BlockScale bs[4];
+    #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    float xv[16];
-#pragma unroll
+    #pragma unroll
                     for (int r = 0; r < 16; ++r)
-                        xv[r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
-                    quant_col16<false>(xv, bs[j].r, nw, pk[j][0], pk[j][1]);
+                        v[j][r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
+                    rht16(v[j], rht_mask);
+                    uint32_t mb = 0u;
+    #pragma unroll
+                    for (int r = 0; r < 16; ++r) mb = max(mb, __float_as_uint(v[j][r]) & 0x7FFFFFFFu);
+                    bs[j] = block_scale_value<FMT>(__uint_as_float(mb), m, rtab);
                 }
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                *reinterpret_cast<uint2*>(&stP[4 * q + j][rbl * 8]) = make_uint2(pk[j][0], pk[j][1]);
-                if (H == 1 || (rbl & 1) == 0)
-                    stS[4 * q + j][(sg * kColGroupRB + rbl) / H] = (uint8_t)bs[j].code;
-            }
-        }
-        // SR: this group's values are consumed; the next group's loads go out
-        // now and overlap the stores below (same registers, none added)
-        if (SR && nit < nitems) load(cn, ng, lo, hi);
-        __syncthreads();
-        // payload: 2 lanes per column, 32 bytes each (the group's valid row
-        // blocks only; a full group is 64 contiguous bytes)
-        {
-            const int col = t >> 1, half = t & 1;
-            const int64_t gc = ci.cw + col;
-            const int64_t rb0 = (ci.r_begin + g * (kColGroupRB * 16)) / 16;
-            const int nvalid = (int)min((int64_t)kColGroupRB, (ci.r_end / 16) - rb0);
-            if (gc < cols) {
-                uint8_t* dst = payload_t + gc * ldo + rb0 * 8 + half * 32;
-                const uint8_t* s = &stP[col][half * 32];
-                if (nvalid == kColGroupRB && (ldo & 15) == 0) {
-                    *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(s);
-                    *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(s + 16);
+                uint32_t pk[4][2];
+                if (SR) {
+                    auto get = [&](int j, int r) -> float { return v[j][r]; };
+                    if (vec8)
+                        sr_cols16x4_v<true, S23>(get, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c, (uint64_t)cols,
+                                            tid, key0, key1, pk);
+                    else
+                        sr_cols16x4_v<false, S23>(get, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c, (uint64_t)cols,
+                                             tid, key0, key1, pk);
                 } else {
-                    for (int k = half * 4; k < half * 4 + 4; ++k)
-                        if (k < nvalid)
-                            *reinterpret_cast<uint2*>(dst + (k - half * 4) * 8) =
-                                *reinterpret_cast<const uint2*>(s + (k - half * 4) * 8);
+                    const uint32_t nw[16] = {};
+    #pragma unroll
+                    for (int j = 0; j < 4; ++j) quant_col16<false>(v[j], bs[j].r, nw, pk[j][0], pk[j][1]);
+                }
+    #pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    *reinterpret_cast<uint2*>(&stP[4 * q + j][rbl * 8]) = make_uint2(pk[j][0], pk[j][1]);
+                    stS[4 * q + j][sg * kColGroupRB + rbl] = (uint8_t)bs[j].code;
+                }
+            } else if (!RHT && r0 < ci.r_end && c < cols) {
+                // packed 16-bit maxima of |x|: columns (c, c+1) and (c+2, c+3)
+                uint32_t mL = 0u, mH = 0u;
+    #pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    mL = pk_max_u16(mL, lo[r] & 0x7FFF7FFFu);
+                    mH = pk_max_u16(mH, hi[r] & 0x7FFF7FFFu);
+                }
+                uint32_t mx[4] = {mL & 0xFFFFu, mL >> 16, mH & 0xFFFFu, mH >> 16};
+                if (H == 2) {
+    #pragma unroll
+                    for (int j = 0; j < 4; ++j) mx[j] = max(mx[j], (uint32_t)__shfl_xor((int)mx[j], 32));
+                }
+                BlockScale bs[4];
+    #pragma unroll
+                for (int j = 0; j < 4; ++j) bs[j] = block_scale<FMT>(mx[j], m, rtab);
+                uint32_t pk[4][2];
+                if (SR) {
+                    if (vec8)
+                        sr_cols16x4<true, S23>(lo, hi, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c,
+                                          (uint64_t)cols, tid, key0, key1, pk);
+                    else
+                        sr_cols16x4<false, S23>(lo, hi, bs, (uint64_t)r0 * (uint64_t)cols + (uint64_t)c,
+                                           (uint64_t)cols, tid, key0, key1, pk);
+                } else {
+                    const uint32_t nw[16] = {};
+    #pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        float xv[16];
+    #pragma unroll
+                        for (int r = 0; r < 16; ++r)
+                            xv[r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
+                        quant_col16<false>(xv, bs[j].r, nw, pk[j][0], pk[j][1]);
+                    }
+                }
+    #pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    *reinterpret_cast<uint2*>(&stP[4 * q + j][rbl * 8]) = make_uint2(pk[j][0], pk[j][1]);
+                    if (H == 1 || (rbl & 1) == 0)
+                        stS[4 * q + j][(sg * kColGroupRB + rbl) / H] = (uint8_t)bs[j].code;
                 }
             }
-            // scales: at the end of the item (or of a full 64-block chunk);
-            // SB bytes per column for a full chunk, half of them per lane
-            if (sg == kColScaleGroups - 1 || g == ci.ngroups - 1) {
-                constexpr int SB = kColGroupRB * kColScaleGroups / H;
-                const int64_t rbs = (rb0 - (int64_t)sg * kColGroupRB) / H;
-                const int ns = (int)((rb0 + nvalid) / H - rbs);
+            // SR: this group's values are consumed; the next group's loads go out
+            // now and overlap the stores below (same registers, none added)
+            if (SR && nit < nitems) load(cn, ng, lo, hi);
+            __syncthreads();
+            // payload: 2 lanes per column, 32 bytes each (the group's valid row
+            // blocks only; a full group is 64 contiguous bytes)
+            {
+                const int col = t >> 1, half = t & 1;
+                const int64_t gc = ci.cw + col;
+                const int64_t rb0 = (ci.r_begin + g * (kColGroupRB * 16)) / 16;
+                const int nvalid = (int)min((int64_t)kColGroupRB, (ci.r_end / 16) - rb0);
                 if (gc < cols) {
-                    uint8_t* dst = scales_t + gc * nrb + rbs + half * (SB / 2);
-                    const uint8_t* s = &stS[col][half * (SB / 2)];
-                    const int lo_k = half * (SB / 2), hi_k = min(ns, (half + 1) * (SB / 2));
-                    if (hi_k - lo_k == SB / 2 && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
-#pragma unroll
-                        for (int v = 0; v < SB / 32; ++v)
-                            reinterpret_cast<uint4*>(dst)[v] = reinterpret_cast<const uint4*>(s)[v];
+                    uint8_t* dst = payload_t + gc * ldo + rb0 * 8 + half * 32;
+                    const uint8_t* s = &stP[col][half * 32];
+                    if (nvalid == kColGroupRB && (ldo & 15) == 0) {
+                        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(s);
+                        *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(s + 16);
                     } else {
-                        for (int k = lo_k; k < hi_k; ++k) dst[k - lo_k] = s[k - lo_k];
+                        for (int k = half * 4; k < half * 4 + 4; ++k)
+                            if (k < nvalid)
+                                *reinterpret_cast<uint2*>(dst + (k - half * 4) * 8) =
+                                    *reinterpret_cast<const uint2*>(s + (k - half * 4) * 8);
+                    }
+                }
+                // scales: at the end of the item (or of a full 64-block chunk);
+                // SB bytes per column for a full chunk, half of them per lane
+                if (sg == kColScaleGroups - 1 || g == ci.ngroups - 1) {
+                    constexpr int SB = kColGroupRB * kColScaleGroups / H;
+                    const int64_t rbs = (rb0 - (int64_t)sg * kColGroupRB) / H;
+                    const int ns = (int)((rb0 + nvalid) / H - rbs);
+                    if (gc < cols) {
+                        uint8_t* dst = scales_t + gc * nrb + rbs + half * (SB / 2);
+                        const uint8_t* s = &stS[col][half * (SB / 2)];
+                        const int lo_k = half * (SB / 2), hi_k = min(ns, (half + 1) * (SB / 2));
+                        if (hi_k - lo_k == SB / 2 && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
+    #pragma unroll
+                            for (int v = 0; v < SB / 32; ++v)
+                                reinterpret_cast<uint4*>(dst)[v] = reinterpret_cast<const uint4*>(s)[v];
+                        } else {
+                            for (int k = lo_k; k < hi_k; ++k) dst[k - lo_k] = s[k - lo_k];
+                        }
                     }
                 }
             }
-        }
-        __syncthreads();
-        if (nit >= nitems) break;                               // uniform
-        it = nit;
-        g = ng;
-        ci = cn;
-        if (!SR) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                lo[r] = nlo[r];
-                hi[r] = nhi[r];
+            __syncthreads();
+            if (nit >= nitems) break;                               // uniform
+            it = nit;
+            g = ng;
+            ci = cn;
+            if (!SR) {
+    #pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    lo[r] = nlo[r];
+                    hi[r] = nhi[r];
+                }
             }
         }
-    }
+    };
+    if (SR && FMT != (int)ScaleKind::E8M0 && m.G <= kS23MaxG)
+        run(std::integral_constant<bool, SR && FMT != (int)ScaleKind::E8M0>{});
+    else
+        run(std::false_type{});
 }
 
 // ------------------------------------------------------------ tiles (2D) --

@@ -160,7 +160,9 @@ def test_held_reference_saturation_and_underflow():
     bits = synthetic.activation(8, 64, 256, 0.01, 50.0)
     xd = to_dev(bits)
     amax = torch.zeros(1, dtype=torch.float32, device="cuda")
-    for g in [1e-3, 0.05, 1.0, 1e4, 1e9, 0.0, 2.0 ** -100]:
+    # 1e-25: a tensor multiplier above 2^80, where the SR quantizers take
+    # their unscaled conversion form
+    for g in [1e-3, 0.05, 1.0, 1e4, 1e9, 0.0, 2.0 ** -100, 1e-25]:
         set_amax(amax, g)
         for axis in [0, 1]:
             for mode in ["rn", "sr"]:
@@ -244,12 +246,14 @@ def _all_bf16(rows, cols, seed):
     return np.ascontiguousarray(np.tile(v, -(-n // v.size))[:n].reshape(rows, cols))
 
 
-@pytest.mark.parametrize("g", [1.0, 3.0e4, 2.0 ** -20])
+@pytest.mark.parametrize("g", [1.0, 3.0e4, 2.0 ** -20, 1e-25])
 @pytest.mark.parametrize("mode", ["rn", "sr"])
 def test_every_bf16_value(g, mode):
     """All quantizers on inputs holding every non-NaN bf16 value, under held
     amax values that put most of them below, inside and above the E2M1 range
-    of their blocks: payload and scales bit-exact with the oracle."""
+    of their blocks: payload and scales bit-exact with the oracle.  With
+    g = 1e-25 the tensor multiplier exceeds 2^80 and the SR quantizers use
+    their unscaled conversion form; the others use the scaled form."""
     say("every bf16 value", g, mode)
     amax = torch.zeros(1, dtype=torch.float32, device="cuda")
     set_amax(amax, g)

@@ -868,46 +868,76 @@ __device__ __forceinline__ void store_item(f32x16_t (&acc)[4][4], const WorkItem
                                                 pack_bf16x2(alpha * a[4 * g + 2], alpha * a[4 * g + 3])};
                     }
             };
+            // the round's accumulators are read only where they are packed:
+            // an empty statement that takes them as VGPR operands is where
+            // the compiler copies each one out of the AccVGPRs, once (with
+            // AccVGPR operands it moved them to other AccVGPRs first, 32
+            // moves per round)
+            auto take = [&](int q, u32x2_t (&v)[8]) {
+                asm volatile("" : "+v"(acc[q >> 1][2 * (q & 1)]), "+v"(acc[q >> 1][2 * (q & 1) + 1]));
+                pack(q, v);
+            };
+            u32x2_t v[8], vn[8];
+            take(0, v);
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
-                // the round's accumulators are read only from here on
-                asm volatile("" : "+a"(acc[q >> 1][2 * (q & 1)]), "+a"(acc[q >> 1][2 * (q & 1) + 1]));
-                u32x2_t v[8];
-                pack(q, v);
 #pragma unroll
                 for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
                     for (int g = 0; g < 4; ++g)
                         *reinterpret_cast<u32x2_t*>(wrow + (((4 * jj + g) ^ wsw) << 4) + hi * 8) = v[4 * jj + g];
+                // the next round's values are formed while these writes land
+                if (q < 7) take(q + 1, vn);
                 wave_lds_sync();
                 const int i = q >> 1, h = q & 1;
+                // all four reads first: the compiler cannot tell that the
+                // buffer stores do not alias the LDS, so a read written
+                // after a store would wait for it (one LDS round trip per
+                // store instead of one per round)
+                u32x4_t d[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) d[t] = *reinterpret_cast<const u32x4_t*>(rd[t]);
 #pragma unroll
                 for (int t = 0; t < 4; ++t)
-                    __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4_t*>(rd[t]), cr,
-                                                           vb[h] + (uint32_t)((32 * i + 8 * t) * N * 2), 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b128(d[t], cr, vb[h] + (uint32_t)((32 * i + 8 * t) * N * 2),
+                                                           0, 0);
                 wave_lds_sync();
+#pragma unroll
+                for (int k = 0; k < 8; ++k) v[k] = vn[k];
             }
         } else {
-            // round q = 4i + j: 32 rows x 32 columns
+            // round q = 4i + j: 32 rows x 32 columns; the next round's
+            // values are formed while a round's writes land
+            auto take = [&](int q, f32x4_t (&v)[4]) {
+                const int i = q >> 2, j = q & 3;
+                asm volatile("" : "+v"(acc[i][j]));      // read out here, once
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    v[g] = f32x4_t{alpha * acc[i][j][4 * g], alpha * acc[i][j][4 * g + 1],
+                                   alpha * acc[i][j][4 * g + 2], alpha * acc[i][j][4 * g + 3]};
+            };
+            f32x4_t v[4], vn[4];
+            take(0, v);
 #pragma unroll
             for (int q = 0; q < 16; ++q) {
                 const int i = q >> 2, j = q & 3;
-                asm volatile("" : "+a"(acc[i][j]));
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const f32x4_t v = {alpha * acc[i][j][4 * g], alpha * acc[i][j][4 * g + 1],
-                                       alpha * acc[i][j][4 * g + 2], alpha * acc[i][j][4 * g + 3]};
-                    *reinterpret_cast<f32x4_t*>(wrow + (((2 * g + hi) ^ wsw) << 4)) = v;
-                }
+                for (int g = 0; g < 4; ++g) *reinterpret_cast<f32x4_t*>(wrow + (((2 * g + hi) ^ wsw) << 4)) = v[g];
+                if (q < 15) take(q + 1, vn);
                 wave_lds_sync();
+                u32x4_t d[4];                               // all reads before the stores
+#pragma unroll
+                for (int t = 0; t < 4; ++t) d[t] = *reinterpret_cast<const u32x4_t*>(rd[t]);
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
                     const int m = (int)mb + 32 * i + 8 * t;
                     const int n = (int)n0 + wn * 128 + 32 * j + 4 * rc;
                     const uint32_t vo = (m < M && n < N) ? ((uint32_t)m * (uint32_t)N + (uint32_t)n) * 4u : kOff;
-                    __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4_t*>(rd[t]), cr, vo, 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b128(d[t], cr, vo, 0, 0);
                 }
                 wave_lds_sync();
+#pragma unroll
+                for (int g = 0; g < 4; ++g) v[g] = vn[g];
             }
         }
         return;

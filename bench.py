@@ -459,7 +459,7 @@ def drift_bench(args):
     }), flush=True)
 
 
-def matmul_ref(T, K, N, dev):
+def matmul_ref(T, K, N, dev, verbose=True):
     """bf16 inputs, library GEMM (hipBLASLt through torch.matmul): what a plain
     dense bf16 product of the step's three shapes reaches on this GPU, as a
     ceiling reference for the FP4 GEMMs.  Operands are contiguous (the
@@ -486,9 +486,25 @@ def matmul_ref(T, K, N, dev):
         tf = 2.0 * m * n * k / (ms * 1e-3) / 1e12
         out[name] = {"m": m, "k": k, "n": n, "ms": round(ms, 4), "TFLOP/s": round(tf, 1),
                      "frac_bf16": round(tf / BF16_PEAK_TFLOPS, 4)}
-        print(f"[matmul-ref] {name} {m}x{k}x{n}: {ms:.3f} ms {tf:.1f} TFLOP/s", flush=True)
+        if verbose:
+            print(f"[matmul-ref] {name} {m}x{k}x{n}: {ms:.3f} ms {tf:.1f} TFLOP/s", flush=True)
         del a, b, c
-    print(json.dumps({"matmul_ref_bf16": out}), flush=True)
+    return out
+
+
+def copy_ceiling(dev, nbytes=352 * 2 ** 20, nsets=4):
+    """A plain device copy (torch) of nbytes over nsets rotating buffer pairs:
+    the HBM rate a streaming kernel reaches on this GPU (bytes read plus
+    bytes written, per second), as a ceiling reference for the quantizers."""
+    import torch
+    n = nbytes // 4
+    src = [torch.full((n,), 1.0 + i, dtype=torch.float32, device=dev) for i in range(nsets)]
+    dst = [torch.empty(n, dtype=torch.float32, device=dev) for _ in range(nsets)]
+    med, _, p = _time_kernel(lambda i: dst[i].copy_(src[i]), nsets, reps=20, warm=4)
+    del src, dst
+    gbs = 2 * nbytes / (med * 1e-3) / 1e9
+    return {"bytes_moved": 2 * nbytes, "ms": round(med, 5), "GB/s": round(gbs, 1),
+            "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "ms_p10_p50_p90": p}
 
 
 def gemm_shapes(dev):
@@ -698,7 +714,7 @@ def main():
         print(f"copied {args.copy_ref} bytes 5 times", flush=True)
         return
     if args.matmul_ref:
-        matmul_ref(T, K, N, dev)
+        print(json.dumps({"matmul_ref_bf16": matmul_ref(T, K, N, dev)}), flush=True)
         return
     if args.gemm_shapes:
         gemm_shapes(dev)
@@ -938,6 +954,16 @@ def main():
     if args.pm is None and not args.rht and not args.step_only:
         out["quantizer_workload"] = quantizer_workload(dev)
         out["small_linear"] = small_linear_latency(dev)
+        # measured ceilings on this GPU (references only, not the product
+        # path): a plain device copy for the quantizers, a bf16 library GEMM
+        # of the same shapes for the FP4 GEMMs
+        cp = copy_ceiling(dev)
+        mm = matmul_ref(T, K, N, dev, verbose=False)
+        for n in qbytes:
+            kernels[n]["frac_copy"] = round(kernels[n]["GB/s"] / cp["GB/s"], 4)
+        for n in ["gemm_fprop", "gemm_dgrad", "gemm_wgrad"]:
+            kernels[n]["frac_matmul_ref"] = round(kernels[n]["TFLOP/s"] / mm[n[5:]]["TFLOP/s"], 4)
+        out["ceilings"] = {"device_copy": cp, "bf16_matmul": mm}
     if cpu is not None:
         out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)

@@ -395,6 +395,48 @@ __global__ __launch_bounds__(kThreads) void quant_rows_kernel(
         run(std::false_type{});
 }
 
+// Tiles of the 2D and dual-axis quantizers: 128 columns x 8 tile rows of 16.
+constexpr int kTileCols = 128;
+constexpr int kTileRowTiles = 8;
+
+// The 64-byte runs of a transposed payload assembled in LDS, laid out
+// [tile row][column] (st[k][8 c .. 8 c + 7]: the 8 bytes of 16-row tile row
+// k of column cw + c, so that each lane writes its 4 columns of one tile row
+// as one contiguous 32-byte piece, free of bank conflicts), written to
+// dst[(cw + c) * ld + off ...]: four adjacent lanes write one column's run as
+// 16-byte pieces, so one store instruction writes 16 whole 64-byte runs.
+// nvalid: tile rows inside the tensor; a run that is not whole, or a row
+// stride that is not a multiple of 16, goes out as 8-byte pieces.
+__device__ __forceinline__ void store_cols64(const uint8_t (*st)[kTileCols * 8], uint8_t* __restrict__ dst,
+                                             int64_t cw, int64_t cols, int64_t ld, int64_t off, int nvalid,
+                                             int t) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int chunk = t + kThreads * u;
+        const int col = chunk >> 2, part = chunk & 3;
+        const int64_t gc = cw + col;
+        if (col >= kTileCols || gc >= cols) continue;
+        uint8_t* d = dst + gc * ld + off + part * 16;
+        const uint2 a = *reinterpret_cast<const uint2*>(&st[2 * part][col * 8]);
+        const uint2 b = *reinterpret_cast<const uint2*>(&st[2 * part + 1][col * 8]);
+        if (nvalid == kTileRowTiles && (ld & 15) == 0) {
+            *reinterpret_cast<uint4*>(d) = make_uint4(a.x, a.y, b.x, b.y);
+        } else {
+            if (2 * part < nvalid) *reinterpret_cast<uint2*>(d) = a;
+            if (2 * part + 1 < nvalid) *reinterpret_cast<uint2*>(d + 8) = b;
+        }
+    }
+}
+
+// A lane's 4 adjacent columns c = 4q .. 4q+3 of one tile row (pk[j][0..1]:
+// 8 payload bytes of column 4q + j) into the staging row st (see
+// store_cols64): one contiguous 32-byte piece.
+__device__ __forceinline__ void stage_cols4(uint8_t* st, int q, const uint32_t (&pk)[4][2]) {
+    uint4* d = reinterpret_cast<uint4*>(st + 32 * q);
+    d[0] = make_uint4(pk[0][0], pk[0][1], pk[1][0], pk[1][1]);
+    d[1] = make_uint4(pk[2][0], pk[2][1], pk[3][0], pk[3][1]);
+}
+
 // ------------------------------------------------ columns (1D, transposed) --
 // Blocks are 16 consecutive rows of one column; output is the row blocking
 // of x^T: payload_t [cols, rows/2], scales_t [cols, rows/16].
@@ -404,10 +446,12 @@ __global__ __launch_bounds__(kThreads) void quant_rows_kernel(
 // q = t % 32 holds the 4 adjacent columns 4q .. 4q+3), loading the next group
 // -- possibly of its next item -- while it quantizes the current one.  Per
 // group each column gains 8 x 8 = 64 payload bytes, assembled in LDS and
-// written by 2 lanes per column; scale bytes collect in LDS over the item
+// written as whole 64-byte runs (store_cols64); scale bytes collect in LDS over the item
 // (up to 64 bytes per column) before they are written.
 constexpr int kColCols = 128;
 constexpr int kColGroupRB = 8;
+static_assert(kColCols == kTileCols && kColGroupRB == kTileRowTiles,
+              "the column quantizer stages its groups like the tiles");
 constexpr int kColScaleGroups = 8;
 
 struct ColItem {
@@ -509,7 +553,7 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
     float* __restrict__ dec_out, uint32_t rht_mask) {
     static_assert(!RHT || (FMT != (int)ScaleKind::E8M0 && H == 1), "transformed blocks are 16 rows");
     static_assert(FMT != (int)ScaleKind::E8M0 || H == 2, "E8M0 blocks are 32");
-    __shared__ __attribute__((aligned(16))) uint8_t stP[kColCols][kColGroupRB * 8];
+    __shared__ __attribute__((aligned(16))) uint8_t stP[kColGroupRB][kColCols * 8];
     __shared__ __attribute__((aligned(16))) uint8_t stS[kColCols][kColGroupRB * kColScaleGroups];
     __shared__ float rtab[256];
     // Blocks of 32 rows (H = 2): the two 16-row blocks of a wave (lanes l and
@@ -574,14 +618,14 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
             if (RHT && r0 < ci.r_end && c < cols) {
                 float v[4][16];
                 BlockScale bs[4];
-    #pragma unroll
+#pragma unroll
                 for (int j = 0; j < 4; ++j) {
-    #pragma unroll
+#pragma unroll
                     for (int r = 0; r < 16; ++r)
                         v[j][r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
                     rht16(v[j], rht_mask);
                     uint32_t mb = 0u;
-    #pragma unroll
+#pragma unroll
                     for (int r = 0; r < 16; ++r) mb = max(mb, __float_as_uint(v[j][r]) & 0x7FFFFFFFu);
                     bs[j] = block_scale_value<FMT>(__uint_as_float(mb), m, rtab);
                 }
@@ -596,29 +640,27 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
                                              tid, key0, key1, pk);
                 } else {
                     const uint32_t nw[16] = {};
-    #pragma unroll
+#pragma unroll
                     for (int j = 0; j < 4; ++j) quant_col16<false>(v[j], bs[j].r, nw, pk[j][0], pk[j][1]);
                 }
-    #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    *reinterpret_cast<uint2*>(&stP[4 * q + j][rbl * 8]) = make_uint2(pk[j][0], pk[j][1]);
-                    stS[4 * q + j][sg * kColGroupRB + rbl] = (uint8_t)bs[j].code;
-                }
+                stage_cols4(stP[rbl], q, pk);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) stS[4 * q + j][sg * kColGroupRB + rbl] = (uint8_t)bs[j].code;
             } else if (!RHT && r0 < ci.r_end && c < cols) {
                 // packed 16-bit maxima of |x|: columns (c, c+1) and (c+2, c+3)
                 uint32_t mL = 0u, mH = 0u;
-    #pragma unroll
+#pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     mL = pk_max_u16(mL, lo[r] & 0x7FFF7FFFu);
                     mH = pk_max_u16(mH, hi[r] & 0x7FFF7FFFu);
                 }
                 uint32_t mx[4] = {mL & 0xFFFFu, mL >> 16, mH & 0xFFFFu, mH >> 16};
                 if (H == 2) {
-    #pragma unroll
+#pragma unroll
                     for (int j = 0; j < 4; ++j) mx[j] = max(mx[j], (uint32_t)__shfl_xor((int)mx[j], 32));
                 }
                 BlockScale bs[4];
-    #pragma unroll
+#pragma unroll
                 for (int j = 0; j < 4; ++j) bs[j] = block_scale<FMT>(mx[j], m, rtab);
                 uint32_t pk[4][2];
                 if (SR) {
@@ -630,46 +672,33 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
                                            (uint64_t)cols, tid, key0, key1, pk);
                 } else {
                     const uint32_t nw[16] = {};
-    #pragma unroll
+#pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         float xv[16];
-    #pragma unroll
+#pragma unroll
                         for (int r = 0; r < 16; ++r)
                             xv[r] = (j & 1) ? bf16_hi(j < 2 ? lo[r] : hi[r]) : bf16_lo(j < 2 ? lo[r] : hi[r]);
                         quant_col16<false>(xv, bs[j].r, nw, pk[j][0], pk[j][1]);
                     }
                 }
-    #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    *reinterpret_cast<uint2*>(&stP[4 * q + j][rbl * 8]) = make_uint2(pk[j][0], pk[j][1]);
+                stage_cols4(stP[rbl], q, pk);
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
                     if (H == 1 || (rbl & 1) == 0)
                         stS[4 * q + j][(sg * kColGroupRB + rbl) / H] = (uint8_t)bs[j].code;
-                }
             }
             // SR: this group's values are consumed; the next group's loads go out
             // now and overlap the stores below (same registers, none added)
             if (SR && nit < nitems) load(cn, ng, lo, hi);
             __syncthreads();
-            // payload: 2 lanes per column, 32 bytes each (the group's valid row
+            // payload: 64-byte runs per column (the group's valid row
             // blocks only; a full group is 64 contiguous bytes)
             {
                 const int col = t >> 1, half = t & 1;
                 const int64_t gc = ci.cw + col;
                 const int64_t rb0 = (ci.r_begin + g * (kColGroupRB * 16)) / 16;
                 const int nvalid = (int)min((int64_t)kColGroupRB, (ci.r_end / 16) - rb0);
-                if (gc < cols) {
-                    uint8_t* dst = payload_t + gc * ldo + rb0 * 8 + half * 32;
-                    const uint8_t* s = &stP[col][half * 32];
-                    if (nvalid == kColGroupRB && (ldo & 15) == 0) {
-                        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(s);
-                        *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(s + 16);
-                    } else {
-                        for (int k = half * 4; k < half * 4 + 4; ++k)
-                            if (k < nvalid)
-                                *reinterpret_cast<uint2*>(dst + (k - half * 4) * 8) =
-                                    *reinterpret_cast<const uint2*>(s + (k - half * 4) * 8);
-                    }
-                }
+                store_cols64(stP, payload_t, ci.cw, cols, ldo, rb0 * 8, nvalid, t);
                 // scales: at the end of the item (or of a full 64-block chunk);
                 // SB bytes per column for a full chunk, half of them per lane
                 if (sg == kColScaleGroups - 1 || g == ci.ngroups - 1) {
@@ -681,7 +710,7 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
                         const uint8_t* s = &stS[col][half * (SB / 2)];
                         const int lo_k = half * (SB / 2), hi_k = min(ns, (half + 1) * (SB / 2));
                         if (hi_k - lo_k == SB / 2 && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
-    #pragma unroll
+#pragma unroll
                             for (int v = 0; v < SB / 32; ++v)
                                 reinterpret_cast<uint4*>(dst)[v] = reinterpret_cast<const uint4*>(s)[v];
                         } else {
@@ -696,7 +725,7 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
             g = ng;
             ci = cn;
             if (!SR) {
-    #pragma unroll
+#pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     lo[r] = nlo[r];
                     hi[r] = nhi[r];
@@ -717,8 +746,6 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(
 // swaps).  The row-major payload is stored straight from registers (32 lanes
 // x 2 bytes = 64 contiguous bytes per row); the transposed payload gains 8
 // bytes per tile row per column and is assembled in LDS, 64 bytes per column.
-constexpr int kTileCols = 128;
-constexpr int kTileRowTiles = 8;
 
 // TB: tile edge, 16 (the recipe) or 32 (the block-size control: a 32 x 32
 // tile spans the 8 lanes of 32 columns and the lane pair l, l + 32 of two
@@ -761,7 +788,7 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
     float T, uint32_t key0, uint32_t key1, uint32_t tid, uint8_t* __restrict__ payload,
     uint8_t* __restrict__ scales, uint8_t* __restrict__ payload_t, uint8_t* __restrict__ scales_t,
     float* __restrict__ dec_out) {
-    __shared__ __attribute__((aligned(16))) uint8_t stT[kTileCols][kTileRowTiles * 8];
+    __shared__ __attribute__((aligned(16))) uint8_t stT[kTileRowTiles][kTileCols * 8];
     __shared__ float rtab[256];
     static_assert(FMT != (int)ScaleKind::E8M0, "2D tiles take UE5M3 or E4M3 scales");
     const Multipliers m = kernel_multipliers<FMT>(amax_dev, T);
@@ -853,30 +880,13 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
             if (scales_t != nullptr) scales_t[(c / 32) * (ntr / 2) + tr / 2] = (uint8_t)bs.code;
         }
         if (payload_t != nullptr) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                *reinterpret_cast<uint2*>(&stT[4 * q + j][trl * 8]) = make_uint2(colpk[j][0], colpk[j][1]);
+            stage_cols4(stT[trl], q, colpk);
         }
     }
     if (payload_t == nullptr) return;                                 // uniform
     __syncthreads();
-    const int col = t >> 1, half = t & 1;
-    const int64_t gc = cw + col;
-    const int64_t tr0 = br * kTileRowTiles;
-    const int nvalid = (int)min((int64_t)kTileRowTiles, ntr - tr0);
-    if (gc < cols) {
-        uint8_t* dst = payload_t + gc * (rows / 2) + tr0 * 8 + half * 32;
-        const uint8_t* s = &stT[col][half * 32];
-        if (nvalid == kTileRowTiles && ((rows / 2) & 15) == 0) {
-            *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(s);
-            *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(s + 16);
-        } else {
-            for (int k = half * 4; k < half * 4 + 4; ++k)
-                if (k < nvalid)
-                    *reinterpret_cast<uint2*>(dst + (k - half * 4) * 8) =
-                        *reinterpret_cast<const uint2*>(s + (k - half * 4) * 8);
-        }
-    }
+    store_cols64(stT, payload_t, cw, cols, rows / 2, br * kTileRowTiles * 8,
+                 (int)min((int64_t)kTileRowTiles, ntr - br * kTileRowTiles), t);
 }
 
 // ------------------------------------------------- both axes in one pass --
@@ -910,7 +920,7 @@ __global__ __launch_bounds__(kThreads) void quant_tiles_kernel(
 template <int FMT>
 __device__ __forceinline__ void dual_rn_tile(const uint32_t (&lo)[16], const uint32_t (&hi)[16],
                                              const Multipliers& m, const float* rtab,
-                                             uint8_t (*P)[kTileRowTiles * 8],
+                                             uint8_t (*P)[kTileCols * 8],
                                              uint8_t (*SC)[kTileRowTiles], uint8_t (*SRo)[kTileCols / 16],
                                              int q, int trl, uint8_t* __restrict__ prow, int64_t rstride) {
     uint32_t mcL = 0u, mcH = 0u;              // packed column maxima: (c, c+1), (c+2, c+3)
@@ -975,15 +985,13 @@ __device__ __forceinline__ void dual_rn_tile(const uint32_t (&lo)[16], const uin
             if ((k & 3) == 3) w = rn_pair<3>(w, y0, y1);
         }
     }
+    stage_cols4(P[trl], q, cp);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        *reinterpret_cast<uint2*>(&P[4 * q + j][trl * 8]) = make_uint2(cp[j][0], cp[j][1]);
-        SC[4 * q + j][trl] = (uint8_t)bc[j].code;
-    }
+    for (int j = 0; j < 4; ++j) SC[4 * q + j][trl] = (uint8_t)bc[j].code;
 }
 
 struct DualStage {
-    uint8_t P[kTileCols][kTileRowTiles * 8];          // transposed payload, 64 B per column
+    uint8_t P[kTileRowTiles][kTileCols * 8];          // transposed payload (see store_cols64)
     uint8_t SR[kTileRowTiles * 16][kTileCols / 16];   // row scales, 8 per row
     uint8_t SC[kTileCols][kTileRowTiles];             // column scales, 8 per column
 };
@@ -1075,11 +1083,9 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
                     quant_col16<false>(xv, bc[j].r, nw, pk[j][0], pk[j][1]);
                 }
             }
+            stage_cols4(st.P[trl], q, pk);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                *reinterpret_cast<uint2*>(&st.P[4 * q + j][trl * 8]) = make_uint2(pk[j][0], pk[j][1]);
-                st.SC[4 * q + j][trl] = (uint8_t)bc[j].code;
-            }
+            for (int j = 0; j < 4; ++j) st.SC[4 * q + j][trl] = (uint8_t)bc[j].code;
             // row blocks: one per row over the lane quad 4k .. 4k+3.  Maxima
             // are combined by quad permutations; lane k of the quad derives
             // the scales of rows k, k+4, k+8, k+12 and the others take them
@@ -1132,24 +1138,8 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(
         }
         __syncthreads();
         const int nvalid = (int)min((int64_t)kTileRowTiles, ntr - tr0);
-        // transposed payload: 2 lanes per column, 32 bytes each
-        {
-            const int col = t >> 1, half = t & 1;
-            const int64_t gc = cw + col;
-            if (gc < cols) {
-                uint8_t* dst = payload_c + gc * (rows / 2) + tr0 * 8 + half * 32;
-                const uint8_t* sp = &st.P[col][half * 32];
-                if (nvalid == kTileRowTiles && ((rows / 2) & 15) == 0) {
-                    *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(sp);
-                    *reinterpret_cast<uint4*>(dst + 16) = *reinterpret_cast<const uint4*>(sp + 16);
-                } else {
-                    for (int k = half * 4; k < half * 4 + 4; ++k)
-                        if (k < nvalid)
-                            *reinterpret_cast<uint2*>(dst + (k - half * 4) * 8) =
-                                *reinterpret_cast<const uint2*>(sp + (k - half * 4) * 8);
-                }
-            }
-        }
+        // transposed payload: 64-byte runs per column
+        store_cols64(st.P, payload_c, cw, cols, rows / 2, tr0 * 8, nvalid, t);
         if (t < kTileCols) {
             // column scales [cols, rows/16]: 8 bytes per column
             const int64_t gc = cw + t;

@@ -902,8 +902,10 @@ __device__ __forceinline__ void store_item(f32x16_t (&acc)[4][4], const WorkItem
                     __builtin_amdgcn_raw_buffer_store_b128(d[t], cr, vb[h] + (uint32_t)((32 * i + 8 * t) * N * 2),
                                                            0, 0);
                 wave_lds_sync();
+                if (q < 7) {
 #pragma unroll
-                for (int k = 0; k < 8; ++k) v[k] = vn[k];
+                    for (int k = 0; k < 8; ++k) v[k] = vn[k];
+                }
             }
         } else {
             // round q = 4i + j: 32 rows x 32 columns; the next round's
@@ -936,8 +938,10 @@ __device__ __forceinline__ void store_item(f32x16_t (&acc)[4][4], const WorkItem
                     __builtin_amdgcn_raw_buffer_store_b128(d[t], cr, vo, 0, 0);
                 }
                 wave_lds_sync();
+                if (q < 15) {
 #pragma unroll
-                for (int g = 0; g < 4; ++g) v[g] = vn[g];
+                    for (int g = 0; g < 4; ++g) v[g] = vn[g];
+                }
             }
         }
         return;

@@ -138,6 +138,21 @@ __device__ __forceinline__ bool wide_row(const RowSlice& r, int nvalid) {
     return hi - lo > 16;
 }
 
+// wide_row for a group of four whole blocks from the packed codes alone (one
+// code per byte of c4).  It leaves out only code-0 blocks, not blocks whose
+// nibbles are all zero, so its span is never below wide_row's: a row it
+// passes as narrow is narrow (a wider span only sends a group to the exact
+// path).  Scale exponents L + 18 = max(e, 1) rise with the code, so the
+// span is that of the largest code and the smallest nonzero one.
+__device__ __forceinline__ bool wide_codes(uint32_t c4) {
+    const uint32_t b0 = c4 & 0xFFu, b1 = (c4 >> 8) & 0xFFu, b2 = (c4 >> 16) & 0xFFu, b3 = c4 >> 24;
+    const uint32_t top = max(max(b0, b1), max(b2, b3));
+    // code - 1 wraps code 0 to the largest value: the minimum of these plus
+    // one is the smallest nonzero code (0 when every code is 0)
+    const uint32_t low = min(min(b0 - 1u, b1 - 1u), min(b2 - 1u, b3 - 1u)) + 1u;
+    return max((int)(top >> 3), 1) - max((int)(low >> 3), 1) > 16;
+}
+
 // FULLK: K % 64 == 0, so every group has four whole blocks and a row's four
 // scale codes of a group are one aligned word (cheaper loads and decode).
 template <int BMODE, bool OUT_BF16, bool FULLK>
@@ -200,7 +215,7 @@ __global__ __launch_bounds__(PM_THREADS, 2) void gemm_pm_kernel(
         const int nv0 = nvalid(0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) store_block<FULLK, FULLK>(rs, j, j < nv0, &stages[0][srow * PM_LDSK]);
-        int wide = __syncthreads_or(wide_row(rs, nv0) ? 1 : 0);
+        int wide = __syncthreads_or((FULLK ? wide_codes(rs.code[0]) : wide_row(rs, nv0)) ? 1 : 0);
         load_slice<FULLK, FULLK>(rs, src, min((int64_t)4, last), kbt);
 
         for (int64_t g = 0; g < nk; ++g) {
@@ -212,7 +227,7 @@ __global__ __launch_bounds__(PM_THREADS, 2) void gemm_pm_kernel(
                 const int nv = nvalid(g + 1);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) store_block<FULLK, FULLK>(rs, j, j < nv, nxt + srow * PM_LDSK);
-                wide_next = wide_row(rs, nv) ? 1 : 0;
+                wide_next = (FULLK ? wide_codes(rs.code[0]) : wide_row(rs, nv)) ? 1 : 0;
                 load_slice<FULLK, FULLK>(rs, src, min((g + 2) * 4, last), kbt);
             }
             // group g: one zero-accumulator MFMA per 16-k block and 32x32 tile

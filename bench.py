@@ -36,7 +36,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
 VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12   # 32-bit (and binary64 add) VALU lane ops/s
 PM_VALU_PER_GROUP = 9          # probe-matched output model: VALU ops per output per 64-product group
-PM_VALU_MEASURED = 11.3        # the same, as issued (SQ_INSTS_VALU of the fprop launch): model + decode, span check, addressing
+PM_VALU_MEASURED = 11.1        # the same, as issued (SQ_INSTS_VALU of the fprop launch): model + decode, span check, addressing
 METRIC = "quantize GB/s + emulated FP4 GEMM TFLOP/s (fprop+dgrad+wgrad), % roofline"
 
 

@@ -162,6 +162,11 @@ __global__ __launch_bounds__(PM_THREADS, 2) void gemm_pm_kernel(
     const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec, void* __restrict__ C, float amul,
     float grid_d, float inv_grid_d) {
     __shared__ __attribute__((aligned(16))) uint16_t stages[2][PM_STAGE];
+    // span flag of group g in wflag[g % 3]: set by any thread whose row is
+    // wide while it decodes the group, read by all after the next barrier,
+    // cleared by thread 0 two groups later (after a barrier that follows
+    // every read of it, before the barrier that precedes its next setting)
+    __shared__ int wflag[3];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -215,19 +220,23 @@ __global__ __launch_bounds__(PM_THREADS, 2) void gemm_pm_kernel(
         const int nv0 = nvalid(0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) store_block<FULLK, FULLK>(rs, j, j < nv0, &stages[0][srow * PM_LDSK]);
-        int wide = __syncthreads_or((FULLK ? wide_codes(rs.code[0]) : wide_row(rs, nv0)) ? 1 : 0);
+        if (tid == 0) wflag[0] = wflag[1] = wflag[2] = 0;
+        __syncthreads();
+        if (FULLK ? wide_codes(rs.code[0]) : wide_row(rs, nv0)) wflag[0] = 1;
         load_slice<FULLK, FULLK>(rs, src, min((int64_t)4, last), kbt);
+        __syncthreads();
+        int wide = __builtin_amdgcn_readfirstlane(wflag[0]);
+        int fnext = 1, fclear = 2;                       // (g + 1) % 3, (g + 2) % 3
 
         for (int64_t g = 0; g < nk; ++g) {
             const uint16_t* cur = stages[g & 1];
             uint16_t* nxt = stages[(g + 1) & 1];
             // decode group g + 1 (its bytes arrived during group g - 1)
-            int wide_next = 0;
             if (g + 1 < nk) {
                 const int nv = nvalid(g + 1);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) store_block<FULLK, FULLK>(rs, j, j < nv, nxt + srow * PM_LDSK);
-                wide_next = (FULLK ? wide_codes(rs.code[0]) : wide_row(rs, nv)) ? 1 : 0;
+                if (FULLK ? wide_codes(rs.code[0]) : wide_row(rs, nv)) wflag[fnext] = 1;
                 load_slice<FULLK, FULLK>(rs, src, min((g + 2) * 4, last), kbt);
             }
             // group g: one zero-accumulator MFMA per 16-k block and 32x32 tile
@@ -275,7 +284,11 @@ __global__ __launch_bounds__(PM_THREADS, 2) void gemm_pm_kernel(
                 }
             }
             // group g + 1 complete in LDS, group g's stage free; its span flag
-            wide = __syncthreads_or(wide_next);
+            if (tid == 0) wflag[fclear] = 0;
+            __syncthreads();
+            wide = __builtin_amdgcn_readfirstlane(wflag[fnext]);
+            fnext = fclear;
+            fclear = fclear == 2 ? 0 : fclear + 1;
         }
     }
 

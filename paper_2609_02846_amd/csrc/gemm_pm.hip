@@ -17,12 +17,19 @@
 //    core's result is exact whenever the exact value is representable;
 //    inexact sums are not rounded to nearest by it, which is why a group is
 //    never accumulated inside the matrix core);
-//  * the four block sums are added in binary64: exact when their bits span at
-//    most 53 positions.  Each workgroup checks this per group from the scale
-//    codes (every operand row's nonzero blocks within 16 binades of each
-//    other bounds the span by 2 x 16 + 19 + 2 bits); a group that fails the
-//    check takes an exact 128-bit integer path instead;
-//  * p_j = the binary32 RNE conversion of the exact binary64 sum;
+//  * each workgroup takes, per group, the largest scale-exponent span (the
+//    largest minus the smallest LSB exponent of a row's nonzero blocks) over
+//    its A rows, sA, and over its B rows, sB.  Block j's sum is N_j 2^E_j with
+//    |N_j| <= 16 x (12 x 15)^2 < 2^19 and E_j = La_j + Lb_j - 8, so the
+//    exponents of an output's nonzero block sums lie within sA + sB of each
+//    other;
+//  * sA + sB <= 4: the pairs s_0 + s_1 and s_2 + s_3 are exact in binary32
+//    (|N| 2^d + |N'| < 2^19 (2^4 + 1) < 2^24), so p_j is one RNE binary32
+//    add of the two exact pair sums;
+//  * otherwise, with sA, sB <= 16: the four block sums are added in binary64,
+//    exactly (their bits span at most 2 x 16 + 19 + 2 <= 53 positions), and
+//    p_j is the binary32 RNE conversion of that sum;
+//  * sA or sB > 16: an exact 128-bit integer sum, rounded once;
 //  * c + p_j toward zero: one v_add_f32 with the single-precision round mode
 //    set to toward-zero around the adds (the mode is restored before any
 //    other instruction).
@@ -121,10 +128,11 @@ __host__ __device__ __noinline__ float rne32_sum4_exact(float b0, float b1, floa
     return neg ? -r : r;
 }
 
-// True when this operand row's nonzero blocks of a group (nvalid of them)
-// have scale LSB exponents more than 16 apart.  Scale s = i * 2^L with L =
-// e - 18 (exponent field e >= 1, i = 8 + m) or L = -17 (e = 0, i = m).
-__device__ __forceinline__ bool wide_row(const RowSlice& r, int nvalid) {
+// Span of one operand row's group: the largest minus the smallest scale LSB
+// exponent over its nonzero blocks (nvalid of them), 0 when none is
+// nonzero.  Scale s = i * 2^L with L = e - 18 (exponent field e >= 1,
+// i = 8 + m) or L = -17 (e = 0, i = m).
+__device__ __forceinline__ int span_row(const RowSlice& r, int nvalid) {
     int lo = 1 << 10, hi = -(1 << 10);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -135,22 +143,34 @@ __device__ __forceinline__ bool wide_row(const RowSlice& r, int nvalid) {
         lo = nz ? min(lo, L) : lo;
         hi = nz ? max(hi, L) : hi;
     }
-    return hi - lo > 16;
+    return hi >= lo ? hi - lo : 0;
 }
 
-// wide_row for a group of four whole blocks from the packed codes alone (one
+// span_row for a group of four whole blocks from the packed codes alone (one
 // code per byte of c4).  It leaves out only code-0 blocks, not blocks whose
-// nibbles are all zero, so its span is never below wide_row's: a row it
-// passes as narrow is narrow (a wider span only sends a group to the exact
-// path).  Scale exponents L + 18 = max(e, 1) rise with the code, so the
-// span is that of the largest code and the smallest nonzero one.
-__device__ __forceinline__ bool wide_codes(uint32_t c4) {
+// nibbles are all zero, so it is never below span_row (a wider span only
+// sends a group to a slower exact path).  Scale exponents L + 18 = max(e, 1)
+// rise with the code, so the span is that of the largest code and the
+// smallest nonzero one.
+__device__ __forceinline__ int span_codes(uint32_t c4) {
     const uint32_t b0 = c4 & 0xFFu, b1 = (c4 >> 8) & 0xFFu, b2 = (c4 >> 16) & 0xFFu, b3 = c4 >> 24;
     const uint32_t top = max(max(b0, b1), max(b2, b3));
     // code - 1 wraps code 0 to the largest value: the minimum of these plus
     // one is the smallest nonzero code (0 when every code is 0)
     const uint32_t low = min(min(b0 - 1u, b1 - 1u), min(b2 - 1u, b3 - 1u)) + 1u;
-    return max((int)(top >> 3), 1) - max((int)(low >> 3), 1) > 16;
+    return max((int)(top >> 3), 1) - max((int)(low >> 3), 1);
+}
+
+// Raise *dst to the largest v of the wave: maxima over each row of 16 lanes
+// by DPP shifts (lane 16 r + 15 ends with its row's), then one LDS atomic
+// per row.  A maximum from all 64 lanes at one address would be served one
+// lane at a time, and the fragment reads queued behind it would wait.
+__device__ __forceinline__ void wave_raise(unsigned* dst, unsigned v, int lane) {
+    v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, true));   // row_shr:1
+    v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, true));   // row_shr:2
+    v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, true));   // row_shr:4
+    v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, true));   // row_shr:8
+    if ((lane & 15) == 15) atomicMax(dst, v);
 }
 
 // FULLK: K % 64 == 0, so every group has four whole blocks and a row's four
@@ -162,11 +182,12 @@ __global__ __launch_bounds__(PM_THREADS, 2) void gemm_pm_kernel(
     const uint8_t* __restrict__ Bs, const float* __restrict__ b_dec, void* __restrict__ C, float amul,
     float grid_d, float inv_grid_d) {
     __shared__ __attribute__((aligned(16))) uint16_t stages[2][PM_STAGE];
-    // span flag of group g in wflag[g % 3]: set by any thread whose row is
-    // wide while it decodes the group, read by all after the next barrier,
-    // cleared by thread 0 two groups later (after a barrier that follows
-    // every read of it, before the barrier that precedes its next setting)
-    __shared__ int wflag[3];
+    // largest row span of group g over the A rows (wspan[g % 3][0]) and over
+    // the B rows ([1]): raised by every wave while it decodes the group,
+    // read by all after the next barrier, cleared by thread 0 two groups
+    // later (after a barrier that follows every read of them, before the
+    // barrier that precedes their next raising)
+    __shared__ unsigned wspan[3][2];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -220,12 +241,20 @@ __global__ __launch_bounds__(PM_THREADS, 2) void gemm_pm_kernel(
         const int nv0 = nvalid(0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) store_block<FULLK, FULLK>(rs, j, j < nv0, &stages[0][srow * PM_LDSK]);
-        if (tid == 0) wflag[0] = wflag[1] = wflag[2] = 0;
+        if (tid < 6) wspan[tid >> 1][tid & 1] = 0u;
         __syncthreads();
-        if (FULLK ? wide_codes(rs.code[0]) : wide_row(rs, nv0)) wflag[0] = 1;
+        wave_raise(&wspan[0][is_a ? 0 : 1], (unsigned)(FULLK ? span_codes(rs.code[0]) : span_row(rs, nv0)), lane);
         load_slice<FULLK, FULLK>(rs, src, min((int64_t)4, last), kbt);
         __syncthreads();
-        int wide = __builtin_amdgcn_readfirstlane(wflag[0]);
+        // the group's path from the two spans (uniform): 0 when the block
+        // pairs add exactly in binary32, 1 when the four block sums add
+        // exactly in binary64, 2 otherwise (exact integer sum)
+        auto path_of = [&](int f) {
+            const int sa = __builtin_amdgcn_readfirstlane((int)wspan[f][0]);
+            const int sb = __builtin_amdgcn_readfirstlane((int)wspan[f][1]);
+            return (sa > 16 || sb > 16) ? 2 : (sa + sb <= 4 ? 0 : 1);
+        };
+        int path = path_of(0);
         int fnext = 1, fclear = 2;                       // (g + 1) % 3, (g + 2) % 3
 
         for (int64_t g = 0; g < nk; ++g) {
@@ -236,7 +265,8 @@ __global__ __launch_bounds__(PM_THREADS, 2) void gemm_pm_kernel(
                 const int nv = nvalid(g + 1);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) store_block<FULLK, FULLK>(rs, j, j < nv, nxt + srow * PM_LDSK);
-                if (FULLK ? wide_codes(rs.code[0]) : wide_row(rs, nv)) wflag[fnext] = 1;
+                wave_raise(&wspan[fnext][is_a ? 0 : 1], (unsigned)(FULLK ? span_codes(rs.code[0]) : span_row(rs, nv)),
+                           lane);
                 load_slice<FULLK, FULLK>(rs, src, min((g + 2) * 4, last), kbt);
             }
             // group g: one zero-accumulator MFMA per 16-k block and 32x32 tile
@@ -267,7 +297,10 @@ __global__ __launch_bounds__(PM_THREADS, 2) void gemm_pm_kernel(
                     const f32x16_t s2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[2], bf[j][2], z, 0, 0, 0);
                     const f32x16_t s3 = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[3], bf[j][3], z, 0, 0, 0);
                     float p[16];
-                    if (!wide) {
+                    if (path == 0) {
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) p[r] = (s0[r] + s1[r]) + (s2[r] + s3[r]);
+                    } else if (path == 1) {
 #pragma unroll
                         for (int r = 0; r < 16; ++r) {
                             double sum = (double)s0[r] + (double)s1[r];
@@ -284,9 +317,9 @@ __global__ __launch_bounds__(PM_THREADS, 2) void gemm_pm_kernel(
                 }
             }
             // group g + 1 complete in LDS, group g's stage free; its span flag
-            if (tid == 0) wflag[fclear] = 0;
+            if (tid < 2) wspan[fclear][tid] = 0u;
             __syncthreads();
-            wide = __builtin_amdgcn_readfirstlane(wflag[fnext]);
+            path = path_of(fnext);
             fnext = fclear;
             fclear = fclear == 2 ? 0 : fclear + 1;
         }

@@ -143,6 +143,55 @@ def test_pm_wide_span_groups():
         _check(c, A, B, al, d, idx, f"wide span d={d}")
 
 
+def _pair_bound_operands(M, N, K, span_a, span_b, seed):
+    """Raw operands whose groups put the block pairs (0, 1) and (2, 3) at the
+    edge of exact binary32 addition: blocks 0, 2, 3 at the largest block sum
+    (every nibble 6, scale integer 15: 518400 x 2^E), block 1 of odd products (nibbles
+    0.5, 1.5 and 6 with both signs) with its scale exponent span_a lower on
+    A and span_b lower on B, so that block 1's sums sit 2^(span_a + span_b)
+    below block 0's; blocks 2 and 3 at block 0's exponent, so that adding
+    the two pair sums usually rounds.  Every fourth A row and every second
+    B tile keep all four exponents equal (span 0), so the group's span is a
+    maximum over rows."""
+    rng = np.random.default_rng(seed)
+    nb = K // 16
+
+    def payload(rows):
+        big = np.full((rows, nb, 16), 0x7, np.uint8)
+        odd = rng.choice(np.array([0x1, 0x3, 0x7, 0x9, 0xB, 0xF], np.uint8), (rows, nb, 16))
+        nib = np.where((np.arange(nb) % 4 == 1)[None, :, None], odd, big)
+        nib = nib.reshape(rows, K)
+        return (nib[:, 0::2] | (nib[:, 1::2] << 4)).astype(np.uint8)
+
+    def codes(rows, e_top, span, flat_every):
+        e = np.full((rows, nb), e_top, np.int64)
+        e[:, 1::4] = e_top - span
+        e[::flat_every, :] = e_top
+        return ((e << 3) | 7).astype(np.uint8)
+
+    return payload(M), codes(M, 12, span_a, 4), payload(N), codes(N // 16, 10, span_b, 2)
+
+
+@pytest.mark.parametrize("K", [128, 144])
+def test_pm_pair_path_at_its_bound(K):
+    """Spans adding up to 4 take the binary32 pair path (its bound: block
+    sums up to 518400 x 2^E, pairs 2^4 apart), 5 the binary64 path; every
+    output of each launch against the oracle, with and without the snap.
+    K = 144 has a partial last group (the per-block span check)."""
+    M, N = 64, 64
+    for span_a, span_b in ((3, 1), (4, 0), (0, 4), (2, 2), (3, 2), (5, 0)):
+        pay_a, sa, pay_b, sb = _pair_bound_operands(M, N, K, span_a, span_b, 10 * span_a + span_b)
+        A = oq.decoded_1d(pay_a, sa, 1)
+        B = oq.decoded_2d(pay_b, sb)
+        idx = [(m, n) for m in range(M) for n in range(N)]
+        for d in (0, 1024):
+            say("gemm_pm pair bound", K, span_a, span_b, "grid", d)
+            c = ue.gemm_pm("nt", M, N, K, u8_to_dev(pay_a), u8_to_dev(sa), f32_scalar_dev(1.0),
+                           u8_to_dev(pay_b), u8_to_dev(sb), f32_scalar_dev(1.0), grid=d)
+            torch.cuda.synchronize()
+            _check(c, A, B, np.float32(1.0), d, idx, f"pair bound K={K} spans {span_a}+{span_b} d={d}")
+
+
 def test_pm_tie_broken_by_tiny_block():
     """One group whose block sums are 2^24, 1 and +-2^-30: the exact sum sits
     2^-30 off the binary32 tie 2^24 + 1, so RNE gives 2^24 + 2 (or 2^24);

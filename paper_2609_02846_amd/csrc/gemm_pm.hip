@@ -161,9 +161,9 @@ __device__ __forceinline__ int span_codes(uint32_t c4) {
     return max((int)(top >> 3), 1) - max((int)(low >> 3), 1);
 }
 
-// Raise *dst to the largest v of the wave: maxima over each row of 16 lanes
-// by DPP shifts (lane 16 r + 15 ends with its row's), then one LDS atomic
-// per row.  A maximum from all 64 lanes at one address would be served one
+// Raise *dst to the largest v of the wave (every lane active: the decode
+// roles are whole waves): maxima over each row of 16 lanes by DPP shifts
+// (lane 16 r + 15 ends with its row's), then one LDS atomic per row.  A maximum from all 64 lanes at one address would be served one
 // lane at a time, and the fragment reads queued behind it would wait.
 __device__ __forceinline__ void wave_raise(unsigned* dst, unsigned v, int lane) {
     v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, true));   // row_shr:1
